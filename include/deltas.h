@@ -1,0 +1,193 @@
+/*
+ * deltas.h -- C ABI of the DeltaS hot path on MI355X (gfx950).
+ *
+ * Three operations, following the paper (DeltaS: reading the gated
+ * linear-attention state for KV-cache eviction in streaming video):
+ *
+ *   gdn_chunk_fwd   gated-delta-rule forward of one linear-attention layer
+ *                   (Section 3.2, Eq. 1 / Eq. 2) over packed streams, with
+ *                   the per-frame state-drift sums of Eq. 3 fused in;
+ *   deltas_drift    per-frame drift scores from those sums (Eq. 3 and the
+ *                   line of Algorithm 1 that averages over layers);
+ *   kv_evict_topk   one eviction step of Algorithm 1 / Section 3.3:
+ *                   sink + recent window + N temporal spans with per-span
+ *                   top-k and fill, then an order-preserving in-place gather
+ *                   of every full-attention layer's K and V rows.
+ *
+ * Conventions shared by every entry point
+ *   - Pointers are DEVICE pointers unless marked "host".  The caller owns
+ *     every buffer; the library never allocates device memory.  Calls that
+ *     need scratch memory take a caller-provided workspace whose size comes
+ *     from the matching *_workspace_bytes query.
+ *   - Every call is asynchronous on `stream` (a hipStream_t passed as void*;
+ *     NULL is the default stream) and never synchronises the host.
+ *   - Arguments are validated on the host before any launch; on failure the
+ *     call returns a non-zero status and writes nothing.  Launch failures
+ *     return DS_E_HIP.  Faults inside a kernel surface at the caller's next
+ *     synchronisation.  Nothing aborts or throws across this boundary.
+ *   - Device pointers must be 16-byte aligned.
+ *   - The library keeps no state between calls except a thread-local string
+ *     describing the last error (ds_last_error).
+ */
+#ifndef DELTAS_H
+#define DELTAS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t ds_status;
+enum {
+    DS_OK = 0,
+    DS_E_NULL = 1,        /* a required pointer is NULL */
+    DS_E_SHAPE = 2,       /* inconsistent sizes */
+    DS_E_DTYPE = 3,       /* unknown dtype code */
+    DS_E_ALIGN = 4,       /* pointer not 16-byte aligned */
+    DS_E_UNSUPPORTED = 5, /* valid but not implemented (e.g. head dim) */
+    DS_E_ARG = 6,         /* other invalid argument */
+    DS_E_HIP = 7,         /* a HIP runtime call failed */
+    DS_E_WORKSPACE = 8    /* workspace NULL or smaller than required */
+};
+
+enum { DS_BF16 = 0, DS_F32 = 1 };
+
+enum {
+    DS_DRIFT_LAYER_FROB = 0, /* Eq. 3: per layer ||dS||_F / ||S_before||_F over all its heads, mean over layers */
+    DS_DRIFT_HEAD_MEAN = 1,  /* mean over layers and heads of the per-head ratio */
+    DS_DRIFT_PER_HEAD = 2    /* the per-(layer, frame, head) ratios */
+};
+
+/* Static description of a status code. */
+const char *ds_status_string(ds_status s);
+/* Detail of the last failing call on this host thread ("" if none). */
+const char *ds_last_error(void);
+
+/* ------------------------------------------------------------------------
+ * gdn_chunk_fwd -- one gated-delta-rule layer over packed streams
+ * ------------------------------------------------------------------------
+ * Computes, for every stream b and v-head j (reading qk-head
+ * h = j * H_k / H_v), token by token (Section 3.2, Eq. 2):
+ *     alpha_t = exp(g_t);  e_t = beta_t (v_t - alpha_t S_{t-1} k_t)
+ *     S_t = alpha_t S_{t-1} + e_t k_t^T;   o_t = scale * S_t q_t
+ * where S (d_v x d_k, fp32) starts from state_in.  The kernels evaluate it
+ * tile by tile (64 tokens) in an equivalent closed form; results match the
+ * recurrence up to rounding.
+ *
+ * Frames: every frame_len tokens from each stream's first token, plus the
+ * stream's ragged tail, is one frame (frame_len = 0: the whole stream is one
+ * frame).  At the end of frame f the call writes, per v-head, the two sums
+ * behind the state drift of Eq. 3:
+ *     drift_partials[f][j][0] = ||S_end - S_start||_F^2
+ *     drift_partials[f][j][1] = ||S_start||_F^2
+ * (S_start = the state when the frame began, held on chip -- the temporary
+ * copy of the previous state of Section 3.2), and optionally the state
+ * itself into snapshots[f][j].  Frames are numbered stream by stream.
+ *
+ * Shapes and layouts (row-major, innermost last):
+ *   q, k        bf16 [T_total][H_k][d_k]  (k expected L2-normalised per row)
+ *   v           bf16 [T_total][H_v][d_v]
+ *   g, beta     fp32 [T_total][H_v]       (g <= 0 is the log decay)
+ *   cu_seqlens  int32 [B+1], stream b = tokens [cu[b], cu[b+1]);
+ *               nondecreasing, cu[0] = 0, cu[B] = T_total.  NULL iff B == 1.
+ *               (Out-of-range values are clamped so that no access leaves
+ *               the buffers; results are then unspecified.)
+ *   state_in    fp32 [B][H_v][d_v][d_k] or NULL (zeros)
+ *   state_out   fp32 [B][H_v][d_v][d_k]; may alias state_in
+ *   o           [T_total][H_v][d_v] of dtype o_dtype (DS_BF16 or DS_F32)
+ *   drift_partials fp32 [n_frames][H_v][2] or NULL
+ *   snapshots   fp32 [n_frames][H_v][d_v][d_k] or NULL
+ * Supported: d_k = d_v in {64, 128}; H_v a multiple of H_k; frame_len a
+ * multiple of 64 or 0.  bf16 inputs are converted to fp16 for the matrix
+ * cores, so |q|, |k|, |v| must stay below 65504.
+ * n_frames must equal the number of frames of all streams.
+ */
+typedef struct {
+    int32_t B;         /* number of streams (>= 1) */
+    int32_t T_total;   /* tokens over all streams (>= 0) */
+    int32_t H_k;       /* query/key heads */
+    int32_t H_v;       /* value heads (state heads) */
+    int32_t d_k;       /* key head dim */
+    int32_t d_v;       /* value head dim */
+    int32_t frame_len; /* tokens per frame (multiple of 64) or 0 */
+    int32_t n_frames;  /* frames over all streams */
+} ds_gdn_shape;
+
+/* Workspace bytes gdn_chunk_fwd needs for this shape (0 on a bad shape). */
+size_t ds_gdn_workspace_bytes(const ds_gdn_shape *shape);
+
+ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k, const void *v,
+                        const float *g, const float *beta, const int32_t *cu_seqlens,
+                        const float *state_in, float *state_out, void *o, int32_t o_dtype,
+                        float scale, float *drift_partials, float *snapshots, void *workspace,
+                        size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * deltas_drift -- state drift per frame (Section 3.2, Eq. 3)
+ * ------------------------------------------------------------------------
+ * partials: fp32 [L][F][H_v][2] (num, den) as written by gdn_chunk_fwd for
+ * L layers (layer l's F frames at offset l * F * H_v * 2).
+ *   DS_DRIFT_LAYER_FROB: scores[f] = mean_l sqrt(sum_h num / sum_h den)
+ *   DS_DRIFT_HEAD_MEAN:  scores[f] = mean_{l,h} sqrt(num / den)
+ *   DS_DRIFT_PER_HEAD:   scores[l][f][h] = sqrt(num / den)
+ * den = 0 gives +inf when num > 0 and 0 otherwise; a mean containing +inf
+ * is +inf.  scores: fp32 [F] (or [L][F][H_v] for PER_HEAD).
+ */
+ds_status deltas_drift(const float *partials, int32_t L, int32_t F, int32_t H_v, int32_t mode,
+                       float *scores, void *stream);
+
+/* ------------------------------------------------------------------------
+ * kv_evict_topk -- one eviction step of Algorithm 1 (Section 3.3)
+ * ------------------------------------------------------------------------
+ * The cache holds `len` tokens (host-known) in slots [0, len) of every
+ * layer; slot i carries its original position pos[i] and the index of the
+ * chunk (frame) it arrived with, chunk_id[i].  A token's score is
+ * chunk_scores[chunk_id[i]].  If len <= M the call does nothing and sets
+ * *new_len = len.  Otherwise it keeps exactly M slots:
+ *   - the first n_sink and the last n_window slots;
+ *   - the candidates in between are split into N = max(n_buckets, 1) spans
+ *     of chunk arrival time, span(a) = floor(N (a - a_min) / (a_max - a_min + 1));
+ *     each span keeps its best floor((M - n_sink - n_window) / N)
+ *     candidates, and the leftover slots go to the best candidates not yet
+ *     kept.  "Best" orders by (score desc, chunk_id desc, pos desc): ties go
+ *     to newer tokens.
+ * The kept slots are compacted in place, in ascending slot order, in every
+ * layer's K and V rows and in pos and chunk_id (positions are moved, never
+ * rewritten).  Rows in [M, len) are unspecified afterwards.
+ *
+ * Layouts: k_layers / v_layers are HOST arrays of n_layers device pointers,
+ * each to [capacity][row_bytes] bytes (row_bytes a multiple of 16);
+ * pos, chunk_id: int32 [capacity]; chunk_scores fp32 [num_chunks], no NaN;
+ * keep_out: int32 [M] (the kept slot indices) or NULL; new_len: host int32.
+ * Cache invariants (as produced by appending chunks in arrival order and
+ * compacting in order): chunk_id nondecreasing and pos strictly increasing
+ * over [0, len), 0 <= chunk_id < num_chunks.  If the device finds them
+ * broken it leaves the cache untouched and records the failure in the
+ * workspace (see ds_kv_device_status).
+ * Requires 0 <= n_sink, 0 <= n_window, n_sink + n_window <= M,
+ * len <= capacity, n_buckets <= 64.
+ */
+typedef struct {
+    int32_t n_layers;  /* full-attention layers sharing the ranking */
+    int32_t row_bytes; /* bytes of one token's K (or V) row in one layer */
+    int32_t capacity;  /* slots allocated per layer */
+} ds_kv_shape;
+
+size_t ds_kv_workspace_bytes(const ds_kv_shape *shape);
+
+ds_status kv_evict_topk(const ds_kv_shape *shape, void *const *k_layers, void *const *v_layers,
+                        int32_t *pos, int32_t *chunk_id, const float *chunk_scores,
+                        int32_t num_chunks, int32_t len, int32_t M, int32_t n_sink,
+                        int32_t n_window, int32_t n_buckets, int32_t *keep_out, int32_t *new_len,
+                        void *workspace, size_t workspace_bytes, void *stream);
+
+/* Device address of the int32 status word kv_evict_topk leaves in its
+ * workspace: 0 = ok, 1 = cache invariants broken (cache left untouched). */
+int32_t *ds_kv_device_status(void *workspace);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DELTAS_H */

@@ -1,0 +1,187 @@
+"""DeltaS hot path on MI355X: Python binding of libdeltas (C ABI in include/deltas.h).
+
+The binding only marshals arguments: torch tensors provide device memory
+and the current HIP stream; every step of the computation runs in the HIP
+kernels of libdeltas.so.  There is no fallback -- if the library is not
+built, every entry point raises.
+"""
+from __future__ import annotations
+
+import ctypes
+from pathlib import Path
+
+import torch
+
+PKG = Path(__file__).resolve().parent
+LIB_PATH = PKG / "libdeltas.so"
+
+DS_OK = 0
+DS_BF16, DS_F32 = 0, 1
+LAYER_FROB, HEAD_MEAN, PER_HEAD = 0, 1, 2
+
+EXPORTED = [
+    "ds_status_string", "ds_last_error", "ds_gdn_workspace_bytes", "gdn_chunk_fwd", "deltas_drift",
+    "ds_kv_workspace_bytes", "kv_evict_topk", "ds_kv_device_status",
+]
+
+
+class GdnShape(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("B", "T_total", "H_k", "H_v", "d_k", "d_v", "frame_len", "n_frames")]
+
+
+class KvShape(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("n_layers", "row_bytes", "capacity")]
+
+
+class DeltasError(RuntimeError):
+    def __init__(self, status, detail):
+        super().__init__(f"status {status}: {detail}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """Load libdeltas.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not LIB_PATH.exists():
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2609_27470_amd.build.build()")
+        L = ctypes.CDLL(str(LIB_PATH))
+        P, I32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        L.ds_status_string.argtypes = [I32]
+        L.ds_status_string.restype = ctypes.c_char_p
+        L.ds_last_error.argtypes = []
+        L.ds_last_error.restype = ctypes.c_char_p
+        L.ds_gdn_workspace_bytes.argtypes = [ctypes.POINTER(GdnShape)]
+        L.ds_gdn_workspace_bytes.restype = SZ
+        L.gdn_chunk_fwd.argtypes = [ctypes.POINTER(GdnShape), P, P, P, P, P, P, P, P, P, I32, ctypes.c_float,
+                                    P, P, P, SZ, P]
+        L.gdn_chunk_fwd.restype = I32
+        L.deltas_drift.argtypes = [P, I32, I32, I32, I32, P, P]
+        L.deltas_drift.restype = I32
+        L.ds_kv_workspace_bytes.argtypes = [ctypes.POINTER(KvShape)]
+        L.ds_kv_workspace_bytes.restype = SZ
+        L.kv_evict_topk.argtypes = [ctypes.POINTER(KvShape), P, P, P, P, P, I32, I32, I32, I32, I32, I32, P,
+                                    ctypes.POINTER(I32), P, SZ, P]
+        L.kv_evict_topk.restype = I32
+        L.ds_kv_device_status.argtypes = [P]
+        L.ds_kv_device_status.restype = P
+        _lib = L
+    return _lib
+
+
+def _check(status):
+    if status != DS_OK:
+        L = lib()
+        raise DeltasError(status, L.ds_status_string(status).decode() + ": " + L.ds_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def frames_of_length(n: int, frame_len: int) -> int:
+    if n <= 0:
+        return 0
+    if frame_len <= 0:
+        return 1
+    return (n + frame_len - 1) // frame_len
+
+
+def gdn_shape(lengths, H_k, H_v, d, frame_len):
+    """ds_gdn_shape for streams of the given (host-known) lengths."""
+    lengths = [int(x) for x in lengths]
+    return GdnShape(len(lengths), sum(lengths), H_k, H_v, d, d, frame_len,
+                    sum(frames_of_length(n, frame_len) for n in lengths))
+
+
+def gdn_workspace_bytes(shape: GdnShape) -> int:
+    return int(lib().ds_gdn_workspace_bytes(ctypes.byref(shape)))
+
+
+def gdn_chunk_fwd(q, k, v, g, beta, lengths, frame_len, cu_seqlens=None, state_in=None, state_out=None,
+                  o=None, o_dtype=torch.float32, scale=1.0, drift_partials=True, snapshots=False,
+                  workspace=None, stream=None):
+    """One gated-delta-rule layer over packed streams (see gdn_chunk_fwd in deltas.h).
+
+    q, k: bf16 [T][H_k][d]; v: bf16 [T][H_v][d]; g, beta: fp32 [T][H_v];
+    lengths: host list of stream lengths; cu_seqlens: device int32 [B+1]
+    (built from lengths when None).  Returns a dict with o, state,
+    drift_partials [F][H_v][2] (or None) and snapshots (or None).
+    """
+    T, H_k, d = q.shape
+    H_v = v.shape[1]
+    shape = gdn_shape(lengths, H_k, H_v, d, frame_len)
+    dev = q.device
+    if cu_seqlens is None and shape.B > 1:
+        cu = [0]
+        for n in lengths:
+            cu.append(cu[-1] + int(n))
+        cu_seqlens = torch.tensor(cu, dtype=torch.int32, device=dev)
+    if state_out is None:
+        state_out = torch.empty((shape.B, H_v, d, d), dtype=torch.float32, device=dev)
+    if o is None:
+        o = torch.empty((T, H_v, d), dtype=o_dtype, device=dev)
+    od = DS_BF16 if o.dtype == torch.bfloat16 else DS_F32
+    dp = torch.empty((shape.n_frames, H_v, 2), dtype=torch.float32, device=dev) if drift_partials is True \
+        else drift_partials if drift_partials is not False else None
+    sn = torch.empty((shape.n_frames, H_v, d, d), dtype=torch.float32, device=dev) if snapshots is True \
+        else snapshots if snapshots is not False else None
+    need = gdn_workspace_bytes(shape)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    _check(lib().gdn_chunk_fwd(ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
+                               _ptr(cu_seqlens), _ptr(state_in), _ptr(state_out), _ptr(o), od, float(scale),
+                               _ptr(dp), _ptr(sn), _ptr(workspace), workspace.numel(), _stream(stream)))
+    return dict(o=o, state=state_out, drift_partials=dp, snapshots=sn, workspace=workspace)
+
+
+def deltas_drift(partials, mode=LAYER_FROB, scores=None, stream=None):
+    """Per-frame drift from [L][F][H_v][2] sums (see deltas_drift in deltas.h)."""
+    L, F, H, _ = partials.shape
+    if scores is None:
+        shape = (L, F, H) if mode == PER_HEAD else (F,)
+        scores = torch.empty(shape, dtype=torch.float32, device=partials.device)
+    _check(lib().deltas_drift(_ptr(partials), L, F, H, mode, _ptr(scores), _stream(stream)))
+    return scores
+
+
+def kv_workspace_bytes(n_layers, row_bytes, capacity) -> int:
+    return int(lib().ds_kv_workspace_bytes(ctypes.byref(KvShape(n_layers, row_bytes, capacity))))
+
+
+def kv_evict_topk(k_layers, v_layers, pos, chunk_id, chunk_scores, length, M, n_sink, n_window, n_buckets,
+                  keep_out=None, workspace=None, stream=None):
+    """One eviction step (see kv_evict_topk in deltas.h).
+
+    k_layers / v_layers: lists of device tensors [capacity][row elems] (any
+    dtype, rows of row_bytes bytes).  Returns (new_len, workspace).
+    """
+    L = len(k_layers)
+    capacity = k_layers[0].shape[0]
+    row_bytes = k_layers[0][0].numel() * k_layers[0].element_size()
+    shape = KvShape(L, row_bytes, capacity)
+    need = int(lib().ds_kv_workspace_bytes(ctypes.byref(shape)))
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=pos.device)
+    kp = (ctypes.c_void_p * L)(*[t.data_ptr() for t in k_layers])
+    vp = (ctypes.c_void_p * L)(*[t.data_ptr() for t in v_layers])
+    new_len = ctypes.c_int32(0)
+    _check(lib().kv_evict_topk(ctypes.byref(shape), kp, vp, _ptr(pos), _ptr(chunk_id), _ptr(chunk_scores),
+                               int(chunk_scores.numel()), int(length), int(M), int(n_sink), int(n_window),
+                               int(n_buckets), _ptr(keep_out), ctypes.byref(new_len), _ptr(workspace),
+                               workspace.numel(), _stream(stream)))
+    return int(new_len.value), workspace
+
+
+def kv_device_status(workspace):
+    """(invariant status, skip flag, wait-timeout flag) left by the last kv_evict_topk (synchronises)."""
+    return workspace[:12].view(torch.int32).cpu().tolist()

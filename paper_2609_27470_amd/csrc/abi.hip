@@ -1,0 +1,210 @@
+// C ABI of libdeltas: argument validation, workspace sizing, launches.
+// Every check runs on the host before the first launch; a rejected call
+// writes nothing.  Nothing here throws or aborts.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "deltas.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+ds_status fail(ds_status s, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+ds_status hip_fail(hipError_t e, const char *where) {
+    return fail(DS_E_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool misaligned(const void *p) { return p && (((uintptr_t)p) & 15u) != 0; }
+
+ds_status check_gdn_shape(const ds_gdn_shape *s) {
+    if (!s) return fail(DS_E_NULL, "shape is NULL");
+    if (s->B < 1 || s->T_total < 0 || s->H_k < 1 || s->H_v < 1 || s->n_frames < 0)
+        return fail(DS_E_SHAPE, "bad sizes (B=%d T_total=%d H_k=%d H_v=%d n_frames=%d)", s->B, s->T_total,
+                    s->H_k, s->H_v, s->n_frames);
+    if (s->H_v % s->H_k != 0) return fail(DS_E_SHAPE, "H_v=%d is not a multiple of H_k=%d", s->H_v, s->H_k);
+    if (s->d_k != s->d_v || (s->d_k != 64 && s->d_k != 128))
+        return fail(DS_E_UNSUPPORTED, "head dims d_k=%d d_v=%d (supported: d_k = d_v in {64, 128})", s->d_k,
+                    s->d_v);
+    if (s->frame_len < 0 || s->frame_len % 64 != 0)
+        return fail(DS_E_UNSUPPORTED, "frame_len=%d must be 0 or a multiple of 64", s->frame_len);
+    // keep every index of the kernels inside 32-bit ranges where they use them
+    if ((long long)s->T_total * s->H_v > (1LL << 31) / 2 || (long long)s->B * s->H_v * (s->d_v / 16) > (1LL << 30))
+        return fail(DS_E_UNSUPPORTED, "problem too large for one call");
+    return DS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *ds_status_string(ds_status s) {
+    switch (s) {
+    case DS_OK: return "ok";
+    case DS_E_NULL: return "required pointer is NULL";
+    case DS_E_SHAPE: return "inconsistent sizes";
+    case DS_E_DTYPE: return "unknown dtype";
+    case DS_E_ALIGN: return "pointer not 16-byte aligned";
+    case DS_E_UNSUPPORTED: return "unsupported configuration";
+    case DS_E_ARG: return "invalid argument";
+    case DS_E_HIP: return "HIP runtime error";
+    case DS_E_WORKSPACE: return "workspace missing or too small";
+    default: return "unknown status";
+    }
+}
+
+const char *ds_last_error(void) { return g_last_error; }
+
+size_t ds_gdn_workspace_bytes(const ds_gdn_shape *shape) {
+    if (check_gdn_shape(shape) != DS_OK) return 0;
+    return ds::gdn_workspace_layout(shape->B, shape->T_total, shape->H_v, shape->d_v, shape->n_frames).total;
+}
+
+ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k, const void *v, const float *g,
+                        const float *beta, const int32_t *cu_seqlens, const float *state_in, float *state_out,
+                        void *o, int32_t o_dtype, float scale, float *drift_partials, float *snapshots,
+                        void *workspace, size_t workspace_bytes, void *stream) {
+    g_last_error[0] = 0;
+    ds_status st = check_gdn_shape(shape);
+    if (st != DS_OK) return st;
+    const ds_gdn_shape &s = *shape;
+    if (s.T_total > 0 && (!q || !k || !v || !g || !beta || !o))
+        return fail(DS_E_NULL, "q, k, v, g, beta and o are required");
+    if (!state_out) return fail(DS_E_NULL, "state_out is required");
+    if (s.B > 1 && !cu_seqlens) return fail(DS_E_NULL, "cu_seqlens is required when B > 1");
+    if (o_dtype != DS_BF16 && o_dtype != DS_F32) return fail(DS_E_DTYPE, "o_dtype=%d", o_dtype);
+    const void *ptrs[] = {q, k, v, g, beta, cu_seqlens, state_in, state_out, o, drift_partials, snapshots, workspace};
+    for (const void *p : ptrs)
+        if (misaligned(p)) return fail(DS_E_ALIGN, "a pointer is not 16-byte aligned");
+    const ds::GdnWorkspace lay = ds::gdn_workspace_layout(s.B, s.T_total, s.H_v, s.d_v, s.n_frames);
+    if (!workspace || workspace_bytes < lay.total)
+        return fail(DS_E_WORKSPACE, "workspace needs %zu bytes, got %zu", lay.total, workspace_bytes);
+    if (s.n_frames > 0 && s.frame_len == 0 && s.n_frames > s.B)
+        return fail(DS_E_SHAPE, "n_frames=%d exceeds B=%d with frame_len=0", s.n_frames, s.B);
+    if (s.frame_len > 0 && (long long)s.n_frames > (long long)s.T_total / s.frame_len + s.B)
+        return fail(DS_E_SHAPE, "n_frames=%d is more than the streams can hold", s.n_frames);
+
+    ds::GdnLaunch p;
+    p.q = (const uint16_t *)q;
+    p.k = (const uint16_t *)k;
+    p.v = (const uint16_t *)v;
+    p.g = g;
+    p.beta = beta;
+    p.cu_seqlens = cu_seqlens;
+    p.B = s.B;
+    p.T_total = s.T_total;
+    p.H_k = s.H_k;
+    p.H_v = s.H_v;
+    p.d = s.d_k;
+    p.frame_len = s.frame_len;
+    p.n_frames = s.n_frames;
+    p.state_in = state_in;
+    p.state_out = state_out;
+    p.o = o;
+    p.o_bf16 = (o_dtype == DS_BF16);
+    p.scale = scale;
+    p.drift_partials = drift_partials;
+    p.snapshots = snapshots;
+    char *ws = (char *)workspace;
+    p.wsT = (_Float16 *)(ws + lay.offT);
+    p.wsP = (_Float16 *)(ws + lay.offP);
+    p.wsGam = (float *)(ws + lay.offGam);
+    p.wsDrift = (float *)(ws + lay.offDrift);
+    p.tiles_max = lay.tiles_max;
+    p.n_split = lay.n_split;
+    hipError_t e = ds::launch_gdn(p, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "gdn_chunk_fwd launch");
+    return DS_OK;
+}
+
+ds_status deltas_drift(const float *partials, int32_t L, int32_t F, int32_t H_v, int32_t mode, float *scores,
+                       void *stream) {
+    g_last_error[0] = 0;
+    if (L < 0 || F < 0 || H_v < 1) return fail(DS_E_SHAPE, "L=%d F=%d H_v=%d", L, F, H_v);
+    if (mode < DS_DRIFT_LAYER_FROB || mode > DS_DRIFT_PER_HEAD) return fail(DS_E_ARG, "mode=%d", mode);
+    if ((long long)L * F * H_v == 0) return DS_OK;
+    if (!partials || !scores) return fail(DS_E_NULL, "partials and scores are required");
+    if ((long long)L * F * H_v * 2 > (1LL << 31)) return fail(DS_E_UNSUPPORTED, "too many partials");
+    hipError_t e = ds::launch_drift(partials, L, F, H_v, mode, scores, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "deltas_drift launch");
+    return DS_OK;
+}
+
+size_t ds_kv_workspace_bytes(const ds_kv_shape *shape) {
+    if (!shape || shape->n_layers < 1 || shape->row_bytes < 16 || shape->row_bytes % 16 || shape->capacity < 1 ||
+        2 * shape->n_layers > ds::KV_MAX_PLANES)
+        return 0;
+    return ds::kv_workspace_layout(shape->n_layers, shape->row_bytes, shape->capacity).total;
+}
+
+int32_t *ds_kv_device_status(void *workspace) { return (int32_t *)workspace; }
+
+ds_status kv_evict_topk(const ds_kv_shape *shape, void *const *k_layers, void *const *v_layers, int32_t *pos,
+                        int32_t *chunk_id, const float *chunk_scores, int32_t num_chunks, int32_t len, int32_t M,
+                        int32_t n_sink, int32_t n_window, int32_t n_buckets, int32_t *keep_out, int32_t *new_len,
+                        void *workspace, size_t workspace_bytes, void *stream) {
+    g_last_error[0] = 0;
+    if (!shape || !new_len) return fail(DS_E_NULL, "shape and new_len are required");
+    const ds_kv_shape &s = *shape;
+    if (s.n_layers < 1 || 2 * s.n_layers > ds::KV_MAX_PLANES)
+        return fail(DS_E_UNSUPPORTED, "n_layers=%d (1..%d)", s.n_layers, ds::KV_MAX_PLANES / 2);
+    if (s.row_bytes < 16 || s.row_bytes % 16) return fail(DS_E_SHAPE, "row_bytes=%d must be a positive multiple of 16", s.row_bytes);
+    if (s.capacity < 1) return fail(DS_E_SHAPE, "capacity=%d", s.capacity);
+    if (len < 0 || len > s.capacity) return fail(DS_E_SHAPE, "len=%d outside [0, capacity=%d]", len, s.capacity);
+    if (M < 0 || n_sink < 0 || n_window < 0 || (long long)n_sink + n_window > M)
+        return fail(DS_E_ARG, "need 0 <= n_sink, 0 <= n_window, n_sink + n_window <= M (got %d, %d, %d)", n_sink,
+                    n_window, M);
+    if (n_buckets < 0 || n_buckets > 64) return fail(DS_E_ARG, "n_buckets=%d (0..64)", n_buckets);
+    if (num_chunks < 1) return fail(DS_E_ARG, "num_chunks=%d", num_chunks);
+    if ((long long)s.capacity * s.row_bytes > (1LL << 40)) return fail(DS_E_UNSUPPORTED, "cache too large");
+    if (len <= M) {
+        *new_len = len;
+        return DS_OK;
+    }
+    if (!k_layers || !v_layers || !pos || !chunk_id || !chunk_scores)
+        return fail(DS_E_NULL, "cache pointers, pos, chunk_id and chunk_scores are required");
+    ds::KvLaunch p;
+    p.n_planes = 2 * s.n_layers;
+    for (int l = 0; l < s.n_layers; ++l) {
+        if (!k_layers[l] || !v_layers[l]) return fail(DS_E_NULL, "layer %d has a NULL K or V pointer", l);
+        if (misaligned(k_layers[l]) || misaligned(v_layers[l]))
+            return fail(DS_E_ALIGN, "layer %d K/V not 16-byte aligned", l);
+        p.planes[l] = (char *)k_layers[l];
+        p.planes[s.n_layers + l] = (char *)v_layers[l];
+    }
+    const void *ptrs[] = {pos, chunk_id, chunk_scores, keep_out, workspace};
+    for (const void *q : ptrs)
+        if (misaligned(q)) return fail(DS_E_ALIGN, "a pointer is not 16-byte aligned");
+    const ds::KvWorkspace lay = ds::kv_workspace_layout(s.n_layers, s.row_bytes, s.capacity);
+    if (!workspace || workspace_bytes < lay.total)
+        return fail(DS_E_WORKSPACE, "workspace needs %zu bytes, got %zu", lay.total, workspace_bytes);
+    p.row_bytes = s.row_bytes;
+    p.capacity = s.capacity;
+    p.pos = pos;
+    p.chunk_id = chunk_id;
+    p.chunk_scores = chunk_scores;
+    p.num_chunks = num_chunks;
+    p.len = len;
+    p.M = M;
+    p.n_sink = n_sink;
+    p.n_window = n_window;
+    p.n_buckets = n_buckets;
+    p.keep_out = keep_out;
+    p.ws = (char *)workspace;
+    p.lay = lay;
+    hipError_t e = ds::launch_kv_evict(p, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "kv_evict_topk launch");
+    *new_len = M;
+    return DS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,66 @@
+// Internal launch interface between the C ABI (abi.hip) and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ds {
+
+// ---------------------------------------------------------------- GDN forward
+struct GdnLaunch {
+    const uint16_t *q, *k, *v;
+    const float *g, *beta;
+    const int32_t *cu_seqlens;
+    int B, T_total, H_k, H_v, d;  // d = d_k = d_v
+    int frame_len, n_frames;
+    const float *state_in;
+    float *state_out;
+    void *o;
+    int o_bf16;
+    float scale;
+    float *drift_partials;  // [n_frames][H_v][2] or null
+    float *snapshots;       // [n_frames][H_v][d][d] or null
+    // workspace pieces
+    _Float16 *wsT;      // [tiles_max][H_v][64][64]  T diag(beta), fp16
+    _Float16 *wsP;      // [tiles_max][H_v][64][64]  D (.) tril(Q K^T), fp16
+    float *wsGam;       // [tiles_max][H_v][64]      in-tile cumulative log decay
+    float *wsDrift;     // [n_frames][H_v][n_split][2]
+    int tiles_max;
+    int n_split;        // d_v slices of 16 per (stream, v-head)
+};
+
+// Workspace layout shared by the size query and the launcher.
+struct GdnWorkspace {
+    size_t offT, offP, offGam, offDrift, total;
+    int tiles_max, n_split;
+};
+GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_v, int d, int n_frames);
+hipError_t launch_gdn(const GdnLaunch &p, hipStream_t stream);
+
+// ---------------------------------------------------------------- drift reduce
+hipError_t launch_drift(const float *partials, int L, int F, int H_v, int mode, float *scores,
+                        hipStream_t stream);
+
+// ---------------------------------------------------------------- KV eviction
+constexpr int KV_MAX_PLANES = 64;  // 2 * n_layers
+
+struct KvWorkspace {
+    size_t offStatus, offKeep, offInv, offMask, offRunStart, offRunKey, offRunBkt, offRunTake,
+        offFlags, total;
+    int n_chunks;  // 64 KiB pieces of one token's rows over all layers
+};
+KvWorkspace kv_workspace_layout(int n_layers, int row_bytes, int capacity);
+
+struct KvLaunch {
+    char *planes[KV_MAX_PLANES];  // K of layer 0..L-1, then V of layer 0..L-1
+    int n_planes, row_bytes, capacity;
+    int32_t *pos, *chunk_id;
+    const float *chunk_scores;
+    int num_chunks, len, M, n_sink, n_window, n_buckets;
+    int32_t *keep_out;
+    char *ws;
+    KvWorkspace lay;
+};
+hipError_t launch_kv_evict(const KvLaunch &p, hipStream_t stream);
+
+}  // namespace ds

@@ -1,0 +1,168 @@
+"""GPU parity of kv_evict_topk: the keep list is bit-exact with the oracle's
+selection, and the compacted K/V rows, positions and chunk ids are bit-exact
+with the oracle's gather (position-keyed rows regenerate the expected cache)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from gpu_helpers import DEV
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ds():
+    import paper_2609_27470_amd as ds
+    ds.lib()
+    return ds
+
+
+def make_cache(L, row_elems, capacity, chunk, pos):
+    """K/V planes whose row at slot i is the hash row of position pos[i]."""
+    n = len(pos)
+    pos_t = torch.zeros(capacity, dtype=torch.int64, device=DEV)
+    pos_t[:n] = torch.as_tensor(np.asarray(pos, np.int64), device=DEV)
+    ks, vs = [], []
+    for l in range(L):
+        kk = torch.zeros((capacity, row_elems), dtype=torch.int16, device=DEV)
+        vv = torch.zeros((capacity, row_elems), dtype=torch.int16, device=DEV)
+        kk[:n] = synth.kv_row_bits_torch(l, 0, pos_t[:n], row_elems)
+        vv[:n] = synth.kv_row_bits_torch(l, 1, pos_t[:n], row_elems)
+        ks.append(kk)
+        vs.append(vv)
+    p = torch.zeros(capacity, dtype=torch.int32, device=DEV)
+    c = torch.zeros(capacity, dtype=torch.int32, device=DEV)
+    p[:n] = torch.as_tensor(np.asarray(pos, np.int32), device=DEV)
+    c[:n] = torch.as_tensor(np.asarray(chunk, np.int32), device=DEV)
+    return ks, vs, p, c
+
+
+def check_cache(ks, vs, p, c, M, exp_pos, exp_chunk):
+    assert np.array_equal(p[:M].cpu().numpy(), exp_pos)
+    assert np.array_equal(c[:M].cpu().numpy(), exp_chunk)
+    ep = torch.as_tensor(np.asarray(exp_pos, np.int64), device=DEV)
+    for l, (kk, vv) in enumerate(zip(ks, vs)):
+        assert torch.equal(kk[:M], synth.kv_row_bits_torch(l, 0, ep, kk.shape[1])), f"K layer {l}"
+        assert torch.equal(vv[:M], synth.kv_row_bits_torch(l, 1, ep, vv.shape[1])), f"V layer {l}"
+
+
+def one_event(ds, L, row_elems, chunk, pos, scores, M, ns, nw, nb, capacity=None):
+    n = len(pos)
+    capacity = capacity or n
+    ks, vs, p, c = make_cache(L, row_elems, capacity, chunk, pos)
+    sc = torch.as_tensor(np.asarray(scores, np.float32), device=DEV)
+    keep = torch.full((max(M, 1),), -1, dtype=torch.int32, device=DEV)
+    new_len, ws = ds.kv_evict_topk(ks, vs, p, c, sc, n, M, ns, nw, nb, keep_out=keep)
+    torch.cuda.synchronize()
+    ref = oracle.select_keep(chunk, pos, scores, n, M, ns, nw, nb)
+    if n <= M:
+        assert new_len == n
+        check_cache(ks, vs, p, c, n, np.asarray(pos), np.asarray(chunk))
+        return
+    assert new_len == M
+    assert keep[:M].cpu().tolist() == ref
+    st = ds.kv_device_status(ws)
+    assert st[0] == 0 and st[2] == 0, st
+    check_cache(ks, vs, p, c, M, np.asarray(pos)[ref], np.asarray(chunk)[ref])
+
+
+def random_cache(rng, n_chunks, lo, hi, thin=0.8):
+    lens = rng.integers(lo, hi + 1, n_chunks)
+    chunk = np.repeat(np.arange(n_chunks), lens)
+    keep = rng.random(len(chunk)) < thin
+    chunk = chunk[keep]
+    pos = (np.nonzero(keep)[0] + 3).astype(np.int64)
+    return chunk.astype(np.int32), pos.astype(np.int32)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_small_caches(ds, seed):
+    rng = np.random.default_rng(1000 + seed)
+    chunk, pos = random_cache(rng, int(rng.integers(3, 40)), 1, 60)
+    n = len(chunk)
+    scores = rng.choice([0.1, 0.25, 0.5, 1.0, 2.0], size=int(chunk.max()) + 1).astype(np.float32)
+    if seed % 3 == 0:
+        scores[0] = np.inf
+    ns = int(rng.integers(0, 5))
+    nw = int(rng.integers(0, 40))
+    M = int(rng.integers(ns + nw, n + 3))
+    nb = int(rng.integers(0, 9))
+    one_event(ds, 2, 64 * (1 + seed % 3), chunk, pos, scores, M, ns, nw, nb)
+
+
+def test_golden_examples_on_gpu(ds):
+    import json, math, os
+    gd = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "select_examples.json")))
+    chunk = np.array(gd["cache"]["chunk_id"], np.int32)
+    pos = np.array(gd["cache"]["pos"], np.int32)
+    for c in gd["cases"]:
+        sc = [math.inf if s == "inf" else float(s) for s in c["chunk_scores"]]
+        one_event(ds, 1, 8, chunk, pos, sc, c["M"], c["n_sink"], c["n_window"], c["n_buckets"])
+
+
+def test_equal_scores_keep_newest(ds):
+    chunk = np.repeat(np.arange(10), 50).astype(np.int32)
+    pos = np.arange(500, dtype=np.int32)
+    one_event(ds, 1, 64, chunk, pos, np.full(10, 0.5, np.float32), 123, 0, 0, 1)
+
+
+@pytest.mark.parametrize("policy", [(0, 0, 1), (4, 1024, 4)])
+def test_eviction_loop_shape(ds, policy):
+    """The eviction-loop cache at full size: 8 layers x (K, V) x 8 heads x 256
+    bf16 (4 KiB rows), 17 chunks of 1024 tokens, budget 16384, capacity 17408."""
+    ns, nw, nb = policy
+    rng = np.random.default_rng(5)
+    chunk = np.repeat(np.arange(17), 1024).astype(np.int32)
+    pos = np.arange(17 * 1024, dtype=np.int32) + 40000
+    scores = rng.random(17).astype(np.float32)
+    scores[3] = np.inf
+    one_event(ds, 8, 2048, chunk, pos, scores, 16384, ns, nw, nb)
+
+
+def test_repeated_events_stream(ds):
+    """Append a chunk per step and evict down to M every time the cache
+    overflows; after every step the cache equals the oracle's replay."""
+    L, row, M, F, capacity = 3, 128, 700, 96, 700 + 96
+    rng = np.random.default_rng(11)
+    steps = 40
+    scores_all = rng.random(steps).astype(np.float32)
+    scores_all[0] = np.inf
+    ks, vs, p, c = make_cache(L, row, capacity, [], [])
+    sc = torch.as_tensor(scores_all, device=DEV)
+    ref_pos, ref_chunk = np.zeros(0, np.int64), np.zeros(0, np.int64)
+    n = 0
+    ws = None
+    for f in range(steps):
+        new_pos = np.arange(f * F, (f + 1) * F, dtype=np.int64)
+        pt = torch.as_tensor(new_pos, device=DEV)
+        for l in range(L):
+            ks[l][n:n + F] = synth.kv_row_bits_torch(l, 0, pt, row)
+            vs[l][n:n + F] = synth.kv_row_bits_torch(l, 1, pt, row)
+        p[n:n + F] = pt.to(torch.int32)
+        c[n:n + F] = f
+        n += F
+        ref_pos = np.concatenate([ref_pos, new_pos])
+        ref_chunk = np.concatenate([ref_chunk, np.full(F, f)])
+        new_len, ws = ds.kv_evict_topk(ks, vs, p, c, sc, n, M, 4, 64, 4, workspace=ws)
+        if n > M:
+            keep = oracle.select_keep(ref_chunk, ref_pos, scores_all, n, M, 4, 64, 4)
+            ref_pos, ref_chunk = ref_pos[keep], ref_chunk[keep]
+        n = new_len
+        torch.cuda.synchronize()
+        check_cache(ks, vs, p, c, n, ref_pos, ref_chunk)
+
+
+def test_broken_invariants_leave_cache_untouched(ds):
+    chunk = np.repeat(np.arange(6), 20).astype(np.int32)
+    chunk[50] = 0                                   # chunk ids go backwards
+    pos = np.arange(120, dtype=np.int32)
+    ks, vs, p, c = make_cache(1, 64, 120, chunk, pos)
+    before = ks[0].clone()
+    sc = torch.ones(6, dtype=torch.float32, device=DEV)
+    new_len, ws = ds.kv_evict_topk(ks, vs, p, c, sc, 120, 60, 0, 0, 1)
+    torch.cuda.synchronize()
+    assert ds.kv_device_status(ws)[0] == 1
+    assert torch.equal(ks[0], before)
+    assert np.array_equal(p.cpu().numpy(), pos)
