@@ -1,0 +1,268 @@
+"""Benchmark of the DeltaS hot path on one MI355X.
+
+One step = one pass of the whole path over one batch of synthetic input,
+with every input already resident in HBM:
+  1. gdn_chunk_fwd over the single-layer workload (16 qk / 32 v heads,
+     d = 128, T = 32768 tokens, frames of 1024, bf16 in/out, fp32 state),
+     with the per-frame drift sums fused in;
+  2. deltas_drift: Eq. 3 scores of the 32 frames into the chunk-score table;
+  3. the newest chunk's K/V rows (1024 tokens) are appended to the
+     full-attention cache (8 layers x 8 KV heads x 256 bf16, budget 16384,
+     capacity 17408), as the streaming loop does after each chunk;
+  4. kv_evict_topk: one eviction event (17408 -> 16384 tokens, keep the top
+     chunks by drift, ties to newer), compacting K/V in place.
+
+Prints ONE JSON line.  Per-call times come from HIP events recorded on the
+stream the calls are launched on.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "GDN+drift tokens/s per GPU; MFMA util %; drift overhead % of GDN fwd"
+HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = 2500.0     # dense bf16/fp16
+
+# single-layer workload
+H_K, H_V, D, T, FRAME = 16, 32, 128, 32768, 1024
+C = 64
+# eviction-loop cache
+KV_LAYERS, KV_HEADS, KV_DIM, BUDGET, CAPACITY = 8, 8, 256, 16384, 16384 + 1024
+
+
+def algorithmic_work(T_tokens, H_k, H_v, d, C=64):
+    """Dense-tile chunkwise flops and the bytes a single pass must move.
+
+    flops/token = H_k 4 C d (K K^T, Q K^T) + H_v (4 C d + 6 d d + 2/3 C^2);
+    bytes/token = q, k (bf16, H_k d each) + v, o (bf16, H_v d each) + g, beta (fp32).
+    """
+    flops = T_tokens * (H_k * 4 * C * d + H_v * (4 * C * d + 6 * d * d + (2.0 / 3.0) * C * C))
+    bytes_ = T_tokens * (H_k * d * 2 * 2 + H_v * d * 2 * 2 + H_v * 4 * 2)
+    return flops, bytes_
+
+
+def cpu_baseline(x, budget_s=12.0):
+    """The fp64 oracle timed on this host's cores over a bounded prefix of the
+    same stream (all heads), plus one eviction (selection + gather) on the
+    same cache shape; scaled to tokens/s of the full step."""
+    import oracle
+    threads = oracle.max_threads()
+    n = 256
+    while True:
+        sl = slice(0, n)
+        t0 = time.perf_counter()
+        oracle.gdn_forward(x.q[sl], x.k[sl], x.v[sl], x.g[sl], x.beta[sl], np.array([0, n], np.int32), FRAME)
+        dt = time.perf_counter() - t0
+        if dt * 4 > budget_s or n * 4 > T:
+            break
+        n *= 4
+    gdn_s_per_token = dt / n
+    # one eviction event on the eviction-loop cache shape
+    rng = np.random.default_rng(0)
+    chunk = np.repeat(np.arange(17), 1024)
+    pos = np.arange(CAPACITY)
+    scores = rng.random(17)
+    t0 = time.perf_counter()
+    keep = oracle.select_keep(chunk, pos, scores, CAPACITY, BUDGET, 0, 0, 1)
+    rows = np.zeros((CAPACITY, KV_HEADS * KV_DIM), np.uint16)
+    sel_s = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.compact(rows, keep)
+    gather_one = time.perf_counter() - t0
+    evict_s = sel_s + gather_one * 2 * KV_LAYERS
+    step_s = gdn_s_per_token * T + evict_s
+    return {"value": T / step_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"fp64 token recurrence of all 32 heads over the first {n} of the {T} tokens "
+                      f"({dt:.1f} s, scaled to the full stream) + one eviction (selection in Python, "
+                      f"numpy gather of 16 planes of {CAPACITY}x4 KiB rows)"}
+
+
+def copy_calibration(nbytes):
+    import torch
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": nbytes}))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0,
+                    help="only run a plain device copy of this many bytes (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the hot path runs on a single MI355X; see DESIGN.md for how it would shard).",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
+
+    import torch
+    import paper_2609_27470_amd as ds
+    import synth
+    ds.lib()
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+
+    # ---------------- inputs (host generation, then resident in HBM)
+    x = synth.workload_inputs("single_layer")
+    to = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dev).view(dt)
+    q, k, v = to(x.q.view(np.int16), torch.bfloat16), to(x.k.view(np.int16), torch.bfloat16), \
+        to(x.v.view(np.int16), torch.bfloat16)
+    g, beta = to(x.g, torch.float32), to(x.beta, torch.float32)
+    o = torch.empty((T, H_V, D), dtype=torch.bfloat16, device=dev)
+    state = torch.empty((1, H_V, D, D), dtype=torch.float32, device=dev)
+    n_frames = T // FRAME
+    partials = torch.empty((n_frames, H_V, 2), dtype=torch.float32, device=dev)
+    shape = ds.gdn_shape([T], H_K, H_V, D, FRAME)
+    ws = torch.empty(ds.gdn_workspace_bytes(shape), dtype=torch.uint8, device=dev)
+
+    # ---------------- KV cache: one tensor [2L][capacity][row] so a chunk append is one copy
+    row_elems = KV_HEADS * KV_DIM
+    total_steps = args.warmup + args.steps + 64
+    cache = torch.empty((2 * KV_LAYERS, CAPACITY, row_elems), dtype=torch.int16, device=dev)
+    pos_init = torch.arange(CAPACITY, dtype=torch.int64, device=dev)
+    for p in range(2 * KV_LAYERS):
+        cache[p] = synth.kv_row_bits_torch(p % KV_LAYERS, p // KV_LAYERS, pos_init, row_elems)
+    new_rows = cache[:, :1024].clone()
+    k_layers = [cache[l] for l in range(KV_LAYERS)]
+    v_layers = [cache[KV_LAYERS + l] for l in range(KV_LAYERS)]
+    kv_pos = torch.zeros(CAPACITY, dtype=torch.int32, device=dev)
+    kv_chunk = torch.zeros(CAPACITY, dtype=torch.int32, device=dev)
+    kv_pos[:BUDGET] = torch.arange(BUDGET, dtype=torch.int32, device=dev)
+    kv_chunk[:BUDGET] = torch.arange(BUDGET, dtype=torch.int32, device=dev) // 1024
+    n_init_chunks = BUDGET // 1024
+    table = torch.zeros(n_init_chunks + n_frames * total_steps, dtype=torch.float32, device=dev)
+    table[:n_init_chunks] = torch.rand(n_init_chunks, generator=torch.Generator().manual_seed(0)).to(dev)
+    kv_ws = torch.empty(ds.kv_workspace_bytes(KV_LAYERS, row_elems * 2, CAPACITY), dtype=torch.uint8, device=dev)
+    append_pos = torch.arange(1024, dtype=torch.int32, device=dev)
+    state_ref = {"len": BUDGET, "next_pos": BUDGET, "step": 0}
+
+    def step(evs=None):
+        s = state_ref["step"]
+        base = n_init_chunks + n_frames * s
+        if evs is not None:
+            evs[0].record(stream)
+        ds.gdn_chunk_fwd(q, k, v, g, beta, [T], FRAME, state_out=state, o=o, drift_partials=partials,
+                         workspace=ws)
+        if evs is not None:
+            evs[1].record(stream)
+        ds.deltas_drift(partials.view(1, n_frames, H_V, 2), ds.LAYER_FROB, scores=table[base:base + n_frames])
+        if evs is not None:
+            evs[2].record(stream)
+        # append the newest chunk (1024 tokens): rows, positions, chunk id
+        n = state_ref["len"]
+        cache[:, n:n + 1024].copy_(new_rows)
+        kv_pos[n:n + 1024] = append_pos + state_ref["next_pos"]
+        kv_chunk[n:n + 1024] = base + n_frames - 1
+        state_ref["next_pos"] += 1024
+        if evs is not None:
+            evs[3].record(stream)
+        new_len, _ = ds.kv_evict_topk(k_layers, v_layers, kv_pos, kv_chunk, table, n + 1024, BUDGET, 0, 0, 1,
+                                      workspace=kv_ws)
+        if evs is not None:
+            evs[4].record(stream)
+        state_ref["len"] = new_len
+        state_ref["step"] = s + 1
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = 1e3 * wall / args.steps
+    seg = np.array([[evs[i][j].elapsed_time(evs[i][j + 1]) for j in range(4)] for i in range(args.steps)])
+    gdn_ms, drift_ms, append_ms, evict_ms = seg.mean(axis=0)
+    status = ds.kv_device_status(kv_ws)
+    if status[0] != 0 or status[2] != 0:
+        raise RuntimeError(f"eviction reported device status {status}")
+
+    # ---------------- forward without drift (for the drift overhead), same stream
+    reps = max(5, args.steps)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(2):
+        ds.gdn_chunk_fwd(q, k, v, g, beta, [T], FRAME, state_out=state, o=o, drift_partials=False, workspace=ws)
+    e0.record(stream)
+    for _ in range(reps):
+        ds.gdn_chunk_fwd(q, k, v, g, beta, [T], FRAME, state_out=state, o=o, drift_partials=False, workspace=ws)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    nodrift_ms = e0.elapsed_time(e1) / reps
+    drift_overhead = 100.0 * ((gdn_ms + drift_ms) / nodrift_ms - 1.0)
+
+    flops, bytes_ = algorithmic_work(T, H_K, H_V, D)
+    achieved_gbs = bytes_ / (gdn_ms * 1e-3) / 1e9
+    achieved_tflops = flops / (gdn_ms * 1e-3) / 1e12
+
+    traffic = None
+    tf = os.path.join(ROOT, "profiles", "gdn_chunk_fwd_single_layer_traffic.json")
+    if os.path.exists(tf):
+        try:
+            traffic = json.load(open(tf)).get("bytes_per_launch")
+        except Exception:
+            traffic = None
+
+    out = {
+        "metric": METRIC,
+        "value": T / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "single_layer GDN (H_k=16, H_v=32, d=128, T=32768, frames of 1024) + drift "
+                        "+ one eviction event (8 layers x 8 KV heads x 256 bf16, M=16384, capacity 17408, "
+                        "top chunks by drift, ties to newer)",
+            "global_batch": 1, "seq_len": T, "parallelism": "none",
+        },
+        "roofline": {
+            "bound": "hbm", "achieved": achieved_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": achieved_gbs / HBM_PEAK_GBS, "traffic": traffic,
+            "kernel": "gdn_chunk_fwd (gdn_prep + gdn_seq + drift finalize)",
+            "algorithmic_bytes_per_launch": bytes_, "launch_ms": gdn_ms,
+        },
+        "gdn_drift_tokens_per_s": T / ((gdn_ms + drift_ms) * 1e-3),
+        "mfma_util_pct": 100.0 * achieved_tflops / MFMA_PEAK_TFLOPS,
+        "algorithmic_tflops": achieved_tflops,
+        "drift_overhead_pct": drift_overhead,
+        "drift_overhead_paper_pct": 1.9,
+        "breakdown_ms": {"gdn_chunk_fwd": gdn_ms, "deltas_drift": drift_ms, "kv_append": append_ms,
+                         "kv_evict_topk": evict_ms, "gdn_chunk_fwd_without_drift": nodrift_ms},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(x)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

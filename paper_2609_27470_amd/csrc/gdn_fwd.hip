@@ -233,7 +233,7 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
 // gdn_seq: one workgroup per (stream, v-head, 16 consecutive rows of S).
 // Wave w owns state columns [w D/4, (w+1) D/4) of those 16 rows.
 // ============================================================================
-template <int D, bool OUT_BF16>
+template <int D, bool OUT_BF16, bool DRIFT>
 __global__ __launch_bounds__(256) void gdn_seq_kernel(GdnArgs a) {
     constexpr int KS = D / 32;
     constexpr int NB = D / 64;    // 16-column state blocks per wave
@@ -436,7 +436,7 @@ __global__ __launch_bounds__(256) void gdn_seq_kernel(GdnArgs a) {
 
         // ---- frame end: drift sums of this slice, optional snapshot
         const int done = TILE * lt + n;
-        if ((a.frame_len > 0 && done % a.frame_len == 0) || done == len) {
+        if (DRIFT && ((a.frame_len > 0 && done % a.frame_len == 0) || done == len)) {
             float num = 0.f, den = 0.f;
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
@@ -559,10 +559,19 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
         if (e != hipSuccess) return e;
     }
     const int n_wg = p.B * p.H_v * p.n_split;
-    if (p.o_bf16)
-        hipLaunchKernelGGL((gdn_seq_kernel<D, true>), dim3(n_wg), dim3(256), 0, stream, a);
-    else
-        hipLaunchKernelGGL((gdn_seq_kernel<D, false>), dim3(n_wg), dim3(256), 0, stream, a);
+    // the frame-end work is compiled out when neither drift sums nor snapshots are asked for
+    const bool drift = p.drift_partials || p.snapshots;
+    if (p.o_bf16) {
+        if (drift)
+            hipLaunchKernelGGL((gdn_seq_kernel<D, true, true>), dim3(n_wg), dim3(256), 0, stream, a);
+        else
+            hipLaunchKernelGGL((gdn_seq_kernel<D, true, false>), dim3(n_wg), dim3(256), 0, stream, a);
+    } else {
+        if (drift)
+            hipLaunchKernelGGL((gdn_seq_kernel<D, false, true>), dim3(n_wg), dim3(256), 0, stream, a);
+        else
+            hipLaunchKernelGGL((gdn_seq_kernel<D, false, false>), dim3(n_wg), dim3(256), 0, stream, a);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (p.drift_partials && p.n_frames > 0) {
