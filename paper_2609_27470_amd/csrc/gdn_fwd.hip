@@ -142,6 +142,7 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
                 const float y = __shfl_up(s, off, 64);
                 if (lane >= off) s += y;
             }
+            s *= 1.4426950408889634f;  // gamma in base-2 units: exp(gamma) = exp2(s)
             gam_s[lane] = s;
             beta_s[lane] = bv;
             a.wsGam[tv * 64 + lane] = s;
@@ -156,7 +157,7 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
                 const int r = 16 * w + 4 * lg + e, i = 16 * nb + ln;
                 float av = 0.f, pv = 0.f;
                 if (nb <= w && i <= r) {
-                    const float dri = expf(gam_s[r] - gam_s[i]);
+                    const float dri = exp2f(gam_s[r] - gam_s[i]);
                     pv = dri * gq[nb][e];
                     if (i < r) av = beta_s[r] * dri * gk[nb][e];
                 }
@@ -232,18 +233,102 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
 // ============================================================================
 // gdn_seq: one workgroup per (stream, v-head, 16 consecutive rows of S).
 // Wave w owns state columns [w D/4, (w+1) D/4) of those 16 rows.
+//
+// Precision: k and q stay bf16 (as given) and meet the state through bf16
+// matrix-core products against a two-term bf16 split of the fp32 state
+// (S ~ S_hi + S_lo, relative error ~2^-17); the writes D_last E enter the
+// state update the same way.  The tile-local operands (R, E, T diag(beta),
+// P) are fp16.  All accumulation is fp32.
+//
+// The next tile's operands are loaded into registers while the current tile
+// computes (two register sets, the loop is unrolled twice); LDS staging
+// buffers alternate between tiles so one tile needs 3 barriers.  K and the
+// state are staged row-major and read as transposed fragments with
+// ds_read_b64_tr_b16.
 // ============================================================================
+template <int D>
+struct SeqTile {
+    uint4 k[D / 32], q[D / 32];  // bf16 rows 16 w + ln of k and q (8 dims per k-step)
+    uint4 t[2], p[2];            // fp16 T diag(beta), P fragments of rows 16 w + ln
+    float4 gam;                  // gamma (base-2 units) of rows 16 w + 4 lg + e
+    float gam_last;
+    uint32_t v[4];               // bf16 v of rows 16 w + 4 lg + e, column v0 + ln
+};
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+// Transposed 16-bit fragment read: within each group of 16 lanes, lane l
+// receives element (l % 4) of the 4 elements addressed by lanes l/4 + 4 e.
+__device__ __forceinline__ v4i16 ds_read_tr16(const void *p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)p);
+}
+__device__ __forceinline__ bf16x8 cat_bf16(v4i16 a, v4i16 b) {
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+// Rows past the end of a ragged tile are clamped to its last row: their
+// products only meet zero entries of T diag(beta) and P (beta = 0 and k = 0
+// there in the prep kernel) and their outputs are never stored.
+template <int D>
+__device__ __forceinline__ void seq_load(const GdnArgs &a, SeqTile<D> &s, int t0, int n, size_t tv, int qh,
+                                         int j, int v0, int w, int ln, int lg) {
+    const uint16_t *kb = a.k + (size_t)t0 * a.H_k * D;
+    const uint16_t *qb = a.q + (size_t)t0 * a.H_k * D;
+    const uint32_t ra = (uint32_t)min(16 * w + ln, n - 1);
+    const uint32_t off = (ra * (uint32_t)a.H_k + (uint32_t)qh) * D + 8 * lg;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+        s.k[ks] = *(const uint4 *)(kb + off + 32 * ks);
+        s.q[ks] = *(const uint4 *)(qb + off + 32 * ks);
+    }
+    const uint16_t *vb = a.v + (size_t)t0 * a.H_v * D + (size_t)j * D + v0 + ln;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const uint32_t r = (uint32_t)min(16 * w + 4 * lg + e, n - 1);
+        s.v[e] = vb[r * (uint32_t)a.H_v * D];
+    }
+    const float *gb = a.wsGam + tv * 64;
+    s.gam = *(const float4 *)(gb + 16 * w + 4 * lg);
+    s.gam_last = gb[63];
+    const _Float16 *tb = a.wsT + tv * 4096, *pb = a.wsP + tv * 4096;
+    const uint32_t toff = (16 * w + ln) * 64 + 8 * lg;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+        s.t[ks] = *(const uint4 *)(tb + toff + 32 * ks);
+        s.p[ks] = *(const uint4 *)(pb + toff + 32 * ks);
+    }
+}
+
+// fp32 pair -> bf16 pair (round to nearest even), packed in one dword
+__device__ __forceinline__ uint32_t bf16_pack(float x, float y) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    bf16x2 r = {(__bf16)x, (__bf16)y};
+    return __builtin_bit_cast(uint32_t, r);
+}
+__device__ __forceinline__ float bf16_lo_f(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi_f(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
 template <int D, bool OUT_BF16, bool DRIFT>
-__global__ __launch_bounds__(256) void gdn_seq_kernel(GdnArgs a) {
-    constexpr int KS = D / 32;
-    constexpr int NB = D / 64;    // 16-column state blocks per wave
-    constexpr int TLD = 72;       // halves per LDS row of K^T, R^T, E^T
-    constexpr int SLD = D + 8;    // halves per LDS row of S0
-    __shared__ __align__(16) _Float16 KT[D * TLD];
-    __shared__ __align__(16) _Float16 S0h[16 * SLD];
-    __shared__ __align__(16) _Float16 RT[16 * TLD];
-    __shared__ __align__(16) _Float16 ET[16 * TLD];
-    __shared__ __align__(16) _Float16 DET[16 * TLD];
+struct SeqCtx {
+    static constexpr int KS = D / 32;
+    static constexpr int NB = D / 64;  // 16-column state blocks per wave
+    static constexpr int KLD = D + 8;  // bf16 per LDS row of the K tile
+    static constexpr int SLD = 20;     // bf16 per LDS row of S^T (16 rows of S + pad)
+    static constexpr int TLD = 72;     // 16-bit elements per LDS row of R^T, E^T, (D E)^T
+};
+
+template <int D, bool OUT_BF16, bool DRIFT>
+__global__ __launch_bounds__(256, 1) void gdn_seq_kernel(GdnArgs a) {
+    using C = SeqCtx<D, OUT_BF16, DRIFT>;
+    constexpr int KS = C::KS, NB = C::NB, KLD = C::KLD, SLD = C::SLD, TLD = C::TLD;
+    __shared__ __align__(16) uint16_t Ks[2][64 * KLD];
+    __shared__ __align__(16) uint16_t SThi[2][D * SLD];
+    __shared__ __align__(16) uint16_t STlo[2][D * SLD];
+    __shared__ __align__(16) _Float16 RT[2][16 * TLD];
+    __shared__ __align__(16) _Float16 ET[2][16 * TLD];
+    __shared__ __align__(16) uint16_t DThi[2][16 * TLD];
+    __shared__ __align__(16) uint16_t DTlo[2][16 * TLD];
     __shared__ float red[8];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, ln = lane & 15, lg = lane >> 4;
@@ -293,79 +378,62 @@ __global__ __launch_bounds__(256) void gdn_seq_kernel(GdnArgs a) {
         S_start[nb] = S[nb];
     }
 
-    const uint4 zero4 = make_uint4(0, 0, 0, 0);
-    const int n_tiles = (len + TILE - 1) / TILE;
+    // per-lane LDS addresses that do not change from tile to tile
+    const int trow = ln >> 2, tcol = 4 * (ln & 3);  // source element of a transposed read
     int frame = frame_base;
-    for (int lt = 0; lt < n_tiles; ++lt) {
+
+    auto step = [&](int lt, SeqTile<D> &cur, SeqTile<D> &nxt, int n_tiles) {
         const int t0 = st + TILE * lt, n = min(TILE, en - t0);
-        const size_t tv = (size_t)(tile_base + lt) * a.H_v + j;
+        const int buf = lt & 1;
+        uint16_t *ks_ = Ks[buf], *sthi = SThi[buf], *stlo = STlo[buf], *dthi = DThi[buf], *dtlo = DTlo[buf];
+        _Float16 *rt = RT[buf], *et = ET[buf];
 
-        // ---- loads: k, q fragments of rows 16 w + ln; per-row v and gamma
-        half8 kh[KS], qf[KS];
+        // ---- prefetch the next tile (the last tile reloads itself)
         {
-            const int r = 16 * w + ln;
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                uint4 kr = zero4, qr = zero4;
-                if (r < n) {
-                    const size_t off = ((size_t)(t0 + r) * a.H_k + qh) * D + 32 * ks + 8 * lg;
-                    kr = *(const uint4 *)(a.k + off);
-                    qr = *(const uint4 *)(a.q + off);
-                }
-                kh[ks] = bf16x8_to_f16(kr);
-                qf[ks] = bf16x8_to_f16(qr);
-            }
-        }
-        float vrow[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int r = 16 * w + 4 * lg + e;
-            vrow[e] = (r < n) ? bf16_to_f32(a.v[((size_t)(t0 + r) * a.H_v + j) * D + v0 + ln]) : 0.f;
-        }
-        const float4 g4 = *(const float4 *)(a.wsGam + tv * 64 + 16 * w + 4 * lg);
-        const float gam[4] = {g4.x, g4.y, g4.z, g4.w};
-        const float gam_last = a.wsGam[tv * 64 + 63];
-        uint4 ta[2], pa[2];
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            ta[ks] = zero4;
-            pa[ks] = zero4;
-            if (ks <= (w >> 1)) {
-                const size_t off = tv * 4096 + (size_t)(16 * w + ln) * 64 + 32 * ks + 8 * lg;
-                ta[ks] = *(const uint4 *)(a.wsT + off);
-                pa[ks] = *(const uint4 *)(a.wsP + off);
-            }
+            const int lnx = min(lt + 1, n_tiles - 1);
+            const int nt0 = st + TILE * lnx;
+            seq_load<D>(a, nxt, nt0, min(TILE, en - nt0), (size_t)(tile_base + lnx) * a.H_v + j, qh, j, v0, w,
+                        ln, lg);
         }
 
-        // ---- K^T and the entry state (fp16) into LDS
+        // ---- K rows (bf16, as loaded) and S^T split in two bf16 terms -> LDS
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
+        for (int ks = 0; ks < KS; ++ks) *(uint4 *)(&ks_[(16 * w + ln) * KLD + 32 * ks + 8 * lg]) = cur.k[ks];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) KT[(32 * ks + 8 * lg + e) * TLD + 16 * w + ln] = kh[ks][e];
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) S0h[(4 * lg + e) * SLD + w * (D / 4) + 16 * nb + ln] = (_Float16)S[nb][e];
+        for (int nb = 0; nb < NB; ++nb) {
+            const uint32_t h01 = bf16_pack(S[nb][0], S[nb][1]), h23 = bf16_pack(S[nb][2], S[nb][3]);
+            const uint32_t l01 = bf16_pack(S[nb][0] - bf16_lo_f(h01), S[nb][1] - bf16_hi_f(h01));
+            const uint32_t l23 = bf16_pack(S[nb][2] - bf16_lo_f(h23), S[nb][3] - bf16_hi_f(h23));
+            const int off = (w * (D / 4) + 16 * nb + ln) * SLD + 4 * lg;
+            *(uint2 *)(&sthi[off]) = make_uint2(h01, h23);
+            *(uint2 *)(&stlo[off]) = make_uint2(l01, l23);
+        }
         __syncthreads();
 
         // ---- K S0^T and Q S0^T for rows 16 w .. 16 w + 15
         f32x4 xk = {0.f, 0.f, 0.f, 0.f}, xq = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-            const half8 bs = *(const half8 *)(&S0h[ln * SLD + 32 * ks + 8 * lg]);
-            xk = mfma_f16(kh[ks], bs, xk);
-            xq = mfma_f16(qf[ks], bs, xq);
+            const int r0 = (32 * ks + 8 * lg + trow) * SLD + tcol;
+            const bf16x8 bh = cat_bf16(ds_read_tr16(&sthi[r0]), ds_read_tr16(&sthi[r0 + 4 * SLD]));
+            const bf16x8 bl = cat_bf16(ds_read_tr16(&stlo[r0]), ds_read_tr16(&stlo[r0 + 4 * SLD]));
+            const bf16x8 ka = as_bf16x8(cur.k[ks]), qa = as_bf16x8(cur.q[ks]);
+            xk = mfma_bf16(ka, bh, xk);
+            xq = mfma_bf16(qa, bh, xq);
+            xk = mfma_bf16(ka, bl, xk);
+            xq = mfma_bf16(qa, bl, xq);
         }
         // ---- residual R = V - diag(Gamma) K S0^T  -> R^T in LDS
+        const float gam[4] = {cur.gam.x, cur.gam.y, cur.gam.z, cur.gam.w};
         float Gam[4];
         {
             _Float16 rr[4] __attribute__((aligned(8)));
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                Gam[e] = expf(gam[e]);
-                rr[e] = (_Float16)(vrow[e] - Gam[e] * xk[e]);
+                Gam[e] = __builtin_amdgcn_exp2f(gam[e]);
+                rr[e] = (_Float16)(__uint_as_float(cur.v[e] << 16) - Gam[e] * xk[e]);
             }
-            *(uint2 *)(&RT[ln * TLD + 16 * w + 4 * lg]) = *(const uint2 *)rr;
+            *(uint2 *)(&rt[ln * TLD + 16 * w + 4 * lg]) = *(const uint2 *)rr;
         }
         __syncthreads();
 
@@ -374,19 +442,25 @@ __global__ __launch_bounds__(256) void gdn_seq_kernel(GdnArgs a) {
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
             if (ks <= (w >> 1)) {
-                const half8 br = *(const half8 *)(&RT[ln * TLD + 32 * ks + 8 * lg]);
-                E = mfma_f16(as_half8(ta[ks]), br, E);
+                const half8 br = *(const half8 *)(&rt[ln * TLD + 32 * ks + 8 * lg]);
+                E = mfma_f16(as_half8(cur.t[ks]), br, E);
             }
         }
         {
-            _Float16 ee[4] __attribute__((aligned(8))), de[4] __attribute__((aligned(8)));
+            _Float16 ee[4] __attribute__((aligned(8)));
+            float de[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 ee[e] = (_Float16)E[e];
-                de[e] = (_Float16)(E[e] * expf(gam_last - gam[e]));
+                de[e] = E[e] * __builtin_amdgcn_exp2f(cur.gam_last - gam[e]);
             }
-            *(uint2 *)(&ET[ln * TLD + 16 * w + 4 * lg]) = *(const uint2 *)ee;
-            *(uint2 *)(&DET[ln * TLD + 16 * w + 4 * lg]) = *(const uint2 *)de;
+            const uint32_t h01 = bf16_pack(de[0], de[1]), h23 = bf16_pack(de[2], de[3]);
+            const uint32_t l01 = bf16_pack(de[0] - bf16_lo_f(h01), de[1] - bf16_hi_f(h01));
+            const uint32_t l23 = bf16_pack(de[2] - bf16_lo_f(h23), de[3] - bf16_hi_f(h23));
+            const int off = ln * TLD + 16 * w + 4 * lg;
+            *(uint2 *)(&et[off]) = *(const uint2 *)ee;
+            *(uint2 *)(&dthi[off]) = make_uint2(h01, h23);
+            *(uint2 *)(&dtlo[off]) = make_uint2(l01, l23);
         }
         __syncthreads();
 
@@ -398,38 +472,44 @@ __global__ __launch_bounds__(256) void gdn_seq_kernel(GdnArgs a) {
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 if (ks <= (w >> 1)) {
-                    const half8 be = *(const half8 *)(&ET[ln * TLD + 32 * ks + 8 * lg]);
-                    oacc = mfma_f16(as_half8(pa[ks]), be, oacc);
+                    const half8 be = *(const half8 *)(&et[ln * TLD + 32 * ks + 8 * lg]);
+                    oacc = mfma_f16(as_half8(cur.p[ks]), be, oacc);
                 }
             }
+            if (OUT_BF16) {
+                uint16_t *ob = (uint16_t *)a.o + (size_t)t0 * a.H_v * D + (size_t)j * D + v0 + ln;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int r = 16 * w + 4 * lg + e;
-                if (r < n) {
-                    const size_t off = ((size_t)(t0 + r) * a.H_v + j) * D + v0 + ln;
-                    const float val = a.scale * oacc[e];
-                    if (OUT_BF16)
-                        ((uint16_t *)a.o)[off] = f32_to_bf16(val);
-                    else
-                        ((float *)a.o)[off] = val;
+                for (int e = 0; e < 4; ++e) {
+                    const int r = 16 * w + 4 * lg + e;
+                    if (r < n) ob[(uint32_t)r * a.H_v * D] = __builtin_bit_cast(uint16_t, (__bf16)(a.scale * oacc[e]));
+                }
+            } else {
+                float *ob = (float *)a.o + (size_t)t0 * a.H_v * D + (size_t)j * D + v0 + ln;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int r = 16 * w + 4 * lg + e;
+                    if (r < n) ob[(uint32_t)r * a.H_v * D] = a.scale * oacc[e];
                 }
             }
         }
 
         // ---- state update S = Gamma_last S0 + (D_last E)^T K
         {
-            const float gl = expf(gam_last);
+            const float gl = __builtin_amdgcn_exp2f(cur.gam_last);
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) S[nb][e] *= gl;
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
-                const half8 ad = *(const half8 *)(&DET[ln * TLD + 32 * ks + 8 * lg]);
+                const bf16x8 ah = as_bf16x8(*(const uint4 *)(&dthi[ln * TLD + 32 * ks + 8 * lg]));
+                const bf16x8 al = as_bf16x8(*(const uint4 *)(&dtlo[ln * TLD + 32 * ks + 8 * lg]));
 #pragma unroll
                 for (int nb = 0; nb < NB; ++nb) {
-                    const half8 bk = *(const half8 *)(&KT[(w * (D / 4) + 16 * nb + ln) * TLD + 32 * ks + 8 * lg]);
-                    S[nb] = mfma_f16(ad, bk, S[nb]);
+                    const int r0 = (32 * ks + 8 * lg + trow) * KLD + w * (D / 4) + 16 * nb + tcol;
+                    const bf16x8 bk = cat_bf16(ds_read_tr16(&ks_[r0]), ds_read_tr16(&ks_[r0 + 4 * KLD]));
+                    S[nb] = mfma_bf16(ah, bk, S[nb]);
+                    S[nb] = mfma_bf16(al, bk, S[nb]);
                 }
             }
         }
@@ -470,7 +550,16 @@ __global__ __launch_bounds__(256) void gdn_seq_kernel(GdnArgs a) {
             }
             ++frame;
         }
-        __syncthreads();
+    };
+
+    const int n_tiles = (len + TILE - 1) / TILE;
+    if (n_tiles > 0) {
+        SeqTile<D> ta, tb;
+        seq_load<D>(a, ta, st, min(TILE, len), (size_t)tile_base * a.H_v + j, qh, j, v0, w, ln, lg);
+        for (int lt = 0; lt < n_tiles; lt += 2) {
+            step(lt, ta, tb, n_tiles);
+            if (lt + 1 < n_tiles) step(lt + 1, tb, ta, n_tiles);
+        }
     }
 
 #pragma unroll

@@ -23,7 +23,7 @@ struct GdnLaunch {
     // workspace pieces
     _Float16 *wsT;      // [tiles_max][H_v][64][64]  T diag(beta), fp16
     _Float16 *wsP;      // [tiles_max][H_v][64][64]  D (.) tril(Q K^T), fp16
-    float *wsGam;       // [tiles_max][H_v][64]      in-tile cumulative log decay
+    float *wsGam;       // [tiles_max][H_v][64]      in-tile cumulative log decay times log2(e)
     float *wsDrift;     // [n_frames][H_v][n_split][2]
     int tiles_max;
     int n_split;        // d_v slices of 16 per (stream, v-head)
