@@ -156,7 +156,9 @@ def main():
     append_pos = torch.arange(1024, dtype=torch.int32, device=dev)
     state_ref = {"len": BUDGET, "next_pos": BUDGET, "step": 0}
 
-    def step(evs=None):
+    keep_hist = torch.empty((args.steps, BUDGET), dtype=torch.int32, device=dev)
+
+    def step(evs=None, keep_out=None):
         s = state_ref["step"]
         base = n_init_chunks + n_frames * s
         if evs is not None:
@@ -177,7 +179,7 @@ def main():
         if evs is not None:
             evs[3].record(stream)
         new_len, _ = ds.kv_evict_topk(k_layers, v_layers, kv_pos, kv_chunk, table, n + 1024, BUDGET, 0, 0, 1,
-                                      workspace=kv_ws)
+                                      keep_out=keep_out, workspace=kv_ws)
         if evs is not None:
             evs[4].record(stream)
         state_ref["len"] = new_len
@@ -191,28 +193,50 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(evs[i])
+        step(evs[i], keep_hist[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = 1e3 * wall / args.steps
     seg = np.array([[evs[i][j].elapsed_time(evs[i][j + 1]) for j in range(4)] for i in range(args.steps)])
     gdn_ms, drift_ms, append_ms, evict_ms = seg.mean(axis=0)
+    # rows each eviction moved (the kept slots form a suffix of moves)
+    kh = keep_hist.cpu().numpy()
+    ar = np.arange(BUDGET)
+    moved_rows = np.array([BUDGET - (np.argmax(r != ar) if np.any(r != ar) else BUDGET) for r in kh])
+    moved_bytes = moved_rows * 2 * KV_LAYERS * KV_HEADS * KV_DIM * 2
     status = ds.kv_device_status(kv_ws)
     if status[0] != 0 or status[2] != 0:
         raise RuntimeError(f"eviction reported device status {status}")
 
-    # ---------------- forward without drift (for the drift overhead), same stream
+    # ---------------- drift overhead: the forward with the fused drift sums
+    # plus deltas_drift, against the same forward compiled without the
+    # frame-end epilogue; both as back-to-back loops on the same stream,
+    # interleaved so cache state is the same for both
     reps = max(5, args.steps)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    for _ in range(2):
+    scores_tmp = torch.empty(n_frames, dtype=torch.float32, device=dev)
+
+    def fwd_drift():
+        ds.gdn_chunk_fwd(q, k, v, g, beta, [T], FRAME, state_out=state, o=o, drift_partials=partials, workspace=ws)
+        ds.deltas_drift(partials.view(1, n_frames, H_V, 2), ds.LAYER_FROB, scores=scores_tmp)
+
+    def fwd_plain():
         ds.gdn_chunk_fwd(q, k, v, g, beta, [T], FRAME, state_out=state, o=o, drift_partials=False, workspace=ws)
-    e0.record(stream)
-    for _ in range(reps):
-        ds.gdn_chunk_fwd(q, k, v, g, beta, [T], FRAME, state_out=state, o=o, drift_partials=False, workspace=ws)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    nodrift_ms = e0.elapsed_time(e1) / reps
-    drift_overhead = 100.0 * ((gdn_ms + drift_ms) / nodrift_ms - 1.0)
+
+    t_with, t_without = [], []
+    for rnd in range(4):
+        for fn, acc in ((fwd_drift, t_with), (fwd_plain, t_without)) if rnd % 2 == 0 else \
+                ((fwd_plain, t_without), (fwd_drift, t_with)):
+            fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            acc.append(e0.elapsed_time(e1) / reps)
+    withdrift_ms = float(np.median(t_with))
+    nodrift_ms = float(np.median(t_without))
+    drift_overhead = 100.0 * (withdrift_ms / nodrift_ms - 1.0)
 
     flops, bytes_ = algorithmic_work(T, H_K, H_V, D)
     achieved_gbs = bytes_ / (gdn_ms * 1e-3) / 1e9
@@ -255,9 +279,12 @@ def main():
         "mfma_util_pct": 100.0 * achieved_tflops / MFMA_PEAK_TFLOPS,
         "algorithmic_tflops": achieved_tflops,
         "drift_overhead_pct": drift_overhead,
+        "evict_moved_rows_mean": float(moved_rows.mean()),
+        "evict_gather_gbs": float((2 * moved_bytes).mean() / (evict_ms * 1e-3) / 1e9),
         "drift_overhead_paper_pct": 1.9,
         "breakdown_ms": {"gdn_chunk_fwd": gdn_ms, "deltas_drift": drift_ms, "kv_append": append_ms,
-                         "kv_evict_topk": evict_ms, "gdn_chunk_fwd_without_drift": nodrift_ms},
+                         "kv_evict_topk": evict_ms, "isolated_fwd_with_drift": withdrift_ms,
+                         "isolated_fwd_without_drift": nodrift_ms},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(x)

@@ -166,7 +166,7 @@ ds_status deltas_drift(const float *partials, int32_t L, int32_t F, int32_t H_v,
  * over [0, len), 0 <= chunk_id < num_chunks.  If the device finds them
  * broken it leaves the cache untouched and records the failure in the
  * workspace (see ds_kv_device_status).
- * Requires 0 <= n_sink, 0 <= n_window, n_sink + n_window <= M,
+ * Requires 0 <= n_sink, 0 <= n_window, n_sink + n_window <= M, row_bytes <= 65536,
  * len <= capacity, n_buckets <= 64.
  */
 typedef struct {

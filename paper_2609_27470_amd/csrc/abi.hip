@@ -140,8 +140,8 @@ ds_status deltas_drift(const float *partials, int32_t L, int32_t F, int32_t H_v,
 }
 
 size_t ds_kv_workspace_bytes(const ds_kv_shape *shape) {
-    if (!shape || shape->n_layers < 1 || shape->row_bytes < 16 || shape->row_bytes % 16 || shape->capacity < 1 ||
-        2 * shape->n_layers > ds::KV_MAX_PLANES)
+    if (!shape || shape->n_layers < 1 || shape->row_bytes < 16 || shape->row_bytes % 16 || shape->row_bytes > 65536 ||
+        shape->capacity < 1 || 2 * shape->n_layers > ds::KV_MAX_PLANES)
         return 0;
     return ds::kv_workspace_layout(shape->n_layers, shape->row_bytes, shape->capacity).total;
 }
@@ -158,6 +158,7 @@ ds_status kv_evict_topk(const ds_kv_shape *shape, void *const *k_layers, void *c
     if (s.n_layers < 1 || 2 * s.n_layers > ds::KV_MAX_PLANES)
         return fail(DS_E_UNSUPPORTED, "n_layers=%d (1..%d)", s.n_layers, ds::KV_MAX_PLANES / 2);
     if (s.row_bytes < 16 || s.row_bytes % 16) return fail(DS_E_SHAPE, "row_bytes=%d must be a positive multiple of 16", s.row_bytes);
+    if (s.row_bytes > 65536) return fail(DS_E_UNSUPPORTED, "row_bytes=%d (at most 65536)", s.row_bytes);
     if (s.capacity < 1) return fail(DS_E_SHAPE, "capacity=%d", s.capacity);
     if (len < 0 || len > s.capacity) return fail(DS_E_SHAPE, "len=%d outside [0, capacity=%d]", len, s.capacity);
     if (M < 0 || n_sink < 0 || n_window < 0 || (long long)n_sink + n_window > M)
@@ -165,7 +166,8 @@ ds_status kv_evict_topk(const ds_kv_shape *shape, void *const *k_layers, void *c
                     n_window, M);
     if (n_buckets < 0 || n_buckets > 64) return fail(DS_E_ARG, "n_buckets=%d (0..64)", n_buckets);
     if (num_chunks < 1) return fail(DS_E_ARG, "num_chunks=%d", num_chunks);
-    if ((long long)s.capacity * s.row_bytes > (1LL << 40)) return fail(DS_E_UNSUPPORTED, "cache too large");
+    if ((long long)s.capacity * s.row_bytes > (1LL << 40) || 2LL * s.n_layers * s.row_bytes >= (1LL << 31))
+        return fail(DS_E_UNSUPPORTED, "cache too large");
     if (len <= M) {
         *new_len = len;
         return DS_OK;

@@ -8,6 +8,7 @@ namespace ds {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // Matrix-core fragment layouts of v_mfma_f32_16x16x32_{f16,bf16} on a wave of
 // 64 lanes, with ln = lane % 16 and lg = lane / 16:
@@ -45,6 +46,8 @@ __device__ __forceinline__ half8 bf16x8_to_f16(uint4 r) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 r) { return __builtin_bit_cast(bf16x8, r); }
 __device__ __forceinline__ half8 as_half8(uint4 r) { return __builtin_bit_cast(half8, r); }
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 r) { return __builtin_bit_cast(bf16x8, r); }
+__device__ __forceinline__ half8 as_half8(u32x4 r) { return __builtin_bit_cast(half8, r); }
 __device__ __forceinline__ uint4 as_uint4(half8 h) { return __builtin_bit_cast(uint4, h); }
 
 __device__ __forceinline__ float wave_sum(float x) {

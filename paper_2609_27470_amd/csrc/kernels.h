@@ -21,10 +21,10 @@ struct GdnLaunch {
     float *drift_partials;  // [n_frames][H_v][2] or null
     float *snapshots;       // [n_frames][H_v][d][d] or null
     // workspace pieces
-    _Float16 *wsT;      // [tiles_max][H_v][64][64]  T diag(beta), fp16
-    _Float16 *wsP;      // [tiles_max][H_v][64][64]  D (.) tril(Q K^T), fp16
+    _Float16 *wsT;      // [tiles_max][H_v][6][64][8]  T diag(beta), fp16 A-fragments
+    _Float16 *wsP;      // [tiles_max][H_v][6][64][8]  D (.) tril(Q K^T), fp16 A-fragments
     float *wsGam;       // [tiles_max][H_v][64]      in-tile cumulative log decay times log2(e)
-    float *wsDrift;     // [n_frames][H_v][n_split][2]
+    float *wsDrift;     // [n_frames][H_v][n_split][16][2] (one pair per row of 16 lanes)
     int tiles_max;
     int n_split;        // d_v slices of 16 per (stream, v-head)
 };
@@ -45,8 +45,8 @@ hipError_t launch_drift(const float *partials, int L, int F, int H_v, int mode, 
 constexpr int KV_MAX_PLANES = 64;  // 2 * n_layers
 
 struct KvWorkspace {
-    size_t offStatus, offKeep, offInv, offMask, offRunStart, offRunKey, offRunBkt, offRunTake,
-        offFlags, total;
+    size_t offStatus, offPlanes, offKeep, offInv, offThRun, offRunStart, offRunKey, offRunBkt, offRunTake,
+        offRunFrom, offFlags, total;
     int n_chunks;  // 64 KiB pieces of one token's rows over all layers
 };
 KvWorkspace kv_workspace_layout(int n_layers, int row_bytes, int capacity);

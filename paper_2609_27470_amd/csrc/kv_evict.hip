@@ -12,8 +12,10 @@
 //     newest tokens first (ties within a chunk go to the newer position);
 //   * the leftover budget is filled the same way over all spans from the
 //     tokens not yet kept;
-//   * kept slots -> ascending keep list, its inverse on [0, M), and a
-//     per-destination flag array for the gather.
+//   * kept slots -> ascending keep list and its inverse on [0, M).
+// Slot data is read in blocks of 32 consecutive slots per thread with
+// 16-byte loads, so each pass over the cache costs one memory round trip per
+// 32 Ki slots.
 // kv_gather moves the kept rows down in place.  Slot d receives row keep[d]
 // (keep[d] >= d).  Writing slot d is safe once the reader of row d -- the
 // destination inv[d] < d, if row d is kept -- has its data in registers.
@@ -26,22 +28,30 @@
 namespace ds {
 
 constexpr int SEL_THREADS = 1024;
+constexpr int SEL_PER = 32;                         // consecutive slots per thread per pass block
+constexpr int SEL_BLOCK = SEL_THREADS * SEL_PER;
 constexpr int GATHER_U = 16;                        // uint4 per thread per group
-constexpr int GATHER_BYTES = 256 * 16 * GATHER_U;   // 64 KiB per group
 constexpr int SPIN_LIMIT = 1 << 22;
+
+// pointer into global memory (lets the compiler emit global rather than flat accesses)
+#define GPTR(T) __attribute__((address_space(1))) T *
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 struct KvArgs {
     const int32_t *pos_in;
     const int32_t *chunk;
     const float *scores;
     int num_chunks, len, M, n_s, n_w, N;
-    int n_flags;
-    int32_t *status;   // [0] invariants broken, [1] skip gather, [2] wait timed out
+    int n_flags, n_chunks;
+    int32_t *status;   // [0] invariants broken, [1] skip gather, [2] wait timed out, [3] first moved slot
     uint32_t *ticket;
-    int32_t *keep, *inv, *mask, *run_start, *run_bkt, *run_take;
+    int32_t *keep, *inv, *run_start, *run_bkt, *run_take, *run_from, *th_run;
     unsigned long long *run_key;
     int32_t *flags;
     int32_t *keep_out;
+    char **plane_tab;  // device copy of the plane pointers, read by the gather
+    char *planes[KV_MAX_PLANES];
+    int n_planes;
 };
 
 __device__ __forceinline__ uint32_t orderable(float f) {
@@ -93,6 +103,23 @@ __device__ long long block_sum_ll(long long x, long long *s_tmp) {
     return r;
 }
 
+// SEL_PER consecutive int32 from [lo, lo + SEL_PER); entries at or past len read as 0.
+__device__ __forceinline__ void load_block(const int32_t *p, int lo, int len, int (&out)[SEL_PER]) {
+    if (lo + SEL_PER <= len) {
+#pragma unroll
+        for (int q = 0; q < SEL_PER / 4; ++q) {
+            const int4 v = *(const int4 *)(p + lo + 4 * q);
+            out[4 * q] = v.x;
+            out[4 * q + 1] = v.y;
+            out[4 * q + 2] = v.z;
+            out[4 * q + 3] = v.w;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < SEL_PER; ++k) out[k] = (lo + k < len) ? p[lo + k] : 0;
+    }
+}
+
 __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     __shared__ int s_scan[SEL_THREADS / 64 + 1];
     __shared__ long long s_ll[SEL_THREADS / 64 + 1];
@@ -106,18 +133,52 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
         *a.ticket = 0u;
         s_bad = 0;
     }
-    for (int i = tid; i < a.n_flags; i += SEL_THREADS) a.flags[i] = 0;
-    __syncthreads();
+    // copy of the plane table with constant indices (no dynamic indexing of
+    // the kernel-argument array)
+#pragma unroll
+    for (int p = 0; p < KV_MAX_PLANES; ++p)
+        if (p == tid && p < a.n_planes) a.plane_tab[p] = a.planes[p];
 
-    // ---- cache invariants: chunk ids in range and nondecreasing, positions increasing
-    {
-        int bad = 0;
-        for (int i = tid; i < a.len; i += SEL_THREADS) {
-            const int c = a.chunk[i];
-            if (c < 0 || c >= a.num_chunks) bad = 1;
-            if (i > 0 && (c < a.chunk[i - 1] || a.pos_in[i] <= a.pos_in[i - 1])) bad = 1;
+    const int c0 = a.n_s, c1 = a.len - a.n_w;
+
+    // ---- pass 1: cache invariants and runs of equal chunk id among the
+    // candidates [c0, c1); th_run[block][thread] = runs starting before the
+    // thread's slots
+    int R = 0;
+    for (int base = 0; base < a.len; base += SEL_BLOCK) {
+        const int lo = base + tid * SEL_PER;
+        int ch[SEL_PER], ps[SEL_PER];
+        load_block(a.chunk, lo, a.len, ch);
+        load_block(a.pos_in, lo, a.len, ps);
+        const bool has_prev = lo > 0 && lo <= a.len;
+        const int pc0 = has_prev ? a.chunk[lo - 1] : -1;
+        int pc = pc0, pp = has_prev ? a.pos_in[lo - 1] : 0;
+        int bad = 0, cnt = 0;
+#pragma unroll
+        for (int k = 0; k < SEL_PER; ++k) {
+            const int i = lo + k;
+            if (i < a.len) {
+                if (ch[k] < 0 || ch[k] >= a.num_chunks) bad = 1;
+                if (i > 0 && (ch[k] < pc || ps[k] <= pp)) bad = 1;
+                if (i >= c0 && i < c1 && (i == c0 || ch[k] != pc)) ++cnt;
+                pc = ch[k];
+                pp = ps[k];
+            }
         }
         if (bad) atomicOr(&s_bad, 1);
+        int tot = 0;
+        int off = R + block_excl_scan(cnt, s_scan, tot);
+        a.th_run[base / SEL_PER + tid] = off;
+        pc = pc0;
+#pragma unroll
+        for (int k = 0; k < SEL_PER; ++k) {
+            const int i = lo + k;
+            if (i < a.len) {
+                if (i >= c0 && i < c1 && (i == c0 || ch[k] != pc)) a.run_start[off++] = i;
+                pc = ch[k];
+            }
+        }
+        R += tot;
     }
     __syncthreads();
     if (s_bad) {
@@ -127,30 +188,19 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
         }
         return;
     }
-
-    // ---- runs of equal chunk id among the candidates [c0, c1)
-    const int c0 = a.n_s, c1 = a.len - a.n_w, ncand = c1 - c0;
-    int R = 0;
-    {
-        const int per = (ncand + SEL_THREADS - 1) / SEL_THREADS;
-        const int lo = c0 + tid * per, hi = min(lo + per, c1);
-        int cnt = 0;
-        for (int i = lo; i < hi; ++i) cnt += (i == c0 || a.chunk[i] != a.chunk[i - 1]);
-        int off = block_excl_scan(cnt, s_scan, R);
-        for (int i = lo; i < hi; ++i)
-            if (i == c0 || a.chunk[i] != a.chunk[i - 1]) a.run_start[off++] = i;
-        if (tid == 0) a.run_start[R] = c1;
-    }
+    if (tid == 0) a.run_start[R] = c1;
     __syncthreads();
 
+    // ---- run keys and spans
+    const int ncand = c1 - c0;
     const int a_min = (ncand > 0) ? a.chunk[c0] : 0;
     const int a_max = (ncand > 0) ? a.chunk[c1 - 1] : 0;
     const long long span = (long long)a_max - a_min + 1;
     const int N = max(1, a.N);
     for (int r = tid; r < R; r += SEL_THREADS) {
-        const int ch = a.chunk[a.run_start[r]];
-        a.run_key[r] = ((unsigned long long)orderable(a.scores[ch]) << 32) | (unsigned)ch;
-        a.run_bkt[r] = (int)(((long long)N * (ch - a_min)) / span);
+        const int chn = a.chunk[a.run_start[r]];
+        a.run_key[r] = ((unsigned long long)orderable(a.scores[chn]) << 32) | (unsigned)chn;
+        a.run_bkt[r] = (int)(((long long)N * (chn - a_min)) / span);
     }
     __syncthreads();
 
@@ -171,145 +221,210 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     taken = block_sum_ll(taken, s_ll);
     const long long fill = (long long)(a.M - a.n_s - a.n_w) - taken;
 
-    // ---- fill: best remaining tokens over all spans
+    // ---- fill with the best remaining tokens over all spans; a run keeps
+    // its newest tokens, slots [run_from, run end)
     for (int r = tid; r < R; r += SEL_THREADS) {
         const unsigned long long key = a.run_key[r];
-        const long long left = (a.run_start[r + 1] - a.run_start[r]) - a.run_take[r];
+        const long long ln = a.run_start[r + 1] - a.run_start[r];
+        const long long left = ln - a.run_take[r];
         long long above = 0;
         for (int r2 = 0; r2 < R; ++r2)
             if (a.run_key[r2] > key) above += (a.run_start[r2 + 1] - a.run_start[r2]) - a.run_take[r2];
         const long long f = min(left, max(0LL, fill - above));
-        a.mask[a.len + r] = (int)(a.run_take[r] + f);  // staged per-run keep count
+        a.run_from[r] = a.run_start[r + 1] - (int)(a.run_take[r] + f);
     }
     __syncthreads();
 
-    // ---- keep mask over slots: sinks, window, newest kept tokens of each run
-    for (int i = tid; i < a.len; i += SEL_THREADS) a.mask[i] = (i < a.n_s || i >= c1) ? 1 : 0;
-    __syncthreads();
-    for (int r = tid; r < R; r += SEL_THREADS) {
-        const int e = a.run_start[r + 1], kcount = a.mask[a.len + r];
-        for (int i = e - kcount; i < e; ++i) a.mask[i] = 1;
-    }
-    __syncthreads();
-
-    // ---- keep list (ascending) and its inverse on destinations [0, M)
-    {
-        const int per = (a.len + SEL_THREADS - 1) / SEL_THREADS;
-        const int lo = tid * per, hi = min(lo + per, a.len);
-        int cnt = 0;
-        for (int i = lo; i < hi; ++i) cnt += a.mask[i];
-        int tot = 0;
-        int off = block_excl_scan(cnt, s_scan, tot);
-        for (int i = lo; i < hi; ++i) {
-            if (a.mask[i]) {
-                if (off < a.M) {
-                    a.keep[off] = i;
-                    if (a.keep_out) a.keep_out[off] = i;
+    // ---- pass 2: keep list (ascending) and its inverse on destinations [0, M)
+    int total_kept = 0;
+    int first_move = a.M;  // smallest destination d with keep[d] != d
+    for (int base = 0; base < a.len; base += SEL_BLOCK) {
+        const int lo = base + tid * SEL_PER;
+        int ch[SEL_PER];
+        load_block(a.chunk, lo, a.len, ch);
+        int pc = (lo > 0 && lo <= a.len) ? a.chunk[lo - 1] : -1;
+        int r = (lo < a.len) ? a.th_run[base / SEL_PER + tid] - 1 : -1;  // run holding the slot before lo
+        int from = (r >= 0 && r < R) ? a.run_from[r] : 0;
+        unsigned mask = 0;
+#pragma unroll
+        for (int k = 0; k < SEL_PER; ++k) {
+            const int i = lo + k;
+            if (i < a.len) {
+                bool kept = true;
+                if (i >= c0 && i < c1) {
+                    if (i == c0 || ch[k] != pc) {
+                        ++r;
+                        from = a.run_from[r];
+                    }
+                    kept = i >= from;
                 }
-                if (i < a.M) a.inv[i] = off;
-                ++off;
-            } else if (i < a.M) {
-                a.inv[i] = -1;
+                if (kept) mask |= 1u << k;
+                pc = ch[k];
             }
         }
-        if (tid == 0 && tot != a.M) {  // cannot happen for valid arguments; never move data then
+        int tot = 0;
+        int off = total_kept + block_excl_scan(__popc(mask), s_scan, tot);
+#pragma unroll
+        for (int k = 0; k < SEL_PER; ++k) {
+            const int i = lo + k;
+            if (i < a.len) {
+                if (mask & (1u << k)) {
+                    if (off < a.M) {
+                        a.keep[off] = i;
+                        if (a.keep_out) a.keep_out[off] = i;
+                        if (off != i) first_move = min(first_move, off);
+                    }
+                    if (i < a.M) a.inv[i] = off;
+                    ++off;
+                } else if (i < a.M) {
+                    a.inv[i] = -1;
+                }
+            }
+        }
+        total_kept += tot;
+    }
+    // ---- moving destinations form the suffix [first_move, M) (keep[d] - d is
+    // nondecreasing); clear their flags for the gather
+    {
+        __shared__ int s_first;
+        if (tid == 0) s_first = a.M;
+        __syncthreads();
+        if (first_move < a.M) atomicMin(&s_first, first_move);
+        __syncthreads();
+        first_move = s_first;
+    }
+    if (tid == 0) {
+        a.status[3] = first_move;
+        if (total_kept != a.M) {  // cannot happen for valid arguments; never move data then
             a.status[0] = 2;
             a.status[1] = 1;
         }
     }
+    for (int i = first_move * a.n_chunks + tid; i < a.n_flags; i += SEL_THREADS) a.flags[i] = 0;
 }
 
 struct GatherArgs {
-    char *planes[KV_MAX_PLANES];
-    int n_planes, row_bytes, M, n_chunks;
-    long long total_bytes;  // n_planes * row_bytes
+    char *const *plane_tab;
+    uint32_t row_bytes, row_units;  // bytes and 16-byte units of one plane row
+    int n_planes, planes_per_group;
+    int M, n_chunks;
     int32_t *pos, *chunk;
     const int32_t *keep, *inv;
     int32_t *flags, *status;
     uint32_t *ticket;
 };
 
+// Moving destinations [first, M) are handed out in ticket order, ROWS
+// consecutive slots per ticket; for each slot and each group of planes the
+// workgroup reads the source rows, signals, waits for the reader of the slot
+// and writes.  KPR = 16-byte units per thread per plane row
+// (row_bytes <= 4096 KPR); a plane group holds 16 / KPR plane rows.
+constexpr int GATHER_ROWS = 8;
+
+template <int KPR>
 __global__ __launch_bounds__(256) void kv_gather_kernel(GatherArgs a) {
+    constexpr int PPG = GATHER_U / KPR;
     __shared__ int s_t;
     if (a.status[1]) return;
+    const int first = a.status[3];
+    const int n_work = (a.M - first + GATHER_ROWS - 1) / GATHER_ROWS;
+    if ((int)blockIdx.x >= n_work) return;  // more workgroups than moving rows: take no ticket
     const int tid = threadIdx.x;
     if (tid == 0) s_t = (int)atomicAdd(a.ticket, 1u);
     __syncthreads();
-    const int t = s_t;
-    const int d = t / a.n_chunks, c = t % a.n_chunks;
-    if (d >= a.M) return;
-    const int src = a.keep[d];
-    if (src == d) return;  // row already in place; nobody else reads it
+    const int d_lo = first + s_t * GATHER_ROWS;
+    const int d_hi = min(d_lo + GATHER_ROWS, a.M);
 
-    // ---- read the source row (this group's 64 KiB piece of it)
-    uint4 buf[GATHER_U];
-    const long long base = (long long)c * GATHER_BYTES;
-#pragma unroll
-    for (int u = 0; u < GATHER_U; ++u) {
-        const long long o = base + 16LL * (tid + 256 * u);
-        if (o < a.total_bytes) {
-            const int p = (int)(o / a.row_bytes), wi = (int)(o % a.row_bytes);
-            buf[u] = *(const uint4 *)(a.planes[p] + (size_t)src * a.row_bytes + wi);
-        }
-    }
-    int pv = 0, cv = 0;
-    if (c == 0 && tid == 0) {
-        pv = a.pos[src];
-        cv = a.chunk[src];
-    }
-    __builtin_amdgcn_s_waitcnt(0);  // every load of this thread has returned
-    __syncthreads();
-    if (tid == 0) __hip_atomic_store(&a.flags[t], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-
-    // ---- wait until the reader of row d (a lower ticket) holds its data
-    if (tid == 0) {
-        const int dep = a.inv[d];
-        if (dep >= 0 && dep != d) {
-            int it = 0;
-            const int ft = dep * a.n_chunks + c;
-            while (__hip_atomic_load(&a.flags[ft], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
-                if (++it >= SPIN_LIMIT) {
-                    __hip_atomic_store(&a.status[2], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    break;
+    for (int d = d_lo; d < d_hi; ++d) {
+        const int src = a.keep[d];
+        const int dep = a.inv[d];  // destination whose source is row d (-1 if row d is evicted)
+        for (int c = 0; c < a.n_chunks; ++c) {
+            // ---- read the source rows of this plane group.  Every load is
+            // issued (units past the row or planes past the group re-read a
+            // valid address and are never stored) so the buffer stays in registers.
+            u32x4 buf[GATHER_U];
+            const int p0 = c * a.planes_per_group;
+#pragma clang loop unroll(full)
+            for (int pi = 0; pi < PPG; ++pi) {
+                const int p = min(p0 + pi, a.n_planes - 1);
+                GPTR(const char) row = (GPTR(const char))a.plane_tab[p] + (size_t)src * a.row_bytes;
+#pragma clang loop unroll(full)
+                for (int k = 0; k < KPR; ++k) {
+                    const uint32_t unit = min((uint32_t)(tid + 256 * k), a.row_units - 1);
+                    buf[pi * KPR + k] = *(GPTR(const u32x4))(row + 16u * unit);
                 }
-                __builtin_amdgcn_s_sleep(2);
+            }
+            int pv = 0, cv = 0;
+            if (c == 0 && tid == 0) {
+                pv = a.pos[src];
+                cv = a.chunk[src];
+            }
+            __builtin_amdgcn_s_waitcnt(0);  // every load of this thread has returned
+            __syncthreads();
+            if (tid == 0) {
+                __hip_atomic_store(&a.flags[d * a.n_chunks + c], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                // ---- wait until the reader of row d (a lower slot, hence an
+                // earlier ticket or an earlier iteration here) holds its data
+                if (dep >= 0 && dep != d) {
+                    int it = 0;
+                    const int ft = dep * a.n_chunks + c;
+                    while (__hip_atomic_load(&a.flags[ft], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
+                        if (++it >= SPIN_LIMIT) {
+                            __hip_atomic_store(&a.status[2], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            break;
+                        }
+                        __builtin_amdgcn_s_sleep(2);
+                    }
+                }
+            }
+            __syncthreads();
+            // ---- write slot d
+#pragma clang loop unroll(full)
+            for (int pi = 0; pi < PPG; ++pi) {
+                const int p = p0 + pi;
+                const bool plane_ok = pi < a.planes_per_group && p < a.n_planes;
+                GPTR(char) row = (GPTR(char))a.plane_tab[min(p, a.n_planes - 1)] + (size_t)d * a.row_bytes;
+#pragma clang loop unroll(full)
+                for (int k = 0; k < KPR; ++k) {
+                    const uint32_t unit = (uint32_t)(tid + 256 * k);
+                    if (plane_ok && unit < a.row_units) *(GPTR(u32x4))(row + 16u * unit) = buf[pi * KPR + k];
+                }
+            }
+            if (c == 0 && tid == 0) {
+                a.pos[d] = pv;
+                a.chunk[d] = cv;
             }
         }
     }
-    __syncthreads();
+}
 
-    // ---- write slot d
-#pragma unroll
-    for (int u = 0; u < GATHER_U; ++u) {
-        const long long o = base + 16LL * (tid + 256 * u);
-        if (o < a.total_bytes) {
-            const int p = (int)(o / a.row_bytes), wi = (int)(o % a.row_bytes);
-            *(uint4 *)(a.planes[p] + (size_t)d * a.row_bytes + wi) = buf[u];
-        }
-    }
-    if (c == 0 && tid == 0) {
-        a.pos[d] = pv;
-        a.chunk[d] = cv;
-    }
+// 16-byte units per thread per plane row, rounded up to a power of two.
+static int gather_kpr(int row_bytes) {
+    const int need = (row_bytes + 4095) / 4096;
+    int k = 1;
+    while (k < need) k *= 2;
+    return k;
 }
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 KvWorkspace kv_workspace_layout(int n_layers, int row_bytes, int capacity) {
     KvWorkspace w{};
-    const long long total = 2LL * n_layers * row_bytes;
-    w.n_chunks = (int)((total + GATHER_BYTES - 1) / GATHER_BYTES);
-    if (w.n_chunks < 1) w.n_chunks = 1;
+    const int ppg = GATHER_U / gather_kpr(row_bytes);
+    w.n_chunks = (2 * n_layers + ppg - 1) / ppg;
     const size_t cap = (size_t)capacity;
+    const size_t blocks = (cap + SEL_BLOCK - 1) / SEL_BLOCK;
     size_t off = 0;
     w.offStatus = off;
     off = align256(off + 64);
+    w.offPlanes = off;
+    off = align256(off + KV_MAX_PLANES * sizeof(char *));
     w.offKeep = off;
     off = align256(off + cap * 4);
     w.offInv = off;
     off = align256(off + cap * 4);
-    w.offMask = off;
-    off = align256(off + 2 * cap * 4);  // slot mask + per-run keep counts
+    w.offThRun = off;
+    off = align256(off + blocks * SEL_THREADS * 4);
     w.offRunStart = off;
     off = align256(off + (cap + 1) * 4);
     w.offRunKey = off;
@@ -317,6 +432,8 @@ KvWorkspace kv_workspace_layout(int n_layers, int row_bytes, int capacity) {
     w.offRunBkt = off;
     off = align256(off + cap * 4);
     w.offRunTake = off;
+    off = align256(off + cap * 4);
+    w.offRunFrom = off;
     off = align256(off + cap * 4);
     w.offFlags = off;
     off = align256(off + cap * (size_t)w.n_chunks * 4);
@@ -337,28 +454,37 @@ hipError_t launch_kv_evict(const KvLaunch &p, hipStream_t stream) {
     a.n_w = p.n_window;
     a.N = p.n_buckets;
     a.n_flags = p.M * p.lay.n_chunks;
+    a.n_chunks = p.lay.n_chunks;
     a.status = (int32_t *)(ws + p.lay.offStatus);
     a.ticket = (uint32_t *)(ws + p.lay.offStatus + 32);
     a.keep = (int32_t *)(ws + p.lay.offKeep);
     a.inv = (int32_t *)(ws + p.lay.offInv);
-    a.mask = (int32_t *)(ws + p.lay.offMask);
+    a.th_run = (int32_t *)(ws + p.lay.offThRun);
     a.run_start = (int32_t *)(ws + p.lay.offRunStart);
     a.run_key = (unsigned long long *)(ws + p.lay.offRunKey);
     a.run_bkt = (int32_t *)(ws + p.lay.offRunBkt);
     a.run_take = (int32_t *)(ws + p.lay.offRunTake);
+    a.run_from = (int32_t *)(ws + p.lay.offRunFrom);
     a.flags = (int32_t *)(ws + p.lay.offFlags);
     a.keep_out = p.keep_out;
+    a.plane_tab = (char **)(ws + p.lay.offPlanes);
+    for (int i = 0; i < KV_MAX_PLANES; ++i) a.planes[i] = i < p.n_planes ? p.planes[i] : nullptr;
+    a.n_planes = p.n_planes;
     hipLaunchKernelGGL(kv_select_kernel, dim3(1), dim3(SEL_THREADS), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
 
+    const long long groups = (long long)p.M * p.lay.n_chunks;
+    if (groups == 0) return hipSuccess;
     GatherArgs g;
-    for (int i = 0; i < KV_MAX_PLANES; ++i) g.planes[i] = i < p.n_planes ? p.planes[i] : nullptr;
+    const int kpr = gather_kpr(p.row_bytes);
+    g.plane_tab = a.plane_tab;
+    g.row_bytes = (uint32_t)p.row_bytes;
+    g.row_units = (uint32_t)(p.row_bytes / 16);
     g.n_planes = p.n_planes;
-    g.row_bytes = p.row_bytes;
+    g.planes_per_group = GATHER_U / kpr;
     g.M = p.M;
     g.n_chunks = p.lay.n_chunks;
-    g.total_bytes = (long long)p.n_planes * p.row_bytes;
     g.pos = p.pos;
     g.chunk = p.chunk_id;
     g.keep = a.keep;
@@ -366,9 +492,14 @@ hipError_t launch_kv_evict(const KvLaunch &p, hipStream_t stream) {
     g.flags = a.flags;
     g.status = a.status;
     g.ticket = a.ticket;
-    const long long groups = (long long)p.M * p.lay.n_chunks;
-    if (groups == 0) return hipSuccess;
-    hipLaunchKernelGGL(kv_gather_kernel, dim3((unsigned)groups), dim3(256), 0, stream, g);
+    const dim3 grid((unsigned)((p.M + GATHER_ROWS - 1) / GATHER_ROWS)), blk(256);
+    switch (kpr) {
+    case 1: hipLaunchKernelGGL(kv_gather_kernel<1>, grid, blk, 0, stream, g); break;
+    case 2: hipLaunchKernelGGL(kv_gather_kernel<2>, grid, blk, 0, stream, g); break;
+    case 4: hipLaunchKernelGGL(kv_gather_kernel<4>, grid, blk, 0, stream, g); break;
+    case 8: hipLaunchKernelGGL(kv_gather_kernel<8>, grid, blk, 0, stream, g); break;
+    default: hipLaunchKernelGGL(kv_gather_kernel<16>, grid, blk, 0, stream, g); break;
+    }
     return hipGetLastError();
 }
 
