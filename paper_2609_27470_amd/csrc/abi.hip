@@ -66,7 +66,7 @@ const char *ds_last_error(void) { return g_last_error; }
 
 size_t ds_gdn_workspace_bytes(const ds_gdn_shape *shape) {
     if (check_gdn_shape(shape) != DS_OK) return 0;
-    return ds::gdn_workspace_layout(shape->B, shape->T_total, shape->H_v, shape->d_v, shape->n_frames).total;
+    return ds::gdn_workspace_layout(shape->B, shape->T_total, shape->H_k, shape->H_v, shape->d_v, shape->n_frames).total;
 }
 
 ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k, const void *v, const float *g,
@@ -85,7 +85,7 @@ ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k,
     const void *ptrs[] = {q, k, v, g, beta, cu_seqlens, state_in, state_out, o, drift_partials, snapshots, workspace};
     for (const void *p : ptrs)
         if (misaligned(p)) return fail(DS_E_ALIGN, "a pointer is not 16-byte aligned");
-    const ds::GdnWorkspace lay = ds::gdn_workspace_layout(s.B, s.T_total, s.H_v, s.d_v, s.n_frames);
+    const ds::GdnWorkspace lay = ds::gdn_workspace_layout(s.B, s.T_total, s.H_k, s.H_v, s.d_v, s.n_frames);
     if (!workspace || workspace_bytes < lay.total)
         return fail(DS_E_WORKSPACE, "workspace needs %zu bytes, got %zu", lay.total, workspace_bytes);
     if (s.n_frames > 0 && s.frame_len == 0 && s.n_frames > s.B)
@@ -118,6 +118,7 @@ ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k,
     p.wsT = (_Float16 *)(ws + lay.offT);
     p.wsP = (_Float16 *)(ws + lay.offP);
     p.wsGam = (float *)(ws + lay.offGam);
+    p.wsKT = (uint16_t *)(ws + lay.offKT);
     p.wsDrift = (float *)(ws + lay.offDrift);
     p.tiles_max = lay.tiles_max;
     p.n_split = lay.n_split;

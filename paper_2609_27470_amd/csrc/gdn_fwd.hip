@@ -13,12 +13,15 @@
 // Two kernels share the work:
 //   gdn_prep  (all tiles in parallel): the state-independent part -- K K^T,
 //             Q K^T on bf16 matrix cores, T = (I + A)^{-1} in fp32, written
-//             as fp16 T diag(beta) and P = D (.) tril(Q K^T), plus gamma;
+//             as fp16 T diag(beta) and P = D (.) tril(Q K^T), plus the decay factors
+//             exp(gamma_r) and exp(gamma_last - gamma_r);
 //   gdn_seq   (one workgroup per (stream, v-head, 16 rows of S)): walks the
 //             tiles in order, keeps its rows of S in fp32 registers, does the
 //             state-dependent products on fp16 matrix cores, writes o, and at
 //             every frame end the drift sums of Eq. 3 for its rows.
 //   gdn_drift_finalize sums the partial drift sums in a fixed order.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -28,8 +31,10 @@ constexpr int TILE = 64;
 
 // T diag(beta) and P are stored per (tile, v-head) as the six non-zero
 // 16 x 32 A-fragments of v_mfma_f32_16x16x32_f16 (row block w = 0..3,
-// k-step ks <= w / 2), 64 lanes x 8 halves each, lane l holding row
-// 16 w + l % 16, columns 32 ks + 8 (l / 16) .. + 7.
+// k-step ks <= w / 2), 64 lanes x 8 halves each: lane l holds row
+// 16 w + l % 16, and its half i the column kappa(ks, l / 16, i) =
+// 32 ks + 16 (i / 4) + 4 (l / 16) + i % 4 -- the order in which the
+// sequential kernel's B operands (tiles of R and E) hold the tokens.
 constexpr int FRAG_HALVES = 64 * 8;
 constexpr int TP_HALVES = 6 * FRAG_HALVES;
 __host__ __device__ constexpr int frag_index(int w, int ks) { return w < 2 ? w : 2 + 2 * (w - 2) + ks; }
@@ -47,6 +52,7 @@ struct GdnArgs {
     float *snapshots;
     _Float16 *wsT, *wsP;
     float *wsGam, *wsDrift;
+    uint16_t *wsKT;
     int n_split;
 };
 
@@ -81,6 +87,27 @@ __device__ __forceinline__ f32x4 mfma_f32_16x16x4(float a, float b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+// Transposed 16-bit fragment read: within each group of 16 lanes, lane l
+// receives element (l % 4) of the 4 elements addressed by lane l/4 + 4 e.
+__device__ __forceinline__ v4i16 ds_read_tr16(const void *p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)p);
+}
+__device__ __forceinline__ u32x4 cat_u32x4(v4i16 a, v4i16 b) {
+    return __builtin_bit_cast(u32x4, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+// K tile staged row-major in LDS (D bf16 per row) with the 16-byte chunks of
+// a row permuted by an XOR with swz(row), so that both the row writes and the
+// transposing reads (4 rows x 4 chunks per 16 lanes) spread over the banks.
+template <int D>
+__device__ __forceinline__ int swz(int row) {
+    if (D == 128) return ((row & 3) << 2) | ((row >> 2) & 3);
+    return (((row >> 1) & 1) << 2) | ((row >> 2) & 3);
+}
+
 template <int D>
 __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
     constexpr int KS = D / 32;   // 32-wide k-steps over the head dim
@@ -96,7 +123,10 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
     const int h = j / a.group;
     int t0 = 0, n = 0;
     if (!locate_tile(a.st, ti, t0, n)) return;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, ln = lane & 15, lg = lane >> 4;
+    // the wave index in a scalar register: branches on it are then plain jumps
+    // rather than masked code (matrix-core ops ignore the execution mask)
+    const int tid = threadIdx.x, lane = tid & 63, ln = lane & 15, lg = lane >> 4;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const size_t tv = (size_t)ti * a.H_v + j;
     const uint4 zero4 = make_uint4(0, 0, 0, 0);
 
@@ -120,6 +150,31 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
             ka[ks] = (r < n) ? *(const uint4 *)(a.k + off) : zero4;
         }
     }
+    // ---- K^T as A-fragments of the sequential kernel's state update, once per
+    // qk-head: fragment (kb, ks) = 2 kb + ks, lane (ln, lg), half i holds
+    // K[kappa(ks, lg, i)][sigma(kb, ln)] (token and dim relabellings of the
+    // sequential kernel), read from a K tile in LDS by transposing reads.
+    if (j % a.group == 0) {
+        constexpr int NKB = D / 16;
+        uint16_t *Kl = (uint16_t *)As;  // 64 x D bf16 fits in As
+        {
+            const int row = 16 * w + ln;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) *(uint4 *)(&Kl[row * D + 8 * ((4 * ks + lg) ^ swz<D>(row))]) = ka[ks];
+        }
+        __syncthreads();
+        u32x4 *dst = (u32x4 *)a.wsKT + ((size_t)ti * a.H_k + h) * (2 * NKB) * 64;
+#pragma unroll
+        for (int f = w; f < 2 * NKB; f += 4) {
+            const int kb = f >> 1, ks = f & 1;
+            const int r0 = 32 * ks + 4 * lg + (ln >> 2), r1 = r0 + 16;
+            const int ch = 4 * (kb >> 1) + (ln & 3), half = 4 * (kb & 1);
+            dst[f * 64 + lane] = cat_u32x4(ds_read_tr16(&Kl[r0 * D + 8 * (ch ^ swz<D>(r0)) + half]),
+                                           ds_read_tr16(&Kl[r1 * D + 8 * (ch ^ swz<D>(r1)) + half]));
+        }
+        __syncthreads();
+    }
+
     float gv = 0.f, bv = 0.f;
     if (w == 0 && lane < n) {
         gv = a.g[(size_t)(t0 + lane) * a.H_v + j];
@@ -137,7 +192,10 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
         s *= 1.4426950408889634f;  // exp(gamma) = exp2(s)
         gam_s[lane] = s;
         beta_s[lane] = bv;
-        a.wsGam[tv * 64 + lane] = s;
+        // padding rows have g = 0, so row 63 carries the tile's last gamma
+        const float s_last = __shfl(s, 63, 64);
+        a.wsGam[tv * 128 + lane] = __builtin_amdgcn_exp2f(s);
+        a.wsGam[tv * 128 + 64 + lane] = __builtin_amdgcn_exp2f(s_last - s);
     }
 
     // ---- Gram blocks of row block w: K K^T and Q K^T for column blocks nb <= w
@@ -192,8 +250,10 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
         for (int c = tid - 64; c < 6 * 64; c += 192) {
             const int f = c >> 6, l = c & 63;
             const int fw = f < 2 ? f : 2 + ((f - 2) >> 1), fks = f < 2 ? 0 : ((f - 2) & 1);
-            const int r = 16 * fw + (l & 15), c8 = 32 * fks + 8 * (l >> 4);
-            *(uint4 *)(a.wsP + tv * TP_HALVES + f * FRAG_HALVES + l * 8) = *(const uint4 *)(&Ps[r * PLD + c8]);
+            const int r = 16 * fw + (l & 15), c4 = 32 * fks + 4 * (l >> 4);
+            uint2 *dst = (uint2 *)(a.wsP + tv * TP_HALVES + f * FRAG_HALVES + l * 8);
+            dst[0] = *(const uint2 *)(&Ps[r * PLD + c4]);
+            dst[1] = *(const uint2 *)(&Ps[r * PLD + c4 + 16]);
         }
     }
     __syncthreads();
@@ -234,11 +294,11 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
     for (int c = tid; c < 6 * 64; c += 256) {
         const int f = c >> 6, l = c & 63;
         const int fw = f < 2 ? f : 2 + ((f - 2) >> 1), fks = f < 2 ? 0 : ((f - 2) & 1);
-        const int r = 16 * fw + (l & 15), c8 = 32 * fks + 8 * (l >> 4);
+        const int r = 16 * fw + (l & 15), c4 = 32 * fks + 4 * (l >> 4);
         half8 tv8;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-            const int i = c8 + e;
+            const int i = c4 + 16 * (e >> 2) + (e & 3);
             tv8[e] = (_Float16)((i <= r) ? Ts[r * ALD + i] * beta_s[i] : 0.f);
         }
         *(uint4 *)(a.wsT + tv * TP_HALVES + f * FRAG_HALVES + l * 8) = as_uint4(tv8);
@@ -247,77 +307,48 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
 
 // ============================================================================
 // gdn_seq: one workgroup of 8 waves per (stream, v-head, 16 consecutive rows
-// of S).  Waves 0-3 ("state waves") carry the recurrence: wave w owns state
-// columns [w D/4, (w+1) D/4) of the 16 rows and, per tile, computes the rows
-// 16 w .. 16 w + 15 of K S0^T, the residual and the writes E, and its block
-// of the state update.  Waves 4-7 ("helper waves", helper h = w - 4 shares a
-// SIMD with state wave h) do everything off that chain: they load the
-// operands two tiles ahead, stage K, T diag(beta), v and gamma of the next
-// tile in LDS, compute Q S0^T and the outputs O = diag(Gamma) Q S0^T + P E,
-// and store o.  All 8 waves meet at the same 3 barriers per tile.
+// of S):
+//   waves 0 and 1, state:  carry the recurrence for the 16 rows of S in fp32
+//                    registers, wave h owning the state columns (dims of k)
+//                    of its half.  Per tile: each computes its half of
+//                    K S0^T, the two halves are exchanged through LDS (a flag
+//                    handshake between the two waves), both form
+//                    R = V - diag(Gamma) K S0^T and E = T diag(beta) R, and each
+//                    updates its half, S = Gamma_last S0 + (D_last E)^T K.
+//                    Every product's result becomes the next product's B
+//                    operand inside the registers.  S0 and E are published in
+//                    LDS for the output waves; frame ends write drift sums.
+//   waves 2 and 3, output:  one tile behind, O = diag(Gamma) Q S0^T + P E for
+//                    row blocks {0, 1} and {2, 3}; they load q, P and Gamma
+//                    themselves.
+//   waves 4 - 7, loaders: each loads a quarter of the K and K^T fragments,
+//                    T diag(beta), v and the decay factors of a tile three tiles
+//                    ahead and stages it in LDS one tile ahead.
+// All eight waves meet at one barrier per tile.  A single wave moves data
+// from L2 and from LDS at a limited rate, which is why the chain is shared by
+// two waves, every tile is loaded by four waves, and every operand is staged
+// in fragment order (contiguous 16-byte accesses).
+//
+// Fragment bookkeeping.  The C layout of v_mfma_f32_16x16x32 (lane (ln, lg)
+// holds rows 4 lg + e of column ln) of two row blocks 2 s and 2 s + 1 is,
+// read as 8 values per lane, exactly a B operand (rows 8 lg .. 8 lg + 7 of a
+// 32-row k-step) once the k-step's 32 rows are relabelled; the A operand that
+// meets it is loaded with the same relabelling.  Two relabellings are used:
+//   state rows  (k, the columns of S):  block kb, C row m  <->  k = sigma(kb, m)
+//       sigma(kb, m) = 32 (kb / 2) + 8 (m / 4) + 4 (kb % 2) + m % 4,
+//     so that S0 as a B operand runs over k = 32 ks + 8 lg + i in order and K
+//     and Q are read as plain 16-byte rows;
+//   token rows  (R, E, O):  C rows stay in order (row block rb, row 4 lg + e
+//     is token 16 rb + 4 lg + e), so as a B operand element i of k-step ks
+//     is token kappa(ks, lg, i) = 32 ks + 16 (i / 4) + 4 lg + i % 4; the
+//     prep kernel writes T diag(beta), P and the K^T fragments with their
+//     token columns in that order.
 //
 // Precision: k and q stay bf16 (as given) and meet the fp32 state through
 // bf16 matrix-core products against a two-term bf16 split of the state
-// (S ~ S_hi + S_lo, relative error ~2^-17); the writes D_last E enter the
-// state update the same way.  The tile-local operands (R, E, T diag(beta),
-// P) are fp16.  All accumulation is fp32.  K and the state are staged
-// row-major and read as transposed fragments with ds_read_b64_tr_b16.
+// (S ~ S_hi + S_lo, relative error ~2^-17); D_last E enters the state update
+// the same way.  R, E, T diag(beta) and P are fp16.  All accumulation is fp32.
 // ============================================================================
-template <int D>
-struct SeqTile {
-    u32x4 k[D / 32], q[D / 32];  // bf16 rows 16 h + ln of k and q (8 dims per k-step)
-    u32x4 t[2], p[2];            // fp16 T diag(beta), P fragments of rows 16 h + ln
-    float4 gam;                  // gamma (base-2 units) of rows 16 h + 4 lg + e
-    float gam_last;
-    uint32_t v[4];               // bf16 v of rows 16 h + 4 lg + e, column v0 + ln
-};
-
-typedef short v4i16 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
-
-// Transposed 16-bit fragment read: within each group of 16 lanes, lane l
-// receives element (l % 4) of the 4 elements addressed by lanes l/4 + 4 e.
-__device__ __forceinline__ v4i16 ds_read_tr16(const void *p) {
-    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)p);
-}
-__device__ __forceinline__ bf16x8 cat_bf16(v4i16 a, v4i16 b) {
-    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
-}
-
-// Operands of one tile for row block h (rows 16 h ..).  Rows past the end of
-// a ragged tile are clamped to its last row: their products only meet zero
-// entries of T diag(beta) and P (beta = 0 and k = 0 there in the prep kernel)
-// and their outputs are never stored.
-template <int D>
-__device__ __forceinline__ void seq_load(const GdnArgs &a, SeqTile<D> &s, int t0, int n, size_t tv, int qh,
-                                         int j, int v0, int h, int ln, int lg) {
-    const uint16_t *kb = a.k + (size_t)t0 * a.H_k * D;
-    const uint16_t *qb = a.q + (size_t)t0 * a.H_k * D;
-    const uint32_t ra = (uint32_t)min(16 * h + ln, n - 1);
-    const uint32_t off = (ra * (uint32_t)a.H_k + (uint32_t)qh) * D + 8 * lg;
-#pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) {
-        s.k[ks] = *(const u32x4 *)(kb + off + 32 * ks);
-        s.q[ks] = *(const u32x4 *)(qb + off + 32 * ks);
-    }
-    const uint16_t *vb = a.v + (size_t)t0 * a.H_v * D + (size_t)j * D + v0 + ln;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const uint32_t r = (uint32_t)min(16 * h + 4 * lg + e, n - 1);
-        s.v[e] = vb[r * (uint32_t)a.H_v * D];
-    }
-    const float *gb = a.wsGam + tv * 64;
-    s.gam = *(const float4 *)(gb + 16 * h + 4 * lg);
-    s.gam_last = gb[63];
-    const _Float16 *tb = a.wsT + tv * TP_HALVES, *pb = a.wsP + tv * TP_HALVES;
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-        // row blocks 0 and 1 have a single k-step; their second load repeats the first
-        const int f = frag_index(h, (h >= 2) ? ks : 0);
-        s.t[ks] = *(const u32x4 *)(tb + f * FRAG_HALVES + 8 * (ln + 16 * lg));
-        s.p[ks] = *(const u32x4 *)(pb + f * FRAG_HALVES + 8 * (ln + 16 * lg));
-    }
-}
 
 // fp32 pair -> bf16 pair (round to nearest even), packed in one dword
 __device__ __forceinline__ uint32_t bf16_pack(float x, float y) {
@@ -328,49 +359,103 @@ __device__ __forceinline__ uint32_t bf16_pack(float x, float y) {
 __device__ __forceinline__ float bf16_lo_f(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi_f(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// Inclusive prefix sum within each row of 16 lanes (DPP row shifts); lane 15
-// of a row ends with the row's total.
-__device__ __forceinline__ float row16_sum(float x) {
-    x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x111, 0xF, 0xF, true));
-    x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x112, 0xF, 0xF, true));
-    x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x114, 0xF, 0xF, true));
-    x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x118, 0xF, 0xF, true));
-    return x;
+// Two C blocks -> one B operand as two bf16 terms (x ~ hi + lo).  The
+// remainder x - hi comes from one bf16 dot product per value,
+// x + hi . (-1, 0), which is exact (hi and x are within a factor of 2).
+// The constant pairs are kept in scalar registers: as a literal operand the
+// compiler encodes (-1, 0) as the fp32 inline constant -1.0, which the
+// hardware does not read as that bf16 pair.
+__device__ __forceinline__ void split_bf16(const f32x4 &a, const f32x4 &b, u32x4 &hi, u32x4 &lo) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    uint32_t c0 = 0x0000bf80u, c1 = 0xbf800000u;  // (-1, 0) and (0, -1)
+    asm volatile("" : "+s"(c0), "+s"(c1));
+    const bf16x2 m0 = __builtin_bit_cast(bf16x2, c0), m1 = __builtin_bit_cast(bf16x2, c1);
+    const float x[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        const uint32_t h = bf16_pack(x[2 * p], x[2 * p + 1]);
+        const bf16x2 hv = __builtin_bit_cast(bf16x2, h);
+        hi[p] = h;
+        lo[p] = bf16_pack(__builtin_amdgcn_fdot2_f32_bf16(hv, m0, x[2 * p], false),
+                          __builtin_amdgcn_fdot2_f32_bf16(hv, m1, x[2 * p + 1], false));
+    }
+}
+// Two C blocks -> one fp16 B operand.
+__device__ __forceinline__ half8 to_half8(const f32x4 &a, const f32x4 &b) {
+    half8 r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        r[e] = (_Float16)a[e];
+        r[4 + e] = (_Float16)b[e];
+    }
+    return r;
 }
 
 template <int D>
 struct SeqShared {
-    static constexpr int KLD = D + 8;  // bf16 per LDS row of the K tile
-    static constexpr int SLD = 20;     // bf16 per LDS row of S^T (16 rows of S + pad)
-    static constexpr int TLD = 72;     // 16-bit elements per LDS row of R^T, E^T, (D E)^T
-    uint16_t Ks[2][64 * KLD];          // K tile of the tile (row-major, bf16)
-    u32x4 Tst[2][4][2][64];            // T diag(beta) fragments per state wave and lane
-    uint2 Vst[2][4][64];               // v (4 bf16) per state wave and lane
-    float4 Gst[2][4][64];              // gamma of the lane's 4 rows
-    float Glast[2];                    // gamma of the tile's last row
-    uint16_t SThi[2][D * SLD];         // S^T, high bf16 term
-    uint16_t STlo[2][D * SLD];         // S^T, low bf16 term
-    _Float16 RT[2][16 * TLD];          // R^T
-    _Float16 ET[2][16 * TLD];          // E^T
-    uint16_t DThi[2][16 * TLD];        // (D_last E)^T, high bf16 term
-    uint16_t DTlo[2][16 * TLD];        // (D_last E)^T, low bf16 term
+    static constexpr int KS = D / 32, NKB = D / 16;
+    u32x4 KA[2][4 * KS][64];   // K as A operand: fragment (rb, ks) = 4 ks + rb... see ka_index
+    u32x4 KT[2][2 * NKB][64];  // K^T as A operand: fragment (kb, ks) = 2 kb + ks
+    u32x4 T[2][6][64];         // T diag(beta) A-fragments
+    uint16_t V[2][64 * 16];    // v[token][v0 .. v0 + 15] (bf16, read transposed)
+    uint32_t Ost[2][32 * 16];  // per output wave: its 32 rows of o, staged for 16-byte row stores
+    float G[2][2][64];         // Gamma_r and D_last,r
+    f32x4 X[2][2][4][64];      // exchanged halves of K S0^T: [tile % 2][state wave][rb][lane]
+    u32x4 Shi[2][KS][64];      // S0 as B operand, high bf16 term (for the output waves)
+    u32x4 Slo[2][KS][64];      // low bf16 term
+    u32x4 E[2][2][64];         // E as B operand (fp16)
+    int xflag[2];              // tiles whose half of K S0^T each state wave has published
 };
+__host__ __device__ constexpr int ka_index(int rb, int ks) { return 4 * ks + rb; }
+
+// One loader's quarter of a tile: K fragments ka_index = 4 x .. 4 x + 3 (D = 128;
+// two per loader for D = 64), K^T fragments likewise, T diag(beta) fragments
+// {2 x, 2 x + 1} for x < 2 and {4 + x - 2} otherwise, v of row block rb = x,
+// and Gamma (x = 0) or D_last (x = 1).
+template <int D>
+struct LoadSet {
+    static constexpr int NK = D / 32;  // K and K^T fragments per loader
+    u32x4 ka[NK], kt[NK];
+    u32x4 t[2];
+    u32x4 v;        // v[16 x + lane / 2][v0 + 8 (lane % 2) .. + 7] (lanes >= 32 repeat)
+    float g;        // Gamma (x = 0) or D_last (x = 1) of token lane
+};
+
+// Output-wave registers for one tile (two row blocks).
+template <int D>
+struct OutSet {
+    u32x4 q[2][D / 32];  // q rows 16 rb + ln, dims 32 ks + 8 lg .. + 7
+    u32x4 p[4];          // P fragments of the two row blocks (2 or 4 used)
+    float4 gam[2];       // Gamma of rows 16 rb + 4 lg + e
+};
+
+constexpr int SEQ_SPIN_LIMIT = 1 << 22;
+
+// Workgroup barrier that orders LDS only.  The waves of this kernel exchange
+// data through LDS alone, so the barrier need not wait for their global loads
+// in flight (a full __syncthreads would, and so drain every prefetch).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 
 template <int D, bool OUT_BF16, bool DRIFT>
 __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
-    constexpr int KS = D / 32;
-    constexpr int NB = D / 64;  // 16-column state blocks per state wave
+    constexpr int KS = D / 32;   // k-steps over the head dim
+    constexpr int NKB = D / 16;  // 16-row blocks of S^T
+    constexpr int HKS = KS / 2, HKB = NKB / 2;  // per state wave
     using SH = SeqShared<D>;
-    constexpr int KLD = SH::KLD, SLD = SH::SLD, TLD = SH::TLD;
     __shared__ __align__(16) SH sh;
 
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, ln = lane & 15, lg = lane >> 4;
-    const bool state_wave = w < 4;
-    const int h = w & 3;  // row block (and state column block) of this wave
+    // the wave index in a scalar register: branches on it are then plain jumps
+    // rather than masked code (matrix-core ops ignore the execution mask)
+    const int tid = threadIdx.x, lane = tid & 63, ln = lane & 15, lg = lane >> 4;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
 
     // ---- workgroup -> (stream, v-head, slice).  All workgroups that read one
     // qk-head of one stream land on the same XCD (dispatch is round-robin
-    // over the 8 XCDs) so its q/k tiles are shared through that XCD's L2.
+    // over the 8 XCDs) so its tiles are shared through that XCD's L2.
     const int gsz = a.group * a.n_split;
     const int n_groups = a.st.B * a.H_k;
     const int bid = blockIdx.x;
@@ -400,250 +485,344 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
     });
     const int len = en - st;
     const int n_tiles = (len + TILE - 1) / TILE;
-    const int trow = ln >> 2, tcol = 4 * (ln & 3);  // source element of a transposed read
+    if (tid < 2) sh.xflag[tid] = 0;
 
-    // ---- state (state waves): rows v0 + 4 lg + e, columns h D/4 + 16 nb + ln
-    const size_t sbase = ((size_t)b * a.H_v + j) * D * D;
-    f32x4 S[NB], S_start[NB];
+    if (w < 2) {
+        // ================================================================ state
+        const int hh = w;  // half of the state columns: blocks kb in [hh HKB, (hh + 1) HKB)
+        // S^T block kb, lane (ln, lg), element e  =  S[v0 + ln][sigma(kb, 4 lg + e)]
+        auto scol = [&](int kb, int e) { return 32 * (kb >> 1) + 8 * lg + 4 * (kb & 1) + e; };
+        const size_t sbase = ((size_t)b * a.H_v + j) * D * D + (size_t)(v0 + ln) * D;
+        f32x4 S[HKB], S0f[HKB];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
+        for (int c = 0; c < HKB; ++c) {
+            const int kb = hh * HKB + c;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int vr = v0 + 4 * lg + e, c = h * (D / 4) + 16 * nb + ln;
-            S[nb][e] = (state_wave && a.state_in) ? a.state_in[sbase + (size_t)vr * D + c] : 0.f;
+            for (int e = 0; e < 4; ++e) S[c][e] = a.state_in ? a.state_in[sbase + scol(kb, e)] : 0.f;
+            S0f[c] = S[c];
         }
-        S_start[nb] = S[nb];
-    }
-    int frame = frame_base;
+        int frame = frame_base;
 
-    // S split in two bf16 terms -> S^T buffer `buf`
-    auto write_state = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-            const uint32_t h01 = bf16_pack(S[nb][0], S[nb][1]), h23 = bf16_pack(S[nb][2], S[nb][3]);
-            const uint32_t l01 = bf16_pack(S[nb][0] - bf16_lo_f(h01), S[nb][1] - bf16_hi_f(h01));
-            const uint32_t l23 = bf16_pack(S[nb][2] - bf16_lo_f(h23), S[nb][3] - bf16_hi_f(h23));
-            const int off = (h * (D / 4) + 16 * nb + ln) * SLD + 4 * lg;
-            *(uint2 *)(&sh.SThi[buf][off]) = make_uint2(h01, h23);
-            *(uint2 *)(&sh.STlo[buf][off]) = make_uint2(l01, l23);
-        }
-    };
-    // helper: stage tile data of row block h into buffer `buf`
-    auto stage = [&](const SeqTile<D> &s, int buf) __attribute__((always_inline)) {
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) *(u32x4 *)(&sh.Ks[buf][(16 * h + ln) * KLD + 32 * ks + 8 * lg]) = s.k[ks];
-        sh.Tst[buf][h][0][lane] = s.t[0];
-        sh.Tst[buf][h][1][lane] = s.t[1];
-        sh.Vst[buf][h][lane] = make_uint2(s.v[0] | (s.v[1] << 16), s.v[2] | (s.v[3] << 16));
-        sh.Gst[buf][h][lane] = s.gam;
-        if (h == 0 && lane == 0) sh.Glast[buf] = s.gam_last;
-    };
-    auto load_tile = [&](SeqTile<D> &s, int lt) __attribute__((always_inline)) {
-        const int lc = min(lt, n_tiles - 1), t0 = st + TILE * lc;
-        seq_load<D>(a, s, t0, min(TILE, en - t0), (size_t)(tile_base + lc) * a.H_v + j, qh, j, v0, h, ln, lg);
-    };
+        auto tile = [&](int lt, auto bufc) __attribute__((always_inline)) {
+            constexpr int buf = decltype(bufc)::value;  // == lt % 2
+            const int n = min(TILE, len - TILE * lt);
+            lds_barrier();
 
-    // ---- state waves: the recurrence, 3 barriers per tile
-    auto state_step = [&](int lt) __attribute__((always_inline)) {
-        const int t0 = st + TILE * lt, n = min(TILE, en - t0);
-        const int buf = lt & 1;
-        __syncthreads();  // ---- A: tile lt staged, S^T of tile lt written
-        {
-            // K S0^T for rows 16 h .. 16 h + 15, then R = V - diag(Gamma) K S0^T
-            f32x4 xk0 = {0.f, 0.f, 0.f, 0.f}, xk1 = {0.f, 0.f, 0.f, 0.f};
+            // Gamma_last S0 first: the split below may then consume S0's registers
+            const float gl = sh.G[buf][0][63];
+            f32x4 Sn[HKB];
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const int r0 = (32 * ks + 8 * lg + trow) * SLD + tcol;
-                const bf16x8 bh = cat_bf16(ds_read_tr16(&sh.SThi[buf][r0]), ds_read_tr16(&sh.SThi[buf][r0 + 4 * SLD]));
-                const bf16x8 bl = cat_bf16(ds_read_tr16(&sh.STlo[buf][r0]), ds_read_tr16(&sh.STlo[buf][r0 + 4 * SLD]));
-                const bf16x8 ka = as_bf16x8(*(const u32x4 *)(&sh.Ks[buf][(16 * h + ln) * KLD + 32 * ks + 8 * lg]));
-                xk0 = mfma_bf16(ka, bh, xk0);
-                xk1 = mfma_bf16(ka, bl, xk1);
+            for (int c = 0; c < HKB; ++c)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) Sn[c][e] = gl * S[c][e];
+
+            // own half of S0 as B operand (two bf16 terms), also published
+            u32x4 shi[HKS], slo[HKS];
+#pragma unroll
+            for (int c = 0; c < HKS; ++c) {
+                split_bf16(S[2 * c], S[2 * c + 1], shi[c], slo[c]);
+                sh.Shi[buf][hh * HKS + c][lane] = shi[c];
+                sh.Slo[buf][hh * HKS + c][lane] = slo[c];
             }
-            const uint2 vv = sh.Vst[buf][h][lane];
-            const float4 g4 = sh.Gst[buf][h][lane];
-            const float gam[4] = {g4.x, g4.y, g4.z, g4.w};
-            const float vr[4] = {__uint_as_float(vv.x << 16), __uint_as_float(vv.x & 0xffff0000u),
-                                 __uint_as_float(vv.y << 16), __uint_as_float(vv.y & 0xffff0000u)};
-            _Float16 rr[4] __attribute__((aligned(8)));
+
+            // every operand of the tile read now, so that the reads overlap the work below
+            bf16x8 ktf[2][HKB];
+            half8 tf[6];
+            float4 gam4[4], dl4[4];
+            v4i16 vv4[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-                rr[e] = (_Float16)(vr[e] - __builtin_amdgcn_exp2f(gam[e]) * (xk0[e] + xk1[e]));
-            *(uint2 *)(&sh.RT[buf][ln * TLD + 16 * h + 4 * lg]) = *(const uint2 *)rr;
-        }
-        __syncthreads();  // ---- B: R^T complete
-        {
-            // writes E = T diag(beta) R; D_last E split in two bf16 terms
-            f32x4 E = {0.f, 0.f, 0.f, 0.f};
+            for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+                for (int c = 0; c < HKB; ++c) ktf[ks][c] = as_bf16x8(sh.KT[buf][2 * (hh * HKB + c) + ks][lane]);
+#pragma unroll
+            for (int f = 0; f < 6; ++f) tf[f] = as_half8(sh.T[buf][f][lane]);
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) {
+                gam4[rb] = *(const float4 *)(&sh.G[buf][0][16 * rb + 4 * lg]);
+                dl4[rb] = *(const float4 *)(&sh.G[buf][1][16 * rb + 4 * lg]);
+                // v[16 rb + 4 lg + e][ln], e = 0..3, by a transposing read
+                vv4[rb] = ds_read_tr16(&sh.V[buf][(16 * rb + 4 * lg + (ln >> 2)) * 16 + 4 * (ln & 3)]);
+            }
+
+            // own half of K S0^T  (token rows 16 rb + 4 lg + e, column v0 + ln)
+            f32x4 acc[4];
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int c = 0; c < HKS; ++c) {
+                bf16x8 ka[4];
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) ka[rb] = as_bf16x8(sh.KA[buf][ka_index(rb, hh * HKS + c)][lane]);
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) acc[rb] = mfma_bf16(ka[rb], as_bf16x8(shi[c]), acc[rb]);
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) acc[rb] = mfma_bf16(ka[rb], as_bf16x8(slo[c]), acc[rb]);
+            }
+            // exchange with the other state wave
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) sh.X[buf][hh][rb][lane] = acc[rb];
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+            __hip_atomic_store(&sh.xflag[hh], lt + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            for (int spin = 0; spin < SEQ_SPIN_LIMIT; ++spin)
+                if (__hip_atomic_load(&sh.xflag[hh ^ 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) > lt) break;
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+            f32x4 ks0[4];
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) {
+                const f32x4 o = sh.X[buf][hh ^ 1][rb][lane];
+                ks0[rb] = hh == 0 ? acc[rb] + o : o + acc[rb];  // same value in both waves
+            }
+
+            // R = V - diag(Gamma) K S0^T
+            f32x4 R[4];
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) {
+                const float4 g4 = gam4[rb];
+                R[rb][0] = bf16_to_f32((uint16_t)vv4[rb][0]) - g4.x * ks0[rb][0];
+                R[rb][1] = bf16_to_f32((uint16_t)vv4[rb][1]) - g4.y * ks0[rb][1];
+                R[rb][2] = bf16_to_f32((uint16_t)vv4[rb][2]) - g4.z * ks0[rb][2];
+                R[rb][3] = bf16_to_f32((uint16_t)vv4[rb][3]) - g4.w * ks0[rb][3];
+            }
+
+            // E = T diag(beta) R
+            const half8 rf0 = to_half8(R[0], R[1]), rf1 = to_half8(R[2], R[3]);
+            f32x4 E[4];
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) E[rb] = mfma_f16(tf[frag_index(rb, 0)], rf0, f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+            for (int rb = 2; rb < 4; ++rb) E[rb] = mfma_f16(tf[frag_index(rb, 1)], rf1, E[rb]);
+            if (hh == 0) {
+                sh.E[buf][0][lane] = __builtin_bit_cast(u32x4, to_half8(E[0], E[1]));
+                sh.E[buf][1][lane] = __builtin_bit_cast(u32x4, to_half8(E[2], E[3]));
+            }
+
+            // D_last E as B operand (two bf16 terms)
+            f32x4 DE[4];
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) {
+                const float4 d4 = dl4[rb];
+                DE[rb][0] = E[rb][0] * d4.x;
+                DE[rb][1] = E[rb][1] * d4.y;
+                DE[rb][2] = E[rb][2] * d4.z;
+                DE[rb][3] = E[rb][3] * d4.w;
+            }
+            u32x4 dhi[2], dlo[2];
+            split_bf16(DE[0], DE[1], dhi[0], dlo[0]);
+            split_bf16(DE[2], DE[3], dhi[1], dlo[1]);
+
+            // own half of S = Gamma_last S0 + (D_last E)^T K
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
-                if (ks <= (h >> 1)) {
-                    const half8 br = *(const half8 *)(&sh.RT[buf][ln * TLD + 32 * ks + 8 * lg]);
-                    E = mfma_f16(as_half8(sh.Tst[buf][h][ks][lane]), br, E);
-                }
-            }
-            const float4 g4 = sh.Gst[buf][h][lane];
-            const float gam[4] = {g4.x, g4.y, g4.z, g4.w};
-            const float glast = sh.Glast[buf];
-            _Float16 ee[4] __attribute__((aligned(8)));
-            float de[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                ee[e] = (_Float16)E[e];
-                de[e] = E[e] * __builtin_amdgcn_exp2f(glast - gam[e]);
-            }
-            const uint32_t h01 = bf16_pack(de[0], de[1]), h23 = bf16_pack(de[2], de[3]);
-            const uint32_t l01 = bf16_pack(de[0] - bf16_lo_f(h01), de[1] - bf16_hi_f(h01));
-            const uint32_t l23 = bf16_pack(de[2] - bf16_lo_f(h23), de[3] - bf16_hi_f(h23));
-            const int off = ln * TLD + 16 * h + 4 * lg;
-            *(uint2 *)(&sh.ET[buf][off]) = *(const uint2 *)ee;
-            *(uint2 *)(&sh.DThi[buf][off]) = make_uint2(h01, h23);
-            *(uint2 *)(&sh.DTlo[buf][off]) = make_uint2(l01, l23);
-        }
-        __syncthreads();  // ---- C: E^T and (D_last E)^T complete
-        {
-            // S = Gamma_last S0 + (D_last E)^T K
-            const float gl = __builtin_amdgcn_exp2f(sh.Glast[buf]);
-            f32x4 Sl[NB];
+                for (int c = 0; c < HKB; ++c) Sn[c] = mfma_bf16(ktf[ks][c], as_bf16x8(dhi[ks]), Sn[c]);
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) S[nb][e] *= gl;
-                Sl[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+                for (int c = 0; c < HKB; ++c) Sn[c] = mfma_bf16(ktf[ks][c], as_bf16x8(dlo[ks]), Sn[c]);
             }
 #pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
-                const bf16x8 ah = as_bf16x8(*(const u32x4 *)(&sh.DThi[buf][ln * TLD + 32 * ks + 8 * lg]));
-                const bf16x8 al = as_bf16x8(*(const u32x4 *)(&sh.DTlo[buf][ln * TLD + 32 * ks + 8 * lg]));
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb) {
-                    const int r0 = (32 * ks + 8 * lg + trow) * KLD + h * (D / 4) + 16 * nb + tcol;
-                    const bf16x8 bk = cat_bf16(ds_read_tr16(&sh.Ks[buf][r0]), ds_read_tr16(&sh.Ks[buf][r0 + 4 * KLD]));
-                    S[nb] = mfma_bf16(ah, bk, S[nb]);
-                    Sl[nb] = mfma_bf16(al, bk, Sl[nb]);
-                }
-            }
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) S[nb] += Sl[nb];
+            for (int c = 0; c < HKB; ++c) S[c] = Sn[c];
 
-            // frame end: drift sums of this slice (one pair per row of 16
-            // lanes, reduced later in a fixed order), optional snapshot
+            // frame end: drift sums of this half of the slice, optional snapshot
             const int done = TILE * lt + n;
             if (DRIFT && ((a.frame_len > 0 && done % a.frame_len == 0) || done == len)) {
                 float num = 0.f, den = 0.f;
 #pragma unroll
-                for (int nb = 0; nb < NB; ++nb)
+                for (int c = 0; c < HKB; ++c)
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        const float dl = S[nb][e] - S_start[nb][e];
+                        const float dl = S[c][e] - S0f[c][e];
                         num += dl * dl;
-                        den += S_start[nb][e] * S_start[nb][e];
+                        den += S0f[c][e] * S0f[c][e];
                     }
-                num = row16_sum(num);
-                den = row16_sum(den);
-                if (ln == 15 && a.wsDrift && frame < a.n_frames) {
-                    float *dst = a.wsDrift + ((((size_t)frame * a.H_v + j) * a.n_split + sl) * 16 + 4 * h + lg) * 2;
+                num = wave_sum(num);
+                den = wave_sum(den);
+                if (lane == 0 && a.wsDrift && frame < a.n_frames) {
+                    float *dst = a.wsDrift + ((((size_t)frame * a.H_v + j) * a.n_split + sl) * 2 + hh) * 2;
                     dst[0] = num;
                     dst[1] = den;
                 }
                 if (a.snapshots && frame < a.n_frames) {
-                    const size_t fb = ((size_t)frame * a.H_v + j) * D * D;
+                    float *snap = a.snapshots + ((size_t)frame * a.H_v + j) * D * D + (size_t)(v0 + ln) * D;
 #pragma unroll
-                    for (int nb = 0; nb < NB; ++nb)
+                    for (int c = 0; c < HKB; ++c)
 #pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            a.snapshots[fb + (size_t)(v0 + 4 * lg + e) * D + h * (D / 4) + 16 * nb + ln] = S[nb][e];
+                        for (int e = 0; e < 4; ++e) snap[scol(hh * HKB + c, e)] = S[c][e];
                 }
 #pragma unroll
-                for (int nb = 0; nb < NB; ++nb) S_start[nb] = S[nb];
+                for (int c = 0; c < HKB; ++c) S0f[c] = S[c];
                 ++frame;
             }
-            if (lt + 1 < n_tiles) write_state(buf ^ 1);
+        };
+        for (int lt = 0; lt < n_tiles; lt += 2) {
+            tile(lt, std::integral_constant<int, 0>());
+            if (lt + 1 < n_tiles) tile(lt + 1, std::integral_constant<int, 1>());
         }
-    };
-
-    // ---- helper waves: three register sets -- cur (tile lt), nxt (tile
-    // lt + 1, loaded one tile ago, staged at the end of this tile) and nn
-    // (tile lt + 2, loaded now)
-    auto helper_step = [&](int lt, SeqTile<D> &cur, SeqTile<D> &nxt, SeqTile<D> &nn) __attribute__((always_inline)) {
-        if (lt >= n_tiles) return;  // uniform over the workgroup
-        const int t0 = st + TILE * lt, n = min(TILE, en - t0);
-        const int buf = lt & 1;
-        __syncthreads();  // ---- A
-        // Q S0^T for rows 16 h .. 16 h + 15 (kept for the outputs)
-        f32x4 xq = {0.f, 0.f, 0.f, 0.f}, xq1 = {0.f, 0.f, 0.f, 0.f};
+        if (n_tiles > 0) lds_barrier();  // the output waves' last tile
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            const int r0 = (32 * ks + 8 * lg + trow) * SLD + tcol;
-            const bf16x8 bh = cat_bf16(ds_read_tr16(&sh.SThi[buf][r0]), ds_read_tr16(&sh.SThi[buf][r0 + 4 * SLD]));
-            const bf16x8 bl = cat_bf16(ds_read_tr16(&sh.STlo[buf][r0]), ds_read_tr16(&sh.STlo[buf][r0 + 4 * SLD]));
-            const bf16x8 qa = as_bf16x8(cur.q[ks]);
-            xq = mfma_bf16(qa, bh, xq);
-            xq1 = mfma_bf16(qa, bl, xq1);
-        }
-        xq += xq1;
-        load_tile(nn, lt + 2);
-        __syncthreads();  // ---- B
-        __syncthreads();  // ---- C
-        // outputs O = diag(Gamma) Q S0^T + P E for rows 16 h .. 16 h + 15
-        const float gam[4] = {cur.gam.x, cur.gam.y, cur.gam.z, cur.gam.w};
-        f32x4 oacc;
+        for (int c = 0; c < HKB; ++c)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) oacc[e] = __builtin_amdgcn_exp2f(gam[e]) * xq[e];
+            for (int e = 0; e < 4; ++e) a.state_out[sbase + scol(hh * HKB + c, e)] = S[c][e];
+    } else if (w < 4) {
+        // =============================================================== output
+        const int pr = w - 2;  // row blocks 2 pr and 2 pr + 1
+        // (tiles past the end are clamped to the last one so that every
+        // iteration issues the same memory operations)
+        auto load = [&](OutSet<D> &s, int lt_) __attribute__((always_inline)) {
+            const int lt = min(lt_, n_tiles - 1);
+            const int t0 = st + TILE * lt, n = min(TILE, en - t0);
+            const size_t tv = (size_t)(tile_base + lt) * a.H_v + j;
+            const uint16_t *qb = a.q + (size_t)t0 * a.H_k * D + (size_t)qh * D + 8 * lg;
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            if (ks <= (h >> 1)) {
-                const half8 be = *(const half8 *)(&sh.ET[buf][ln * TLD + 32 * ks + 8 * lg]);
-                oacc = mfma_f16(as_half8(cur.p[ks]), be, oacc);
+            for (int r = 0; r < 2; ++r) {
+                const uint32_t row = (uint32_t)min(16 * (2 * pr + r) + ln, n - 1);
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) s.q[r][ks] = *(const u32x4 *)(qb + row * (uint32_t)a.H_k * D + 32 * ks);
+            }
+            const u32x4 *pb = (const u32x4 *)(a.wsP + tv * TP_HALVES);
+            // fragments of row blocks 2 pr, 2 pr + 1: {0, 1} or {2, 3, 4, 5}
+#pragma unroll
+            for (int f = 0; f < 4; ++f) s.p[f] = pb[(pr == 0 ? min(f, 1) : 2 + f) * 64 + lane];
+            const float *gb = a.wsGam + tv * 128;
+#pragma unroll
+            for (int r = 0; r < 2; ++r) s.gam[r] = *(const float4 *)(gb + 16 * (2 * pr + r) + 4 * lg);
+        };
+        auto compute = [&](const OutSet<D> &s, int lt, auto bufc) __attribute__((always_inline)) {
+            constexpr int buf = decltype(bufc)::value;  // == lt % 2
+            const int t0 = st + TILE * lt, n = min(TILE, en - t0);
+            f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                const bf16x8 bh = as_bf16x8(sh.Shi[buf][ks][lane]), bl = as_bf16x8(sh.Slo[buf][ks][lane]);
+#pragma unroll
+                for (int r = 0; r < 2; ++r) acc[r] = mfma_bf16(as_bf16x8(s.q[r][ks]), bh, acc[r]);
+#pragma unroll
+                for (int r = 0; r < 2; ++r) acc[r] = mfma_bf16(as_bf16x8(s.q[r][ks]), bl, acc[r]);
+            }
+#pragma unroll
+            for (int r = 0; r < 2; ++r) {
+                acc[r][0] *= s.gam[r].x;
+                acc[r][1] *= s.gam[r].y;
+                acc[r][2] *= s.gam[r].z;
+                acc[r][3] *= s.gam[r].w;
+            }
+            const half8 ef0 = as_half8(sh.E[buf][0][lane]);
+            if (pr == 0) {
+                acc[0] = mfma_f16(as_half8(s.p[0]), ef0, acc[0]);
+                acc[1] = mfma_f16(as_half8(s.p[1]), ef0, acc[1]);
+            } else {
+                const half8 ef1 = as_half8(sh.E[buf][1][lane]);
+                acc[0] = mfma_f16(as_half8(s.p[0]), ef0, acc[0]);
+                acc[1] = mfma_f16(as_half8(s.p[2]), ef0, acc[1]);
+                acc[0] = mfma_f16(as_half8(s.p[1]), ef1, acc[0]);
+                acc[1] = mfma_f16(as_half8(s.p[3]), ef1, acc[1]);
+            }
+            // o: the wave's 32 x 16 block goes through LDS (private to the wave)
+            // and leaves as 16-byte row pieces, through a buffer resource covering
+            // the tile's n valid rows: pieces of rows past a ragged tile's end fall
+            // outside it and are dropped
+            constexpr int ES = OUT_BF16 ? 2 : 4;
+            uint32_t *ost = sh.Ost[pr];
+            if (OUT_BF16) {
+                uint16_t *o16 = (uint16_t *)ost;  // [32 rows][16] bf16
+#pragma unroll
+                for (int r = 0; r < 2; ++r)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        o16[(16 * r + 4 * lg + e) * 16 + ln] = __builtin_bit_cast(uint16_t, (__bf16)(a.scale * acc[r][e]));
+            } else {
+#pragma unroll
+                for (int r = 0; r < 2; ++r)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) ost[(16 * r + 4 * lg + e) * 16 + ln] = __builtin_bit_cast(uint32_t, a.scale * acc[r][e]);
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");  // (own wave's LDS, in order)
+            const uint32_t row_bytes = (uint32_t)a.H_v * D * ES;
+            const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                (char *)a.o + (size_t)t0 * row_bytes, (short)0, (int)(row_bytes * (uint32_t)n), 0x00020000);
+            constexpr int PIECES = 16 * ES / 16;  // 16-byte pieces per row of the block
+#pragma unroll
+            for (int c = 0; c < 32 * PIECES / 64; ++c) {
+                const int idx = 64 * c + lane, rr = idx / PIECES, pc = idx % PIECES;
+                const u32x4 val = *(const u32x4 *)((const char *)ost + rr * 16 * ES + 16 * pc);
+                const uint32_t off = (uint32_t)(32 * pr + rr) * row_bytes + (uint32_t)(j * D + v0) * ES + 16 * pc;
+                __builtin_amdgcn_raw_buffer_store_b128(val, rs, off, 0, 0);
+            }
+        };
+        // iteration it computes tile it - 1 and then loads tile it + 1 into the
+        // same register set (set (it + 1) % 2)
+        auto step = [&](int it, OutSet<D> &s, auto bufc) __attribute__((always_inline)) {
+            lds_barrier();
+            if (it >= 1) compute(s, it - 1, bufc);
+            load(s, it + 1);
+        };
+        if (n_tiles > 0) {
+            OutSet<D> sa, sb;
+            load(sa, 0);
+            for (int it = 0; it <= n_tiles; it += 2) {
+                step(it, sb, std::integral_constant<int, 1>());
+                if (it + 1 <= n_tiles) step(it + 1, sa, std::integral_constant<int, 0>());
             }
         }
-        if (OUT_BF16) {
-            uint16_t *ob = (uint16_t *)a.o + (size_t)t0 * a.H_v * D + (size_t)j * D + v0 + ln;
+    } else {
+        // ============================================================== loaders
+        const int x = w - 4;  // quarter of every tile
+        constexpr int NK = LoadSet<D>::NK;
+        const int nt = x < 2 ? 2 : 1;  // T diag(beta) fragments of this loader
+        const int t_first = x < 2 ? 2 * x : 4 + (x - 2);
+        auto load = [&](LoadSet<D> &s, int lt_) __attribute__((always_inline)) {
+            const int lt = min(lt_, n_tiles - 1);  // clamped: every call issues the same loads
+            const int t0 = st + TILE * lt, n = min(TILE, en - t0);
+            const size_t tv = (size_t)(tile_base + lt) * a.H_v + j;
+            const uint16_t *kb = a.k + (size_t)t0 * a.H_k * D + (size_t)qh * D + 8 * lg;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int r = 16 * h + 4 * lg + e;
-                if (r < n) ob[(uint32_t)r * a.H_v * D] = __builtin_bit_cast(uint16_t, (__bf16)(a.scale * oacc[e]));
+            for (int c = 0; c < NK; ++c) {
+                const int f = NK * x + c, rb = f & 3, ks = f >> 2;  // f = ka_index(rb, ks)
+                const uint32_t r = (uint32_t)min(16 * rb + ln, n - 1);
+                s.ka[c] = *(const u32x4 *)(kb + r * (uint32_t)a.H_k * D + 32 * ks);
             }
-        } else {
-            float *ob = (float *)a.o + (size_t)t0 * a.H_v * D + (size_t)j * D + v0 + ln;
+            const u32x4 *ktb = (const u32x4 *)a.wsKT + ((size_t)(tile_base + lt) * a.H_k + qh) * (2 * NKB) * 64;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int r = 16 * h + 4 * lg + e;
-                if (r < n) ob[(uint32_t)r * a.H_v * D] = a.scale * oacc[e];
+            for (int c = 0; c < NK; ++c) s.kt[c] = ktb[(NK * x + c) * 64 + lane];
+            const u32x4 *tb = (const u32x4 *)(a.wsT + tv * TP_HALVES);
+#pragma unroll
+            for (int c = 0; c < 2; ++c) s.t[c] = tb[(t_first + min(c, nt - 1)) * 64 + lane];
+            const uint16_t *vb = a.v + ((size_t)t0 * a.H_v + j) * D + v0 + 8 * (lane & 1);
+            s.v = *(const u32x4 *)(vb + (uint32_t)min(16 * x + ((lane & 31) >> 1), n - 1) * (uint32_t)a.H_v * D);
+            s.g = a.wsGam[tv * 128 + 64 * min(x, 1) + lane];
+        };
+        auto stage = [&](const LoadSet<D> &s, auto bufc) __attribute__((always_inline)) {
+            constexpr int buf = decltype(bufc)::value;
+#pragma unroll
+            for (int c = 0; c < NK; ++c) {
+                sh.KA[buf][NK * x + c][lane] = s.ka[c];
+                sh.KT[buf][NK * x + c][lane] = s.kt[c];
+            }
+            sh.T[buf][t_first][lane] = s.t[0];
+            if (nt == 2) sh.T[buf][t_first + 1][lane] = s.t[1];
+            if (lane < 32) *(u32x4 *)(&sh.V[buf][(16 * x + (lane >> 1)) * 16 + 8 * (lane & 1)]) = s.v;
+            if (x < 2) sh.G[buf][x][lane] = s.g;
+        };
+        // tile t lives in register set t % 2 and LDS buffer t % 2.  Iteration it
+        // stages tile it + 1 and then loads tile it + 3 into the set just freed.
+        if (n_tiles > 0) {
+            LoadSet<D> s0, s1;
+            load(s0, 0);
+            load(s1, 1);
+            stage(s0, std::integral_constant<int, 0>());
+            load(s0, 2);
+            auto step = [&](int it, LoadSet<D> &s, auto bufc) __attribute__((always_inline)) {
+                lds_barrier();
+                if (it + 1 < n_tiles) stage(s, bufc);
+                load(s, it + 3);
+            };
+            for (int it = 0; it <= n_tiles; it += 2) {
+                step(it, s1, std::integral_constant<int, 1>());
+                if (it + 1 <= n_tiles) step(it + 1, s0, std::integral_constant<int, 0>());
             }
         }
-        if (lt + 1 < n_tiles) stage(nxt, buf ^ 1);
-    };
-
-    if (n_tiles > 0) {
-        if (state_wave) {
-            write_state(0);
-            for (int lt = 0; lt < n_tiles; ++lt) state_step(lt);
-        } else {
-            SeqTile<D> ta, tb, tc;
-            load_tile(ta, 0);
-            load_tile(tb, 1);
-            stage(ta, 0);
-            for (int lt = 0; lt < n_tiles; lt += 3) {
-                helper_step(lt, ta, tb, tc);
-                helper_step(lt + 1, tb, tc, ta);
-                helper_step(lt + 2, tc, ta, tb);
-            }
-        }
-    }
-
-    if (state_wave) {
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int vr = v0 + 4 * lg + e, c = h * (D / 4) + 16 * nb + ln;
-                a.state_out[sbase + (size_t)vr * D + c] = S[nb][e];
-            }
     }
 }
 
-// Sum of the per-row drift sums of every slice (fixed order) -> [n_frames][H_v][2].
+// Sum of the drift sums of every slice (fixed order) -> [n_frames][H_v][2].
 // Entries past the real frame count are zeroed.
 __global__ __launch_bounds__(256) void gdn_drift_finalize_kernel(const float *ws, float *out, int n_frames,
                                                                   int H_v, int n_split, Streams st,
@@ -658,9 +837,9 @@ __global__ __launch_bounds__(256) void gdn_drift_finalize_kernel(const float *ws
     const int f = idx / H_v;
     float num = 0.f, den = 0.f;
     if (f < real) {
-        for (int s = 0; s < n_split * 16; ++s) {
-            num += ws[((size_t)idx * n_split * 16 + s) * 2];
-            den += ws[((size_t)idx * n_split * 16 + s) * 2 + 1];
+        for (int s = 0; s < 2 * n_split; ++s) {
+            num += ws[((size_t)idx * 2 * n_split + s) * 2];
+            den += ws[((size_t)idx * 2 * n_split + s) * 2 + 1];
         }
     }
     out[(size_t)idx * 2] = num;
@@ -672,7 +851,7 @@ __global__ __launch_bounds__(256) void gdn_drift_finalize_kernel(const float *ws
 // ============================================================================
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_v, int d, int n_frames) {
+GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, int n_frames) {
     GdnWorkspace w{};
     w.tiles_max = (int)(((long long)T_total + 63LL * B) / 64);
     w.n_split = d / 16;
@@ -681,10 +860,12 @@ GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_v, int d, int n_fram
     off = align256(off + (size_t)w.tiles_max * H_v * TP_HALVES * sizeof(_Float16));
     w.offP = off;
     off = align256(off + (size_t)w.tiles_max * H_v * TP_HALVES * sizeof(_Float16));
+    w.offKT = off;
+    off = align256(off + (size_t)w.tiles_max * H_k * (d / 8) * 64 * 16);
     w.offGam = off;
-    off = align256(off + (size_t)w.tiles_max * H_v * 64 * sizeof(float));
+    off = align256(off + (size_t)w.tiles_max * H_v * 128 * sizeof(float));
     w.offDrift = off;
-    off = align256(off + (size_t)n_frames * H_v * w.n_split * 16 * 2 * sizeof(float));
+    off = align256(off + (size_t)n_frames * H_v * w.n_split * 2 * 2 * sizeof(float));
     w.total = off;
     return w;
 }
@@ -711,6 +892,7 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     a.wsT = p.wsT;
     a.wsP = p.wsP;
     a.wsGam = p.wsGam;
+    a.wsKT = p.wsKT;
     a.wsDrift = p.drift_partials ? p.wsDrift : nullptr;
     a.n_split = p.n_split;
 
