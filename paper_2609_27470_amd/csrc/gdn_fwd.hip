@@ -76,12 +76,15 @@ __device__ bool locate_tile(const Streams &s, int ti, int &t0, int &n) {
 }
 
 // ============================================================================
-// gdn_prep: one workgroup per (tile, v-head).  Every global load is issued
-// up front; K K^T and Q K^T run on bf16 matrix cores (fragments straight from
-// global memory, exact bf16 inputs, fp32 accumulation); the inverse of the
-// unit lower-triangular I + A is blocked in 16 x 16 blocks: the diagonal
-// blocks by forward substitution, the off-diagonal ones on fp32 matrix cores,
-// T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj, by distance from the diagonal.
+// gdn_prep: one workgroup per (tile, qk-head).  The K and Q rows of the tile
+// are loaded once as whole 16-byte chunks and staged in LDS; the Gram blocks
+// K K^T and Q K^T run on bf16 matrix cores (exact bf16 inputs, fp32
+// accumulation) and stay in registers; the K^T fragments of the sequential
+// kernel are written once per qk-head.  Then, for every v-head of the group
+// (its own gates): the inverse of the unit lower-triangular I + A is blocked
+// in 16 x 16 blocks, the diagonal blocks by forward substitution and the
+// off-diagonal ones on fp32 matrix cores, T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj,
+// by distance from the diagonal.
 // ============================================================================
 __device__ __forceinline__ f32x4 mfma_f32_16x16x4(float a, float b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -111,58 +114,55 @@ __device__ __forceinline__ int swz(int row) {
 template <int D>
 __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
     constexpr int KS = D / 32;   // 32-wide k-steps over the head dim
-    constexpr int ALD = 65;      // floats per LDS row of A and T
-    constexpr int PLD = 72;      // halves per LDS row of P
-    __shared__ float As[64 * ALD];
-    __shared__ float Ts[64 * ALD];
+    constexpr int CH = D / 8;    // 16-byte chunks per K or Q row
+    constexpr int NKB = D / 16;
+    constexpr int RPI = 64 / CH;  // rows per 64-lane row load
+    constexpr int NI = 16 / RPI;  // row loads per wave (16 rows each)
+    constexpr int ALD = 68;       // floats per LDS row of A and T (bank-conflict-free writes)
+    constexpr int PLD = 72;       // halves per LDS row of P
+    constexpr int RB = (64 * D * 2 > 64 * ALD * 4) ? 64 * D * 2 : 64 * ALD * 4;
+    // K and Q tiles while the Gram blocks are formed, then A and T
+    __shared__ __align__(16) char reg_k[RB], reg_q[RB];
     __shared__ float Ys[4][256];
     __shared__ __align__(16) _Float16 Ps[64 * PLD];
     __shared__ float gam_s[64], beta_s[64];
+    uint16_t *Kl = (uint16_t *)reg_k, *Ql = (uint16_t *)reg_q;
+    float *As = (float *)reg_k, *Ts = (float *)reg_q;
 
-    const int ti = blockIdx.x, j = blockIdx.y;
-    const int h = j / a.group;
+    const int ti = blockIdx.x, h = blockIdx.y;  // tile, qk-head
     int t0 = 0, n = 0;
     if (!locate_tile(a.st, ti, t0, n)) return;
-    // the wave index in a scalar register: branches on it are then plain jumps
-    // rather than masked code (matrix-core ops ignore the execution mask)
     const int tid = threadIdx.x, lane = tid & 63, ln = lane & 15, lg = lane >> 4;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const size_t tv = (size_t)ti * a.H_v + j;
-    const uint4 zero4 = make_uint4(0, 0, 0, 0);
 
-    // ---- loads: k rows of every 16-row block up to w, q rows of block w, gates
-    uint4 kf[4][KS], ka[KS], qa[KS];
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb) {
-        const int r = 16 * nb + ln;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            kf[nb][ks] = zero4;
-            if (nb <= w && r < n) kf[nb][ks] = *(const uint4 *)(a.k + ((size_t)(t0 + r) * a.H_k + h) * D + 32 * ks + 8 * lg);
-        }
-    }
+    // ---- K and Q rows 16 w .. 16 w + 15: whole 16-byte chunks, RPI rows per
+    // load; rows past a ragged tile's end are loaded clamped and zeroed here
     {
-        const int r = 16 * w + ln;
+        u32x4 kv[NI], qv[NI];
+        const uint16_t *kb = a.k + (size_t)t0 * a.H_k * D + (size_t)h * D;
+        const uint16_t *qb = a.q + (size_t)t0 * a.H_k * D + (size_t)h * D;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            const size_t off = ((size_t)(t0 + r) * a.H_k + h) * D + 32 * ks + 8 * lg;
-            qa[ks] = (r < n) ? *(const uint4 *)(a.q + off) : zero4;
-            ka[ks] = (r < n) ? *(const uint4 *)(a.k + off) : zero4;
+        for (int c = 0; c < NI; ++c) {
+            const int row = 16 * w + RPI * c + lane / CH, ch = lane % CH;
+            const uint32_t off = (uint32_t)min(row, n - 1) * (uint32_t)a.H_k * D + 8 * ch;
+            kv[c] = *(const u32x4 *)(kb + off);
+            qv[c] = *(const u32x4 *)(qb + off);
+        }
+#pragma unroll
+        for (int c = 0; c < NI; ++c) {
+            const int row = 16 * w + RPI * c + lane / CH, ch = lane % CH;
+            const u32x4 z = {0u, 0u, 0u, 0u};
+            *(u32x4 *)(&Kl[row * D + 8 * (ch ^ swz<D>(row))]) = row < n ? kv[c] : z;
+            *(u32x4 *)(&Ql[row * D + 8 * (ch ^ swz<D>(row))]) = row < n ? qv[c] : z;
         }
     }
-    // ---- K^T as A-fragments of the sequential kernel's state update, once per
-    // qk-head: fragment (kb, ks) = 2 kb + ks, lane (ln, lg), half i holds
-    // K[kappa(ks, lg, i)][sigma(kb, ln)] (token and dim relabellings of the
-    // sequential kernel), read from a K tile in LDS by transposing reads.
-    if (j % a.group == 0) {
-        constexpr int NKB = D / 16;
-        uint16_t *Kl = (uint16_t *)As;  // 64 x D bf16 fits in As
-        {
-            const int row = 16 * w + ln;
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) *(uint4 *)(&Kl[row * D + 8 * ((4 * ks + lg) ^ swz<D>(row))]) = ka[ks];
-        }
-        __syncthreads();
+    __syncthreads();
+
+    // ---- K^T as A-fragments of the sequential kernel's state update:
+    // fragment (kb, ks) = 2 kb + ks, lane (ln, lg), half i holds
+    // K[kappa(ks, lg, i)][sigma(kb, ln)] (the token and dim relabellings of the
+    // sequential kernel), by transposing reads of the K tile
+    {
         u32x4 *dst = (u32x4 *)a.wsKT + ((size_t)ti * a.H_k + h) * (2 * NKB) * 64;
 #pragma unroll
         for (int f = w; f < 2 * NKB; f += 4) {
@@ -172,136 +172,150 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
             dst[f * 64 + lane] = cat_u32x4(ds_read_tr16(&Kl[r0 * D + 8 * (ch ^ swz<D>(r0)) + half]),
                                            ds_read_tr16(&Kl[r1 * D + 8 * (ch ^ swz<D>(r1)) + half]));
         }
-        __syncthreads();
     }
 
-    float gv = 0.f, bv = 0.f;
-    if (w == 0 && lane < n) {
-        gv = a.g[(size_t)(t0 + lane) * a.H_v + j];
-        bv = a.beta[(size_t)(t0 + lane) * a.H_v + j];
-    }
-
-    // ---- gamma = inclusive prefix sum of g, in base-2 units
-    if (w == 0) {
-        float s = gv;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-            const float y = __shfl_up(s, off, 64);
-            if (lane >= off) s += y;
-        }
-        s *= 1.4426950408889634f;  // exp(gamma) = exp2(s)
-        gam_s[lane] = s;
-        beta_s[lane] = bv;
-        // padding rows have g = 0, so row 63 carries the tile's last gamma
-        const float s_last = __shfl(s, 63, 64);
-        a.wsGam[tv * 128 + lane] = __builtin_amdgcn_exp2f(s);
-        a.wsGam[tv * 128 + 64 + lane] = __builtin_amdgcn_exp2f(s_last - s);
-    }
-
-    // ---- Gram blocks of row block w: K K^T and Q K^T for column blocks nb <= w
+    // ---- Gram blocks of row block w: K K^T and Q K^T for column blocks nb <= w,
+    // fragments straight from LDS (a B fragment of K^T is an A fragment of K)
     f32x4 gk[4], gq[4];
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
         gk[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
         gq[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-        if (nb <= w) {
+    }
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                gk[nb] = mfma_bf16(as_bf16x8(ka[ks]), as_bf16x8(kf[nb][ks]), gk[nb]);
-                gq[nb] = mfma_bf16(as_bf16x8(qa[ks]), as_bf16x8(kf[nb][ks]), gq[nb]);
+    for (int ks = 0; ks < KS; ++ks) {
+        const int ra = 16 * w + ln, ca = 8 * ((4 * ks + lg) ^ swz<D>(ra));
+        const bf16x8 ak = as_bf16x8(*(const u32x4 *)(&Kl[ra * D + ca]));
+        const bf16x8 aq = as_bf16x8(*(const u32x4 *)(&Ql[ra * D + ca]));
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) {
+            if (nb <= w) {
+                const int rb = 16 * nb + ln;
+                const bf16x8 bk = as_bf16x8(*(const u32x4 *)(&Kl[rb * D + 8 * ((4 * ks + lg) ^ swz<D>(rb))]));
+                gk[nb] = mfma_bf16(ak, bk, gk[nb]);
+                gq[nb] = mfma_bf16(aq, bk, gq[nb]);
             }
         }
     }
-    __syncthreads();
+    __syncthreads();  // K and Q tiles are dead from here on (A and T reuse them)
 
-    // ---- A (strictly lower) and P (lower incl. diagonal), rows of block w
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int r = 16 * w + 4 * lg + e, i = 16 * nb + ln;
-            float av = 0.f, pv = 0.f;
-            if (nb <= w && i <= r) {
-                const float dri = exp2f(gam_s[r] - gam_s[i]);
-                pv = dri * gq[nb][e];
-                if (i < r) av = beta_s[r] * dri * gk[nb][e];
+    // ---- per v-head of the qk-head's group
+    for (int jj = 0; jj < a.group; ++jj) {
+        const int j = h * a.group + jj;
+        const size_t tv = (size_t)ti * a.H_v + j;
+
+        // gamma = inclusive prefix sum of g, in base-2 units
+        if (w == 0) {
+            float gv = 0.f, bv = 0.f;
+            if (lane < n) {
+                gv = a.g[(size_t)(t0 + lane) * a.H_v + j];
+                bv = a.beta[(size_t)(t0 + lane) * a.H_v + j];
             }
-            As[r * ALD + i] = av;
-            Ps[r * PLD + i] = (_Float16)pv;
+            float s = gv;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const float y = __shfl_up(s, off, 64);
+                if (lane >= off) s += y;
+            }
+            s *= 1.4426950408889634f;  // exp(gamma) = exp2(s)
+            gam_s[lane] = s;
+            beta_s[lane] = bv;
+            // padding rows have g = 0, so row 63 carries the tile's last gamma
+            const float s_last = __shfl(s, 63, 64);
+            a.wsGam[tv * 128 + lane] = __builtin_amdgcn_exp2f(s);
+            a.wsGam[tv * 128 + 64 + lane] = __builtin_amdgcn_exp2f(s_last - s);
         }
-    }
-    __syncthreads();
+        __syncthreads();
 
-    // ---- diagonal blocks (lane = 16 * block + column)
-    if (w == 0) {
-        const int o = 16 * (lane >> 4), c = lane & 15;
-        float x[16];
+        // A (strictly lower) and P (lower incl. diagonal), rows of block w
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            float s = (r == c) ? 1.f : 0.f;
+        for (int nb = 0; nb < 4; ++nb) {
 #pragma unroll
-            for (int i = 0; i < r; ++i) s -= As[(o + r) * ALD + o + i] * x[i];
-            x[r] = s;
+            for (int e = 0; e < 4; ++e) {
+                const int r = 16 * w + 4 * lg + e, i = 16 * nb + ln;
+                float av = 0.f, pv = 0.f;
+                if (nb <= w && i <= r) {
+                    const float dri = __builtin_amdgcn_exp2f(gam_s[r] - gam_s[i]);
+                    pv = dri * gq[nb][e];
+                    if (i < r) av = beta_s[r] * dri * gk[nb][e];
+                }
+                As[r * ALD + i] = av;
+                Ps[r * PLD + i] = (_Float16)pv;
+            }
         }
+        __syncthreads();
+
+        // diagonal blocks (wave 0, lane = 16 * block + column); P fragments (waves 1-3)
+        if (w == 0) {
+            const int o = 16 * (lane >> 4), c = lane & 15;
+            float x[16];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) Ts[(o + r) * ALD + o + c] = x[r];
-    } else {
-        // P (fp16) -> workspace in fragment order, 16 B per lane
-        for (int c = tid - 64; c < 6 * 64; c += 192) {
+            for (int r = 0; r < 16; ++r) {
+                float s = (r == c) ? 1.f : 0.f;
+#pragma unroll
+                for (int i = 0; i < r; ++i) s -= As[(o + r) * ALD + o + i] * x[i];
+                x[r] = s;
+            }
+#pragma unroll
+            for (int r = 0; r < 16; ++r) Ts[(o + r) * ALD + o + c] = x[r];
+        } else {
+            for (int c = tid - 64; c < 6 * 64; c += 192) {
+                const int f = c >> 6, l = c & 63;
+                const int fw = f < 2 ? f : 2 + ((f - 2) >> 1), fks = f < 2 ? 0 : ((f - 2) & 1);
+                const int r = 16 * fw + (l & 15), c4 = 32 * fks + 4 * (l >> 4);
+                uint2 *dst = (uint2 *)(a.wsP + tv * TP_HALVES + f * FRAG_HALVES + l * 8);
+                dst[0] = *(const uint2 *)(&Ps[r * PLD + c4]);
+                dst[1] = *(const uint2 *)(&Ps[r * PLD + c4 + 16]);
+            }
+        }
+        __syncthreads();
+
+        // off-diagonal blocks.  16x16x4 fp32 fragments: A lane = [ln][lg],
+        // B lane = [lg][ln], C lane = [4 lg + e][ln].
+        for (int d = 1; d <= 3; ++d) {
+            const int p = w;  // pair handled by this wave: block row bi = p + d, column bj = p
+            if (p + d <= 3) {
+                const int bi = p + d, bj = p;
+                f32x4 y = {0.f, 0.f, 0.f, 0.f};
+                for (int kb = bj; kb < bi; ++kb) {
+#pragma unroll
+                    for (int s = 0; s < 4; ++s) {
+                        const float av = As[(16 * bi + ln) * ALD + 16 * kb + 4 * s + lg];
+                        const float tb = Ts[(16 * kb + 4 * s + lg) * ALD + 16 * bj + ln];
+                        y = mfma_f32_16x16x4(av, tb, y);
+                    }
+                }
+                float *yw = Ys[w];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) yw[(4 * lg + e) * 16 + ln] = y[e];
+                __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's Y is in LDS
+                f32x4 t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int s = 0; s < 4; ++s) {
+                    const float ta = Ts[(16 * bi + ln) * ALD + 16 * bi + 4 * s + lg];
+                    const float yb = yw[(4 * s + lg) * 16 + ln];
+                    t = mfma_f32_16x16x4(ta, yb, t);
+                }
+#pragma unroll
+                for (int e = 0; e < 4; ++e) Ts[(16 * bi + 4 * lg + e) * ALD + 16 * bj + ln] = -t[e];
+            }
+            __syncthreads();
+        }
+
+        // T diag(beta) (fp16, zero above the diagonal) in fragment order
+        for (int c = tid; c < 6 * 64; c += 256) {
             const int f = c >> 6, l = c & 63;
             const int fw = f < 2 ? f : 2 + ((f - 2) >> 1), fks = f < 2 ? 0 : ((f - 2) & 1);
             const int r = 16 * fw + (l & 15), c4 = 32 * fks + 4 * (l >> 4);
-            uint2 *dst = (uint2 *)(a.wsP + tv * TP_HALVES + f * FRAG_HALVES + l * 8);
-            dst[0] = *(const uint2 *)(&Ps[r * PLD + c4]);
-            dst[1] = *(const uint2 *)(&Ps[r * PLD + c4 + 16]);
-        }
-    }
-    __syncthreads();
-
-    // ---- off-diagonal blocks.  16x16x4 fp32 fragments: A lane = [ln][lg],
-    // B lane = [lg][ln], C lane = [4 lg + e][ln].
-    for (int d = 1; d <= 3; ++d) {
-        const int p = w;  // pair handled by this wave: block row bi = p + d, column bj = p
-        if (p + d <= 3) {
-            const int bi = p + d, bj = p;
-            f32x4 y = {0.f, 0.f, 0.f, 0.f};
-            for (int kb = bj; kb < bi; ++kb) {
+            half8 tv8;
 #pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    const float av = As[(16 * bi + ln) * ALD + 16 * kb + 4 * s + lg];
-                    const float tb = Ts[(16 * kb + 4 * s + lg) * ALD + 16 * bj + ln];
-                    y = mfma_f32_16x16x4(av, tb, y);
-                }
+            for (int e = 0; e < 8; ++e) {
+                const int i = c4 + 16 * (e >> 2) + (e & 3);
+                tv8[e] = (_Float16)((i <= r) ? Ts[r * ALD + i] * beta_s[i] : 0.f);
             }
-            float *yw = Ys[w];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) yw[(4 * lg + e) * 16 + ln] = y[e];
-            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's Y is in LDS
-            f32x4 t = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const float ta = Ts[(16 * bi + ln) * ALD + 16 * bi + 4 * s + lg];
-                const float yb = yw[(4 * s + lg) * 16 + ln];
-                t = mfma_f32_16x16x4(ta, yb, t);
-            }
-#pragma unroll
-            for (int e = 0; e < 4; ++e) Ts[(16 * bi + 4 * lg + e) * ALD + 16 * bj + ln] = -t[e];
+            *(uint4 *)(a.wsT + tv * TP_HALVES + f * FRAG_HALVES + l * 8) = as_uint4(tv8);
         }
-        __syncthreads();
-    }
-
-    // ---- T diag(beta) (fp16, zero above the diagonal) in fragment order
-    for (int c = tid; c < 6 * 64; c += 256) {
-        const int f = c >> 6, l = c & 63;
-        const int fw = f < 2 ? f : 2 + ((f - 2) >> 1), fks = f < 2 ? 0 : ((f - 2) & 1);
-        const int r = 16 * fw + (l & 15), c4 = 32 * fks + 4 * (l >> 4);
-        half8 tv8;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int i = c4 + 16 * (e >> 2) + (e & 3);
-            tv8[e] = (_Float16)((i <= r) ? Ts[r * ALD + i] * beta_s[i] : 0.f);
-        }
-        *(uint4 *)(a.wsT + tv * TP_HALVES + f * FRAG_HALVES + l * 8) = as_uint4(tv8);
+        __syncthreads();  // before the next v-head reuses A, T, P and the gates
     }
 }
 
@@ -897,7 +911,7 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     a.n_split = p.n_split;
 
     if (p.tiles_max > 0) {
-        hipLaunchKernelGGL(gdn_prep_kernel<D>, dim3(p.tiles_max, p.H_v), dim3(256), 0, stream, a);
+        hipLaunchKernelGGL(gdn_prep_kernel<D>, dim3(p.tiles_max, p.H_k), dim3(256), 0, stream, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
