@@ -125,7 +125,8 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
     __shared__ __align__(16) char reg_k[RB], reg_q[RB];
     __shared__ float Ys[4][256];
     __shared__ __align__(16) _Float16 Ps[64 * PLD];
-    __shared__ float gam_s[64], beta_s[64];
+    __shared__ __align__(16) float gam_s[64];
+    __shared__ __align__(16) float beta_s[64];
     uint16_t *Kl = (uint16_t *)reg_k, *Ql = (uint16_t *)reg_q;
     float *As = (float *)reg_k, *Ts = (float *)reg_q;
 
@@ -134,6 +135,19 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
     if (!locate_tile(a.st, ti, t0, n)) return;
     const int tid = threadIdx.x, lane = tid & 63, ln = lane & 15, lg = lane >> 4;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+    // ---- gates of the group's v-heads (wave 0, lane = token), loaded first
+    constexpr int MAXG = 2;  // v-heads per qk-head handled with prefetched gates (more: loaded in turn)
+    float gpre[MAXG], bpre[MAXG];
+    if (w == 0) {
+        const uint32_t r = (uint32_t)min(lane, n - 1);
+#pragma unroll
+        for (int jj = 0; jj < MAXG; ++jj) {
+            const int j = h * a.group + min(jj, a.group - 1);
+            gpre[jj] = a.g[(size_t)(t0 + r) * a.H_v + j];
+            bpre[jj] = a.beta[(size_t)(t0 + r) * a.H_v + j];
+        }
+    }
 
     // ---- K and Q rows 16 w .. 16 w + 15: whole 16-byte chunks, RPI rows per
     // load; rows past a ragged tile's end are loaded clamped and zeroed here
@@ -207,10 +221,18 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
         // gamma = inclusive prefix sum of g, in base-2 units
         if (w == 0) {
             float gv = 0.f, bv = 0.f;
-            if (lane < n) {
-                gv = a.g[(size_t)(t0 + lane) * a.H_v + j];
-                bv = a.beta[(size_t)(t0 + lane) * a.H_v + j];
+            if (jj < MAXG) {
+#pragma unroll
+                for (int q = 0; q < MAXG; ++q)
+                    if (q == jj) {
+                        gv = gpre[q];
+                        bv = bpre[q];
+                    }
+            } else {
+                gv = a.g[(size_t)(t0 + min(lane, n - 1)) * a.H_v + j];
+                bv = a.beta[(size_t)(t0 + min(lane, n - 1)) * a.H_v + j];
             }
+            if (lane >= n) gv = bv = 0.f;
             float s = gv;
 #pragma unroll
             for (int off = 1; off < 64; off <<= 1) {
@@ -228,19 +250,27 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
         __syncthreads();
 
         // A (strictly lower) and P (lower incl. diagonal), rows of block w
+        {
+            const float4 gr = *(const float4 *)(&gam_s[16 * w + 4 * lg]);
+            const float4 br = *(const float4 *)(&beta_s[16 * w + 4 * lg]);
+            const float grv[4] = {gr.x, gr.y, gr.z, gr.w}, brv[4] = {br.x, br.y, br.z, br.w};
+            float gi[4];
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb) {
+            for (int nb = 0; nb < 4; ++nb) gi[nb] = gam_s[16 * nb + ln];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int r = 16 * w + 4 * lg + e, i = 16 * nb + ln;
-                float av = 0.f, pv = 0.f;
-                if (nb <= w && i <= r) {
-                    const float dri = __builtin_amdgcn_exp2f(gam_s[r] - gam_s[i]);
-                    pv = dri * gq[nb][e];
-                    if (i < r) av = beta_s[r] * dri * gk[nb][e];
+            for (int nb = 0; nb < 4; ++nb) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int r = 16 * w + 4 * lg + e, i = 16 * nb + ln;
+                    float av = 0.f, pv = 0.f;
+                    if (nb <= w && i <= r) {
+                        const float dri = __builtin_amdgcn_exp2f(grv[e] - gi[nb]);
+                        pv = dri * gq[nb][e];
+                        if (i < r) av = brv[e] * dri * gk[nb][e];
+                    }
+                    As[r * ALD + i] = av;
+                    Ps[r * PLD + i] = (_Float16)pv;
                 }
-                As[r * ALD + i] = av;
-                Ps[r * PLD + i] = (_Float16)pv;
             }
         }
         __syncthreads();
