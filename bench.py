@@ -18,6 +18,7 @@ stream the calls are launched on.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -242,12 +243,17 @@ def main():
     achieved_gbs = bytes_ / (gdn_ms * 1e-3) / 1e9
     achieved_tflops = flops / (gdn_ms * 1e-3) / 1e12
 
+    # HBM bytes per launch from the committed counter runs (FETCH_SIZE + WRITE_SIZE,
+    # copy-calibrated), used only while the kernel source is the one measured
     traffic = None
     tf = os.path.join(ROOT, "profiles", "gdn_chunk_fwd_single_layer_traffic.json")
-    if os.path.exists(tf):
+    src = os.path.join(ROOT, "paper_2609_27470_amd", "csrc", "gdn_fwd.hip")
+    if os.path.exists(tf) and os.path.exists(src):
         try:
-            traffic = json.load(open(tf)).get("bytes_per_launch")
-        except Exception:
+            rec = json.load(open(tf))
+            if rec.get("source_sha256") == hashlib.sha256(open(src, "rb").read()).hexdigest():
+                traffic = rec.get("bytes_per_launch")
+        except (OSError, ValueError):
             traffic = None
 
     out = {
