@@ -118,7 +118,6 @@ ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k,
     p.wsT = (_Float16 *)(ws + lay.offT);
     p.wsP = (_Float16 *)(ws + lay.offP);
     p.wsGam = (float *)(ws + lay.offGam);
-    p.wsKT = (uint16_t *)(ws + lay.offKT);
     p.wsDrift = (float *)(ws + lay.offDrift);
     p.tiles_max = lay.tiles_max;
     p.n_split = lay.n_split;

@@ -52,7 +52,6 @@ struct GdnArgs {
     float *snapshots;
     _Float16 *wsT, *wsP;
     float *wsGam, *wsDrift;
-    uint16_t *wsKT;
     int n_split;
 };
 
@@ -79,8 +78,7 @@ __device__ bool locate_tile(const Streams &s, int ti, int &t0, int &n) {
 // gdn_prep: one workgroup per (tile, qk-head).  The K and Q rows of the tile
 // are loaded once as whole 16-byte chunks and staged in LDS; the Gram blocks
 // K K^T and Q K^T run on bf16 matrix cores (exact bf16 inputs, fp32
-// accumulation) and stay in registers; the K^T fragments of the sequential
-// kernel are written once per qk-head.  Then, for every v-head of the group
+// accumulation) and stay in registers.  Then, for every v-head of the group
 // (its own gates): the inverse of the unit lower-triangular I + A is blocked
 // in 16 x 16 blocks, the diagonal blocks by forward substitution and the
 // off-diagonal ones on fp32 matrix cores, T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj,
@@ -171,22 +169,6 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
         }
     }
     __syncthreads();
-
-    // ---- K^T as A-fragments of the sequential kernel's state update:
-    // fragment (kb, ks) = 2 kb + ks, lane (ln, lg), half i holds
-    // K[kappa(ks, lg, i)][sigma(kb, ln)] (the token and dim relabellings of the
-    // sequential kernel), by transposing reads of the K tile
-    {
-        u32x4 *dst = (u32x4 *)a.wsKT + ((size_t)ti * a.H_k + h) * (2 * NKB) * 64;
-#pragma unroll
-        for (int f = w; f < 2 * NKB; f += 4) {
-            const int kb = f >> 1, ks = f & 1;
-            const int r0 = 32 * ks + 4 * lg + (ln >> 2), r1 = r0 + 16;
-            const int ch = 4 * (kb >> 1) + (ln & 3), half = 4 * (kb & 1);
-            dst[f * 64 + lane] = cat_u32x4(ds_read_tr16(&Kl[r0 * D + 8 * (ch ^ swz<D>(r0)) + half]),
-                                           ds_read_tr16(&Kl[r1 * D + 8 * (ch ^ swz<D>(r1)) + half]));
-        }
-    }
 
     // ---- Gram blocks of row block w: K K^T and Q K^T for column blocks nb <= w,
     // fragments straight from LDS (a B fragment of K^T is an A fragment of K)
@@ -365,13 +347,15 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
 //   waves 2 and 3, output:  one tile behind, O = diag(Gamma) Q S0^T + P E for
 //                    row blocks {0, 1} and {2, 3}; they load q, P and Gamma
 //                    themselves.
-//   waves 4 - 7, loaders: each loads a quarter of the K and K^T fragments,
-//                    T diag(beta), v and the decay factors of a tile three tiles
-//                    ahead and stages it in LDS one tile ahead.
+//   waves 4 - 7, loaders: each loads a quarter of the K rows, T diag(beta),
+//                    v rows and the decay factors of a tile three tiles ahead
+//                    and stages it in LDS one tile ahead.  The state waves read
+//                    K as rows (A operand of K S0^T) and, by transposing reads,
+//                    as K^T (A operand of the state update).
 // All eight waves meet at one barrier per tile.  A single wave moves data
 // from L2 and from LDS at a limited rate, which is why the chain is shared by
-// two waves, every tile is loaded by four waves, and every operand is staged
-// in fragment order (contiguous 16-byte accesses).
+// two waves, every tile is loaded by four waves, and operands move as whole
+// 16-byte pieces.
 //
 // Fragment bookkeeping.  The C layout of v_mfma_f32_16x16x32 (lane (ln, lg)
 // holds rows 4 lg + e of column ln) of two row blocks 2 s and 2 s + 1 is,
@@ -385,8 +369,8 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
 //   token rows  (R, E, O):  C rows stay in order (row block rb, row 4 lg + e
 //     is token 16 rb + 4 lg + e), so as a B operand element i of k-step ks
 //     is token kappa(ks, lg, i) = 32 ks + 16 (i / 4) + 4 lg + i % 4; the
-//     prep kernel writes T diag(beta), P and the K^T fragments with their
-//     token columns in that order.
+//     prep kernel writes T diag(beta) and P with their token columns in that
+//     order, and the K^T fragments are read from LDS in it.
 //
 // Precision: k and q stay bf16 (as given) and meet the fp32 state through
 // bf16 matrix-core products against a two-term bf16 split of the state
@@ -438,8 +422,7 @@ __device__ __forceinline__ half8 to_half8(const f32x4 &a, const f32x4 &b) {
 template <int D>
 struct SeqShared {
     static constexpr int KS = D / 32, NKB = D / 16;
-    u32x4 KA[2][4 * KS][64];   // K as A operand: fragment (rb, ks) = 4 ks + rb... see ka_index
-    u32x4 KT[2][2 * NKB][64];  // K^T as A operand: fragment (kb, ks) = 2 kb + ks
+    uint16_t K[2][64 * D];     // K tile, row-major, 16-byte chunks XOR-swizzled by row (swz)
     u32x4 T[2][6][64];         // T diag(beta) A-fragments
     uint16_t V[2][64 * 16];    // v[token][v0 .. v0 + 15] (bf16, read transposed)
     uint32_t Ost[2][32 * 16];  // per output wave: its 32 rows of o, staged for 16-byte row stores
@@ -450,16 +433,15 @@ struct SeqShared {
     u32x4 E[2][2][64];         // E as B operand (fp16)
     int xflag[2];              // tiles whose half of K S0^T each state wave has published
 };
-__host__ __device__ constexpr int ka_index(int rb, int ks) { return 4 * ks + rb; }
 
-// One loader's quarter of a tile: K fragments ka_index = 4 x .. 4 x + 3 (D = 128;
-// two per loader for D = 64), K^T fragments likewise, T diag(beta) fragments
-// {2 x, 2 x + 1} for x < 2 and {4 + x - 2} otherwise, v of row block rb = x,
-// and Gamma (x = 0) or D_last (x = 1).
+// One loader's quarter of a tile: K rows 16 x .. 16 x + 15 (whole 16-byte
+// chunks, 64 / (D / 8) rows per load), T diag(beta) fragments {2 x, 2 x + 1}
+// for x < 2 and {4 + x - 2} otherwise, v rows 16 x .. 16 x + 15, and Gamma
+// (x = 0) or D_last (x = 1).
 template <int D>
 struct LoadSet {
-    static constexpr int NK = D / 32;  // K and K^T fragments per loader
-    u32x4 ka[NK], kt[NK];
+    static constexpr int NK = D / 32;  // row loads of K per loader
+    u32x4 k[NK];
     u32x4 t[2];
     u32x4 v;        // v[16 x + lane / 2][v0 + 8 (lane % 2) .. + 7] (lanes >= 32 repeat)
     float g;        // Gamma (x = 0) or D_last (x = 1) of token lane
@@ -574,10 +556,18 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             half8 tf[6];
             float4 gam4[4], dl4[4];
             v4i16 vv4[4];
+            // K^T fragments by transposing reads: source lane (ln, lg) addresses token
+            // 32 ks + 16 r + 4 lg + ln / 4 and dims 32 (kb / 2) + 8 (ln % 4) + 4 (kb % 2) .. + 3
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-                for (int c = 0; c < HKB; ++c) ktf[ks][c] = as_bf16x8(sh.KT[buf][2 * (hh * HKB + c) + ks][lane]);
+                for (int c = 0; c < HKB; ++c) {
+                    const int kb = hh * HKB + c;
+                    const int r0 = 32 * ks + 4 * lg + (ln >> 2), r1 = r0 + 16;
+                    const int ch = 4 * (kb >> 1) + (ln & 3), half = 4 * (kb & 1);
+                    ktf[ks][c] = __builtin_bit_cast(bf16x8, cat_u32x4(ds_read_tr16(&sh.K[buf][r0 * D + 8 * (ch ^ swz<D>(r0)) + half]),
+                                                                      ds_read_tr16(&sh.K[buf][r1 * D + 8 * (ch ^ swz<D>(r1)) + half])));
+                }
 #pragma unroll
             for (int f = 0; f < 6; ++f) tf[f] = as_half8(sh.T[buf][f][lane]);
 #pragma unroll
@@ -596,7 +586,10 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             for (int c = 0; c < HKS; ++c) {
                 bf16x8 ka[4];
 #pragma unroll
-                for (int rb = 0; rb < 4; ++rb) ka[rb] = as_bf16x8(sh.KA[buf][ka_index(rb, hh * HKS + c)][lane]);
+                for (int rb = 0; rb < 4; ++rb) {
+                    const int row = 16 * rb + ln;
+                    ka[rb] = as_bf16x8(*(const u32x4 *)(&sh.K[buf][row * D + 8 * ((4 * (hh * HKS + c) + lg) ^ swz<D>(row))]));
+                }
 #pragma unroll
                 for (int rb = 0; rb < 4; ++rb) acc[rb] = mfma_bf16(ka[rb], as_bf16x8(shi[c]), acc[rb]);
 #pragma unroll
@@ -816,16 +809,13 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             const int lt = min(lt_, n_tiles - 1);  // clamped: every call issues the same loads
             const int t0 = st + TILE * lt, n = min(TILE, en - t0);
             const size_t tv = (size_t)(tile_base + lt) * a.H_v + j;
-            const uint16_t *kb = a.k + (size_t)t0 * a.H_k * D + (size_t)qh * D + 8 * lg;
+            constexpr int CH = D / 8, RPI = 64 / CH;
+            const uint16_t *kb = a.k + (size_t)t0 * a.H_k * D + (size_t)qh * D + 8 * (lane % CH);
 #pragma unroll
             for (int c = 0; c < NK; ++c) {
-                const int f = NK * x + c, rb = f & 3, ks = f >> 2;  // f = ka_index(rb, ks)
-                const uint32_t r = (uint32_t)min(16 * rb + ln, n - 1);
-                s.ka[c] = *(const u32x4 *)(kb + r * (uint32_t)a.H_k * D + 32 * ks);
+                const uint32_t r = (uint32_t)min(16 * x + RPI * c + lane / CH, n - 1);
+                s.k[c] = *(const u32x4 *)(kb + r * (uint32_t)a.H_k * D);
             }
-            const u32x4 *ktb = (const u32x4 *)a.wsKT + ((size_t)(tile_base + lt) * a.H_k + qh) * (2 * NKB) * 64;
-#pragma unroll
-            for (int c = 0; c < NK; ++c) s.kt[c] = ktb[(NK * x + c) * 64 + lane];
             const u32x4 *tb = (const u32x4 *)(a.wsT + tv * TP_HALVES);
 #pragma unroll
             for (int c = 0; c < 2; ++c) s.t[c] = tb[(t_first + min(c, nt - 1)) * 64 + lane];
@@ -835,10 +825,11 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
         };
         auto stage = [&](const LoadSet<D> &s, auto bufc) __attribute__((always_inline)) {
             constexpr int buf = decltype(bufc)::value;
+            constexpr int CH = D / 8, RPI = 64 / CH;
 #pragma unroll
             for (int c = 0; c < NK; ++c) {
-                sh.KA[buf][NK * x + c][lane] = s.ka[c];
-                sh.KT[buf][NK * x + c][lane] = s.kt[c];
+                const int row = 16 * x + RPI * c + lane / CH, ch = lane % CH;
+                *(u32x4 *)(&sh.K[buf][row * D + 8 * (ch ^ swz<D>(row))]) = s.k[c];
             }
             sh.T[buf][t_first][lane] = s.t[0];
             if (nt == 2) sh.T[buf][t_first + 1][lane] = s.t[1];
@@ -904,8 +895,6 @@ GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, i
     off = align256(off + (size_t)w.tiles_max * H_v * TP_HALVES * sizeof(_Float16));
     w.offP = off;
     off = align256(off + (size_t)w.tiles_max * H_v * TP_HALVES * sizeof(_Float16));
-    w.offKT = off;
-    off = align256(off + (size_t)w.tiles_max * H_k * (d / 8) * 64 * 16);
     w.offGam = off;
     off = align256(off + (size_t)w.tiles_max * H_v * 128 * sizeof(float));
     w.offDrift = off;
@@ -936,7 +925,6 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     a.wsT = p.wsT;
     a.wsP = p.wsP;
     a.wsGam = p.wsGam;
-    a.wsKT = p.wsKT;
     a.wsDrift = p.drift_partials ? p.wsDrift : nullptr;
     a.n_split = p.n_split;
 

@@ -25,14 +25,13 @@ struct GdnLaunch {
     _Float16 *wsP;      // [tiles_max][H_v][6][64][8]  D (.) tril(Q K^T), fp16 A-fragments
     float *wsGam;       // [tiles_max][H_v][2][64]   Gamma_r = exp(gamma_r), D_last,r = exp(gamma_last - gamma_r)
     float *wsDrift;     // [n_frames][H_v][n_split][2][2] (one pair per half slice)
-    uint16_t *wsKT;     // [tiles_max][H_k][2 d/16][64][8] K^T bf16 A-fragments
     int tiles_max;
     int n_split;        // d_v slices of 16 per (stream, v-head)
 };
 
 // Workspace layout shared by the size query and the launcher.
 struct GdnWorkspace {
-    size_t offT, offP, offKT, offGam, offDrift, total;
+    size_t offT, offP, offGam, offDrift, total;
     int tiles_max, n_split;
 };
 GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, int n_frames);

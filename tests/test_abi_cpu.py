@@ -52,9 +52,8 @@ def test_gdn_workspace_size(ds):
     nb = ds.gdn_workspace_bytes(s)
     tiles = 512
     per = 2 * 6 * 64 * 8 * 2 + 128 * 4     # T and P fragments (fp16) + decay factors per (tile, v-head)
-    kt = 16 * 64 * 8 * 2                   # K^T fragments (bf16) per (tile, qk-head)
-    assert nb >= tiles * (32 * per + 16 * kt)
-    assert nb <= tiles * (32 * per + 16 * kt) + 32 * 32 * 8 * 2 * 2 * 4 + 4096   # + drift sums per half slice
+    assert nb >= tiles * 32 * per
+    assert nb <= tiles * 32 * per + 32 * 32 * 8 * 2 * 2 * 4 + 4096   # + drift sums per half slice
     bad = ds.gdn_shape([64], 1, 1, 96, 64)
     assert ds.gdn_workspace_bytes(bad) == 0
 
