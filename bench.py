@@ -239,6 +239,26 @@ def main():
     nodrift_ms = float(np.median(t_without))
     drift_overhead = 100.0 * (withdrift_ms / nodrift_ms - 1.0)
 
+    # the unfused alternative (Section 3.2 as the paper measures it): at every
+    # frame boundary copy the state, and after the frame take the two norms
+    # with deltas_drift_states -- one copy and one call per frame of the stream
+    s_before = torch.empty_like(state)
+    parts_u = torch.empty((1, 1, H_V, 2), dtype=torch.float32, device=dev)
+
+    def drift_unfused():
+        for _ in range(n_frames):
+            s_before.copy_(state)
+            ds.deltas_drift_states(s_before.view(1, 1, H_V, D, D), state.view(1, 1, H_V, D, D), partials=parts_u)
+
+    drift_unfused()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        drift_unfused()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    unfused_ms = e0.elapsed_time(e1) / reps
+
     flops, bytes_ = algorithmic_work(T, H_K, H_V, D)
     achieved_gbs = bytes_ / (gdn_ms * 1e-3) / 1e9
     achieved_tflops = flops / (gdn_ms * 1e-3) / 1e12
@@ -285,6 +305,8 @@ def main():
         "mfma_util_pct": 100.0 * achieved_tflops / MFMA_PEAK_TFLOPS,
         "algorithmic_tflops": achieved_tflops,
         "drift_overhead_pct": drift_overhead,
+        "drift_unfused_ms": unfused_ms,
+        "drift_unfused_overhead_pct": 100.0 * unfused_ms / nodrift_ms,
         "evict_moved_rows_mean": float(moved_rows.mean()),
         "evict_gather_gbs": float((2 * moved_bytes).mean() / (evict_ms * 1e-3) / 1e9),
         "drift_overhead_paper_pct": 1.9,

@@ -139,6 +139,23 @@ ds_status deltas_drift(const float *partials, int32_t L, int32_t F, int32_t H_v,
                        float *scores, void *stream);
 
 /* ------------------------------------------------------------------------
+ * deltas_drift_states -- drift sums from two copies of the state
+ * ------------------------------------------------------------------------
+ * The unfused form of the sums behind Eq. 3 (Section 3.2): the way the paper
+ * measures the signal, by keeping a copy of every layer's state before a
+ * frame and taking two norms after it.  For every (l, b, j):
+ *     partials[l][b][j][0] = ||S_after - S_before||_F^2
+ *     partials[l][b][j][1] = ||S_before||_F^2
+ * S_before, S_after: fp32 [L][B][H_v][d_v][d_k], 16-byte aligned, d_v d_k a
+ * multiple of 4.  partials: fp32 [L][B][H_v][2] (the layout deltas_drift
+ * reads with F = B).  Each sum is accumulated in fp32 per thread and combined
+ * in a fixed order in fp64.  Provided as the cost reference for the fused sums
+ * of gdn_chunk_fwd.
+ */
+ds_status deltas_drift_states(const float *S_before, const float *S_after, int32_t L, int32_t B, int32_t H_v,
+                              int32_t d_v, int32_t d_k, float *partials, void *stream);
+
+/* ------------------------------------------------------------------------
  * kv_evict_topk -- one eviction step of Algorithm 1 (Section 3.3)
  * ------------------------------------------------------------------------
  * The cache holds `len` tokens (host-known) in slots [0, len) of every

@@ -159,6 +159,17 @@ def drift_scores(partials, mode=LAYER_FROB):
     return out
 
 
+def drift_states(S_before, S_after):
+    """The two sums behind Eq. 3 (Section 3.2) from two copies of the state:
+    num = ||S_after - S_before||_F^2 and den = ||S_before||_F^2 per head, for
+    arrays [..., d_v, d_k] -> [..., 2], in fp64."""
+    b = np.asarray(S_before, dtype=np.float64)
+    a = np.asarray(S_after, dtype=np.float64)
+    num = np.sum((a - b) ** 2, axis=(-2, -1))
+    den = np.sum(b ** 2, axis=(-2, -1))
+    return np.stack([num, den], axis=-1)
+
+
 def select_keep(chunk_id, pos, chunk_scores, length, M, n_sink, n_window, n_buckets):
     """Cache slots kept by one eviction step (Section 3.3, Algorithm 1).
 

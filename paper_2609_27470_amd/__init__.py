@@ -21,7 +21,7 @@ LAYER_FROB, HEAD_MEAN, PER_HEAD = 0, 1, 2
 
 EXPORTED = [
     "ds_status_string", "ds_last_error", "ds_gdn_workspace_bytes", "gdn_chunk_fwd", "deltas_drift",
-    "ds_kv_workspace_bytes", "kv_evict_topk", "ds_kv_device_status",
+    "deltas_drift_states", "ds_kv_workspace_bytes", "kv_evict_topk", "ds_kv_device_status",
 ]
 
 
@@ -62,6 +62,8 @@ def lib():
         L.gdn_chunk_fwd.restype = I32
         L.deltas_drift.argtypes = [P, I32, I32, I32, I32, P, P]
         L.deltas_drift.restype = I32
+        L.deltas_drift_states.argtypes = [P, P, I32, I32, I32, I32, I32, P, P]
+        L.deltas_drift_states.restype = I32
         L.ds_kv_workspace_bytes.argtypes = [ctypes.POINTER(KvShape)]
         L.ds_kv_workspace_bytes.restype = SZ
         L.kv_evict_topk.argtypes = [ctypes.POINTER(KvShape), P, P, P, P, P, I32, I32, I32, I32, I32, I32, P,
@@ -152,6 +154,19 @@ def deltas_drift(partials, mode=LAYER_FROB, scores=None, stream=None):
         scores = torch.empty(shape, dtype=torch.float32, device=partials.device)
     _check(lib().deltas_drift(_ptr(partials), L, F, H, mode, _ptr(scores), _stream(stream)))
     return scores
+
+
+def deltas_drift_states(S_before, S_after, partials=None, stream=None):
+    """Drift sums (||S_after - S_before||^2, ||S_before||^2) per state head from two
+    fp32 tensors [L][B][H_v][d_v][d_k] (see deltas_drift_states in deltas.h).
+    Returns partials [L][B][H_v][2]."""
+    if S_before.shape != S_after.shape or S_before.dim() != 5:
+        raise ValueError("S_before and S_after must both be [L][B][H_v][d_v][d_k]")
+    L, B, H, dv, dk = S_before.shape
+    if partials is None:
+        partials = torch.empty((L, B, H, 2), dtype=torch.float32, device=S_before.device)
+    _check(lib().deltas_drift_states(_ptr(S_before), _ptr(S_after), L, B, H, dv, dk, _ptr(partials), _stream(stream)))
+    return partials
 
 
 def kv_workspace_bytes(n_layers, row_bytes, capacity) -> int:

@@ -139,6 +139,22 @@ ds_status deltas_drift(const float *partials, int32_t L, int32_t F, int32_t H_v,
     return DS_OK;
 }
 
+ds_status deltas_drift_states(const float *S_before, const float *S_after, int32_t L, int32_t B, int32_t H_v,
+                              int32_t d_v, int32_t d_k, float *partials, void *stream) {
+    g_last_error[0] = 0;
+    if (L < 0 || B < 0 || H_v < 1 || d_v < 1 || d_k < 1)
+        return fail(DS_E_SHAPE, "L=%d B=%d H_v=%d d_v=%d d_k=%d", L, B, H_v, d_v, d_k);
+    if (((long long)d_v * d_k) % 4 != 0) return fail(DS_E_UNSUPPORTED, "d_v * d_k = %d is not a multiple of 4", d_v * d_k);
+    const long long heads = (long long)L * B * H_v;
+    if (heads == 0) return DS_OK;
+    if (!S_before || !S_after || !partials) return fail(DS_E_NULL, "S_before, S_after and partials are required");
+    if (heads > (1LL << 30) || (long long)d_v * d_k > (1LL << 30)) return fail(DS_E_UNSUPPORTED, "too many states");
+    if (misaligned(S_before) || misaligned(S_after)) return fail(DS_E_ALIGN, "states must be 16-byte aligned");
+    hipError_t e = ds::launch_drift_states(S_before, S_after, (int)heads, d_v * d_k, partials, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "deltas_drift_states launch");
+    return DS_OK;
+}
+
 size_t ds_kv_workspace_bytes(const ds_kv_shape *shape) {
     if (!shape || shape->n_layers < 1 || shape->row_bytes < 16 || shape->row_bytes % 16 || shape->row_bytes > 65536 ||
         shape->capacity < 1 || 2 * shape->n_layers > ds::KV_MAX_PLANES)

@@ -38,6 +38,9 @@ GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, i
 hipError_t launch_gdn(const GdnLaunch &p, hipStream_t stream);
 
 // ---------------------------------------------------------------- drift reduce
+// n_heads heads of n_elem fp32 entries each (n_elem a multiple of 4)
+hipError_t launch_drift_states(const float *before, const float *after, int n_heads, int n_elem, float *partials,
+                               hipStream_t stream);
 hipError_t launch_drift(const float *partials, int L, int F, int H_v, int mode, float *scores,
                         hipStream_t stream);
 

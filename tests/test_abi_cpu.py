@@ -28,7 +28,7 @@ def _declared():
 
 def test_header_declares_the_entry_points():
     names = _declared()
-    for n in ["gdn_chunk_fwd", "deltas_drift", "kv_evict_topk", "ds_gdn_workspace_bytes",
+    for n in ["gdn_chunk_fwd", "deltas_drift", "deltas_drift_states", "kv_evict_topk", "ds_gdn_workspace_bytes",
               "ds_kv_workspace_bytes", "ds_status_string", "ds_last_error", "ds_kv_device_status"]:
         assert n in names
 
@@ -91,6 +91,15 @@ def test_drift_rejects_bad_arguments(ds):
     assert L.deltas_drift(None, 1, 1, 0, 0, None, None) == 2
     assert L.deltas_drift(None, 1, 4, 2, 0, None, None) == 1
     assert L.deltas_drift(None, 0, 4, 2, 0, None, None) == 0               # nothing to do
+
+
+def test_drift_states_rejects_bad_arguments(ds):
+    L = ds.lib()
+    assert L.deltas_drift_states(None, None, 1, 1, 0, 8, 8, None, None) == 2   # H_v < 1
+    assert L.deltas_drift_states(None, None, 1, 1, 1, 3, 3, None, None) == 5   # d_v d_k % 4
+    assert L.deltas_drift_states(None, None, 1, 1, 1, 8, 8, None, None) == 1   # NULL
+    assert L.deltas_drift_states(None, None, 0, 1, 1, 8, 8, None, None) == 0   # nothing to do
+    assert L.deltas_drift_states(8, 16, 1, 1, 1, 8, 8, 32, None) == 4          # misaligned
 
 
 def test_kv_rejects_bad_arguments_and_noop(ds):

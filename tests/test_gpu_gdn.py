@@ -227,3 +227,71 @@ def test_single_layer_full_size_sampled_heads(ds):
         rh = oracle.drift_scores(ref["partials"][None], oracle.PER_HEAD)
         assert drift_rel_err(ph, rh) <= TOL_DRIFT, j
         print(f"head {j}: o {eo:.2e} S {es:.2e}")
+
+
+@pytest.mark.gpu
+def test_drift_states_kernel(ds):
+    """deltas_drift_states on the frame-end snapshots of the tiny workload equals
+    the oracle's sums taken from the same snapshots, and the fused sums of the
+    forward (2 layers x 2 streams x H heads of random states as well)."""
+    x = synth.workload_inputs("tiny")
+    gpu = run_gpu(ds, x, snapshots=True)
+    snaps = gpu["raw"]["snapshots"]                        # [F][H][d][d] fp32 on the device
+    before = torch.cat([torch.zeros_like(snaps[:1]), snaps[:-1]], dim=0)
+    F, H, d, _ = snaps.shape
+    p = ds.deltas_drift_states(before.reshape(1, F, H, d, d).contiguous(), snaps.reshape(1, F, H, d, d).contiguous())
+    torch.cuda.synchronize()
+    ref = oracle.drift_states(before.cpu().numpy(), snaps.cpu().numpy())
+    got = p[0].cpu().numpy().astype(np.float64)
+    assert np.allclose(got, ref, rtol=1e-5, atol=0.0)
+    assert np.allclose(got, gpu["partials"], rtol=1e-3, atol=1e-6)
+    rng = np.random.default_rng(11)
+    A = rng.standard_normal((2, 2, 3, 128, 128)).astype(np.float32)
+    Bm = (A + 0.1 * rng.standard_normal(A.shape)).astype(np.float32)
+    p2 = ds.deltas_drift_states(torch.from_numpy(A).cuda(), torch.from_numpy(Bm).cuda())
+    torch.cuda.synchronize()
+    assert np.allclose(p2.cpu().numpy().astype(np.float64), oracle.drift_states(A, Bm), rtol=1e-5, atol=0.0)
+
+
+def test_varlen_full_lengths_one_group(ds):
+    """The varlen workload's stream lengths at full size (8 packed streams,
+    about 590k tokens) for one GQA group (1 qk-head, 2 v-heads, d = 128, frames
+    of 1024), against the oracle over every stream."""
+    x = synth.workload_inputs("varlen", H_k=1, H_v=2)
+    assert x.T_total > 8 * 16384
+    gpu = run_gpu(ds, x)
+    ref = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, x.frame_len)
+    eo, es = _check_all(gpu, ref, ds)
+    print(f"varlen T_total={x.T_total}: o {eo:.2e} S {es:.2e}")
+
+
+def test_stack_layer_chained_calls_one_group(ds):
+    """One layer of the stack workload at full length (T = 262144, frames of
+    1024) run the way the stack runs it: 256 calls of 1024 tokens with the fp32
+    state carried between calls (ping-pong buffers), one GQA group; against a
+    single oracle pass over the whole stream."""
+    x = synth.workload_inputs("stack", H_k=1, H_v=2)
+    T, C = x.T_total, 1024
+    q, k, v = dev_bf16(x.q), dev_bf16(x.k), dev_bf16(x.v)
+    g, beta = dev_f32(x.g), dev_f32(x.beta)
+    S = torch.zeros((1, 2, 128, 128), dtype=torch.float32, device=DEV)
+    S2 = torch.empty_like(S)
+    o = torch.empty((T, 2, 128), dtype=torch.float32, device=DEV)
+    parts = torch.empty((T // C, 2, 2), dtype=torch.float32, device=DEV)
+    ws = None
+    for c in range(T // C):
+        sl = slice(c * C, (c + 1) * C)
+        r = ds.gdn_chunk_fwd(q[sl], k[sl], v[sl], g[sl], beta[sl], [C], C, state_in=S, state_out=S2, o=o[sl],
+                             workspace=ws)
+        ws = r["workspace"]
+        parts[c] = r["drift_partials"][0]
+        S, S2 = S2, S
+    torch.cuda.synchronize()
+    ref = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, C)
+    eo = rel_fro(o.cpu().numpy().astype(np.float64), ref["o"])
+    es = rel_fro(S.cpu().numpy().astype(np.float64), ref["S"])
+    assert eo <= TOL_O and es <= TOL_O, (eo, es)
+    ph = oracle.drift_scores(parts.cpu().numpy().astype(np.float64)[None], oracle.PER_HEAD)
+    rh = oracle.drift_scores(ref["partials"][None], oracle.PER_HEAD)
+    assert drift_rel_err(ph, rh) <= TOL_DRIFT
+    print(f"stack layer, 256 chained calls: o {eo:.2e} S {es:.2e}")

@@ -383,3 +383,39 @@ def test_paper_size_constants():
     over 8 full-attention layers (Section 3.1 and the model description)."""
     assert 24 * 32 * 128 * 128 * 4 == 48 * 2 ** 20
     assert 8 * 4 * 256 * 2 * 2 == 32 * 2 ** 10
+
+
+# ---------------------------------------------------------------- drift from two states
+def test_drift_states_closed_forms():
+    """drift_states against closed forms: an unchanged state gives num = 0; a
+    zero state before gives den = 0 and num = ||S_after||^2; S_after = c S_before
+    gives num = (c - 1)^2 den; a single changed entry gives num = delta^2."""
+    rng = np.random.default_rng(5)
+    S = rng.standard_normal((2, 3, 4, 8, 8))
+    p = oracle.drift_states(S, S)
+    assert np.all(p[..., 0] == 0.0)
+    assert np.allclose(p[..., 1], np.einsum("...ij,...ij->...", S, S), rtol=1e-14)
+    z = oracle.drift_states(np.zeros_like(S), S)
+    assert np.all(z[..., 1] == 0.0)
+    assert np.allclose(z[..., 0], (S ** 2).sum(axis=(-2, -1)), rtol=1e-14)
+    c = 0.75
+    q = oracle.drift_states(S, c * S)
+    assert np.allclose(q[..., 0], (c - 1.0) ** 2 * q[..., 1], rtol=1e-12)
+    T = S.copy()
+    T[1, 2, 3, 5, 6] += 0.5
+    one = oracle.drift_states(S, T)
+    assert one[1, 2, 3, 0] == pytest.approx(0.25, rel=1e-12)
+    mask = np.ones(one.shape[:-1], bool)
+    mask[1, 2, 3] = False
+    assert np.all(one[..., 0][mask] == 0.0)
+
+
+def test_drift_states_matches_fused_sums():
+    """The fused per-frame sums of the recurrence equal the sums taken from its
+    own frame-end snapshots (the unfused way of Section 3.2)."""
+    x = synth.workload_inputs("tiny")
+    r = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, x.frame_len, snapshots=True)
+    snaps = r["snapshots"]  # [F][H][d][d]
+    before = np.concatenate([np.zeros_like(snaps[:1]), snaps[:-1]], axis=0)
+    p = oracle.drift_states(before, snaps)
+    assert np.allclose(p, r["partials"], rtol=1e-12, atol=1e-300)
