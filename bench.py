@@ -239,6 +239,25 @@ def main():
     nodrift_ms = float(np.median(t_without))
     drift_overhead = 100.0 * (withdrift_ms / nodrift_ms - 1.0)
 
+    # the beta ||e|| signal on top of the drift sums (appendix on retention signals)
+    wparts = torch.empty((n_frames, H_V, 2), dtype=torch.float32, device=dev)
+
+    def fwd_drift_write():
+        ds.gdn_chunk_fwd(q, k, v, g, beta, [T], FRAME, state_out=state, o=o, drift_partials=partials,
+                         write_partials=wparts, workspace=ws)
+
+    fwd_drift_write()
+    t_w = []
+    for rnd in range(3):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fwd_drift_write()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t_w.append(e0.elapsed_time(e1) / reps)
+    write_ms = float(np.median(t_w))
+
     # the unfused alternative (Section 3.2 as the paper measures it): at every
     # frame boundary copy the state, and after the frame take the two norms
     # with deltas_drift_states -- one copy and one call per frame of the stream
@@ -306,6 +325,8 @@ def main():
         "algorithmic_tflops": achieved_tflops,
         "drift_overhead_pct": drift_overhead,
         "drift_unfused_ms": unfused_ms,
+        "write_signal_ms": write_ms,
+        "write_signal_overhead_pct": 100.0 * (write_ms / withdrift_ms - 1.0),
         "drift_unfused_overhead_pct": 100.0 * unfused_ms / nodrift_ms,
         "evict_moved_rows_mean": float(moved_rows.mean()),
         "evict_gather_gbs": float((2 * moved_bytes).mean() / (evict_ms * 1e-3) / 1e9),

@@ -57,7 +57,9 @@ enum { DS_BF16 = 0, DS_F32 = 1 };
 enum {
     DS_DRIFT_LAYER_FROB = 0, /* Eq. 3: per layer ||dS||_F / ||S_before||_F over all its heads, mean over layers */
     DS_DRIFT_HEAD_MEAN = 1,  /* mean over layers and heads of the per-head ratio */
-    DS_DRIFT_PER_HEAD = 2    /* the per-(layer, frame, head) ratios */
+    DS_DRIFT_PER_HEAD = 2,   /* the per-(layer, frame, head) ratios */
+    DS_WRITE_MEAN = 3        /* write_partials of gdn_chunk_fwd: mean over layers, heads and the
+                                frame's tokens of beta ||e|| (the beta ||e|| signal) */
 };
 
 /* Static description of a status code. */
@@ -85,6 +87,13 @@ const char *ds_last_error(void);
  * (S_start = the state when the frame began, held on chip -- the temporary
  * copy of the previous state of Section 3.2), and optionally the state
  * itself into snapshots[f][j].  Frames are numbered stream by stream.
+ * Optionally also the write-magnitude signal compared with the drift in the
+ * appendix on retention signals (row beta ||e||):
+ *     write_partials[f][j][0] = sum over the frame's tokens of beta_t ||e_t||_2
+ *     write_partials[f][j][1] = number of tokens in the frame
+ * with e_t = v_t - alpha_t S_{t-1} k_t; beta_t ||e_t|| is the Frobenius norm of
+ * the token's rank-one write for unit keys.  The writes enter this sum in
+ * fp16, so it carries a relative error of about 1e-3.
  *
  * Shapes and layouts (row-major, innermost last):
  *   q, k        bf16 [T_total][H_k][d_k]  (k expected L2-normalised per row)
@@ -98,6 +107,7 @@ const char *ds_last_error(void);
  *   state_out   fp32 [B][H_v][d_v][d_k]; may alias state_in
  *   o           [T_total][H_v][d_v] of dtype o_dtype (DS_BF16 or DS_F32)
  *   drift_partials fp32 [n_frames][H_v][2] or NULL
+ *   write_partials fp32 [n_frames][H_v][2] or NULL
  *   snapshots   fp32 [n_frames][H_v][d_v][d_k] or NULL
  * Supported: d_k = d_v in {64, 128}; H_v a multiple of H_k; frame_len a
  * multiple of 64 or 0.  bf16 inputs are converted to fp16 for the matrix
@@ -121,8 +131,8 @@ size_t ds_gdn_workspace_bytes(const ds_gdn_shape *shape);
 ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k, const void *v,
                         const float *g, const float *beta, const int32_t *cu_seqlens,
                         const float *state_in, float *state_out, void *o, int32_t o_dtype,
-                        float scale, float *drift_partials, float *snapshots, void *workspace,
-                        size_t workspace_bytes, void *stream);
+                        float scale, float *drift_partials, float *write_partials, float *snapshots,
+                        void *workspace, size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------
  * deltas_drift -- state drift per frame (Section 3.2, Eq. 3)
@@ -132,6 +142,8 @@ ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k,
  *   DS_DRIFT_LAYER_FROB: scores[f] = mean_l sqrt(sum_h num / sum_h den)
  *   DS_DRIFT_HEAD_MEAN:  scores[f] = mean_{l,h} sqrt(num / den)
  *   DS_DRIFT_PER_HEAD:   scores[l][f][h] = sqrt(num / den)
+ *   DS_WRITE_MEAN:       with write_partials (sum, count) in place of (num, den):
+ *                        scores[f] = mean_{l,h} sum / count (0 where count = 0)
  * den = 0 gives +inf when num > 0 and 0 otherwise; a mean containing +inf
  * is +inf.  scores: fp32 [F] (or [L][F][H_v] for PER_HEAD).
  */

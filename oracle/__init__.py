@@ -34,6 +34,7 @@ _lib = None
 LAYER_FROB = 0   # Eq. 3: per layer ||dS||_F / ||S_before||_F over all heads, mean over layers
 HEAD_MEAN = 1    # mean over layers and heads of the per-head ratio
 PER_HEAD = 2     # the per-(layer, frame, head) ratios themselves
+WRITE_MEAN = 3   # (sum, count) write pairs: mean over layers and heads of sum / count
 
 
 def build(force: bool = False) -> Path:
@@ -54,7 +55,7 @@ def _load():
         P = ctypes.c_void_p
         lib.ref_gdn_forward.argtypes = [ctypes.c_int, P, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                         ctypes.c_int, ctypes.c_int, P, P, P, P, P, P,
-                                        ctypes.c_double, P, P, P, P, ctypes.c_int]
+                                        ctypes.c_double, P, P, P, P, P, ctypes.c_int]
         lib.ref_gdn_forward.restype = ctypes.c_int
         lib.ref_max_threads.restype = ctypes.c_int
         _lib = lib
@@ -92,7 +93,11 @@ def gdn_forward(q, k, v, g, beta, cu_seqlens, frame_len, S0=None, scale=1.0,
     first token and the last frame may be partial.
 
     Returns dict(o [T][H_v][d_v], S [B][H_v][d_v][d_k],
-                 partials [F][H_v][2] (num, den), snapshots or None).
+                 partials [F][H_v][2] (num, den),
+                 writes [F][H_v][2] (sum over the frame of beta_t ||v_t - alpha_t S k_t||_2,
+                                     token count) -- the write-magnitude signal,
+                 snapshots or None).
+    
     """
     lib = _load()
     q = np.ascontiguousarray(q, dtype=np.uint16)
@@ -108,14 +113,15 @@ def gdn_forward(q, k, v, g, beta, cu_seqlens, frame_len, S0=None, scale=1.0,
     o = np.zeros((T, H_v, d_v), np.float64)
     S = np.zeros((B, H_v, d_v, d_k), np.float64)
     part = np.zeros((F, H_v, 2), np.float64)
+    wr = np.zeros((F, H_v, 2), np.float64)
     snap = np.zeros((F, H_v, d_v, d_k), np.float64) if snapshots else None
     S0c = None if S0 is None else np.ascontiguousarray(S0, dtype=np.float64)
     rc = lib.ref_gdn_forward(B, _ptr(cu), H_k, H_v, d_k, d_v, int(frame_len), _ptr(q), _ptr(k),
                              _ptr(v), _ptr(g), _ptr(beta), _ptr(S0c), float(scale), _ptr(o),
-                             _ptr(S), _ptr(part), _ptr(snap), int(n_threads))
+                             _ptr(S), _ptr(part), _ptr(wr), _ptr(snap), int(n_threads))
     if rc != 0:
         raise ValueError("oracle rejected the arguments")
-    return dict(o=o, S=S, partials=part, snapshots=snap)
+    return dict(o=o, S=S, partials=part, writes=wr, snapshots=snap)
 
 
 def _ratio(num, den):
@@ -134,6 +140,9 @@ def drift_scores(partials, mode=LAYER_FROB):
       per layer sqrt(sum_h num / sum_h den), then the mean over layers -> [F].
     HEAD_MEAN: mean over layers and heads of sqrt(num / den) -> [F].
     PER_HEAD: sqrt(num / den) -> [L][F][H].
+    WRITE_MEAN: the pairs are the write-magnitude sums (sum over the frame's
+      tokens of beta ||e||, token count) of gdn_forward; the chunk score of the
+      beta ||e|| signal is the mean over layers, heads and tokens -> [F].
     A mean that contains +inf is +inf.
     """
     p = np.asarray(partials, dtype=np.float64)
@@ -151,6 +160,8 @@ def drift_scores(partials, mode=LAYER_FROB):
         for l in range(L):
             if mode == LAYER_FROB:
                 vals.append(_ratio(sum(p[l, f, :, 0]), sum(p[l, f, :, 1])))
+            elif mode == WRITE_MEAN:
+                vals.extend(p[l, f, h, 0] / p[l, f, h, 1] if p[l, f, h, 1] > 0 else 0.0 for h in range(H))
             elif mode == HEAD_MEAN:
                 vals.extend(_ratio(p[l, f, h, 0], p[l, f, h, 1]) for h in range(H))
             else:

@@ -19,6 +19,10 @@
  *       num = ||S_end - S_start||_F^2,  den = ||S_start||_F^2
  *   after which S_start <- S_end.  S_start of the first frame is the entry
  *   state (the copy of the previous state kept for the score, Section 3.2).
+ *   Also per frame the write-magnitude signal of the appendix on retention
+ *   signals (the beta ||e|| row): the sum over the frame's tokens of
+ *   ||e_t||_2 (e_t above already carries beta_t, so this is the Frobenius norm
+ *   of the rank-one write for unit keys) and the number of tokens.
  *
  * Inputs are taken exactly as the GPU consumes them: bf16 bit patterns for
  * q, k, v and fp32 for g, beta, widened to fp64 without rounding.
@@ -55,13 +59,14 @@ static int64_t frames_of(int64_t n, int64_t frame_len)
  * S0: [B][H_v][d_v][d_k] or NULL (zeros).
  * o: [T][H_v][d_v]; S_out: [B][H_v][d_v][d_k];
  * partials: [F_total][H_v][2] (num, den) or NULL;
+ * writes: [F_total][H_v][2] (sum over the frame of ||e_t||_2, token count) or NULL;
  * snapshots: [F_total][H_v][d_v][d_k] (state at each frame end) or NULL.
  * Returns 0, or -1 on a bad argument.
  */
 int ref_gdn_forward(int B, const int32_t *cu_seqlens, int H_k, int H_v, int d_k, int d_v,
                     int frame_len, const uint16_t *q, const uint16_t *k, const uint16_t *v,
                     const float *g, const float *beta, const double *S0, double scale,
-                    double *o, double *S_out, double *partials, double *snapshots,
+                    double *o, double *S_out, double *partials, double *writes, double *snapshots,
                     int n_threads)
 {
     if (B < 0 || H_k <= 0 || H_v <= 0 || d_k <= 0 || d_v <= 0 || H_v % H_k != 0) return -1;
@@ -98,6 +103,8 @@ int ref_gdn_forward(int B, const int32_t *cu_seqlens, int H_k, int H_v, int d_k,
         }
         memcpy(S_start, S, sizeof(double) * ss);
         int64_t frame = frame_base[b];
+        double wsum = 0.0;
+        int64_t wcount = 0;
 
         for (int64_t t = t0; t < t1; ++t) {
             const uint16_t *kp = k + ((size_t)t * H_k + h) * d_k;
@@ -115,6 +122,12 @@ int ref_gdn_forward(int B, const int32_t *cu_seqlens, int H_k, int H_v, int d_k,
                 double sk = 0.0;
                 for (int c = 0; c < d_k; ++c) sk += Sr[c] * kt[c];
                 e[r] = bt * (bf16_to_f64(vp[r]) - alpha * sk);
+            }
+            {
+                double ee = 0.0;
+                for (int r = 0; r < d_v; ++r) ee += e[r] * e[r];
+                wsum += sqrt(ee);
+                ++wcount;
             }
             /* S = alpha * S + e k^T ; o = scale * S q */
             double *op = o + ((size_t)t * H_v + j) * d_v;
@@ -140,6 +153,12 @@ int ref_gdn_forward(int B, const int32_t *cu_seqlens, int H_k, int H_v, int d_k,
                     partials[((size_t)frame * H_v + j) * 2 + 0] = num;
                     partials[((size_t)frame * H_v + j) * 2 + 1] = den;
                 }
+                if (writes) {
+                    writes[((size_t)frame * H_v + j) * 2 + 0] = wsum;
+                    writes[((size_t)frame * H_v + j) * 2 + 1] = (double)wcount;
+                }
+                wsum = 0.0;
+                wcount = 0;
                 if (snapshots) memcpy(snapshots + ((size_t)frame * H_v + j) * ss, S, sizeof(double) * ss);
                 memcpy(S_start, S, sizeof(double) * ss);
                 ++frame;

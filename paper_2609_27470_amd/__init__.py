@@ -17,7 +17,7 @@ LIB_PATH = PKG / "libdeltas.so"
 
 DS_OK = 0
 DS_BF16, DS_F32 = 0, 1
-LAYER_FROB, HEAD_MEAN, PER_HEAD = 0, 1, 2
+LAYER_FROB, HEAD_MEAN, PER_HEAD, WRITE_MEAN = 0, 1, 2, 3
 
 EXPORTED = [
     "ds_status_string", "ds_last_error", "ds_gdn_workspace_bytes", "gdn_chunk_fwd", "deltas_drift",
@@ -58,7 +58,7 @@ def lib():
         L.ds_gdn_workspace_bytes.argtypes = [ctypes.POINTER(GdnShape)]
         L.ds_gdn_workspace_bytes.restype = SZ
         L.gdn_chunk_fwd.argtypes = [ctypes.POINTER(GdnShape), P, P, P, P, P, P, P, P, P, I32, ctypes.c_float,
-                                    P, P, P, SZ, P]
+                                    P, P, P, P, SZ, P]
         L.gdn_chunk_fwd.restype = I32
         L.deltas_drift.argtypes = [P, I32, I32, I32, I32, P, P]
         L.deltas_drift.restype = I32
@@ -110,14 +110,16 @@ def gdn_workspace_bytes(shape: GdnShape) -> int:
 
 
 def gdn_chunk_fwd(q, k, v, g, beta, lengths, frame_len, cu_seqlens=None, state_in=None, state_out=None,
-                  o=None, o_dtype=torch.float32, scale=1.0, drift_partials=True, snapshots=False,
-                  workspace=None, stream=None):
+                  o=None, o_dtype=torch.float32, scale=1.0, drift_partials=True, write_partials=False,
+                  snapshots=False, workspace=None, stream=None):
     """One gated-delta-rule layer over packed streams (see gdn_chunk_fwd in deltas.h).
 
     q, k: bf16 [T][H_k][d]; v: bf16 [T][H_v][d]; g, beta: fp32 [T][H_v];
     lengths: host list of stream lengths; cu_seqlens: device int32 [B+1]
     (built from lengths when None).  Returns a dict with o, state,
-    drift_partials [F][H_v][2] (or None) and snapshots (or None).
+    drift_partials [F][H_v][2] (or None), write_partials [F][H_v][2] (the
+    beta ||e|| sums and token counts, or None) and snapshots (or None).
+    Each output argument may be True (allocate), False (skip) or a tensor.
     """
     T, H_k, d = q.shape
     H_v = v.shape[1]
@@ -135,6 +137,8 @@ def gdn_chunk_fwd(q, k, v, g, beta, lengths, frame_len, cu_seqlens=None, state_i
     od = DS_BF16 if o.dtype == torch.bfloat16 else DS_F32
     dp = torch.empty((shape.n_frames, H_v, 2), dtype=torch.float32, device=dev) if drift_partials is True \
         else drift_partials if drift_partials is not False else None
+    wp = torch.empty((shape.n_frames, H_v, 2), dtype=torch.float32, device=dev) if write_partials is True \
+        else write_partials if write_partials is not False else None
     sn = torch.empty((shape.n_frames, H_v, d, d), dtype=torch.float32, device=dev) if snapshots is True \
         else snapshots if snapshots is not False else None
     need = gdn_workspace_bytes(shape)
@@ -142,8 +146,8 @@ def gdn_chunk_fwd(q, k, v, g, beta, lengths, frame_len, cu_seqlens=None, state_i
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     _check(lib().gdn_chunk_fwd(ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
                                _ptr(cu_seqlens), _ptr(state_in), _ptr(state_out), _ptr(o), od, float(scale),
-                               _ptr(dp), _ptr(sn), _ptr(workspace), workspace.numel(), _stream(stream)))
-    return dict(o=o, state=state_out, drift_partials=dp, snapshots=sn, workspace=workspace)
+                               _ptr(dp), _ptr(wp), _ptr(sn), _ptr(workspace), workspace.numel(), _stream(stream)))
+    return dict(o=o, state=state_out, drift_partials=dp, write_partials=wp, snapshots=sn, workspace=workspace)
 
 
 def deltas_drift(partials, mode=LAYER_FROB, scores=None, stream=None):

@@ -71,7 +71,8 @@ size_t ds_gdn_workspace_bytes(const ds_gdn_shape *shape) {
 
 ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k, const void *v, const float *g,
                         const float *beta, const int32_t *cu_seqlens, const float *state_in, float *state_out,
-                        void *o, int32_t o_dtype, float scale, float *drift_partials, float *snapshots,
+                        void *o, int32_t o_dtype, float scale, float *drift_partials, float *write_partials,
+                        float *snapshots,
                         void *workspace, size_t workspace_bytes, void *stream) {
     g_last_error[0] = 0;
     ds_status st = check_gdn_shape(shape);
@@ -82,7 +83,8 @@ ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k,
     if (!state_out) return fail(DS_E_NULL, "state_out is required");
     if (s.B > 1 && !cu_seqlens) return fail(DS_E_NULL, "cu_seqlens is required when B > 1");
     if (o_dtype != DS_BF16 && o_dtype != DS_F32) return fail(DS_E_DTYPE, "o_dtype=%d", o_dtype);
-    const void *ptrs[] = {q, k, v, g, beta, cu_seqlens, state_in, state_out, o, drift_partials, snapshots, workspace};
+    const void *ptrs[] = {q, k, v, g, beta, cu_seqlens, state_in, state_out, o, drift_partials, write_partials,
+                          snapshots, workspace};
     for (const void *p : ptrs)
         if (misaligned(p)) return fail(DS_E_ALIGN, "a pointer is not 16-byte aligned");
     const ds::GdnWorkspace lay = ds::gdn_workspace_layout(s.B, s.T_total, s.H_k, s.H_v, s.d_v, s.n_frames);
@@ -113,12 +115,14 @@ ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k,
     p.o_bf16 = (o_dtype == DS_BF16);
     p.scale = scale;
     p.drift_partials = drift_partials;
+    p.write_partials = write_partials;
     p.snapshots = snapshots;
     char *ws = (char *)workspace;
     p.wsT = (_Float16 *)(ws + lay.offT);
     p.wsP = (_Float16 *)(ws + lay.offP);
     p.wsGam = (float *)(ws + lay.offGam);
     p.wsDrift = (float *)(ws + lay.offDrift);
+    p.wsWrite = (float *)(ws + lay.offWrite);
     p.tiles_max = lay.tiles_max;
     p.n_split = lay.n_split;
     hipError_t e = ds::launch_gdn(p, (hipStream_t)stream);
@@ -130,7 +134,7 @@ ds_status deltas_drift(const float *partials, int32_t L, int32_t F, int32_t H_v,
                        void *stream) {
     g_last_error[0] = 0;
     if (L < 0 || F < 0 || H_v < 1) return fail(DS_E_SHAPE, "L=%d F=%d H_v=%d", L, F, H_v);
-    if (mode < DS_DRIFT_LAYER_FROB || mode > DS_DRIFT_PER_HEAD) return fail(DS_E_ARG, "mode=%d", mode);
+    if (mode < DS_DRIFT_LAYER_FROB || mode > DS_WRITE_MEAN) return fail(DS_E_ARG, "mode=%d", mode);
     if ((long long)L * F * H_v == 0) return DS_OK;
     if (!partials || !scores) return fail(DS_E_NULL, "partials and scores are required");
     if ((long long)L * F * H_v * 2 > (1LL << 31)) return fail(DS_E_UNSUPPORTED, "too many partials");

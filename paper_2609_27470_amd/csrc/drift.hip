@@ -24,7 +24,14 @@ __global__ __launch_bounds__(256) void drift_frame_kernel(const float *p, int L,
     int cnt = 0;
     for (int l = 0; l < L; ++l) {
         const float *row = p + ((size_t)l * F + f) * H * 2;
-        if (mode == 0) {
+        if (mode == 3) {
+            // (sum, count) pairs: mean over heads of sum / count
+            for (int h = 0; h < H; ++h) {
+                const double c = (double)row[2 * h + 1];
+                acc += c > 0.0 ? (double)row[2 * h] / c : 0.0;
+                ++cnt;
+            }
+        } else if (mode == 0) {
             double num = 0.0, den = 0.0;
             for (int h = 0; h < H; ++h) {
                 num += (double)row[2 * h];

@@ -52,6 +52,7 @@ struct GdnArgs {
     float *snapshots;
     _Float16 *wsT, *wsP;
     float *wsGam, *wsDrift;
+    float *wsWrite;  // per-token sums of squares of E over the slice's columns, or null
     int n_split;
 };
 
@@ -742,6 +743,42 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                 acc[r][3] *= s.gam[r].w;
             }
             const half8 ef0 = as_half8(sh.E[buf][0][lane]);
+            if (a.wsWrite) {
+                // ||E row||^2 over this slice's 16 columns for the wave's 32 tokens
+                // (E k-step pr: lane (ln, lg) element i is token kappa(pr, lg, i),
+                // column ln), summed over the 16 lanes of each row by a transposing
+                // butterfly: after it, lane ln holds the sum for element ln / 2
+                const half8 ef = pr == 0 ? ef0 : as_half8(sh.E[buf][1][lane]);
+                float x[8];
+#pragma unroll
+                for (int i = 0; i < 8; ++i) x[i] = (float)ef[i] * (float)ef[i];
+                const bool b3 = (ln >> 3) & 1, b2 = (ln >> 2) & 1, b1 = (ln >> 1) & 1;
+                float y[4], z[2];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {  // partner ln ^ 8 (rotate the row of 16 by 8)
+                    const float send = b3 ? x[q] : x[4 + q];
+                    const float recv = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                                                                     0, __builtin_bit_cast(int, send), 0x128, 0xF, 0xF, false));
+                    y[q] = (b3 ? x[4 + q] : x[q]) + recv;
+                }
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {  // partner ln ^ 4 (swizzle with xor mask 4)
+                    const float send = b2 ? y[q] : y[2 + q];
+                    const float recv = __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, send), 0x101F));
+                    z[q] = (b2 ? y[2 + q] : y[q]) + recv;
+                }
+                float wsum;
+                {  // partner ln ^ 2, then ln ^ 1 (quad permutations)
+                    const float send = b1 ? z[0] : z[1];
+                    const float recv = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                                                                     0, __builtin_bit_cast(int, send), 0x4E, 0xF, 0xF, false));
+                    wsum = (b1 ? z[1] : z[0]) + recv;
+                    wsum += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, wsum), 0xB1, 0xF,
+                                                                                  0xF, false));
+                }
+                const int i = ln >> 1, tok = 32 * pr + 16 * (i >> 2) + 4 * lg + (i & 3);
+                if ((ln & 1) == 0 && tok < n) a.wsWrite[((size_t)(t0 + tok) * a.H_v + j) * a.n_split + sl] = wsum;
+            }
             if (pr == 0) {
                 acc[0] = mfma_f16(as_half8(s.p[0]), ef0, acc[0]);
                 acc[1] = mfma_f16(as_half8(s.p[1]), ef0, acc[1]);
@@ -881,6 +918,38 @@ __global__ __launch_bounds__(256) void gdn_drift_finalize_kernel(const float *ws
     out[(size_t)idx * 2 + 1] = den;
 }
 
+// Write-magnitude signal per (frame, v-head): the sum over the frame's tokens
+// of sqrt(sum over slices of ||E row||^2) and the token count -> [n_frames][H_v][2].
+// One wave per (frame, v-head); fixed summation order.  Frames past the real
+// count are zeroed.
+__global__ __launch_bounds__(64) void gdn_write_finalize_kernel(const float *ws, float *out, int n_frames, int H_v,
+                                                                 int n_split, Streams st, int frame_len) {
+    const int f = blockIdx.x, j = blockIdx.y, lane = threadIdx.x;
+    int base = 0, tb = 0, te = 0;
+    for_streams(st, [&](int, int s0, int e0) {
+        const int nf = frames_in(e0 - s0, frame_len);
+        if (f < base + nf) {
+            const int lf = f - base;
+            tb = s0 + (frame_len > 0 ? lf * frame_len : 0);
+            te = frame_len > 0 ? min(tb + frame_len, e0) : e0;
+            return true;
+        }
+        base += nf;
+        return false;
+    });
+    double acc = 0.0;
+    for (int t = tb + lane; t < te; t += 64) {
+        float s = 0.f;
+        for (int q = 0; q < n_split; ++q) s += ws[((size_t)t * H_v + j) * n_split + q];
+        acc += sqrt((double)s);
+    }
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    if (lane == 0) {
+        out[((size_t)f * H_v + j) * 2] = (float)acc;
+        out[((size_t)f * H_v + j) * 2 + 1] = (float)(te - tb);
+    }
+}
+
 // ============================================================================
 // host side
 // ============================================================================
@@ -899,6 +968,8 @@ GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, i
     off = align256(off + (size_t)w.tiles_max * H_v * 128 * sizeof(float));
     w.offDrift = off;
     off = align256(off + (size_t)n_frames * H_v * w.n_split * 2 * 2 * sizeof(float));
+    w.offWrite = off;
+    off = align256(off + (size_t)T_total * H_v * w.n_split * sizeof(float));
     w.total = off;
     return w;
 }
@@ -926,6 +997,7 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     a.wsP = p.wsP;
     a.wsGam = p.wsGam;
     a.wsDrift = p.drift_partials ? p.wsDrift : nullptr;
+    a.wsWrite = p.write_partials ? p.wsWrite : nullptr;
     a.n_split = p.n_split;
 
     if (p.tiles_max > 0) {
@@ -953,6 +1025,12 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
         const int n = p.n_frames * p.H_v;
         hipLaunchKernelGGL(gdn_drift_finalize_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, p.wsDrift,
                            p.drift_partials, p.n_frames, p.H_v, p.n_split, a.st, p.frame_len);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (p.write_partials && p.n_frames > 0) {
+        hipLaunchKernelGGL(gdn_write_finalize_kernel, dim3(p.n_frames, p.H_v), dim3(64), 0, stream, p.wsWrite,
+                           p.write_partials, p.n_frames, p.H_v, p.n_split, a.st, p.frame_len);
         e = hipGetLastError();
     }
     return e;

@@ -19,19 +19,21 @@ struct GdnLaunch {
     int o_bf16;
     float scale;
     float *drift_partials;  // [n_frames][H_v][2] or null
+    float *write_partials;  // [n_frames][H_v][2] or null
     float *snapshots;       // [n_frames][H_v][d][d] or null
     // workspace pieces
     _Float16 *wsT;      // [tiles_max][H_v][6][64][8]  T diag(beta), fp16 A-fragments
     _Float16 *wsP;      // [tiles_max][H_v][6][64][8]  D (.) tril(Q K^T), fp16 A-fragments
     float *wsGam;       // [tiles_max][H_v][2][64]   Gamma_r = exp(gamma_r), D_last,r = exp(gamma_last - gamma_r)
     float *wsDrift;     // [n_frames][H_v][n_split][2][2] (one pair per half slice)
+    float *wsWrite;     // [T_total][H_v][n_split] per-token ||E row||^2 over each slice's columns
     int tiles_max;
     int n_split;        // d_v slices of 16 per (stream, v-head)
 };
 
 // Workspace layout shared by the size query and the launcher.
 struct GdnWorkspace {
-    size_t offT, offP, offGam, offDrift, total;
+    size_t offT, offP, offGam, offDrift, offWrite, total;
     int tiles_max, n_split;
 };
 GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, int n_frames);

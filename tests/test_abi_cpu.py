@@ -52,8 +52,9 @@ def test_gdn_workspace_size(ds):
     nb = ds.gdn_workspace_bytes(s)
     tiles = 512
     per = 2 * 6 * 64 * 8 * 2 + 128 * 4     # T and P fragments (fp16) + decay factors per (tile, v-head)
-    assert nb >= tiles * 32 * per
-    assert nb <= tiles * 32 * per + 32 * 32 * 8 * 2 * 2 * 4 + 4096   # + drift sums per half slice
+    wr = 32768 * 32 * 8 * 4                # per-token write norms per 16-row slice
+    assert nb >= tiles * 32 * per + wr
+    assert nb <= tiles * 32 * per + wr + 32 * 32 * 8 * 2 * 2 * 4 + 4096   # + drift sums per half slice
     bad = ds.gdn_shape([64], 1, 1, 96, 64)
     assert ds.gdn_workspace_bytes(bad) == 0
 
@@ -63,11 +64,11 @@ def _call_gdn(ds, shape, **kw):
     P = ctypes.c_void_p
     fake = P(1 << 20)      # never dereferenced: validation fails first
     args = dict(q=fake, k=fake, v=fake, g=fake, beta=fake, cu=None, sin=None, sout=fake, o=fake,
-                od=ds.DS_F32, scale=1.0, dp=None, sn=None, ws=fake, wsb=1 << 40)
+                od=ds.DS_F32, scale=1.0, dp=None, wp=None, sn=None, ws=fake, wsb=1 << 40)
     args.update(kw)
     return L.gdn_chunk_fwd(ctypes.byref(shape), args["q"], args["k"], args["v"], args["g"], args["beta"],
                            args["cu"], args["sin"], args["sout"], args["o"], args["od"], args["scale"],
-                           args["dp"], args["sn"], args["ws"], args["wsb"], None)
+                           args["dp"], args["wp"], args["sn"], args["ws"], args["wsb"], None)
 
 
 def test_gdn_rejects_bad_arguments(ds):

@@ -295,3 +295,42 @@ def test_stack_layer_chained_calls_one_group(ds):
     rh = oracle.drift_scores(ref["partials"][None], oracle.PER_HEAD)
     assert drift_rel_err(ph, rh) <= TOL_DRIFT
     print(f"stack layer, 256 chained calls: o {eo:.2e} S {es:.2e}")
+
+
+def test_write_signal_parity(ds):
+    """The beta ||e|| sums (per frame and v-head) against the oracle on the d=128
+    GQA novelty shape with a ragged tail and a non-zero entry state, and the
+    WRITE_MEAN score of deltas_drift against the oracle's aggregation."""
+    x = synth.workload_inputs("single_layer", T=2048 + 37, H_k=2, H_v=4)
+    S0 = (np.random.default_rng(8).standard_normal((1, 4, 128, 128)) * 0.1).astype(np.float32).astype(np.float64)
+    q, k, v = dev_bf16(x.q), dev_bf16(x.k), dev_bf16(x.v)
+    g, beta = dev_f32(x.g), dev_f32(x.beta)
+    r = ds.gdn_chunk_fwd(q, k, v, g, beta, lengths_of(x), x.frame_len, state_in=dev_f32(S0), write_partials=True)
+    torch.cuda.synchronize()
+    ref = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, x.frame_len, S0=S0)
+    got = r["write_partials"].cpu().numpy().astype(np.float64)
+    assert np.array_equal(got[..., 1], ref["writes"][..., 1])
+    rel = np.abs(got[..., 0] - ref["writes"][..., 0]) / ref["writes"][..., 0]
+    assert rel.max() <= 1e-3, rel.max()
+    sc = ds.deltas_drift(r["write_partials"][None], ds.WRITE_MEAN).cpu().numpy()
+    rs = oracle.drift_scores(ref["writes"][None], oracle.WRITE_MEAN)
+    assert drift_rel_err(sc, rs) <= 1e-3
+    # the other outputs are unchanged by asking for the signal
+    r2 = ds.gdn_chunk_fwd(q, k, v, g, beta, lengths_of(x), x.frame_len, state_in=dev_f32(S0))
+    torch.cuda.synchronize()
+    assert torch.equal(r["o"], r2["o"]) and torch.equal(r["state"], r2["state"])
+    assert torch.equal(r["drift_partials"], r2["drift_partials"])
+
+
+def test_write_signal_varlen(ds):
+    """Write sums over packed streams with empty, sub-tile and multi-frame lengths."""
+    lengths = [1, 63, 64, 0, 65, 300, 1024, 777]
+    x = synth.make_gdn_inputs(lengths, 2, 4, 64, 128, novelty=False, config=3)
+    q, k, v = dev_bf16(x.q), dev_bf16(x.k), dev_bf16(x.v)
+    r = ds.gdn_chunk_fwd(q, k, v, dev_f32(x.g), dev_f32(x.beta), lengths, 128, write_partials=True)
+    torch.cuda.synchronize()
+    ref = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, 128)
+    got = r["write_partials"].cpu().numpy().astype(np.float64)
+    assert np.array_equal(got[..., 1], ref["writes"][..., 1])
+    rel = np.abs(got[..., 0] - ref["writes"][..., 0]) / np.maximum(ref["writes"][..., 0], 1e-30)
+    assert rel.max() <= 1e-3, rel.max()

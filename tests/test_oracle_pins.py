@@ -419,3 +419,69 @@ def test_drift_states_matches_fused_sums():
     before = np.concatenate([np.zeros_like(snaps[:1]), snaps[:-1]], axis=0)
     p = oracle.drift_states(before, snaps)
     assert np.allclose(p, r["partials"], rtol=1e-12, atol=1e-300)
+
+
+# ---------------------------------------------------------------- write-magnitude signal
+def _one_stream(T, H, d, rng, g=None, beta=None):
+    q = to_bf16_bits(rng.standard_normal((T, H, d)))
+    kk = rng.standard_normal((T, H, d))
+    kk /= np.linalg.norm(kk, axis=-1, keepdims=True)
+    k = to_bf16_bits(kk)
+    v = to_bf16_bits(rng.standard_normal((T, H, d)))
+    gg = np.full((T, H), -0.1, np.float32) if g is None else g
+    bb = np.full((T, H), 0.7, np.float32) if beta is None else beta
+    return q, k, v, gg.astype(np.float32), bb.astype(np.float32)
+
+
+def test_write_signal_first_token_closed_form():
+    """From a zero state the first write is beta v: ||e|| = beta ||v||."""
+    rng = np.random.default_rng(21)
+    q, k, v, g, b = _one_stream(1, 3, 16, rng)
+    r = oracle.gdn_forward(q, k, v, g, b, np.array([0, 1], np.int32), 64)
+    vv = bf16_bits_to_f64(v)[0]
+    expect = b[0].astype(np.float64) * np.linalg.norm(vv, axis=-1)
+    assert np.allclose(r["writes"][0, :, 0], expect, rtol=1e-14)
+    assert np.all(r["writes"][0, :, 1] == 1.0)
+
+
+def test_write_signal_equals_one_token_drift():
+    """With g = 0 and unit keys a token's state change is the rank-one write
+    e k^T, so ||Delta S||_F = ||e||: one-token frames make the frame drift num
+    equal to the squared write sum (up to the bf16-rounded key norm)."""
+    rng = np.random.default_rng(22)
+    T, H, d = 40, 2, 32
+    q, k, v, _, b = _one_stream(T, H, d, rng, g=np.zeros((T, H), np.float32),
+                                beta=rng.uniform(0.1, 1.0, (T, H)))
+    r = oracle.gdn_forward(q, k, v, np.zeros((T, H), np.float32), b, np.array([0, T], np.int32), 1)
+    kn = np.linalg.norm(bf16_bits_to_f64(k), axis=-1)            # [T][H], 1 within bf16 rounding
+    assert np.allclose(np.sqrt(r["partials"][..., 0]), r["writes"][..., 0] * kn, rtol=1e-12)
+    assert np.all(r["writes"][..., 1] == 1.0)
+
+
+def test_write_signal_zero_for_represented_pairs():
+    """g = 0, beta = 1, exactly orthonormal keys: a frame that re-presents
+    stored pairs writes nothing (e = 0 exactly)."""
+    d, n = 64, 16
+    keys = to_bf16_bits(synth.orthonormal_keys(d)[:n])   # bf16-exact rows, ||k|| = 1
+    rng = np.random.default_rng(23)
+    vals = to_bf16_bits(rng.standard_normal((n, 1, d)))
+    kb = np.concatenate([keys, keys])[:, None, :]
+    q = kb.copy()
+    v = np.concatenate([vals, vals])
+    T = 2 * n
+    r = oracle.gdn_forward(q, kb, v, np.zeros((T, 1), np.float32), np.ones((T, 1), np.float32),
+                           np.array([0, T], np.int32), n)
+    assert r["writes"][0, 0, 0] > 0.0
+    assert r["writes"][1, 0, 0] == 0.0
+    assert r["writes"][1, 0, 1] == n
+
+
+def test_write_mean_score_aggregation():
+    """WRITE_MEAN averages sum / count over layers and heads."""
+    p = np.zeros((2, 1, 2, 2))
+    p[0, 0, 0] = (3.0, 2.0)
+    p[0, 0, 1] = (1.0, 4.0)
+    p[1, 0, 0] = (0.0, 2.0)
+    p[1, 0, 1] = (10.0, 5.0)
+    s = oracle.drift_scores(p, oracle.WRITE_MEAN)
+    assert s[0] == pytest.approx((1.5 + 0.25 + 0.0 + 2.0) / 4, rel=1e-15)
