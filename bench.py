@@ -209,6 +209,44 @@ def main():
     if status[0] != 0 or status[2] != 0:
         raise RuntimeError(f"eviction reported device status {status}")
 
+    # ---------------- the same eviction loop over a slot-indexed cache: the new
+    # chunk's rows go into the rows the last eviction freed (one index_copy
+    # over the 16 planes), kv_evict_topk_indexed compacts only the table
+    idx_pos = torch.zeros(CAPACITY, dtype=torch.int32, device=dev)
+    idx_chunk = torch.zeros(CAPACITY, dtype=torch.int32, device=dev)
+    idx_slot = torch.zeros(CAPACITY, dtype=torch.int32, device=dev)
+    idx_pos[:BUDGET] = torch.arange(BUDGET, dtype=torch.int32, device=dev)
+    idx_chunk[:BUDGET] = torch.arange(BUDGET, dtype=torch.int32, device=dev) // 1024
+    idx_slot[:BUDGET] = torch.arange(BUDGET, dtype=torch.int32, device=dev)
+    idx_free = torch.arange(BUDGET, CAPACITY, dtype=torch.int32, device=dev)
+    n_idx = args.warmup + args.steps
+    idx_table = torch.rand(n_init_chunks + n_idx, generator=torch.Generator().manual_seed(1)).to(dev)
+    idx_ws = torch.empty(ds.kv_indexed_workspace_bytes(CAPACITY), dtype=torch.uint8, device=dev)
+    idx_freed = torch.empty(CAPACITY - BUDGET, dtype=torch.int32, device=dev)
+    idx_evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    for i in range(n_idx):
+        ev = idx_evs[i - args.warmup] if i >= args.warmup else None
+        if ev:
+            ev[0].record(stream)
+        dst = idx_free.to(torch.int64)
+        cache.index_copy_(1, dst, new_rows)
+        idx_pos[BUDGET:] = append_pos + BUDGET + 1024 * i
+        idx_chunk[BUDGET:] = n_init_chunks + i
+        idx_slot[BUDGET:] = idx_free
+        if ev:
+            ev[1].record(stream)
+        ds.kv_evict_topk_indexed(idx_pos, idx_chunk, idx_slot, idx_table, CAPACITY, BUDGET, 0, 0, 1,
+                                 free_out=idx_freed, workspace=idx_ws)
+        if ev:
+            ev[2].record(stream)
+        idx_free, idx_freed = idx_freed, idx_free
+    torch.cuda.synchronize()
+    status = ds.kv_device_status(idx_ws)
+    if status[0] != 0:
+        raise RuntimeError(f"indexed eviction reported device status {status}")
+    iseg = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(2)] for e in idx_evs])
+    idx_append_ms, idx_evict_ms = iseg.mean(axis=0)
+
     # ---------------- drift overhead: the forward with the fused drift sums
     # plus deltas_drift, against the same forward compiled without the
     # frame-end epilogue; both as back-to-back loops on the same stream,
@@ -331,6 +369,11 @@ def main():
         "evict_moved_rows_mean": float(moved_rows.mean()),
         "evict_gather_gbs": float((2 * moved_bytes).mean() / (evict_ms * 1e-3) / 1e9),
         "drift_overhead_paper_pct": 1.9,
+        "evict_indexed": {
+            "kv_evict_topk_indexed_ms": float(idx_evict_ms), "append_scatter_ms": float(idx_append_ms),
+            "ms_per_step": float(gdn_ms + drift_ms + idx_append_ms + idx_evict_ms),
+            "moved_kv_bytes": 0,
+        },
         "breakdown_ms": {"gdn_chunk_fwd": gdn_ms, "deltas_drift": drift_ms, "kv_append": append_ms,
                          "kv_evict_topk": evict_ms, "isolated_fwd_with_drift": withdrift_ms,
                          "isolated_fwd_without_drift": nodrift_ms},

@@ -13,6 +13,9 @@
  *                   sink + recent window + N temporal spans with per-span
  *                   top-k and fill, then an order-preserving in-place gather
  *                   of every full-attention layer's K and V rows.
+ *   kv_evict_topk_indexed
+ *                   the same step over a slot-indexed cache: identical
+ *                   selection, the K and V rows stay where they are.
  *
  * Conventions shared by every entry point
  *   - Pointers are DEVICE pointers unless marked "host".  The caller owns
@@ -215,6 +218,44 @@ ds_status kv_evict_topk(const ds_kv_shape *shape, void *const *k_layers, void *c
 /* Device address of the int32 status word kv_evict_topk leaves in its
  * workspace: 0 = ok, 1 = cache invariants broken (cache left untouched). */
 int32_t *ds_kv_device_status(void *workspace);
+
+/* ------------------------------------------------------------------------
+ * kv_evict_topk_indexed -- the eviction step of Algorithm 1 (Section 3.3)
+ * without moving K/V data
+ * ------------------------------------------------------------------------
+ * The cache is addressed through a slot table: logical token i (i < len, in
+ * arrival order) lives in physical row slot[i] of every full-attention
+ * layer's K and V; a consumer reads token i's rows at slot[i].  pos,
+ * chunk_id and slot are indexed by logical token and carry the invariants
+ * of kv_evict_topk (chunk_id nondecreasing, pos strictly increasing over
+ * [0, len)); slot holds distinct rows in [0, capacity).
+ * The kept set is exactly kv_evict_topk's (same arguments, same keep_out).
+ * Only the three int32 arrays are compacted, in place and in ascending
+ * logical order: slot'[d] = slot[keep[d]], pos'[d] = pos[keep[d]],
+ * chunk_id'[d] = chunk_id[keep[d]] for d < M, so the logical order still
+ * equals position order (positions are moved, never rewritten).  The
+ * physical rows of the len - M evicted tokens are written to
+ * free_out[0, len - M), in ascending logical order of the evicted tokens;
+ * a caller appends its next tokens into those rows.  No K/V byte is read or
+ * written.  Entries [M, len) of pos, chunk_id and slot are unspecified
+ * afterwards.  If len <= M the call does nothing and sets *new_len = len.
+ *
+ * Layouts: pos, chunk_id, slot: int32 [capacity]; chunk_scores fp32
+ * [num_chunks], no NaN; keep_out int32 [M] (logical indices kept) or NULL;
+ * free_out int32 [len - M] (required); new_len: host int32.  The workspace
+ * (ds_kv_indexed_workspace_bytes) holds the same status word as
+ * kv_evict_topk's (ds_kv_device_status): if the device finds the invariants
+ * broken it writes nothing else.
+ * Requires 0 <= n_sink, 0 <= n_window, n_sink + n_window <= M,
+ * len <= capacity, n_buckets <= 64.
+ */
+size_t ds_kv_indexed_workspace_bytes(int32_t capacity);
+
+ds_status kv_evict_topk_indexed(int32_t capacity, int32_t *pos, int32_t *chunk_id, int32_t *slot,
+                                const float *chunk_scores, int32_t num_chunks, int32_t len, int32_t M,
+                                int32_t n_sink, int32_t n_window, int32_t n_buckets, int32_t *keep_out,
+                                int32_t *free_out, int32_t *new_len, void *workspace,
+                                size_t workspace_bytes, void *stream);
 
 #ifdef __cplusplus
 }

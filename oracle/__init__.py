@@ -11,6 +11,8 @@ Contents
   drift_scores  Eq. 3 and the two other aggregations of the per-head sums
   select_keep   retention policy of Section 3.3 / Algorithm 1 (plain Python)
   compact       the eviction gather KV <- KV[keep] (numpy fancy indexing)
+  compact_indexed  the same eviction over a slot-indexed cache: only the
+                (pos, chunk id, slot) table is gathered; freed rows listed
 
 Readings of the paper that these functions take where it is silent are
 listed in each function's docstring.
@@ -233,3 +235,22 @@ def compact(rows, keep):
     """The eviction gather: new[i] = old[keep[i]] (rows of any dtype)."""
     rows = np.asarray(rows)
     return rows[np.asarray(keep, dtype=np.int64)]
+
+
+def compact_indexed(pos, chunk_id, slot, keep, length):
+    """Eviction over a slot-indexed cache (Section 3.3: same kept set as the
+    gather, Z18 order kept through the table).
+
+    Logical token i lives in physical row slot[i].  The table is gathered
+    like the rows of the plain cache -- new[d] = old[keep[d]] -- and the rows
+    of the tokens not kept are returned in ascending logical order as the
+    free list.  Returns (pos', chunk_id', slot', free), each of the first
+    three of length len(keep).
+    """
+    keep = np.asarray(keep, dtype=np.int64)
+    pos = np.asarray(pos)[:length]
+    chunk_id = np.asarray(chunk_id)[:length]
+    slot = np.asarray(slot)[:length]
+    kept = np.zeros(length, dtype=bool)
+    kept[keep] = True
+    return pos[keep], chunk_id[keep], slot[keep], slot[~kept]

@@ -22,6 +22,7 @@ LAYER_FROB, HEAD_MEAN, PER_HEAD, WRITE_MEAN = 0, 1, 2, 3
 EXPORTED = [
     "ds_status_string", "ds_last_error", "ds_gdn_workspace_bytes", "gdn_chunk_fwd", "deltas_drift",
     "deltas_drift_states", "ds_kv_workspace_bytes", "kv_evict_topk", "ds_kv_device_status",
+    "ds_kv_indexed_workspace_bytes", "kv_evict_topk_indexed",
 ]
 
 
@@ -71,6 +72,11 @@ def lib():
         L.kv_evict_topk.restype = I32
         L.ds_kv_device_status.argtypes = [P]
         L.ds_kv_device_status.restype = P
+        L.ds_kv_indexed_workspace_bytes.argtypes = [I32]
+        L.ds_kv_indexed_workspace_bytes.restype = SZ
+        L.kv_evict_topk_indexed.argtypes = [I32, P, P, P, P, I32, I32, I32, I32, I32, I32, P, P,
+                                            ctypes.POINTER(I32), P, SZ, P]
+        L.kv_evict_topk_indexed.restype = I32
         _lib = L
     return _lib
 
@@ -199,6 +205,38 @@ def kv_evict_topk(k_layers, v_layers, pos, chunk_id, chunk_scores, length, M, n_
                                int(n_buckets), _ptr(keep_out), ctypes.byref(new_len), _ptr(workspace),
                                workspace.numel(), _stream(stream)))
     return int(new_len.value), workspace
+
+
+def kv_indexed_workspace_bytes(capacity) -> int:
+    return int(lib().ds_kv_indexed_workspace_bytes(int(capacity)))
+
+
+def kv_evict_topk_indexed(pos, chunk_id, slot, chunk_scores, length, M, n_sink, n_window, n_buckets,
+                          keep_out=None, free_out=None, workspace=None, stream=None):
+    """One eviction step over a slot-indexed cache (see kv_evict_topk_indexed
+    in deltas.h): pos, chunk_id and slot (int32 [capacity]) are compacted in
+    place; the K/V rows are not touched.  Returns (new_len, workspace,
+    free_out) where free_out[:length - M] lists the freed physical rows.
+    """
+    capacity = slot.numel()
+    for t in (pos, chunk_id, slot):
+        if t.dtype != torch.int32 or t.numel() != capacity:
+            raise ValueError("pos, chunk_id and slot must be int32 tensors of the same length")
+    if free_out is not None and int(length) > int(M) and free_out.numel() < int(length) - int(M):
+        raise ValueError(f"free_out holds {free_out.numel()} entries, {int(length) - int(M)} needed")
+    if keep_out is not None and keep_out.numel() < int(M):
+        raise ValueError(f"keep_out holds {keep_out.numel()} entries, {int(M)} needed")
+    need = int(lib().ds_kv_indexed_workspace_bytes(capacity))
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=pos.device)
+    if free_out is None:
+        free_out = torch.empty(max(int(length) - int(M), 1), dtype=torch.int32, device=pos.device)
+    new_len = ctypes.c_int32(0)
+    _check(lib().kv_evict_topk_indexed(capacity, _ptr(pos), _ptr(chunk_id), _ptr(slot), _ptr(chunk_scores),
+                                       int(chunk_scores.numel()), int(length), int(M), int(n_sink), int(n_window),
+                                       int(n_buckets), _ptr(keep_out), _ptr(free_out), ctypes.byref(new_len),
+                                       _ptr(workspace), workspace.numel(), _stream(stream)))
+    return int(new_len.value), workspace, free_out
 
 
 def kv_device_status(workspace):

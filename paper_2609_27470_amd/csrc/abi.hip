@@ -221,10 +221,66 @@ ds_status kv_evict_topk(const ds_kv_shape *shape, void *const *k_layers, void *c
     p.n_window = n_window;
     p.n_buckets = n_buckets;
     p.keep_out = keep_out;
+    p.slot = nullptr;
+    p.free_out = nullptr;
     p.ws = (char *)workspace;
     p.lay = lay;
     hipError_t e = ds::launch_kv_evict(p, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "kv_evict_topk launch");
+    *new_len = M;
+    return DS_OK;
+}
+
+size_t ds_kv_indexed_workspace_bytes(int32_t capacity) {
+    if (capacity < 1) return 0;
+    return ds::kv_workspace_layout(0, 16, capacity).total;
+}
+
+ds_status kv_evict_topk_indexed(int32_t capacity, int32_t *pos, int32_t *chunk_id, int32_t *slot,
+                                const float *chunk_scores, int32_t num_chunks, int32_t len, int32_t M, int32_t n_sink,
+                                int32_t n_window, int32_t n_buckets, int32_t *keep_out, int32_t *free_out,
+                                int32_t *new_len, void *workspace, size_t workspace_bytes, void *stream) {
+    g_last_error[0] = 0;
+    if (!new_len) return fail(DS_E_NULL, "new_len is required");
+    if (capacity < 1) return fail(DS_E_SHAPE, "capacity=%d", capacity);
+    if (len < 0 || len > capacity) return fail(DS_E_SHAPE, "len=%d outside [0, capacity=%d]", len, capacity);
+    if (M < 0 || n_sink < 0 || n_window < 0 || (long long)n_sink + n_window > M)
+        return fail(DS_E_ARG, "need 0 <= n_sink, 0 <= n_window, n_sink + n_window <= M (got %d, %d, %d)", n_sink,
+                    n_window, M);
+    if (n_buckets < 0 || n_buckets > 64) return fail(DS_E_ARG, "n_buckets=%d (0..64)", n_buckets);
+    if (num_chunks < 1) return fail(DS_E_ARG, "num_chunks=%d", num_chunks);
+    if (len <= M) {
+        *new_len = len;
+        return DS_OK;
+    }
+    if (!pos || !chunk_id || !slot || !chunk_scores || !free_out)
+        return fail(DS_E_NULL, "pos, chunk_id, slot, chunk_scores and free_out are required");
+    const void *ptrs[] = {pos, chunk_id, slot, chunk_scores, keep_out, free_out, workspace};
+    for (const void *q : ptrs)
+        if (misaligned(q)) return fail(DS_E_ALIGN, "a pointer is not 16-byte aligned");
+    const ds::KvWorkspace lay = ds::kv_workspace_layout(0, 16, capacity);
+    if (!workspace || workspace_bytes < lay.total)
+        return fail(DS_E_WORKSPACE, "workspace needs %zu bytes, got %zu", lay.total, workspace_bytes);
+    ds::KvLaunch p{};
+    p.n_planes = 0;
+    p.row_bytes = 16;
+    p.capacity = capacity;
+    p.pos = pos;
+    p.chunk_id = chunk_id;
+    p.chunk_scores = chunk_scores;
+    p.num_chunks = num_chunks;
+    p.len = len;
+    p.M = M;
+    p.n_sink = n_sink;
+    p.n_window = n_window;
+    p.n_buckets = n_buckets;
+    p.keep_out = keep_out;
+    p.slot = slot;
+    p.free_out = free_out;
+    p.ws = (char *)workspace;
+    p.lay = lay;
+    hipError_t e = ds::launch_kv_evict(p, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "kv_evict_topk_indexed launch");
     *new_len = M;
     return DS_OK;
 }

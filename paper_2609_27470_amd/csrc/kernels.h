@@ -54,6 +54,7 @@ struct KvWorkspace {
         offRunFrom, offFlags, total;
     int n_chunks;  // 64 KiB pieces of one token's rows over all layers
 };
+// n_layers = 0: the indexed variant's workspace (no gather flags)
 KvWorkspace kv_workspace_layout(int n_layers, int row_bytes, int capacity);
 
 struct KvLaunch {
@@ -63,6 +64,7 @@ struct KvLaunch {
     const float *chunk_scores;
     int num_chunks, len, M, n_sink, n_window, n_buckets;
     int32_t *keep_out;
+    int32_t *slot, *free_out;  // indexed variant (slot != NULL): no K/V planes, no gather
     char *ws;
     KvWorkspace lay;
 };

@@ -16,6 +16,9 @@
 // Slot data is read in blocks of 32 consecutive slots per thread with
 // 16-byte loads, so each pass over the cache costs one memory round trip per
 // 32 Ki slots.
+// With a slot table (the indexed variant) the K and V rows never move: the
+// select kernel itself compacts pos, chunk_id and slot (the physical row of
+// each logical token) in place and lists the freed physical rows.
 // kv_gather moves the kept rows down in place.  Slot d receives row keep[d]
 // (keep[d] >= d).  Writing slot d is safe once the reader of row d -- the
 // destination inv[d] < d, if row d is kept -- has its data in registers.
@@ -38,8 +41,8 @@ constexpr int SPIN_LIMIT = 1 << 22;
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 struct KvArgs {
-    const int32_t *pos_in;
-    const int32_t *chunk;
+    int32_t *pos;    // written only by the indexed variant
+    int32_t *chunk;
     const float *scores;
     int num_chunks, len, M, n_s, n_w, N;
     int n_flags, n_chunks;
@@ -49,6 +52,8 @@ struct KvArgs {
     unsigned long long *run_key;
     int32_t *flags;
     int32_t *keep_out;
+    int32_t *slot;      // indexed variant: physical row of each logical token (NULL: gather variant)
+    int32_t *free_out;  // indexed variant: physical rows of the evicted tokens
     char **plane_tab;  // device copy of the plane pointers, read by the gather
     char *planes[KV_MAX_PLANES];
     int n_planes;
@@ -149,10 +154,10 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
         const int lo = base + tid * SEL_PER;
         int ch[SEL_PER], ps[SEL_PER];
         load_block(a.chunk, lo, a.len, ch);
-        load_block(a.pos_in, lo, a.len, ps);
+        load_block(a.pos, lo, a.len, ps);
         const bool has_prev = lo > 0 && lo <= a.len;
         const int pc0 = has_prev ? a.chunk[lo - 1] : -1;
-        int pc = pc0, pp = has_prev ? a.pos_in[lo - 1] : 0;
+        int pc = pc0, pp = has_prev ? a.pos[lo - 1] : 0;
         int bad = 0, cnt = 0;
 #pragma unroll
         for (int k = 0; k < SEL_PER; ++k) {
@@ -238,10 +243,12 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     // ---- pass 2: keep list (ascending) and its inverse on destinations [0, M)
     int total_kept = 0;
     int first_move = a.M;  // smallest destination d with keep[d] != d
+    const int n_evict = a.len - a.M;
     for (int base = 0; base < a.len; base += SEL_BLOCK) {
         const int lo = base + tid * SEL_PER;
-        int ch[SEL_PER];
+        int ch[SEL_PER], sl[SEL_PER];
         load_block(a.chunk, lo, a.len, ch);
+        if (a.slot) load_block(a.slot, lo, a.len, sl);
         int pc = (lo > 0 && lo <= a.len) ? a.chunk[lo - 1] : -1;
         int r = (lo < a.len) ? a.th_run[base / SEL_PER + tid] - 1 : -1;  // run holding the slot before lo
         int from = (r >= 0 && r < R) ? a.run_from[r] : 0;
@@ -276,8 +283,10 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
                     }
                     if (i < a.M) a.inv[i] = off;
                     ++off;
-                } else if (i < a.M) {
-                    a.inv[i] = -1;
+                } else {
+                    if (i < a.M) a.inv[i] = -1;
+                    // evicted token i is the (i - off)-th evicted one in logical order
+                    if (a.slot && i - off < n_evict) a.free_out[i - off] = sl[k];
                 }
             }
         }
@@ -301,6 +310,37 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
         }
     }
     for (int i = first_move * a.n_chunks + tid; i < a.n_flags; i += SEL_THREADS) a.flags[i] = 0;
+
+    // ---- indexed variant: pos, chunk_id and slot move down in place,
+    // new[d] = old[keep[d]] for the moving destinations [first_move, M).
+    // keep[d] >= d, so a block of destinations only reads at or above its own
+    // start; each block reads everything before any thread writes, and the
+    // next block's reads lie above what this block writes.
+    if (a.slot && total_kept == a.M) {
+        for (int base = first_move; base < a.M; base += SEL_BLOCK) {
+            int vp[SEL_PER], vc[SEL_PER], vs[SEL_PER];
+#pragma unroll
+            for (int k = 0; k < SEL_PER; ++k) {
+                const int d = base + k * SEL_THREADS + tid;
+                if (d < a.M) {
+                    const int src = a.keep[d];
+                    vp[k] = a.pos[src];
+                    vc[k] = a.chunk[src];
+                    vs[k] = a.slot[src];
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int k = 0; k < SEL_PER; ++k) {
+                const int d = base + k * SEL_THREADS + tid;
+                if (d < a.M) {
+                    a.pos[d] = vp[k];
+                    a.chunk[d] = vc[k];
+                    a.slot[d] = vs[k];
+                }
+            }
+        }
+    }
 }
 
 struct GatherArgs {
@@ -444,7 +484,7 @@ KvWorkspace kv_workspace_layout(int n_layers, int row_bytes, int capacity) {
 hipError_t launch_kv_evict(const KvLaunch &p, hipStream_t stream) {
     char *ws = p.ws;
     KvArgs a;
-    a.pos_in = p.pos;
+    a.pos = p.pos;
     a.chunk = p.chunk_id;
     a.scores = p.chunk_scores;
     a.num_chunks = p.num_chunks;
@@ -467,12 +507,14 @@ hipError_t launch_kv_evict(const KvLaunch &p, hipStream_t stream) {
     a.run_from = (int32_t *)(ws + p.lay.offRunFrom);
     a.flags = (int32_t *)(ws + p.lay.offFlags);
     a.keep_out = p.keep_out;
+    a.slot = p.slot;
+    a.free_out = p.free_out;
     a.plane_tab = (char **)(ws + p.lay.offPlanes);
     for (int i = 0; i < KV_MAX_PLANES; ++i) a.planes[i] = i < p.n_planes ? p.planes[i] : nullptr;
     a.n_planes = p.n_planes;
     hipLaunchKernelGGL(kv_select_kernel, dim3(1), dim3(SEL_THREADS), 0, stream, a);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    if (e != hipSuccess || p.slot) return e;  // the indexed variant moves no rows
 
     const long long groups = (long long)p.M * p.lay.n_chunks;
     if (groups == 0) return hipSuccess;

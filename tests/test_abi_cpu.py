@@ -29,7 +29,8 @@ def _declared():
 def test_header_declares_the_entry_points():
     names = _declared()
     for n in ["gdn_chunk_fwd", "deltas_drift", "deltas_drift_states", "kv_evict_topk", "ds_gdn_workspace_bytes",
-              "ds_kv_workspace_bytes", "ds_status_string", "ds_last_error", "ds_kv_device_status"]:
+              "ds_kv_workspace_bytes", "ds_status_string", "ds_last_error", "ds_kv_device_status",
+              "kv_evict_topk_indexed", "ds_kv_indexed_workspace_bytes"]:
         assert n in names
 
 
@@ -124,3 +125,29 @@ def test_kv_rejects_bad_arguments_and_noop(ds):
     assert call(17408, 16384, 0, 0, 65) == 6                                # too many spans
     assert call(17408, 16384, 0, 0, 1, wsb=8) == 8                          # workspace
     assert call(17408, 16384, 0, 0, 1, shape=ds.KvShape(40, 4096, 17408)) == 5
+
+
+def test_kv_indexed_rejects_bad_arguments_and_noop(ds):
+    L = ds.lib()
+    P = ctypes.c_void_p
+    f = P(1 << 20)
+    nl = ctypes.c_int32(-1)
+    assert ds.kv_indexed_workspace_bytes(17408) > 17408 * 4 * 5
+    assert ds.kv_indexed_workspace_bytes(0) == 0
+    # no gather flags: far smaller than the gather variant's workspace
+    assert ds.kv_indexed_workspace_bytes(17408) < ds.kv_workspace_bytes(8, 4096, 17408)
+
+    def call(length, M, ns, nw, nb, cap=17408, slot=f, free=f, ws=f, wsb=1 << 40):
+        return L.kv_evict_topk_indexed(cap, f, f, slot, f, 1024, length, M, ns, nw, nb, None, free,
+                                       ctypes.byref(nl), ws, wsb, None)
+
+    assert call(100, 200, 4, 8, 4, slot=None, free=None) == 0 and nl.value == 100   # under budget: no-op
+    assert call(20000, 16384, 0, 0, 1) == 2                                 # len > capacity
+    assert call(17408, 16, 10, 10, 1) == 6                                  # reserved > M
+    assert call(17408, 16384, 0, 0, 65) == 6                                # too many spans
+    assert call(17408, 16384, 0, 0, 1, slot=None) == 1                      # slot table required
+    assert call(17408, 16384, 0, 0, 1, free=None) == 1                      # free list required
+    assert call(17408, 16384, 0, 0, 1, free=P((1 << 20) + 4)) == 4          # alignment
+    assert call(17408, 16384, 0, 0, 1, wsb=8) == 8                          # workspace
+    assert L.kv_evict_topk_indexed(17408, f, f, f, f, 1024, 17408, 16384, 0, 0, 1, None, f, None, f,
+                                   1 << 40, None) == 1                      # new_len required

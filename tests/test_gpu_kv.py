@@ -166,3 +166,137 @@ def test_broken_invariants_leave_cache_untouched(ds):
     assert ds.kv_device_status(ws)[0] == 1
     assert torch.equal(ks[0], before)
     assert np.array_equal(p.cpu().numpy(), pos)
+
+
+# ---------------------------------------------------------------- slot-indexed variant
+def indexed_event(ds, chunk, pos, scores, M, ns, nw, nb, seed=0, capacity=None):
+    """kv_evict_topk_indexed on a table whose rows are scattered over the
+    physical cache; keep list, compacted table and free list bit-exact with
+    the oracle."""
+    n = len(pos)
+    capacity = capacity or n + 5
+    rng = np.random.default_rng(seed)
+    slot = rng.permutation(capacity)[:n].astype(np.int32)
+    mk = lambda a: torch.as_tensor(np.concatenate([np.asarray(a, np.int32),
+                                                   np.full(capacity - n, -7, np.int32)]), device=DEV)
+    p, c, s = mk(pos), mk(chunk), mk(slot)
+    sc = torch.as_tensor(np.asarray(scores, np.float32), device=DEV)
+    keep = torch.full((max(M, 1),), -1, dtype=torch.int32, device=DEV)
+    new_len, ws, free = ds.kv_evict_topk_indexed(p, c, s, sc, n, M, ns, nw, nb, keep_out=keep)
+    torch.cuda.synchronize()
+    if n <= M:
+        assert new_len == n
+        assert np.array_equal(s[:n].cpu().numpy(), slot) and np.array_equal(p[:n].cpu().numpy(), pos)
+        return
+    ref = oracle.select_keep(chunk, pos, scores, n, M, ns, nw, nb)
+    assert new_len == M
+    assert ds.kv_device_status(ws)[0] == 0
+    assert keep[:M].cpu().tolist() == ref
+    ep, ec, es, efree = oracle.compact_indexed(pos, chunk, slot, ref, n)
+    assert np.array_equal(p[:M].cpu().numpy(), ep)
+    assert np.array_equal(c[:M].cpu().numpy(), ec)
+    assert np.array_equal(s[:M].cpu().numpy(), es)
+    assert np.array_equal(free[:n - M].cpu().numpy(), efree)
+    assert np.array_equal(s[n:].cpu().numpy(), np.full(capacity - n, -7))   # beyond len: untouched
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_indexed_random_small_caches(ds, seed):
+    rng = np.random.default_rng(2000 + seed)
+    chunk, pos = random_cache(rng, int(rng.integers(3, 40)), 1, 60)
+    n = len(chunk)
+    scores = rng.choice([0.1, 0.25, 0.5, 1.0, 2.0], size=int(chunk.max()) + 1).astype(np.float32)
+    ns = int(rng.integers(0, 5))
+    nw = int(rng.integers(0, 40))
+    M = int(rng.integers(ns + nw, n + 3))
+    indexed_event(ds, chunk, pos, scores, M, ns, nw, int(rng.integers(0, 9)), seed=seed)
+
+
+@pytest.mark.parametrize("policy", [(0, 0, 1), (4, 1024, 4)])
+def test_indexed_eviction_loop_shape(ds, policy):
+    """17 chunks of 1024 tokens down to 16384, capacity 17408."""
+    rng = np.random.default_rng(6)
+    chunk = np.repeat(np.arange(17), 1024).astype(np.int32)
+    pos = np.arange(17 * 1024, dtype=np.int32) + 40000
+    scores = rng.random(17).astype(np.float32)
+    indexed_event(ds, chunk, pos, scores, 16384, *policy, seed=3, capacity=17408)
+
+
+def test_indexed_long_cache_several_blocks(ds):
+    """A cache of ~100k tokens, so that selection and the table compaction
+    both run over several 32768-slot blocks."""
+    rng = np.random.default_rng(8)
+    chunk, pos = random_cache(rng, 90, 900, 1400, thin=0.9)
+    scores = rng.random(90).astype(np.float32)
+    n = len(chunk)
+    indexed_event(ds, chunk, pos, scores, n // 2, 4, 1000, 5, seed=4)
+
+
+def test_indexed_matches_gather_in_a_stream(ds):
+    """Appends write each new chunk's K/V rows into the rows the previous
+    eviction freed (an index_copy by the caller); after every step the rows
+    read through the table equal the position-keyed rows of the gather-based
+    cache, which the gather variant itself rebuilds in the same loop."""
+    L, row, M, F, capacity = 2, 128, 700, 96, 700 + 96
+    rng = np.random.default_rng(12)
+    steps = 30
+    scores_all = rng.random(steps).astype(np.float32)
+    scores_all[0] = np.inf
+    sc = torch.as_tensor(scores_all, device=DEV)
+    # gather-based cache
+    ks, vs, p, c = make_cache(L, row, capacity, [], [])
+    # indexed cache: physical rows + table
+    kx = [torch.zeros((capacity, row), dtype=torch.int16, device=DEV) for _ in range(L)]
+    tp = torch.zeros(capacity, dtype=torch.int32, device=DEV)
+    tc = torch.zeros(capacity, dtype=torch.int32, device=DEV)
+    ts = torch.zeros(capacity, dtype=torch.int32, device=DEV)
+    free = torch.arange(capacity, dtype=torch.int32, device=DEV)
+    n, ws_g, ws_x = 0, None, None
+    for f in range(steps):
+        pt = torch.arange(f * F, (f + 1) * F, dtype=torch.int64, device=DEV) + 77
+        dst = free[:F].to(torch.int64)
+        for l in range(L):
+            rows_k = synth.kv_row_bits_torch(l, 0, pt, row)
+            ks[l][n:n + F] = rows_k
+            vs[l][n:n + F] = synth.kv_row_bits_torch(l, 1, pt, row)
+            kx[l].index_copy_(0, dst, rows_k)
+        p[n:n + F] = pt.to(torch.int32)
+        c[n:n + F] = f
+        tp[n:n + F] = pt.to(torch.int32)
+        tc[n:n + F] = f
+        ts[n:n + F] = dst.to(torch.int32)
+        n += F
+        kg = torch.empty(M, dtype=torch.int32, device=DEV)
+        kxk = torch.empty(M, dtype=torch.int32, device=DEV)
+        new_len, ws_g = ds.kv_evict_topk(ks, vs, p, c, sc, n, M, 4, 64, 4, keep_out=kg, workspace=ws_g)
+        new_x, ws_x, freed = ds.kv_evict_topk_indexed(tp, tc, ts, sc, n, M, 4, 64, 4, keep_out=kxk,
+                                                      workspace=ws_x)
+        assert new_x == new_len
+        free = free[F:]                              # rows never used so far
+        if n > M:
+            assert torch.equal(kg, kxk)
+            free = torch.cat([free, freed[:n - M]])
+        n = new_len
+        torch.cuda.synchronize()
+        assert torch.equal(tp[:n], p[:n]) and torch.equal(tc[:n], c[:n])
+        idx = ts[:n].to(torch.int64)
+        for l in range(L):
+            assert torch.equal(kx[l][idx], ks[l][:n]), f"step {f} layer {l}"
+        assert sorted(torch.cat([ts[:n], free]).cpu().tolist()) == list(range(capacity))
+
+
+def test_indexed_broken_invariants_leave_table_untouched(ds):
+    chunk = np.repeat(np.arange(6), 20).astype(np.int32)
+    pos = np.arange(120, dtype=np.int32)
+    pos[70] = pos[69]                                # positions not increasing
+    p = torch.as_tensor(pos, device=DEV)
+    c = torch.as_tensor(chunk, device=DEV)
+    s = torch.arange(120, dtype=torch.int32, device=DEV)
+    free = torch.full((60,), -3, dtype=torch.int32, device=DEV)
+    sc = torch.ones(6, dtype=torch.float32, device=DEV)
+    new_len, ws, _ = ds.kv_evict_topk_indexed(p, c, s, sc, 120, 60, 0, 0, 1, free_out=free)
+    torch.cuda.synchronize()
+    assert ds.kv_device_status(ws)[0] == 1
+    assert np.array_equal(p.cpu().numpy(), pos) and np.array_equal(c.cpu().numpy(), chunk)
+    assert torch.equal(s, torch.arange(120, dtype=torch.int32, device=DEV))
+    assert torch.equal(free, torch.full((60,), -3, dtype=torch.int32, device=DEV))

@@ -377,6 +377,63 @@ def test_compaction_keeps_positions_and_rows():
     assert np.array_equal(new_rows, synth.kv_row_bits(3, 1, new_pos, 16))
 
 
+def test_indexed_compaction_equals_gather_over_a_stream():
+    """A slot-indexed cache evicts the same tokens as the gather and moves
+    none of their rows: over a stream of appends (new tokens written into the
+    freed rows) and evictions, the rows read through the table always equal
+    the gathered cache, the table is a permutation of the rows in use, and the
+    free list holds exactly the rows of the evicted tokens in logical order."""
+    rng = np.random.default_rng(23)
+    F, M, cap, steps, W = 37, 150, 150 + 37, 30, 8
+    scores = rng.random(steps).astype(np.float32)
+    # gather cache: rows in logical order; indexed cache: physical rows + table
+    dt = synth.kv_row_bits(0, 0, np.zeros(1, np.int64), W).dtype
+    g_rows = np.zeros((0, W), dt)
+    g_pos = np.zeros(0, np.int64)
+    g_chunk = np.zeros(0, np.int64)
+    phys = np.zeros((cap, W), dt)
+    t_pos, t_chunk, t_slot = np.zeros(0, np.int64), np.zeros(0, np.int64), np.zeros(0, np.int64)
+    free = np.arange(cap)
+    for f in range(steps):
+        new_pos = np.arange(f * F, (f + 1) * F) + 500
+        new_rows = synth.kv_row_bits(2, 0, new_pos, W)
+        g_rows = np.concatenate([g_rows, new_rows])
+        g_pos = np.concatenate([g_pos, new_pos])
+        g_chunk = np.concatenate([g_chunk, np.full(F, f)])
+        dst = free[:F]
+        phys[dst] = new_rows
+        t_pos = np.concatenate([t_pos, new_pos])
+        t_chunk = np.concatenate([t_chunk, np.full(F, f)])
+        t_slot = np.concatenate([t_slot, dst])
+        free = free[F:]
+        n = len(g_pos)
+        if n > M:
+            keep = oracle.select_keep(g_chunk, g_pos, scores, n, M, 2, 20, 3)
+            assert keep == oracle.select_keep(t_chunk, t_pos, scores, n, M, 2, 20, 3)
+            before, slot_before = phys.copy(), t_slot.copy()
+            t_pos, t_chunk, t_slot, freed = oracle.compact_indexed(t_pos, t_chunk, t_slot, keep, n)
+            assert np.array_equal(phys, before)                       # no row moved
+            evicted = [i for i in range(n) if i not in set(keep)]
+            assert freed.tolist() == [int(slot_before[i]) for i in evicted]
+            assert len(freed) == n - M
+            free = np.concatenate([free, freed])
+            g_rows, g_pos, g_chunk = oracle.compact(g_rows, keep), g_pos[keep], g_chunk[keep]
+        assert np.array_equal(t_pos, g_pos) and np.array_equal(t_chunk, g_chunk)
+        assert np.array_equal(phys[t_slot], g_rows)
+        assert sorted(np.concatenate([t_slot, free]).tolist()) == list(range(cap))
+
+
+def test_indexed_free_list_by_hand():
+    """A 6-token table with rows scattered in physical memory; keeping logical
+    tokens 1, 2 and 4 frees the rows of tokens 0, 3 and 5, in that order."""
+    pos = np.array([10, 11, 12, 13, 14, 15])
+    chunk = np.array([0, 0, 1, 1, 2, 2])
+    slot = np.array([7, 2, 9, 0, 4, 5])
+    p2, c2, s2, free = oracle.compact_indexed(pos, chunk, slot, [1, 2, 4], 6)
+    assert p2.tolist() == [11, 12, 14] and c2.tolist() == [0, 1, 2]
+    assert s2.tolist() == [2, 9, 4] and free.tolist() == [7, 0, 5]
+
+
 # ---------------------------------------------------------------- P12
 def test_paper_size_constants():
     """48 MiB of recurrent state over 24 layers and 32 KiB of KV per token
