@@ -344,7 +344,8 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
 //                    updates its half, S = Gamma_last S0 + (D_last E)^T K.
 //                    Every product's result becomes the next product's B
 //                    operand inside the registers.  S0 and E are published in
-//                    LDS for the output waves; frame ends write drift sums.
+//                    LDS for the output waves; at a frame end each lane
+//                    leaves its share of the drift sums in LDS.
 //   waves 2 and 3, output:  one tile behind, O = diag(Gamma) Q S0^T + P E for
 //                    row blocks {0, 1} and {2, 3}; they load q, P and Gamma
 //                    themselves.
@@ -352,7 +353,9 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
 //                    v rows and the decay factors of a tile three tiles ahead
 //                    and stages it in LDS one tile ahead.  The state waves read
 //                    K as rows (A operand of K S0^T) and, by transposing reads,
-//                    as K^T (A operand of the state update).
+//                    as K^T (A operand of the state update).  Loader 3 also
+//                    reduces the frame-end drift sums over the lanes, one tile
+//                    later, off the state waves' chain.
 // All eight waves meet at one barrier per tile.  A single wave moves data
 // from L2 and from LDS at a limited rate, which is why the chain is shared by
 // two waves, every tile is loaded by four waves, and operands move as whole
@@ -432,6 +435,7 @@ struct SeqShared {
     u32x4 Shi[2][KS][64];      // S0 as B operand, high bf16 term (for the output waves)
     u32x4 Slo[2][KS][64];      // low bf16 term
     u32x4 E[2][2][64];         // E as B operand (fp16)
+    float2 DR[2][2][64];       // per-lane drift sums of a frame end: [frame % 2][state wave][lane]
     int xflag[2];              // tiles whose half of K S0^T each state wave has published
 };
 
@@ -529,6 +533,7 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             S0f[c] = S[c];
         }
         int frame = frame_base;
+        int frame_end = a.frame_len > 0 ? min(a.frame_len, len) : len;  // tokens done at the next frame end
 
         auto tile = [&](int lt, auto bufc) __attribute__((always_inline)) {
             constexpr int buf = decltype(bufc)::value;  // == lt % 2
@@ -659,9 +664,9 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
 #pragma unroll
             for (int c = 0; c < HKB; ++c) S[c] = Sn[c];
 
-            // frame end: drift sums of this half of the slice, optional snapshot
-            const int done = TILE * lt + n;
-            if (DRIFT && ((a.frame_len > 0 && done % a.frame_len == 0) || done == len)) {
+            // frame end: per-lane drift sums of this half of the slice (a
+            // loader wave reduces them over the lanes), optional snapshot
+            if (DRIFT && TILE * lt + n == frame_end) {
                 float num = 0.f, den = 0.f;
 #pragma unroll
                 for (int c = 0; c < HKB; ++c)
@@ -671,13 +676,7 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                         num += dl * dl;
                         den += S0f[c][e] * S0f[c][e];
                     }
-                num = wave_sum(num);
-                den = wave_sum(den);
-                if (lane == 0 && a.wsDrift && frame < a.n_frames) {
-                    float *dst = a.wsDrift + ((((size_t)frame * a.H_v + j) * a.n_split + sl) * 2 + hh) * 2;
-                    dst[0] = num;
-                    dst[1] = den;
-                }
+                sh.DR[frame & 1][hh][lane] = float2{num, den};
                 if (a.snapshots && frame < a.n_frames) {
                     float *snap = a.snapshots + ((size_t)frame * a.H_v + j) * D * D + (size_t)(v0 + ln) * D;
 #pragma unroll
@@ -688,6 +687,7 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
 #pragma unroll
                 for (int c = 0; c < HKB; ++c) S0f[c] = S[c];
                 ++frame;
+                frame_end = min(frame_end + a.frame_len, len);
             }
         };
         for (int lt = 0; lt < n_tiles; lt += 2) {
@@ -873,6 +873,24 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             if (lane < 32) *(u32x4 *)(&sh.V[buf][(16 * x + (lane >> 1)) * 16 + 8 * (lane & 1)]) = s.v;
             if (x < 2) sh.G[buf][x][lane] = s.g;
         };
+        // drift sums: the state waves leave per-lane sums of a frame ending in
+        // tile t in LDS; loader 3 reduces them after the next barrier (the
+        // buffer of that frame's parity is written again two frames later,
+        // after a barrier this wave only reaches once it is done reading)
+        int frame = frame_base;
+        int frame_end = a.frame_len > 0 ? min(a.frame_len, len) : len;
+        auto drift_reduce = [&](int it) __attribute__((always_inline)) {
+            if (!DRIFT || x != 3 || it < 1) return;
+            const int lt = it - 1;
+            if (TILE * lt + min(TILE, len - TILE * lt) != frame_end) return;
+            if (a.wsDrift && frame < a.n_frames) {
+                const float2 p0 = sh.DR[frame & 1][0][lane], p1 = sh.DR[frame & 1][1][lane];
+                const float num = wave_sum(p0.x + p1.x), den = wave_sum(p0.y + p1.y);
+                if (lane == 0) *(float2 *)(a.wsDrift + (((size_t)frame * a.H_v + j) * a.n_split + sl) * 2) = float2{num, den};
+            }
+            ++frame;
+            frame_end = min(frame_end + a.frame_len, len);
+        };
         // tile t lives in register set t % 2 and LDS buffer t % 2.  Iteration it
         // stages tile it + 1 and then loads tile it + 3 into the set just freed.
         if (n_tiles > 0) {
@@ -885,6 +903,7 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                 lds_barrier();
                 if (it + 1 < n_tiles) stage(s, bufc);
                 load(s, it + 3);
+                drift_reduce(it);
             };
             for (int it = 0; it <= n_tiles; it += 2) {
                 step(it, s1, std::integral_constant<int, 1>());
@@ -909,9 +928,9 @@ __global__ __launch_bounds__(256) void gdn_drift_finalize_kernel(const float *ws
     const int f = idx / H_v;
     float num = 0.f, den = 0.f;
     if (f < real) {
-        for (int s = 0; s < 2 * n_split; ++s) {
-            num += ws[((size_t)idx * 2 * n_split + s) * 2];
-            den += ws[((size_t)idx * 2 * n_split + s) * 2 + 1];
+        for (int s = 0; s < n_split; ++s) {
+            num += ws[((size_t)idx * n_split + s) * 2];
+            den += ws[((size_t)idx * n_split + s) * 2 + 1];
         }
     }
     out[(size_t)idx * 2] = num;
@@ -967,7 +986,7 @@ GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, i
     w.offGam = off;
     off = align256(off + (size_t)w.tiles_max * H_v * 128 * sizeof(float));
     w.offDrift = off;
-    off = align256(off + (size_t)n_frames * H_v * w.n_split * 2 * 2 * sizeof(float));
+    off = align256(off + (size_t)n_frames * H_v * w.n_split * 2 * sizeof(float));
     w.offWrite = off;
     off = align256(off + (size_t)T_total * H_v * w.n_split * sizeof(float));
     w.total = off;
