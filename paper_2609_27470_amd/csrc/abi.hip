@@ -120,6 +120,7 @@ ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k,
     char *ws = (char *)workspace;
     p.wsT = (_Float16 *)(ws + lay.offT);
     p.wsP = (_Float16 *)(ws + lay.offP);
+    p.wsQ = (_Float16 *)(ws + lay.offQ);
     p.wsGam = (float *)(ws + lay.offGam);
     p.wsDrift = (float *)(ws + lay.offDrift);
     p.wsWrite = (float *)(ws + lay.offWrite);

@@ -44,6 +44,8 @@ __device__ __forceinline__ half8 bf16x8_to_f16(uint4 r) {
     return o;
 }
 
+__device__ __forceinline__ half8 bf16x8_to_f16(u32x4 r) { return bf16x8_to_f16(uint4{r[0], r[1], r[2], r[3]}); }
+
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 r) { return __builtin_bit_cast(bf16x8, r); }
 __device__ __forceinline__ half8 as_half8(uint4 r) { return __builtin_bit_cast(half8, r); }
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 r) { return __builtin_bit_cast(bf16x8, r); }

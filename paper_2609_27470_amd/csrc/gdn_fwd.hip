@@ -50,7 +50,7 @@ struct GdnArgs {
     void *o;
     float scale;
     float *snapshots;
-    _Float16 *wsT, *wsP;
+    _Float16 *wsT, *wsP, *wsQ;
     float *wsGam, *wsDrift;
     float *wsWrite;  // per-token sums of squares of E over the slice's columns, or null
     int n_split;
@@ -165,8 +165,11 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
         for (int c = 0; c < NI; ++c) {
             const int row = 16 * w + RPI * c + lane / CH, ch = lane % CH;
             const u32x4 z = {0u, 0u, 0u, 0u};
+            const u32x4 q = row < n ? qv[c] : z;
             *(u32x4 *)(&Kl[row * D + 8 * (ch ^ swz<D>(row))]) = row < n ? kv[c] : z;
-            *(u32x4 *)(&Ql[row * D + 8 * (ch ^ swz<D>(row))]) = row < n ? qv[c] : z;
+            *(u32x4 *)(&Ql[row * D + 8 * (ch ^ swz<D>(row))]) = q;
+            // q rows in fp16 for the output waves of the sequential kernel
+            *(u32x4 *)(a.wsQ + (((size_t)ti * a.H_k + h) * 64 + row) * D + 8 * ch) = __builtin_bit_cast(u32x4, bf16x8_to_f16(q));
         }
     }
     __syncthreads();
@@ -376,42 +379,13 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
 //     prep kernel writes T diag(beta) and P with their token columns in that
 //     order, and the K^T fragments are read from LDS in it.
 //
-// Precision: k and q stay bf16 (as given) and meet the fp32 state through
-// bf16 matrix-core products against a two-term bf16 split of the state
-// (S ~ S_hi + S_lo, relative error ~2^-17); D_last E enters the state update
-// the same way.  R, E, T diag(beta) and P are fp16.  All accumulation is fp32.
+// Precision: the state stays fp32 in registers; as a matrix-core operand it
+// is rounded to fp16 (relative error 2^-11, the same as R and E), and k and q
+// meet it as fp16 (exact conversions of the bf16 inputs in fp16's normal
+// range).  D_last E enters the state update as fp16; R, E, T diag(beta) and
+// P are fp16.  All accumulation is fp32.
 // ============================================================================
 
-// fp32 pair -> bf16 pair (round to nearest even), packed in one dword
-__device__ __forceinline__ uint32_t bf16_pack(float x, float y) {
-    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-    bf16x2 r = {(__bf16)x, (__bf16)y};
-    return __builtin_bit_cast(uint32_t, r);
-}
-__device__ __forceinline__ float bf16_lo_f(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf16_hi_f(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-// Two C blocks -> one B operand as two bf16 terms (x ~ hi + lo).  The
-// remainder x - hi comes from one bf16 dot product per value,
-// x + hi . (-1, 0), which is exact (hi and x are within a factor of 2).
-// The constant pairs are kept in scalar registers: as a literal operand the
-// compiler encodes (-1, 0) as the fp32 inline constant -1.0, which the
-// hardware does not read as that bf16 pair.
-__device__ __forceinline__ void split_bf16(const f32x4 &a, const f32x4 &b, u32x4 &hi, u32x4 &lo) {
-    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-    uint32_t c0 = 0x0000bf80u, c1 = 0xbf800000u;  // (-1, 0) and (0, -1)
-    asm volatile("" : "+s"(c0), "+s"(c1));
-    const bf16x2 m0 = __builtin_bit_cast(bf16x2, c0), m1 = __builtin_bit_cast(bf16x2, c1);
-    const float x[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-        const uint32_t h = bf16_pack(x[2 * p], x[2 * p + 1]);
-        const bf16x2 hv = __builtin_bit_cast(bf16x2, h);
-        hi[p] = h;
-        lo[p] = bf16_pack(__builtin_amdgcn_fdot2_f32_bf16(hv, m0, x[2 * p], false),
-                          __builtin_amdgcn_fdot2_f32_bf16(hv, m1, x[2 * p + 1], false));
-    }
-}
 // Two C blocks -> one fp16 B operand.
 __device__ __forceinline__ half8 to_half8(const f32x4 &a, const f32x4 &b) {
     half8 r;
@@ -426,14 +400,13 @@ __device__ __forceinline__ half8 to_half8(const f32x4 &a, const f32x4 &b) {
 template <int D>
 struct SeqShared {
     static constexpr int KS = D / 32, NKB = D / 16;
-    uint16_t K[2][64 * D];     // K tile, row-major, 16-byte chunks XOR-swizzled by row (swz)
+    uint16_t K[2][64 * D];     // K tile (fp16), row-major, 16-byte chunks XOR-swizzled by row (swz)
     u32x4 T[2][6][64];         // T diag(beta) A-fragments
     uint16_t V[2][64 * 16];    // v[token][v0 .. v0 + 15] (bf16, read transposed)
     uint32_t Ost[2][32 * 16];  // per output wave: its 32 rows of o, staged for 16-byte row stores
     float G[2][2][64];         // Gamma_r and D_last,r
     f32x4 X[2][2][4][64];      // exchanged halves of K S0^T: [tile % 2][state wave][rb][lane]
-    u32x4 Shi[2][KS][64];      // S0 as B operand, high bf16 term (for the output waves)
-    u32x4 Slo[2][KS][64];      // low bf16 term
+    u32x4 S16[2][KS][64];      // S0 as fp16 B operand (for the output waves)
     u32x4 E[2][2][64];         // E as B operand (fp16)
     float2 DR[2][2][64];       // per-lane drift sums of a frame end: [frame % 2][state wave][lane]
     int xflag[2];              // tiles whose half of K S0^T each state wave has published
@@ -455,7 +428,7 @@ struct LoadSet {
 // Output-wave registers for one tile (two row blocks).
 template <int D>
 struct OutSet {
-    u32x4 q[2][D / 32];  // q rows 16 rb + ln, dims 32 ks + 8 lg .. + 7
+    u32x4 q[2][D / 32];  // q rows 16 rb + ln (fp16), dims 32 ks + 8 lg .. + 7
     u32x4 p[4];          // P fragments of the two row blocks (2 or 4 used)
     float4 gam[2];       // Gamma of rows 16 rb + 4 lg + e
 };
@@ -548,17 +521,16 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) Sn[c][e] = gl * S[c][e];
 
-            // own half of S0 as B operand (two bf16 terms), also published
-            u32x4 shi[HKS], slo[HKS];
+            // own half of S0 as fp16 B operand, also published
+            half8 s16[HKS];
 #pragma unroll
             for (int c = 0; c < HKS; ++c) {
-                split_bf16(S[2 * c], S[2 * c + 1], shi[c], slo[c]);
-                sh.Shi[buf][hh * HKS + c][lane] = shi[c];
-                sh.Slo[buf][hh * HKS + c][lane] = slo[c];
+                s16[c] = to_half8(S[2 * c], S[2 * c + 1]);
+                sh.S16[buf][hh * HKS + c][lane] = __builtin_bit_cast(u32x4, s16[c]);
             }
 
             // every operand of the tile read now, so that the reads overlap the work below
-            bf16x8 ktf[2][HKB];
+            half8 ktf[2][HKB];
             half8 tf[6];
             float4 gam4[4], dl4[4];
             v4i16 vv4[4];
@@ -571,8 +543,8 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                     const int kb = hh * HKB + c;
                     const int r0 = 32 * ks + 4 * lg + (ln >> 2), r1 = r0 + 16;
                     const int ch = 4 * (kb >> 1) + (ln & 3), half = 4 * (kb & 1);
-                    ktf[ks][c] = __builtin_bit_cast(bf16x8, cat_u32x4(ds_read_tr16(&sh.K[buf][r0 * D + 8 * (ch ^ swz<D>(r0)) + half]),
-                                                                      ds_read_tr16(&sh.K[buf][r1 * D + 8 * (ch ^ swz<D>(r1)) + half])));
+                    ktf[ks][c] = __builtin_bit_cast(half8, cat_u32x4(ds_read_tr16(&sh.K[buf][r0 * D + 8 * (ch ^ swz<D>(r0)) + half]),
+                                                                     ds_read_tr16(&sh.K[buf][r1 * D + 8 * (ch ^ swz<D>(r1)) + half])));
                 }
 #pragma unroll
             for (int f = 0; f < 6; ++f) tf[f] = as_half8(sh.T[buf][f][lane]);
@@ -590,16 +562,14 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             for (int rb = 0; rb < 4; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int c = 0; c < HKS; ++c) {
-                bf16x8 ka[4];
+                half8 ka[4];
 #pragma unroll
                 for (int rb = 0; rb < 4; ++rb) {
                     const int row = 16 * rb + ln;
-                    ka[rb] = as_bf16x8(*(const u32x4 *)(&sh.K[buf][row * D + 8 * ((4 * (hh * HKS + c) + lg) ^ swz<D>(row))]));
+                    ka[rb] = as_half8(*(const u32x4 *)(&sh.K[buf][row * D + 8 * ((4 * (hh * HKS + c) + lg) ^ swz<D>(row))]));
                 }
 #pragma unroll
-                for (int rb = 0; rb < 4; ++rb) acc[rb] = mfma_bf16(ka[rb], as_bf16x8(shi[c]), acc[rb]);
-#pragma unroll
-                for (int rb = 0; rb < 4; ++rb) acc[rb] = mfma_bf16(ka[rb], as_bf16x8(slo[c]), acc[rb]);
+                for (int rb = 0; rb < 4; ++rb) acc[rb] = mfma_f16(ka[rb], s16[c], acc[rb]);
             }
             // exchange with the other state wave
 #pragma unroll
@@ -639,7 +609,7 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                 sh.E[buf][1][lane] = __builtin_bit_cast(u32x4, to_half8(E[2], E[3]));
             }
 
-            // D_last E as B operand (two bf16 terms)
+            // D_last E as fp16 B operand
             f32x4 DE[4];
 #pragma unroll
             for (int rb = 0; rb < 4; ++rb) {
@@ -649,18 +619,13 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                 DE[rb][2] = E[rb][2] * d4.z;
                 DE[rb][3] = E[rb][3] * d4.w;
             }
-            u32x4 dhi[2], dlo[2];
-            split_bf16(DE[0], DE[1], dhi[0], dlo[0]);
-            split_bf16(DE[2], DE[3], dhi[1], dlo[1]);
+            const half8 d16[2] = {to_half8(DE[0], DE[1]), to_half8(DE[2], DE[3])};
 
             // own half of S = Gamma_last S0 + (D_last E)^T K
 #pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
+            for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-                for (int c = 0; c < HKB; ++c) Sn[c] = mfma_bf16(ktf[ks][c], as_bf16x8(dhi[ks]), Sn[c]);
-#pragma unroll
-                for (int c = 0; c < HKB; ++c) Sn[c] = mfma_bf16(ktf[ks][c], as_bf16x8(dlo[ks]), Sn[c]);
-            }
+                for (int c = 0; c < HKB; ++c) Sn[c] = mfma_f16(ktf[ks][c], d16[ks], Sn[c]);
 #pragma unroll
             for (int c = 0; c < HKB; ++c) S[c] = Sn[c];
 
@@ -706,14 +671,13 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
         // iteration issues the same memory operations)
         auto load = [&](OutSet<D> &s, int lt_) __attribute__((always_inline)) {
             const int lt = min(lt_, n_tiles - 1);
-            const int t0 = st + TILE * lt, n = min(TILE, en - t0);
             const size_t tv = (size_t)(tile_base + lt) * a.H_v + j;
-            const uint16_t *qb = a.q + (size_t)t0 * a.H_k * D + (size_t)qh * D + 8 * lg;
+            const _Float16 *qb = a.wsQ + ((size_t)(tile_base + lt) * a.H_k + qh) * 64 * D + 8 * lg;
 #pragma unroll
             for (int r = 0; r < 2; ++r) {
-                const uint32_t row = (uint32_t)min(16 * (2 * pr + r) + ln, n - 1);
+                const uint32_t row = (uint32_t)(16 * (2 * pr + r) + ln);
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks) s.q[r][ks] = *(const u32x4 *)(qb + row * (uint32_t)a.H_k * D + 32 * ks);
+                for (int ks = 0; ks < KS; ++ks) s.q[r][ks] = *(const u32x4 *)(qb + row * (uint32_t)D + 32 * ks);
             }
             const u32x4 *pb = (const u32x4 *)(a.wsP + tv * TP_HALVES);
             // fragments of row blocks 2 pr, 2 pr + 1: {0, 1} or {2, 3, 4, 5}
@@ -729,11 +693,9 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                const bf16x8 bh = as_bf16x8(sh.Shi[buf][ks][lane]), bl = as_bf16x8(sh.Slo[buf][ks][lane]);
+                const half8 bs = as_half8(sh.S16[buf][ks][lane]);
 #pragma unroll
-                for (int r = 0; r < 2; ++r) acc[r] = mfma_bf16(as_bf16x8(s.q[r][ks]), bh, acc[r]);
-#pragma unroll
-                for (int r = 0; r < 2; ++r) acc[r] = mfma_bf16(as_bf16x8(s.q[r][ks]), bl, acc[r]);
+                for (int r = 0; r < 2; ++r) acc[r] = mfma_f16(as_half8(s.q[r][ks]), bs, acc[r]);
             }
 #pragma unroll
             for (int r = 0; r < 2; ++r) {
@@ -866,7 +828,7 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
 #pragma unroll
             for (int c = 0; c < NK; ++c) {
                 const int row = 16 * x + RPI * c + lane / CH, ch = lane % CH;
-                *(u32x4 *)(&sh.K[buf][row * D + 8 * (ch ^ swz<D>(row))]) = s.k[c];
+                *(u32x4 *)(&sh.K[buf][row * D + 8 * (ch ^ swz<D>(row))]) = __builtin_bit_cast(u32x4, bf16x8_to_f16(s.k[c]));
             }
             sh.T[buf][t_first][lane] = s.t[0];
             if (nt == 2) sh.T[buf][t_first + 1][lane] = s.t[1];
@@ -983,6 +945,8 @@ GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, i
     off = align256(off + (size_t)w.tiles_max * H_v * TP_HALVES * sizeof(_Float16));
     w.offP = off;
     off = align256(off + (size_t)w.tiles_max * H_v * TP_HALVES * sizeof(_Float16));
+    w.offQ = off;
+    off = align256(off + (size_t)w.tiles_max * H_k * 64 * d * sizeof(_Float16));
     w.offGam = off;
     off = align256(off + (size_t)w.tiles_max * H_v * 128 * sizeof(float));
     w.offDrift = off;
@@ -1014,6 +978,7 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     a.snapshots = p.snapshots;
     a.wsT = p.wsT;
     a.wsP = p.wsP;
+    a.wsQ = p.wsQ;
     a.wsGam = p.wsGam;
     a.wsDrift = p.drift_partials ? p.wsDrift : nullptr;
     a.wsWrite = p.write_partials ? p.wsWrite : nullptr;

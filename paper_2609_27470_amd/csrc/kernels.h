@@ -24,8 +24,9 @@ struct GdnLaunch {
     // workspace pieces
     _Float16 *wsT;      // [tiles_max][H_v][6][64][8]  T diag(beta), fp16 A-fragments
     _Float16 *wsP;      // [tiles_max][H_v][6][64][8]  D (.) tril(Q K^T), fp16 A-fragments
+    _Float16 *wsQ;      // [tiles_max][H_k][64][d]     q rows in fp16 (zero past a ragged tile's end)
     float *wsGam;       // [tiles_max][H_v][2][64]   Gamma_r = exp(gamma_r), D_last,r = exp(gamma_last - gamma_r)
-    float *wsDrift;     // [n_frames][H_v][n_split][2][2] (one pair per half slice)
+    float *wsDrift;     // [n_frames][H_v][n_split][2] (one pair per slice)
     float *wsWrite;     // [T_total][H_v][n_split] per-token ||E row||^2 over each slice's columns
     int tiles_max;
     int n_split;        // d_v slices of 16 per (stream, v-head)
@@ -33,7 +34,7 @@ struct GdnLaunch {
 
 // Workspace layout shared by the size query and the launcher.
 struct GdnWorkspace {
-    size_t offT, offP, offGam, offDrift, offWrite, total;
+    size_t offT, offP, offQ, offGam, offDrift, offWrite, total;
     int tiles_max, n_split;
 };
 GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, int n_frames);

@@ -54,8 +54,9 @@ def test_gdn_workspace_size(ds):
     tiles = 512
     per = 2 * 6 * 64 * 8 * 2 + 128 * 4     # T and P fragments (fp16) + decay factors per (tile, v-head)
     wr = 32768 * 32 * 8 * 4                # per-token write norms per 16-row slice
-    assert nb >= tiles * 32 * per + wr
-    assert nb <= tiles * 32 * per + wr + 32 * 32 * 8 * 2 * 2 * 4 + 4096   # + drift sums per half slice
+    qh = tiles * 16 * 64 * 128 * 2         # q tiles in fp16 per qk-head
+    assert nb >= tiles * 32 * per + wr + qh
+    assert nb <= tiles * 32 * per + wr + qh + 32 * 32 * 8 * 2 * 4 + 4096   # + drift sums per slice
     bad = ds.gdn_shape([64], 1, 1, 96, 64)
     assert ds.gdn_workspace_bytes(bad) == 0
 
