@@ -316,6 +316,36 @@ def main():
     torch.cuda.synchronize()
     unfused_ms = e0.elapsed_time(e1) / reps
 
+    # ---------------- decode step (one token per stream, batched): the state is
+    # read and written once per step, so the bound is HBM
+    decode = {}
+    for Bd in (8, 256):
+        gen = torch.Generator(device=dev).manual_seed(Bd)
+        dq = torch.randn((Bd, H_K, D), generator=gen, device=dev)
+        dq = (dq / dq.norm(dim=-1, keepdim=True)).to(torch.bfloat16)
+        dk = torch.randn((Bd, H_K, D), generator=gen, device=dev)
+        dk = (dk / dk.norm(dim=-1, keepdim=True)).to(torch.bfloat16)
+        dv = torch.randn((Bd, H_V, D), generator=gen, device=dev).to(torch.bfloat16)
+        dg = -torch.nn.functional.softplus(torch.randn((Bd, H_V), generator=gen, device=dev))
+        db = torch.sigmoid(torch.randn((Bd, H_V), generator=gen, device=dev))
+        dst = 0.3 * torch.randn((Bd, H_V, D, D), generator=gen, device=dev)
+        do = torch.empty((Bd, H_V, D), dtype=torch.bfloat16, device=dev)
+        step_dec = lambda: ds.gdn_decode_step(dq, dk, dv, dg, db, state_in=dst, state_out=dst, o=do)
+        for _ in range(3):
+            step_dec()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            step_dec()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        dec_ms = e0.elapsed_time(e1) / reps
+        dec_bytes = Bd * H_V * (2 * D * D * 4 + D * 2 + D * 2 + 8) + Bd * H_K * D * 2 * 2
+        decode[f"B{Bd}"] = {"ms": dec_ms, "tokens_per_s": Bd / (dec_ms * 1e-3),
+                            "gbs": dec_bytes / (dec_ms * 1e-3) / 1e9,
+                            "hbm_frac": dec_bytes / (dec_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                            "bytes_per_step": dec_bytes}
+
     flops, bytes_ = algorithmic_work(T, H_K, H_V, D)
     achieved_gbs = bytes_ / (gdn_ms * 1e-3) / 1e9
     achieved_tflops = flops / (gdn_ms * 1e-3) / 1e12
@@ -369,6 +399,7 @@ def main():
         "evict_moved_rows_mean": float(moved_rows.mean()),
         "evict_gather_gbs": float((2 * moved_bytes).mean() / (evict_ms * 1e-3) / 1e9),
         "drift_overhead_paper_pct": 1.9,
+        "decode_step": decode,
         "evict_indexed": {
             "kv_evict_topk_indexed_ms": float(idx_evict_ms), "append_scatter_ms": float(idx_append_ms),
             "ms_per_step": float(gdn_ms + drift_ms + idx_append_ms + idx_evict_ms),

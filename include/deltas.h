@@ -1,14 +1,16 @@
 /*
  * deltas.h -- C ABI of the DeltaS hot path on MI355X (gfx950).
  *
- * Three operations, following the paper (DeltaS: reading the gated
+ * The operations, following the paper (DeltaS: reading the gated
  * linear-attention state for KV-cache eviction in streaming video):
  *
  *   gdn_chunk_fwd   gated-delta-rule forward of one linear-attention layer
  *                   (Section 3.2, Eq. 1 / Eq. 2) over packed streams, with
  *                   the per-frame state-drift sums of Eq. 3 fused in;
- *   deltas_drift    per-frame drift scores from those sums (Eq. 3 and the
- *                   line of Algorithm 1 that averages over layers);
+ *   gdn_decode_step one token per stream of the same recurrence, batched
+ *                   over streams (the step that follows a state restore);
+ *   deltas_drift    per-frame drift scores from those sums (Eq. 3 and
+ *                   Algorithm 1's mean over layers);
  *   kv_evict_topk   one eviction step of Algorithm 1 / Section 3.3:
  *                   sink + recent window + N temporal spans with per-span
  *                   top-k and fill, then an order-preserving in-place gather
@@ -136,6 +138,26 @@ ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k,
                         const float *state_in, float *state_out, void *o, int32_t o_dtype,
                         float scale, float *drift_partials, float *write_partials, float *snapshots,
                         void *workspace, size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * gdn_decode_step -- one token of Eq. 2 for each of B streams
+ * ------------------------------------------------------------------------
+ * For every stream b and v-head j (reading qk-head j * H_k / H_v), with
+ * alpha = exp(g[b][j]) and S = state_in[b][j] (zeros if state_in is NULL):
+ *     e = beta (v - alpha S k),  S' = alpha S + e k^T,  o = scale S' q
+ * (Section 3.2, Eq. 2; o read after the update as in gdn_chunk_fwd).
+ * Layouts: q, k bf16 [B][H_k][d_k]; v bf16 [B][H_v][d_v]; g, beta fp32
+ * [B][H_v]; state_in, state_out fp32 [B][H_v][d_v][d_k]; o [B][H_v][d_v]
+ * in o_dtype (DS_BF16 or DS_F32).  state_out may equal state_in (in-place
+ * update) but must not otherwise overlap it.  Arithmetic is fp32 (no
+ * matrix cores); row sums use a fixed order, so results are reproducible.
+ * No drift sums (a decode step is not a frame).  Requires d_k = d_v in
+ * {64, 128}, H_v a multiple of H_k; B = 0 does nothing.  No workspace.
+ */
+ds_status gdn_decode_step(int32_t B, int32_t H_k, int32_t H_v, int32_t d_k, int32_t d_v, const void *q,
+                          const void *k, const void *v, const float *g, const float *beta,
+                          const float *state_in, float *state_out, void *o, int32_t o_dtype, float scale,
+                          void *stream);
 
 /* ------------------------------------------------------------------------
  * deltas_drift -- state drift per frame (Section 3.2, Eq. 3)

@@ -22,7 +22,7 @@ LAYER_FROB, HEAD_MEAN, PER_HEAD, WRITE_MEAN = 0, 1, 2, 3
 EXPORTED = [
     "ds_status_string", "ds_last_error", "ds_gdn_workspace_bytes", "gdn_chunk_fwd", "deltas_drift",
     "deltas_drift_states", "ds_kv_workspace_bytes", "kv_evict_topk", "ds_kv_device_status",
-    "ds_kv_indexed_workspace_bytes", "kv_evict_topk_indexed",
+    "ds_kv_indexed_workspace_bytes", "kv_evict_topk_indexed", "gdn_decode_step",
 ]
 
 
@@ -61,6 +61,8 @@ def lib():
         L.gdn_chunk_fwd.argtypes = [ctypes.POINTER(GdnShape), P, P, P, P, P, P, P, P, P, I32, ctypes.c_float,
                                     P, P, P, P, SZ, P]
         L.gdn_chunk_fwd.restype = I32
+        L.gdn_decode_step.argtypes = [I32, I32, I32, I32, I32, P, P, P, P, P, P, P, P, I32, ctypes.c_float, P]
+        L.gdn_decode_step.restype = I32
         L.deltas_drift.argtypes = [P, I32, I32, I32, I32, P, P]
         L.deltas_drift.restype = I32
         L.deltas_drift_states.argtypes = [P, P, I32, I32, I32, I32, I32, P, P]
@@ -177,6 +179,40 @@ def deltas_drift_states(S_before, S_after, partials=None, stream=None):
         partials = torch.empty((L, B, H, 2), dtype=torch.float32, device=S_before.device)
     _check(lib().deltas_drift_states(_ptr(S_before), _ptr(S_after), L, B, H, dv, dk, _ptr(partials), _stream(stream)))
     return partials
+
+
+def gdn_decode_step(q, k, v, g, beta, state_in=None, state_out=None, o=None, o_dtype=torch.float32, scale=1.0,
+                    stream=None):
+    """One token per stream (see gdn_decode_step in deltas.h).
+
+    q, k: bf16 [B][H_k][d]; v: bf16 [B][H_v][d]; g, beta: fp32 [B][H_v];
+    state_in / state_out: fp32 [B][H_v][d][d] (state_out may be state_in).
+    Returns dict(o, state).
+    """
+    B, H_k, d = q.shape
+    H_v = v.shape[1]
+    if k.shape != q.shape or v.shape != (B, H_v, d) or g.shape != (B, H_v) or beta.shape != (B, H_v):
+        raise ValueError("shape mismatch")
+    for t in (q, k, v):
+        if t.dtype != torch.bfloat16 or not t.is_contiguous():
+            raise ValueError("q, k, v must be contiguous bf16")
+    for t in (g, beta):
+        if t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError("g, beta must be contiguous fp32")
+    dev = q.device
+    if state_out is None:
+        state_out = torch.empty((B, H_v, d, d), dtype=torch.float32, device=dev)
+    for t in (state_in, state_out):
+        if t is not None and (t.dtype != torch.float32 or t.shape != (B, H_v, d, d) or not t.is_contiguous()):
+            raise ValueError("states must be contiguous fp32 [B][H_v][d][d]")
+    if o is None:
+        o = torch.empty((B, H_v, d), dtype=o_dtype, device=dev)
+    od = DS_BF16 if o.dtype == torch.bfloat16 else DS_F32
+    if o.shape != (B, H_v, d) or not o.is_contiguous() or o.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("o must be contiguous bf16 or fp32 [B][H_v][d]")
+    _check(lib().gdn_decode_step(B, H_k, H_v, d, d, _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
+                                 _ptr(state_in), _ptr(state_out), _ptr(o), od, float(scale), _stream(stream)))
+    return dict(o=o, state=state_out)
 
 
 def kv_workspace_bytes(n_layers, row_bytes, capacity) -> int:

@@ -160,6 +160,46 @@ ds_status deltas_drift_states(const float *S_before, const float *S_after, int32
     return DS_OK;
 }
 
+ds_status gdn_decode_step(int32_t B, int32_t H_k, int32_t H_v, int32_t d_k, int32_t d_v, const void *q,
+                          const void *k, const void *v, const float *g, const float *beta, const float *state_in,
+                          float *state_out, void *o, int32_t o_dtype, float scale, void *stream) {
+    g_last_error[0] = 0;
+    if (B < 0 || H_k < 1 || H_v < 1) return fail(DS_E_SHAPE, "B=%d H_k=%d H_v=%d", B, H_k, H_v);
+    if (H_v % H_k != 0) return fail(DS_E_SHAPE, "H_v=%d is not a multiple of H_k=%d", H_v, H_k);
+    if (d_k != d_v || (d_k != 64 && d_k != 128))
+        return fail(DS_E_UNSUPPORTED, "head dims d_k=%d d_v=%d (supported: d_k = d_v in {64, 128})", d_k, d_v);
+    if (o_dtype != DS_BF16 && o_dtype != DS_F32) return fail(DS_E_DTYPE, "o_dtype=%d", o_dtype);
+    if ((long long)B * H_v * (d_v * d_k / 2048) > (1LL << 31) - 1) return fail(DS_E_UNSUPPORTED, "too many heads");
+    if (B == 0) return DS_OK;
+    if (!q || !k || !v || !g || !beta || !state_out || !o)
+        return fail(DS_E_NULL, "q, k, v, g, beta, state_out and o are required");
+    const void *ptrs[] = {q, k, v, state_in, state_out, o};
+    for (const void *p : ptrs)
+        if (misaligned(p)) return fail(DS_E_ALIGN, "a pointer is not 16-byte aligned");
+    if (state_in && state_in != state_out) {
+        const char *a0 = (const char *)state_in, *b0 = (const char *)state_out;
+        const size_t n = (size_t)B * H_v * d_v * d_k * sizeof(float);
+        if (a0 < b0 + n && b0 < a0 + n) return fail(DS_E_ARG, "state_in and state_out overlap without being equal");
+    }
+    ds::DecodeArgs a;
+    a.q = (const uint16_t *)q;
+    a.k = (const uint16_t *)k;
+    a.v = (const uint16_t *)v;
+    a.g = g;
+    a.beta = beta;
+    a.state_in = state_in;
+    a.state_out = state_out;
+    a.o = o;
+    a.scale = scale;
+    a.B = B;
+    a.H_k = H_k;
+    a.H_v = H_v;
+    a.group = H_v / H_k;
+    hipError_t e = ds::launch_gdn_decode(a, d_k, o_dtype == DS_BF16, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "gdn_decode_step launch");
+    return DS_OK;
+}
+
 size_t ds_kv_workspace_bytes(const ds_kv_shape *shape) {
     if (!shape || shape->n_layers < 1 || shape->row_bytes < 16 || shape->row_bytes % 16 || shape->row_bytes > 65536 ||
         shape->capacity < 1 || 2 * shape->n_layers > ds::KV_MAX_PLANES)

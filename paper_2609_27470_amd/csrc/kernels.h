@@ -40,6 +40,18 @@ struct GdnWorkspace {
 GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, int n_frames);
 hipError_t launch_gdn(const GdnLaunch &p, hipStream_t stream);
 
+// ---------------------------------------------------------------- decode step
+struct DecodeArgs {
+    const uint16_t *q, *k, *v;  // [B][H_k][d], [B][H_k][d], [B][H_v][d] bf16
+    const float *g, *beta;      // [B][H_v]
+    const float *state_in;      // [B][H_v][d][d] or null (zeros)
+    float *state_out;           // [B][H_v][d][d] (may be state_in)
+    void *o;                    // [B][H_v][d] bf16 or fp32
+    float scale;
+    int B, H_k, H_v, group;
+};
+hipError_t launch_gdn_decode(const DecodeArgs &a, int d, bool o_bf16, hipStream_t stream);
+
 // ---------------------------------------------------------------- drift reduce
 // n_heads heads of n_elem fp32 entries each (n_elem a multiple of 4)
 hipError_t launch_drift_states(const float *before, const float *after, int n_heads, int n_elem, float *partials,

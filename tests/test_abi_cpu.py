@@ -152,3 +152,23 @@ def test_kv_indexed_rejects_bad_arguments_and_noop(ds):
     assert call(17408, 16384, 0, 0, 1, wsb=8) == 8                          # workspace
     assert L.kv_evict_topk_indexed(17408, f, f, f, f, 1024, 17408, 16384, 0, 0, 1, None, f, None, f,
                                    1 << 40, None) == 1                      # new_len required
+
+
+def test_decode_rejects_bad_arguments(ds):
+    L = ds.lib()
+    P = ctypes.c_void_p
+    f = P(1 << 20)
+
+    def call(B=4, H_k=2, H_v=4, dk=128, dv=128, q=f, st_in=None, st_out=P(1 << 30), od=ds.DS_F32):
+        return L.gdn_decode_step(B, H_k, H_v, dk, dv, q, f, f, f, f, st_in, st_out, f, od, 1.0, None)
+
+    assert call(B=-1) == 2
+    assert call(H_k=3) == 2                         # H_v not a multiple of H_k
+    assert call(dk=96, dv=96) == 5
+    assert call(dk=64, dv=128) == 5
+    assert call(od=7) == 3
+    assert call(B=0, q=None) == 0                   # nothing to do
+    assert call(q=None) == 1
+    assert call(q=P((1 << 20) + 8)) == 4
+    assert call(st_in=P(1 << 30), st_out=P((1 << 30) + 4096)) == 6   # overlapping states
+    assert b"overlap" in L.ds_last_error()
