@@ -98,6 +98,75 @@ def copy_calibration(nbytes):
     print(json.dumps({"copy_calibration_bytes": nbytes}))
 
 
+def streaming_bench(ds, dev, stream, n_chunks, n_layers=24):
+    """The paper's streaming regime: chunks of 118-132 tokens, each one frame of
+    all 24 linear-attention layers (single-layer head shapes, state carried in
+    place), the chunk score over the layers, append, and eviction with sinks 4,
+    window 1024 and 4 spans at M = 16384 -- per-chunk GPU time of the whole
+    step, starting from a full cache."""
+    import torch
+    from paper_2609_27470_amd.streaming import DeltaSStream
+    gen = torch.Generator(device=dev).manual_seed(7)
+    POOL = 1024
+    def unit(shape):
+        x = torch.randn(shape, generator=gen, device=dev)
+        return (x / x.norm(dim=-1, keepdim=True)).to(torch.bfloat16)
+    pools = (unit((n_layers, POOL, H_K, D)), unit((n_layers, POOL, H_K, D)),
+             torch.randn((n_layers, POOL, H_V, D), generator=gen, device=dev).to(torch.bfloat16),
+             -torch.nn.functional.softplus(torch.randn((n_layers, POOL, H_V), generator=gen, device=dev)),
+             torch.sigmoid(torch.randn((n_layers, POOL, H_V), generator=gen, device=dev)))
+    row_elems = KV_HEADS * KV_DIM
+    total = 8 + n_chunks + 4
+    rng = np.random.default_rng(11)
+    lens = [int(x) for x in rng.integers(118, 133, total)]
+    k_rows = torch.randint(-2000, 2000, (KV_LAYERS, 132, row_elems), dtype=torch.int16, device=dev, generator=gen)
+    v_rows = torch.randint(-2000, 2000, (KV_LAYERS, 132, row_elems), dtype=torch.int16, device=dev, generator=gen)
+    state_io = n_layers * 2 * H_V * D * D * 4   # every layer reads and writes its state once per chunk
+    out = {"layers": n_layers, "policy": "n_sink=4, n_window=1024, N=4, M=16384",
+           "state_io_bytes_per_chunk": state_io}
+    for mode in ("eager", "graph"):
+        s = DeltaSStream(n_layers, H_K, H_V, D, KV_LAYERS, row_elems, BUDGET, 132, BUDGET // 128 + total + 8,
+                         4, 1024, 4, device=dev)
+        # start from a full cache: BUDGET tokens in 128 earlier chunks with random scores
+        s.pos[:BUDGET] = torch.arange(BUDGET, dtype=torch.int32, device=dev)
+        s.chunk_id[:BUDGET] = torch.arange(BUDGET, dtype=torch.int32, device=dev) // 128
+        s.scores[:BUDGET // 128] = torch.rand(BUDGET // 128, generator=gen, device=dev)
+        s.length, s.n_chunks, s.next_pos = BUDGET, BUDGET // 128, BUDGET
+        if mode == "graph":
+            s.capture_graph()
+        off = 0
+        evs = []
+        t_host = 0.0
+        for i, Tc in enumerate(lens):
+            a = off % (POOL - 132)
+            timed = 8 <= i < 8 + n_chunks
+            if timed:
+                e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+                e[0].record(stream)
+                h0 = time.perf_counter()
+            if mode == "eager":
+                s.step([tuple(x[l, a:a + Tc] for x in pools) for l in range(n_layers)],
+                       k_rows[:, :Tc], v_rows[:, :Tc])
+            else:
+                for buf, x in zip(s.inputs, pools):
+                    buf[:, :Tc].copy_(x[:, a:a + Tc])
+                s.step_inputs(Tc, k_rows[:, :Tc], v_rows[:, :Tc])
+            if timed:
+                t_host += time.perf_counter() - h0
+                e[1].record(stream)
+                evs.append((Tc, e))
+            off += Tc
+        torch.cuda.synchronize()
+        ms = np.array([e[0].elapsed_time(e[1]) for _, e in evs])
+        toks = np.array([t for t, _ in evs])
+        out[mode] = {"chunk_tokens_mean": float(toks.mean()), "ms_per_chunk": float(np.median(ms)),
+                     "tokens_per_s": float(toks.sum() / (ms.sum() * 1e-3)),
+                     "host_ms_per_chunk": 1e3 * t_host / len(evs),
+                     "state_io_gbs": float(state_io / (np.median(ms) * 1e-3) / 1e9)}
+        del s
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -346,6 +415,8 @@ def main():
                             "hbm_frac": dec_bytes / (dec_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
                             "bytes_per_step": dec_bytes}
 
+    streaming = streaming_bench(ds, dev, stream, args.steps)
+
     flops, bytes_ = algorithmic_work(T, H_K, H_V, D)
     achieved_gbs = bytes_ / (gdn_ms * 1e-3) / 1e9
     achieved_tflops = flops / (gdn_ms * 1e-3) / 1e12
@@ -400,6 +471,7 @@ def main():
         "evict_gather_gbs": float((2 * moved_bytes).mean() / (evict_ms * 1e-3) / 1e9),
         "drift_overhead_paper_pct": 1.9,
         "decode_step": decode,
+        "streaming": streaming,
         "evict_indexed": {
             "kv_evict_topk_indexed_ms": float(idx_evict_ms), "append_scatter_ms": float(idx_append_ms),
             "ms_per_step": float(gdn_ms + drift_ms + idx_append_ms + idx_evict_ms),

@@ -105,9 +105,13 @@ const char *ds_last_error(void);
  *   v           bf16 [T_total][H_v][d_v]
  *   g, beta     fp32 [T_total][H_v]       (g <= 0 is the log decay)
  *   cu_seqlens  int32 [B+1], stream b = tokens [cu[b], cu[b+1]);
- *               nondecreasing, cu[0] = 0, cu[B] = T_total.  NULL iff B == 1.
- *               (Out-of-range values are clamped so that no access leaves
- *               the buffers; results are then unspecified.)
+ *               nondecreasing, cu[0] = 0, cu[B] <= T_total.  The lengths
+ *               are read on the device, so T_total may be an upper bound
+ *               (it sizes the workspace and the grids): one captured graph
+ *               then serves chunks of any length up to it.  May be NULL
+ *               when B == 1 (the stream is [0, T_total)); required when
+ *               B > 1.  (Out-of-range values are clamped so that no access
+ *               leaves the buffers; results are then unspecified.)
  *   state_in    fp32 [B][H_v][d_v][d_k] or NULL (zeros)
  *   state_out   fp32 [B][H_v][d_v][d_k]; may alias state_in
  *   o           [T_total][H_v][d_v] of dtype o_dtype (DS_BF16 or DS_F32)
@@ -115,9 +119,12 @@ const char *ds_last_error(void);
  *   write_partials fp32 [n_frames][H_v][2] or NULL
  *   snapshots   fp32 [n_frames][H_v][d_v][d_k] or NULL
  * Supported: d_k = d_v in {64, 128}; H_v a multiple of H_k; frame_len a
- * multiple of 64 or 0.  bf16 inputs are converted to fp16 for the matrix
- * cores, so |q|, |k|, |v| must stay below 65504.
- * n_frames must equal the number of frames of all streams.
+ * multiple of 64 or 0.  bf16 inputs and the state enter the matrix cores as
+ * fp16 (fp32 accumulation), so |q|, |k|, |v| and the state's entries must
+ * stay below 65504.
+ * n_frames is the number of frames of all streams at the lengths the host
+ * knows (frame_len = 0: B); for frames that the device lengths do not
+ * reach, the drift and write sums are zero and no snapshot is written.
  */
 typedef struct {
     int32_t B;         /* number of streams (>= 1) */

@@ -15,40 +15,60 @@ __device__ __forceinline__ double drift_ratio(double num, double den) {
     return num > 0.0 ? __builtin_huge_val() : 0.0;
 }
 
+__device__ __forceinline__ double wave_sum_d(double x) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+    return x;
+}
+
+// One workgroup (4 waves) per frame.  Wave w takes layers w, w + 4, ...; its
+// lanes take the heads of a layer (lane, lane + 64, ...), sum in order, and
+// meet in a butterfly; the waves' totals are added in wave order.  Every sum
+// has a fixed order, so the result does not depend on scheduling.
 __global__ __launch_bounds__(256) void drift_frame_kernel(const float *p, int L, int F, int H, int mode,
                                                            float *scores) {
-    const int f = blockIdx.x * 256 + threadIdx.x;
-    if (f >= F) return;
-    double acc = 0.0;
+    const int f = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    double acc = 0.0;  // same value in every lane of the wave
     bool inf = false;
-    int cnt = 0;
-    for (int l = 0; l < L; ++l) {
+    for (int l = w; l < L; l += 4) {
         const float *row = p + ((size_t)l * F + f) * H * 2;
-        if (mode == 3) {
-            // (sum, count) pairs: mean over heads of sum / count
-            for (int h = 0; h < H; ++h) {
-                const double c = (double)row[2 * h + 1];
-                acc += c > 0.0 ? (double)row[2 * h] / c : 0.0;
-                ++cnt;
-            }
-        } else if (mode == 0) {
+        if (mode == 0) {
             double num = 0.0, den = 0.0;
-            for (int h = 0; h < H; ++h) {
+            for (int h = lane; h < H; h += 64) {
                 num += (double)row[2 * h];
                 den += (double)row[2 * h + 1];
             }
-            const double r = drift_ratio(num, den);
+            const double r = drift_ratio(wave_sum_d(num), wave_sum_d(den));
             if (isinf(r)) inf = true; else acc += r;
-            ++cnt;
         } else {
-            for (int h = 0; h < H; ++h) {
-                const double r = drift_ratio((double)row[2 * h], (double)row[2 * h + 1]);
-                if (isinf(r)) inf = true; else acc += r;
-                ++cnt;
+            double x = 0.0;
+            bool xi = false;
+            for (int h = lane; h < H; h += 64) {
+                if (mode == 3) {
+                    const double c = (double)row[2 * h + 1];
+                    x += c > 0.0 ? (double)row[2 * h] / c : 0.0;
+                } else {
+                    const double r = drift_ratio((double)row[2 * h], (double)row[2 * h + 1]);
+                    if (isinf(r)) xi = true; else x += r;
+                }
             }
+            acc += wave_sum_d(x);
+            if (__any(xi)) inf = true;
         }
     }
-    scores[f] = inf ? __builtin_huge_valf() : (cnt ? (float)(acc / cnt) : 0.f);
+    __shared__ double s_acc[4];
+    __shared__ int s_inf[4];
+    if (lane == 0) {
+        s_acc[w] = acc;
+        s_inf[w] = inf;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const double tot = ((s_acc[0] + s_acc[1]) + s_acc[2]) + s_acc[3];
+        const bool any_inf = s_inf[0] | s_inf[1] | s_inf[2] | s_inf[3];
+        const long long cnt = mode == 0 ? (long long)L : (long long)L * H;
+        scores[f] = any_inf ? __builtin_huge_valf() : (cnt ? (float)(tot / (double)cnt) : 0.f);
+    }
 }
 
 __global__ __launch_bounds__(256) void drift_head_kernel(const float *p, int n, float *scores) {
@@ -104,8 +124,7 @@ hipError_t launch_drift(const float *partials, int L, int F, int H_v, int mode, 
         hipLaunchKernelGGL(drift_head_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, partials, n, scores);
     } else {
         if (F == 0) return hipSuccess;
-        hipLaunchKernelGGL(drift_frame_kernel, dim3((F + 255) / 256), dim3(256), 0, stream, partials, L, F, H_v,
-                           mode, scores);
+        hipLaunchKernelGGL(drift_frame_kernel, dim3(F), dim3(256), 0, stream, partials, L, F, H_v, mode, scores);
     }
     return hipGetLastError();
 }

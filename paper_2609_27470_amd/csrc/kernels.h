@@ -64,8 +64,9 @@ constexpr int KV_MAX_PLANES = 64;  // 2 * n_layers
 
 struct KvWorkspace {
     size_t offStatus, offPlanes, offKeep, offInv, offThRun, offRunStart, offRunKey, offRunBkt, offRunTake,
-        offRunFrom, offFlags, total;
-    int n_chunks;  // 64 KiB pieces of one token's rows over all layers
+        offRunFrom, offFlags, offStage, offStageMeta, total;
+    int n_chunks;    // 64 KiB pieces of one token's rows over all layers
+    int stage_rows;  // destinations per staged block
 };
 // n_layers = 0: the indexed variant's workspace (no gather flags)
 KvWorkspace kv_workspace_layout(int n_layers, int row_bytes, int capacity);

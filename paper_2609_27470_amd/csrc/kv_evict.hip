@@ -19,12 +19,21 @@
 // With a slot table (the indexed variant) the K and V rows never move: the
 // select kernel itself compacts pos, chunk_id and slot (the physical row of
 // each logical token) in place and lists the freed physical rows.
-// kv_gather moves the kept rows down in place.  Slot d receives row keep[d]
-// (keep[d] >= d).  Writing slot d is safe once the reader of row d -- the
-// destination inv[d] < d, if row d is kept -- has its data in registers.
-// Workgroups take increasing tickets, signal "read done" before they wait,
-// and only ever wait on lower tickets, so every wait ends; the wait is also
-// bounded and reports a timeout in the status word instead of hanging.
+// The kept rows then move down in place: slot d receives row keep[d]
+// (keep[d] >= d); the shift keep[d] - d never decreases with d.
+// kv_gather handles the destinations whose shift is large.  Writing slot d is
+// safe once the reader of row d -- the destination inv[d] < d, if row d is
+// kept -- has its data in registers.  Workgroups take increasing tickets,
+// signal "read done" before they wait, and only ever wait on lower tickets,
+// so every wait ends; the wait is also bounded and reports a timeout in the
+// status word instead of hanging.  Its parallelism is the shift itself (only
+// rows a shift apart are independent), so destinations with a small shift
+// (fewer than STAGE_BYTES of rows) go first through kv_stage instead: blocks
+// of destinations are copied to a staging area and back in two launches,
+// with no waits at all (a block only reads at or above its own start, and
+// the blocks run in order).
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -35,6 +44,9 @@ constexpr int SEL_PER = 32;                         // consecutive slots per thr
 constexpr int SEL_BLOCK = SEL_THREADS * SEL_PER;
 constexpr int GATHER_U = 16;                        // uint4 per thread per group
 constexpr int SPIN_LIMIT = 1 << 22;
+constexpr long long STAGE_BYTES = 64ll << 20;       // below this much shift, rows are staged
+constexpr long long STAGE_AREA = 1ll << 30;         // staging area of one block of destinations
+constexpr int STAGE_WG = 1024;                      // workgroups per staging launch (each loops over rows)
 
 // pointer into global memory (lets the compiler emit global rather than flat accesses)
 #define GPTR(T) __attribute__((address_space(1))) T *
@@ -46,7 +58,9 @@ struct KvArgs {
     const float *scores;
     int num_chunks, len, M, n_s, n_w, N;
     int n_flags, n_chunks;
-    int32_t *status;   // [0] invariants broken, [1] skip gather, [2] wait timed out, [3] first moved slot
+    int stage_shift;   // destinations with keep[d] - d below this are staged
+    int32_t *status;   // [0] invariants broken, [1] skip gather, [2] wait timed out, [3] first moved slot,
+                       // [4] first slot moved by the ticket gather (the staged ones lie in [3], [4])
     uint32_t *ticket;
     int32_t *keep, *inv, *run_start, *run_bkt, *run_take, *run_from, *th_run;
     unsigned long long *run_key;
@@ -243,6 +257,7 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     // ---- pass 2: keep list (ascending) and its inverse on destinations [0, M)
     int total_kept = 0;
     int first_move = a.M;  // smallest destination d with keep[d] != d
+    int split = a.M;       // smallest destination d with keep[d] - d >= stage_shift
     const int n_evict = a.len - a.M;
     for (int base = 0; base < a.len; base += SEL_BLOCK) {
         const int lo = base + tid * SEL_PER;
@@ -280,6 +295,7 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
                         a.keep[off] = i;
                         if (a.keep_out) a.keep_out[off] = i;
                         if (off != i) first_move = min(first_move, off);
+                        if (i - off >= a.stage_shift) split = min(split, off);
                     }
                     if (i < a.M) a.inv[i] = off;
                     ++off;
@@ -295,15 +311,21 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     // ---- moving destinations form the suffix [first_move, M) (keep[d] - d is
     // nondecreasing); clear their flags for the gather
     {
-        __shared__ int s_first;
-        if (tid == 0) s_first = a.M;
+        __shared__ int s_first, s_split;
+        if (tid == 0) {
+            s_first = a.M;
+            s_split = a.M;
+        }
         __syncthreads();
         if (first_move < a.M) atomicMin(&s_first, first_move);
+        if (split < a.M) atomicMin(&s_split, split);
         __syncthreads();
         first_move = s_first;
+        split = max(s_split, first_move);
     }
     if (tid == 0) {
         a.status[3] = first_move;
+        a.status[4] = split;
         if (total_kept != a.M) {  // cannot happen for valid arguments; never move data then
             a.status[0] = 2;
             a.status[1] = 1;
@@ -366,7 +388,7 @@ __global__ __launch_bounds__(256) void kv_gather_kernel(GatherArgs a) {
     constexpr int PPG = GATHER_U / KPR;
     __shared__ int s_t;
     if (a.status[1]) return;
-    const int first = a.status[3];
+    const int first = a.status[4];
     const int n_work = (a.M - first + GATHER_ROWS - 1) / GATHER_ROWS;
     if ((int)blockIdx.x >= n_work) return;  // more workgroups than moving rows: take no ticket
     const int tid = threadIdx.x;
@@ -405,7 +427,7 @@ __global__ __launch_bounds__(256) void kv_gather_kernel(GatherArgs a) {
                 __hip_atomic_store(&a.flags[d * a.n_chunks + c], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 // ---- wait until the reader of row d (a lower slot, hence an
                 // earlier ticket or an earlier iteration here) holds its data
-                if (dep >= 0 && dep != d) {
+                if (dep >= first && dep != d) {  // readers below `first` were staged earlier
                     int it = 0;
                     const int ft = dep * a.n_chunks + c;
                     while (__hip_atomic_load(&a.flags[ft], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
@@ -436,6 +458,64 @@ __global__ __launch_bounds__(256) void kv_gather_kernel(GatherArgs a) {
             }
         }
     }
+}
+
+struct StageArgs {
+    char *const *plane_tab;
+    uint32_t row_bytes, row_units;
+    int n_planes, planes_per_group, n_chunks;
+    int rows, block;  // destinations [block * rows, (block + 1) * rows)
+    int32_t *pos, *chunk;
+    const int32_t *keep, *status;
+    char *area;       // [rows][n_chunks][256 threads][16 units] 16-byte units
+    int32_t *meta;    // [rows][2] positions and chunk ids
+};
+
+template <int KPR, bool READ>
+__device__ __forceinline__ void kv_stage_row(const StageArgs &a, int r, int c) {
+    constexpr int PPG = GATHER_U / KPR;
+    const int tid = threadIdx.x;
+    const int d = a.block * a.rows + r;
+    GPTR(u32x4) slot = (GPTR(u32x4))(a.area + ((size_t)r * a.n_chunks + c) * (size_t)(GATHER_U * 16 * 256));
+    const int row = READ ? a.keep[d] : d;
+    const int p0 = c * a.planes_per_group;
+#pragma clang loop unroll(full)
+    for (int pi = 0; pi < PPG; ++pi) {
+        const int p = p0 + pi;
+        if (pi >= a.planes_per_group || p >= a.n_planes) break;
+        GPTR(char) base = (GPTR(char))a.plane_tab[p] + (size_t)row * a.row_bytes;
+#pragma clang loop unroll(full)
+        for (int k = 0; k < KPR; ++k) {
+            const uint32_t unit = (uint32_t)(tid + 256 * k);
+            if (unit < a.row_units) {
+                GPTR(u32x4) g = (GPTR(u32x4))(base + 16u * unit);
+                GPTR(u32x4) t = slot + (pi * KPR + k) * 256 + tid;
+                if (READ) *t = *g; else *g = *t;
+            }
+        }
+    }
+    if (c == 0 && tid == 0) {
+        if (READ) {
+            a.meta[2 * r] = a.pos[row];
+            a.meta[2 * r + 1] = a.chunk[row];
+        } else {
+            a.pos[d] = a.meta[2 * r];
+            a.chunk[d] = a.meta[2 * r + 1];
+        }
+    }
+}
+
+// Workgroup x of plane group y handles destinations x, x + STAGE_WG, ... of
+// the block.  READ copies the source rows of the staged destinations into the
+// area, WRITE copies them to their slots.  Destinations outside
+// [status[3], status[4]) are skipped, so a launch with nothing to stage ends
+// at once.
+template <int KPR, bool READ>
+__global__ __launch_bounds__(256) void kv_stage_kernel(StageArgs a) {
+    if (a.status[1]) return;
+    const int lo = max(a.status[3] - a.block * a.rows, 0);
+    const int hi = min(a.status[4] - a.block * a.rows, a.rows);
+    for (int r = lo + (int)blockIdx.x; r < hi; r += (int)gridDim.x) kv_stage_row<KPR, READ>(a, r, (int)blockIdx.y);
 }
 
 // 16-byte units per thread per plane row, rounded up to a power of two.
@@ -477,6 +557,16 @@ KvWorkspace kv_workspace_layout(int n_layers, int row_bytes, int capacity) {
     off = align256(off + cap * 4);
     w.offFlags = off;
     off = align256(off + cap * (size_t)w.n_chunks * 4);
+    w.stage_rows = 0;
+    w.offStage = w.offStageMeta = off;
+    if (w.n_chunks > 0) {
+        const long long per_row = (long long)w.n_chunks * GATHER_U * 16 * 256;
+        w.stage_rows = (int)std::max(1ll, std::min((long long)capacity, STAGE_AREA / per_row));
+        w.offStage = off;
+        off = align256(off + (size_t)w.stage_rows * per_row);
+        w.offStageMeta = off;
+        off = align256(off + (size_t)w.stage_rows * 8);
+    }
     w.total = off;
     return w;
 }
@@ -495,6 +585,12 @@ hipError_t launch_kv_evict(const KvLaunch &p, hipStream_t stream) {
     a.N = p.n_buckets;
     a.n_flags = p.M * p.lay.n_chunks;
     a.n_chunks = p.lay.n_chunks;
+    {
+        // stage destinations whose shift spans less than STAGE_BYTES of rows
+        const long long row_all = (long long)std::max(p.n_planes, 1) * p.row_bytes;
+        a.stage_shift = (int)std::min((long long)p.M + 1, (STAGE_BYTES + row_all - 1) / row_all);
+        if (p.slot) a.stage_shift = p.M + 1;  // the indexed variant moves no rows
+    }
     a.status = (int32_t *)(ws + p.lay.offStatus);
     a.ticket = (uint32_t *)(ws + p.lay.offStatus + 32);
     a.keep = (int32_t *)(ws + p.lay.offKeep);
@@ -534,7 +630,50 @@ hipError_t launch_kv_evict(const KvLaunch &p, hipStream_t stream) {
     g.flags = a.flags;
     g.status = a.status;
     g.ticket = a.ticket;
-    const dim3 grid((unsigned)((p.M + GATHER_ROWS - 1) / GATHER_ROWS)), blk(256);
+    // staged destinations first (block by block, in order), then the ticket gather
+    StageArgs sa;
+    sa.plane_tab = a.plane_tab;
+    sa.row_bytes = g.row_bytes;
+    sa.row_units = g.row_units;
+    sa.n_planes = p.n_planes;
+    sa.planes_per_group = g.planes_per_group;
+    sa.n_chunks = p.lay.n_chunks;
+    sa.rows = p.lay.stage_rows;
+    sa.pos = p.pos;
+    sa.chunk = p.chunk_id;
+    sa.keep = a.keep;
+    sa.status = a.status;
+    sa.area = p.ws + p.lay.offStage;
+    sa.meta = (int32_t *)(p.ws + p.lay.offStageMeta);
+    const dim3 sgrid((unsigned)std::min(sa.rows, STAGE_WG), (unsigned)sa.n_chunks), blk(256);
+    for (int b = 0; (long long)b * sa.rows < p.M; ++b) {
+        sa.block = b;
+        switch (kpr) {
+        case 1:
+            hipLaunchKernelGGL((kv_stage_kernel<1, true>), sgrid, blk, 0, stream, sa);
+            hipLaunchKernelGGL((kv_stage_kernel<1, false>), sgrid, blk, 0, stream, sa);
+            break;
+        case 2:
+            hipLaunchKernelGGL((kv_stage_kernel<2, true>), sgrid, blk, 0, stream, sa);
+            hipLaunchKernelGGL((kv_stage_kernel<2, false>), sgrid, blk, 0, stream, sa);
+            break;
+        case 4:
+            hipLaunchKernelGGL((kv_stage_kernel<4, true>), sgrid, blk, 0, stream, sa);
+            hipLaunchKernelGGL((kv_stage_kernel<4, false>), sgrid, blk, 0, stream, sa);
+            break;
+        case 8:
+            hipLaunchKernelGGL((kv_stage_kernel<8, true>), sgrid, blk, 0, stream, sa);
+            hipLaunchKernelGGL((kv_stage_kernel<8, false>), sgrid, blk, 0, stream, sa);
+            break;
+        default:
+            hipLaunchKernelGGL((kv_stage_kernel<16, true>), sgrid, blk, 0, stream, sa);
+            hipLaunchKernelGGL((kv_stage_kernel<16, false>), sgrid, blk, 0, stream, sa);
+            break;
+        }
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    const dim3 grid((unsigned)((p.M + GATHER_ROWS - 1) / GATHER_ROWS));
     switch (kpr) {
     case 1: hipLaunchKernelGGL(kv_gather_kernel<1>, grid, blk, 0, stream, g); break;
     case 2: hipLaunchKernelGGL(kv_gather_kernel<2>, grid, blk, 0, stream, g); break;

@@ -172,3 +172,16 @@ def test_decode_rejects_bad_arguments(ds):
     assert call(q=P((1 << 20) + 8)) == 4
     assert call(st_in=P(1 << 30), st_out=P((1 << 30) + 4096)) == 6   # overlapping states
     assert b"overlap" in L.ds_last_error()
+
+
+def test_streaming_session_validates_on_host(ds):
+    """The streaming session's argument checks run before any device work."""
+    from paper_2609_27470_amd.streaming import DeltaSStream
+    with pytest.raises(ValueError):
+        DeltaSStream(2, 2, 4, 64, 1, 64, 100, 132, 8, n_sink=50, n_window=60, device="cpu")
+    s = DeltaSStream(2, 2, 4, 64, 1, 64, 600, 132, 8, n_sink=4, n_window=256, device="cpu")
+    assert s.capacity == 600 + 132 and s.state.shape == (2, 1, 4, 64, 64)
+    import torch
+    bad = [(torch.zeros((140, 2, 64), dtype=torch.bfloat16),) * 5] * 2
+    with pytest.raises(ValueError):
+        s.step(bad, None, None)                       # chunk longer than max_chunk

@@ -121,6 +121,30 @@ def test_eviction_loop_shape(ds, policy):
     one_event(ds, 8, 2048, chunk, pos, scores, 16384, ns, nw, nb)
 
 
+def test_staged_and_ticket_regions_in_one_event(ds):
+    """64 KiB of rows per token (8 layers x 4 KiB K and V): the first moved
+    rows shift by 512 slots (less than 64 MiB of rows: staged through the
+    workspace) and the later ones by 1536 (the ticket-ordered gather), in one
+    event: 512 oldest tokens of chunk 2 and all of chunk 12 are evicted."""
+    chunk = np.concatenate([np.repeat(np.arange(17), 1024), np.full(512, 17)]).astype(np.int32)
+    pos = np.arange(len(chunk), dtype=np.int32) + 7
+    scores = np.linspace(0.5, 1.0, 18).astype(np.float32)
+    scores[12] = 0.01
+    scores[2] = 0.02
+    one_event(ds, 8, 2048, chunk, pos, scores, 16384, 0, 0, 1)
+
+
+def test_small_shifts_full_shape(ds):
+    """The paper's policy on the eviction-loop shape with chunks of 125
+    tokens: every event removes a few scattered tokens, so every moved row
+    shifts by less than 1024 slots (all staged)."""
+    rng = np.random.default_rng(9)
+    chunk = np.repeat(np.arange(140), 125)[:16384 + 125].astype(np.int32)
+    pos = np.arange(len(chunk), dtype=np.int32)
+    scores = rng.random(140).astype(np.float32)
+    one_event(ds, 8, 2048, chunk, pos, scores, 16384, 4, 1024, 4)
+
+
 def test_repeated_events_stream(ds):
     """Append a chunk per step and evict down to M every time the cache
     overflows; after every step the cache equals the oracle's replay."""
