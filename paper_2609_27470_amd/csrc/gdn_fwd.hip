@@ -403,8 +403,7 @@ struct SeqShared {
     uint16_t K[2][64 * D];     // K tile (fp16), row-major, 16-byte chunks XOR-swizzled by row (swz)
     u32x4 T[2][6][64];         // T diag(beta) A-fragments
     uint16_t V[2][64 * 16];    // v[token][v0 .. v0 + 15] (bf16, read transposed)
-    uint32_t Ost[2][32 * 16];  // per output wave: its 32 rows of o, staged for 16-byte row stores
-    float G[2][2][64];         // Gamma_r and D_last,r
+    float G[3][2][64];         // Gamma_r and D_last,r of tile t in G[t % 3] (the output waves read it a tile later)
     f32x4 X[2][2][4][64];      // exchanged halves of K S0^T: [tile % 2][state wave][rb][lane]
     u32x4 S16[2][KS][64];      // S0 as fp16 B operand (for the output waves)
     u32x4 E[2][2][64];         // E as B operand (fp16)
@@ -430,7 +429,6 @@ template <int D>
 struct OutSet {
     u32x4 q[2][D / 32];  // q rows 16 rb + ln (fp16), dims 32 ks + 8 lg .. + 7
     u32x4 p[4];          // P fragments of the two row blocks (2 or 4 used)
-    float4 gam[2];       // Gamma of rows 16 rb + 4 lg + e
 };
 
 constexpr int SEQ_SPIN_LIMIT = 1 << 22;
@@ -514,7 +512,8 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             lds_barrier();
 
             // Gamma_last S0 first: the split below may then consume S0's registers
-            const float gl = sh.G[buf][0][63];
+            const int g3 = lt % 3;
+            const float gl = sh.G[g3][0][63];
             f32x4 Sn[HKB];
 #pragma unroll
             for (int c = 0; c < HKB; ++c)
@@ -550,8 +549,8 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             for (int f = 0; f < 6; ++f) tf[f] = as_half8(sh.T[buf][f][lane]);
 #pragma unroll
             for (int rb = 0; rb < 4; ++rb) {
-                gam4[rb] = *(const float4 *)(&sh.G[buf][0][16 * rb + 4 * lg]);
-                dl4[rb] = *(const float4 *)(&sh.G[buf][1][16 * rb + 4 * lg]);
+                gam4[rb] = *(const float4 *)(&sh.G[g3][0][16 * rb + 4 * lg]);
+                dl4[rb] = *(const float4 *)(&sh.G[g3][1][16 * rb + 4 * lg]);
                 // v[16 rb + 4 lg + e][ln], e = 0..3, by a transposing read
                 vv4[rb] = ds_read_tr16(&sh.V[buf][(16 * rb + 4 * lg + (ln >> 2)) * 16 + 4 * (ln & 3)]);
             }
@@ -666,138 +665,134 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             for (int e = 0; e < 4; ++e) a.state_out[sbase + scol(hh * HKB + c, e)] = S[c][e];
     } else if (w < 4) {
         // =============================================================== output
-        const int pr = w - 2;  // row blocks 2 pr and 2 pr + 1
-        // (tiles past the end are clamped to the last one so that every
-        // iteration issues the same memory operations)
-        auto load = [&](OutSet<D> &s, int lt_) __attribute__((always_inline)) {
-            const int lt = min(lt_, n_tiles - 1);
-            const size_t tv = (size_t)(tile_base + lt) * a.H_v + j;
-            const _Float16 *qb = a.wsQ + ((size_t)(tile_base + lt) * a.H_k + qh) * 64 * D + 8 * lg;
+        // O = diag(Gamma) Q S0^T + P E for row blocks {2 PR, 2 PR + 1}, one tile
+        // behind the state waves (Gamma from the loaders' LDS copy)
+        auto run = [&](auto prc) __attribute__((always_inline)) {
+            constexpr int PR = decltype(prc)::value;
+            constexpr int NP = PR == 0 ? 2 : 4;  // P fragments of the two row blocks
+            // (tiles past the end are clamped to the last one so that every
+            // iteration issues the same memory operations)
+            auto load = [&](OutSet<D> &s, int lt_) __attribute__((always_inline)) {
+                const int lt = min(lt_, n_tiles - 1);
+                const size_t tv = (size_t)(tile_base + lt) * a.H_v + j;
+                const _Float16 *qb = a.wsQ + ((size_t)(tile_base + lt) * a.H_k + qh) * 64 * D + 8 * lg;
 #pragma unroll
-            for (int r = 0; r < 2; ++r) {
-                const uint32_t row = (uint32_t)(16 * (2 * pr + r) + ln);
+                for (int r = 0; r < 2; ++r) {
+                    const uint32_t row = (uint32_t)(16 * (2 * PR + r) + ln);
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks) s.q[r][ks] = *(const u32x4 *)(qb + row * (uint32_t)D + 32 * ks);
-            }
-            const u32x4 *pb = (const u32x4 *)(a.wsP + tv * TP_HALVES);
-            // fragments of row blocks 2 pr, 2 pr + 1: {0, 1} or {2, 3, 4, 5}
+                    for (int ks = 0; ks < KS; ++ks) s.q[r][ks] = *(const u32x4 *)(qb + row * (uint32_t)D + 32 * ks);
+                }
+                const u32x4 *pb = (const u32x4 *)(a.wsP + tv * TP_HALVES);
+                // fragments {0, 1} (row blocks 0, 1) or {2, 3, 4, 5} (row blocks 2, 3)
 #pragma unroll
-            for (int f = 0; f < 4; ++f) s.p[f] = pb[(pr == 0 ? min(f, 1) : 2 + f) * 64 + lane];
-            const float *gb = a.wsGam + tv * 128;
+                for (int f = 0; f < NP; ++f) s.p[f] = pb[(PR == 0 ? f : 2 + f) * 64 + lane];
+            };
+            auto compute = [&](const OutSet<D> &s, int lt, auto bufc) __attribute__((always_inline)) {
+                constexpr int buf = decltype(bufc)::value;  // == lt % 2
+                const int t0 = st + TILE * lt, n = min(TILE, en - t0);
+                f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
-            for (int r = 0; r < 2; ++r) s.gam[r] = *(const float4 *)(gb + 16 * (2 * pr + r) + 4 * lg);
-        };
-        auto compute = [&](const OutSet<D> &s, int lt, auto bufc) __attribute__((always_inline)) {
-            constexpr int buf = decltype(bufc)::value;  // == lt % 2
-            const int t0 = st + TILE * lt, n = min(TILE, en - t0);
-            f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+                for (int ks = 0; ks < KS; ++ks) {
+                    const half8 bs = as_half8(sh.S16[buf][ks][lane]);
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const half8 bs = as_half8(sh.S16[buf][ks][lane]);
-#pragma unroll
-                for (int r = 0; r < 2; ++r) acc[r] = mfma_f16(as_half8(s.q[r][ks]), bs, acc[r]);
-            }
-#pragma unroll
-            for (int r = 0; r < 2; ++r) {
-                acc[r][0] *= s.gam[r].x;
-                acc[r][1] *= s.gam[r].y;
-                acc[r][2] *= s.gam[r].z;
-                acc[r][3] *= s.gam[r].w;
-            }
-            const half8 ef0 = as_half8(sh.E[buf][0][lane]);
-            if (a.wsWrite) {
-                // ||E row||^2 over this slice's 16 columns for the wave's 32 tokens
-                // (E k-step pr: lane (ln, lg) element i is token kappa(pr, lg, i),
-                // column ln), summed over the 16 lanes of each row by a transposing
-                // butterfly: after it, lane ln holds the sum for element ln / 2
-                const half8 ef = pr == 0 ? ef0 : as_half8(sh.E[buf][1][lane]);
-                float x[8];
-#pragma unroll
-                for (int i = 0; i < 8; ++i) x[i] = (float)ef[i] * (float)ef[i];
-                const bool b3 = (ln >> 3) & 1, b2 = (ln >> 2) & 1, b1 = (ln >> 1) & 1;
-                float y[4], z[2];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {  // partner ln ^ 8 (rotate the row of 16 by 8)
-                    const float send = b3 ? x[q] : x[4 + q];
-                    const float recv = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
-                                                                     0, __builtin_bit_cast(int, send), 0x128, 0xF, 0xF, false));
-                    y[q] = (b3 ? x[4 + q] : x[q]) + recv;
+                    for (int r = 0; r < 2; ++r) acc[r] = mfma_f16(as_half8(s.q[r][ks]), bs, acc[r]);
                 }
 #pragma unroll
-                for (int q = 0; q < 2; ++q) {  // partner ln ^ 4 (swizzle with xor mask 4)
-                    const float send = b2 ? y[q] : y[2 + q];
-                    const float recv = __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, send), 0x101F));
-                    z[q] = (b2 ? y[2 + q] : y[q]) + recv;
+                for (int r = 0; r < 2; ++r) {
+                    const float4 g4 = *(const float4 *)(&sh.G[lt % 3][0][16 * (2 * PR + r) + 4 * lg]);
+                    acc[r][0] *= g4.x;
+                    acc[r][1] *= g4.y;
+                    acc[r][2] *= g4.z;
+                    acc[r][3] *= g4.w;
                 }
-                float wsum;
-                {  // partner ln ^ 2, then ln ^ 1 (quad permutations)
-                    const float send = b1 ? z[0] : z[1];
-                    const float recv = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
-                                                                     0, __builtin_bit_cast(int, send), 0x4E, 0xF, 0xF, false));
-                    wsum = (b1 ? z[1] : z[0]) + recv;
-                    wsum += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, wsum), 0xB1, 0xF,
-                                                                                  0xF, false));
+                const half8 ef0 = as_half8(sh.E[buf][0][lane]);
+                if (a.wsWrite) {
+                    // ||E row||^2 over this slice's 16 columns for the wave's 32 tokens
+                    // (E k-step PR: lane (ln, lg) element i is token kappa(PR, lg, i),
+                    // column ln), summed over the 16 lanes of each row by a transposing
+                    // butterfly: after it, lane ln holds the sum for element ln / 2
+                    const half8 ef = PR == 0 ? ef0 : as_half8(sh.E[buf][1][lane]);
+                    float x[8];
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) x[i] = (float)ef[i] * (float)ef[i];
+                    const bool b3 = (ln >> 3) & 1, b2 = (ln >> 2) & 1, b1 = (ln >> 1) & 1;
+                    float y[4], z[2];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {  // partner ln ^ 8 (rotate the row of 16 by 8)
+                        const float send = b3 ? x[q] : x[4 + q];
+                        const float recv = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                                                                         0, __builtin_bit_cast(int, send), 0x128, 0xF, 0xF, false));
+                        y[q] = (b3 ? x[4 + q] : x[q]) + recv;
+                    }
+#pragma unroll
+                    for (int q = 0; q < 2; ++q) {  // partner ln ^ 4 (swizzle with xor mask 4)
+                        const float send = b2 ? y[q] : y[2 + q];
+                        const float recv = __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, send), 0x101F));
+                        z[q] = (b2 ? y[2 + q] : y[q]) + recv;
+                    }
+                    float wsum;
+                    {  // partner ln ^ 2, then ln ^ 1 (quad permutations)
+                        const float send = b1 ? z[0] : z[1];
+                        const float recv = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                                                                         0, __builtin_bit_cast(int, send), 0x4E, 0xF, 0xF, false));
+                        wsum = (b1 ? z[1] : z[0]) + recv;
+                        wsum += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, wsum), 0xB1, 0xF,
+                                                                                      0xF, false));
+                    }
+                    const int i = ln >> 1, tok = 32 * PR + 16 * (i >> 2) + 4 * lg + (i & 3);
+                    if ((ln & 1) == 0 && tok < n) a.wsWrite[((size_t)(t0 + tok) * a.H_v + j) * a.n_split + sl] = wsum;
                 }
-                const int i = ln >> 1, tok = 32 * pr + 16 * (i >> 2) + 4 * lg + (i & 3);
-                if ((ln & 1) == 0 && tok < n) a.wsWrite[((size_t)(t0 + tok) * a.H_v + j) * a.n_split + sl] = wsum;
-            }
-            if (pr == 0) {
-                acc[0] = mfma_f16(as_half8(s.p[0]), ef0, acc[0]);
-                acc[1] = mfma_f16(as_half8(s.p[1]), ef0, acc[1]);
-            } else {
-                const half8 ef1 = as_half8(sh.E[buf][1][lane]);
-                acc[0] = mfma_f16(as_half8(s.p[0]), ef0, acc[0]);
-                acc[1] = mfma_f16(as_half8(s.p[2]), ef0, acc[1]);
-                acc[0] = mfma_f16(as_half8(s.p[1]), ef1, acc[0]);
-                acc[1] = mfma_f16(as_half8(s.p[3]), ef1, acc[1]);
-            }
-            // o: the wave's 32 x 16 block goes through LDS (private to the wave)
-            // and leaves as 16-byte row pieces, through a buffer resource covering
-            // the tile's n valid rows: pieces of rows past a ragged tile's end fall
-            // outside it and are dropped
-            constexpr int ES = OUT_BF16 ? 2 : 4;
-            uint32_t *ost = sh.Ost[pr];
-            if (OUT_BF16) {
-                uint16_t *o16 = (uint16_t *)ost;  // [32 rows][16] bf16
+                if (PR == 0) {
+                    acc[0] = mfma_f16(as_half8(s.p[0]), ef0, acc[0]);
+                    acc[1] = mfma_f16(as_half8(s.p[1]), ef0, acc[1]);
+                } else {
+                    const half8 ef1 = as_half8(sh.E[buf][1][lane]);
+                    acc[0] = mfma_f16(as_half8(s.p[0]), ef0, acc[0]);
+                    acc[1] = mfma_f16(as_half8(s.p[2]), ef0, acc[1]);
+                    acc[0] = mfma_f16(as_half8(s.p[1]), ef1, acc[0]);
+                    acc[1] = mfma_f16(as_half8(s.p[3]), ef1, acc[1]);
+                }
+                // o straight from the accumulators (lane (ln, lg): rows 16 r + 4 lg + e
+                // of the wave's 32, column v0 + ln), through a buffer resource covering
+                // the tile's n valid rows: stores past a ragged tile's end fall outside
+                // it and are dropped
+                constexpr int ES = OUT_BF16 ? 2 : 4;
+                const uint32_t row_bytes = (uint32_t)a.H_v * D * ES;
+                const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                    (char *)a.o + (size_t)t0 * row_bytes, (short)0, (int)(row_bytes * (uint32_t)n), 0x00020000);
+                const uint32_t col = (uint32_t)(j * D + v0 + ln) * ES;
 #pragma unroll
                 for (int r = 0; r < 2; ++r)
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        o16[(16 * r + 4 * lg + e) * 16 + ln] = __builtin_bit_cast(uint16_t, (__bf16)(a.scale * acc[r][e]));
-            } else {
-#pragma unroll
-                for (int r = 0; r < 2; ++r)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) ost[(16 * r + 4 * lg + e) * 16 + ln] = __builtin_bit_cast(uint32_t, a.scale * acc[r][e]);
-            }
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");  // (own wave's LDS, in order)
-            const uint32_t row_bytes = (uint32_t)a.H_v * D * ES;
-            const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-                (char *)a.o + (size_t)t0 * row_bytes, (short)0, (int)(row_bytes * (uint32_t)n), 0x00020000);
-            constexpr int PIECES = 16 * ES / 16;  // 16-byte pieces per row of the block
-#pragma unroll
-            for (int c = 0; c < 32 * PIECES / 64; ++c) {
-                const int idx = 64 * c + lane, rr = idx / PIECES, pc = idx % PIECES;
-                const u32x4 val = *(const u32x4 *)((const char *)ost + rr * 16 * ES + 16 * pc);
-                const uint32_t off = (uint32_t)(32 * pr + rr) * row_bytes + (uint32_t)(j * D + v0) * ES + 16 * pc;
-                __builtin_amdgcn_raw_buffer_store_b128(val, rs, off, 0, 0);
+                    for (int e = 0; e < 4; ++e) {
+                        const uint32_t off = (uint32_t)(32 * PR + 16 * r + 4 * lg + e) * row_bytes + col;
+                        const float val = a.scale * acc[r][e];
+                        if (OUT_BF16)
+                            __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, (__bf16)val), rs, off, 0, 0);
+                        else
+                            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, val), rs, off, 0, 0);
+                    }
+            };
+            // iteration it computes tile it - 1 and then loads tile it + 1 into the
+            // same register set (set (it + 1) % 2)
+            auto step = [&](int it, OutSet<D> &s, auto bufc) __attribute__((always_inline)) {
+                lds_barrier();
+                if (it >= 1) compute(s, it - 1, bufc);
+                load(s, it + 1);
+            };
+            if (n_tiles > 0) {
+                OutSet<D> sa, sb;
+                load(sa, 0);
+                for (int it = 0; it <= n_tiles; it += 2) {
+                    step(it, sb, std::integral_constant<int, 1>());
+                    if (it + 1 <= n_tiles) step(it + 1, sa, std::integral_constant<int, 0>());
+                }
             }
         };
-        // iteration it computes tile it - 1 and then loads tile it + 1 into the
-        // same register set (set (it + 1) % 2)
-        auto step = [&](int it, OutSet<D> &s, auto bufc) __attribute__((always_inline)) {
-            lds_barrier();
-            if (it >= 1) compute(s, it - 1, bufc);
-            load(s, it + 1);
-        };
-        if (n_tiles > 0) {
-            OutSet<D> sa, sb;
-            load(sa, 0);
-            for (int it = 0; it <= n_tiles; it += 2) {
-                step(it, sb, std::integral_constant<int, 1>());
-                if (it + 1 <= n_tiles) step(it + 1, sa, std::integral_constant<int, 0>());
-            }
-        }
+        if (w == 2)
+            run(std::integral_constant<int, 0>());
+        else
+            run(std::integral_constant<int, 1>());
     } else {
         // ============================================================== loaders
         const int x = w - 4;  // quarter of every tile
@@ -822,7 +817,7 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             s.v = *(const u32x4 *)(vb + (uint32_t)min(16 * x + ((lane & 31) >> 1), n - 1) * (uint32_t)a.H_v * D);
             s.g = a.wsGam[tv * 128 + 64 * min(x, 1) + lane];
         };
-        auto stage = [&](const LoadSet<D> &s, auto bufc) __attribute__((always_inline)) {
+        auto stage = [&](const LoadSet<D> &s, auto bufc, int g3) __attribute__((always_inline)) {
             constexpr int buf = decltype(bufc)::value;
             constexpr int CH = D / 8, RPI = 64 / CH;
 #pragma unroll
@@ -833,7 +828,7 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             sh.T[buf][t_first][lane] = s.t[0];
             if (nt == 2) sh.T[buf][t_first + 1][lane] = s.t[1];
             if (lane < 32) *(u32x4 *)(&sh.V[buf][(16 * x + (lane >> 1)) * 16 + 8 * (lane & 1)]) = s.v;
-            if (x < 2) sh.G[buf][x][lane] = s.g;
+            if (x < 2) sh.G[g3][x][lane] = s.g;
         };
         // drift sums: the state waves leave per-lane sums of a frame ending in
         // tile t in LDS; loader 3 reduces them after the next barrier (the
@@ -859,11 +854,11 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             LoadSet<D> s0, s1;
             load(s0, 0);
             load(s1, 1);
-            stage(s0, std::integral_constant<int, 0>());
+            stage(s0, std::integral_constant<int, 0>(), 0);
             load(s0, 2);
             auto step = [&](int it, LoadSet<D> &s, auto bufc) __attribute__((always_inline)) {
                 lds_barrier();
-                if (it + 1 < n_tiles) stage(s, bufc);
+                if (it + 1 < n_tiles) stage(s, bufc, (it + 1) % 3);
                 load(s, it + 3);
                 drift_reduce(it);
             };
