@@ -168,8 +168,10 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
             const u32x4 q = row < n ? qv[c] : z;
             *(u32x4 *)(&Kl[row * D + 8 * (ch ^ swz<D>(row))]) = row < n ? kv[c] : z;
             *(u32x4 *)(&Ql[row * D + 8 * (ch ^ swz<D>(row))]) = q;
-            // q rows in fp16 for the output waves of the sequential kernel
-            *(u32x4 *)(a.wsQ + (((size_t)ti * a.H_k + h) * 64 + row) * D + 8 * ch) = __builtin_bit_cast(u32x4, bf16x8_to_f16(q));
+            // q in fp16 for the output waves of the sequential kernel, in A-fragment
+            // order: row block row / 16, k-step ch / 4, lane (ch % 4) * 16 + row % 16
+            const size_t fq = ((size_t)(row >> 4) * KS + (ch >> 2)) * 64 + (ch & 3) * 16 + (row & 15);
+            *(u32x4 *)(a.wsQ + ((size_t)ti * a.H_k + h) * 64 * D + fq * 8) = __builtin_bit_cast(u32x4, bf16x8_to_f16(q));
         }
     }
     __syncthreads();
@@ -675,13 +677,12 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             auto load = [&](OutSet<D> &s, int lt_) __attribute__((always_inline)) {
                 const int lt = min(lt_, n_tiles - 1);
                 const size_t tv = (size_t)(tile_base + lt) * a.H_v + j;
-                const _Float16 *qb = a.wsQ + ((size_t)(tile_base + lt) * a.H_k + qh) * 64 * D + 8 * lg;
+                // q in A-fragment order: one contiguous 1 KiB per (row block, k-step)
+                const u32x4 *qb = (const u32x4 *)(a.wsQ + ((size_t)(tile_base + lt) * a.H_k + qh) * 64 * D);
 #pragma unroll
-                for (int r = 0; r < 2; ++r) {
-                    const uint32_t row = (uint32_t)(16 * (2 * PR + r) + ln);
+                for (int r = 0; r < 2; ++r)
 #pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) s.q[r][ks] = *(const u32x4 *)(qb + row * (uint32_t)D + 32 * ks);
-                }
+                    for (int ks = 0; ks < KS; ++ks) s.q[r][ks] = qb[((2 * PR + r) * KS + ks) * 64 + lane];
                 const u32x4 *pb = (const u32x4 *)(a.wsP + tv * TP_HALVES);
                 // fragments {0, 1} (row blocks 0, 1) or {2, 3, 4, 5} (row blocks 2, 3)
 #pragma unroll
