@@ -413,17 +413,17 @@ struct SeqShared {
     int xflag[2];              // tiles whose half of K S0^T each state wave has published
 };
 
-// One loader's quarter of a tile: K rows 16 x .. 16 x + 15 (whole 16-byte
+// One loader's share of a tile: K rows 16 x .. 16 x + 15 (whole 16-byte
 // chunks, 64 / (D / 8) rows per load), T diag(beta) fragments {2 x, 2 x + 1}
-// for x < 2 and {4 + x - 2} otherwise, v rows 16 x .. 16 x + 15, and Gamma
-// (x = 0) or D_last (x = 1).
+// for x < 2 and {4 + x - 2} otherwise; loaders 0 and 1 also v rows
+// 32 x .. 32 x + 31 and Gamma (x = 0) or D_last (x = 1).
 template <int D>
 struct LoadSet {
     static constexpr int NK = D / 32;  // row loads of K per loader
     u32x4 k[NK];
     u32x4 t[2];
-    u32x4 v;        // v[16 x + lane / 2][v0 + 8 (lane % 2) .. + 7] (lanes >= 32 repeat)
-    float g;        // Gamma (x = 0) or D_last (x = 1) of token lane
+    u32x4 v;        // loaders 0, 1: v[32 x + lane / 2][v0 + 8 (lane % 2) .. + 7]
+    float g;        // loaders 0, 1: Gamma (x = 0) or D_last (x = 1) of token lane
 };
 
 // Output-wave registers for one tile (two row blocks).
@@ -796,78 +796,97 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             run(std::integral_constant<int, 1>());
     } else {
         // ============================================================== loaders
-        const int x = w - 4;  // quarter of every tile
-        constexpr int NK = LoadSet<D>::NK;
-        const int nt = x < 2 ? 2 : 1;  // T diag(beta) fragments of this loader
-        const int t_first = x < 2 ? 2 * x : 4 + (x - 2);
-        auto load = [&](LoadSet<D> &s, int lt_) __attribute__((always_inline)) {
-            const int lt = min(lt_, n_tiles - 1);  // clamped: every call issues the same loads
-            const int t0 = st + TILE * lt, n = min(TILE, en - t0);
-            const size_t tv = (size_t)(tile_base + lt) * a.H_v + j;
-            constexpr int CH = D / 8, RPI = 64 / CH;
-            const uint16_t *kb = a.k + (size_t)t0 * a.H_k * D + (size_t)qh * D + 8 * (lane % CH);
+        // Loader X takes K rows 16 X .. 16 X + 15 of every tile; loaders 0 and 1
+        // also take two T diag(beta) fragments each, 32 v rows each and Gamma /
+        // D_last; loaders 2 and 3 one T fragment each.  Each role is compiled on
+        // its own so that every load is issued unconditionally.
+        auto run = [&](auto xc) __attribute__((always_inline)) {
+            constexpr int X = decltype(xc)::value;
+            constexpr int NK = LoadSet<D>::NK;
+            constexpr int NT = X < 2 ? 2 : 1;                    // T diag(beta) fragments
+            constexpr int T_FIRST = X < 2 ? 2 * X : 4 + (X - 2);
+            auto load = [&](LoadSet<D> &s, int lt_) __attribute__((always_inline)) {
+                const int lt = min(lt_, n_tiles - 1);  // clamped: every call issues the same loads
+                const int t0 = st + TILE * lt, n = min(TILE, en - t0);
+                const size_t tv = (size_t)(tile_base + lt) * a.H_v + j;
+                constexpr int CH = D / 8, RPI = 64 / CH;
+                const uint16_t *kb = a.k + (size_t)t0 * a.H_k * D + (size_t)qh * D + 8 * (lane % CH);
 #pragma unroll
-            for (int c = 0; c < NK; ++c) {
-                const uint32_t r = (uint32_t)min(16 * x + RPI * c + lane / CH, n - 1);
-                s.k[c] = *(const u32x4 *)(kb + r * (uint32_t)a.H_k * D);
-            }
-            const u32x4 *tb = (const u32x4 *)(a.wsT + tv * TP_HALVES);
+                for (int c = 0; c < NK; ++c) {
+                    const uint32_t r = (uint32_t)min(16 * X + RPI * c + lane / CH, n - 1);
+                    s.k[c] = *(const u32x4 *)(kb + r * (uint32_t)a.H_k * D);
+                }
+                const u32x4 *tb = (const u32x4 *)(a.wsT + tv * TP_HALVES);
 #pragma unroll
-            for (int c = 0; c < 2; ++c) s.t[c] = tb[(t_first + min(c, nt - 1)) * 64 + lane];
-            const uint16_t *vb = a.v + ((size_t)t0 * a.H_v + j) * D + v0 + 8 * (lane & 1);
-            s.v = *(const u32x4 *)(vb + (uint32_t)min(16 * x + ((lane & 31) >> 1), n - 1) * (uint32_t)a.H_v * D);
-            s.g = a.wsGam[tv * 128 + 64 * min(x, 1) + lane];
-        };
-        auto stage = [&](const LoadSet<D> &s, auto bufc, int g3) __attribute__((always_inline)) {
-            constexpr int buf = decltype(bufc)::value;
-            constexpr int CH = D / 8, RPI = 64 / CH;
-#pragma unroll
-            for (int c = 0; c < NK; ++c) {
-                const int row = 16 * x + RPI * c + lane / CH, ch = lane % CH;
-                *(u32x4 *)(&sh.K[buf][row * D + 8 * (ch ^ swz<D>(row))]) = __builtin_bit_cast(u32x4, bf16x8_to_f16(s.k[c]));
-            }
-            sh.T[buf][t_first][lane] = s.t[0];
-            if (nt == 2) sh.T[buf][t_first + 1][lane] = s.t[1];
-            if (lane < 32) *(u32x4 *)(&sh.V[buf][(16 * x + (lane >> 1)) * 16 + 8 * (lane & 1)]) = s.v;
-            if (x < 2) sh.G[g3][x][lane] = s.g;
-        };
-        // drift sums: the state waves leave per-lane sums of a frame ending in
-        // tile t in LDS; loader 3 reduces them after the next barrier (the
-        // buffer of that frame's parity is written again two frames later,
-        // after a barrier this wave only reaches once it is done reading)
-        int frame = frame_base;
-        int frame_end = a.frame_len > 0 ? min(a.frame_len, len) : len;
-        auto drift_reduce = [&](int it) __attribute__((always_inline)) {
-            if (!DRIFT || x != 3 || it < 1) return;
-            const int lt = it - 1;
-            if (TILE * lt + min(TILE, len - TILE * lt) != frame_end) return;
-            if (a.wsDrift && frame < a.n_frames) {
-                const float2 p0 = sh.DR[frame & 1][0][lane], p1 = sh.DR[frame & 1][1][lane];
-                const float num = wave_sum(p0.x + p1.x), den = wave_sum(p0.y + p1.y);
-                if (lane == 0) *(float2 *)(a.wsDrift + (((size_t)frame * a.H_v + j) * a.n_split + sl) * 2) = float2{num, den};
-            }
-            ++frame;
-            frame_end = min(frame_end + a.frame_len, len);
-        };
-        // tile t lives in register set t % 2 and LDS buffer t % 2.  Iteration it
-        // stages tile it + 1 and then loads tile it + 3 into the set just freed.
-        if (n_tiles > 0) {
-            LoadSet<D> s0, s1;
-            load(s0, 0);
-            load(s1, 1);
-            stage(s0, std::integral_constant<int, 0>(), 0);
-            load(s0, 2);
-            auto step = [&](int it, LoadSet<D> &s, auto bufc) __attribute__((always_inline)) {
-                lds_barrier();
-                if (it + 1 < n_tiles) stage(s, bufc, (it + 1) % 3);
-                load(s, it + 3);
-                drift_reduce(it);
+                for (int c = 0; c < NT; ++c) s.t[c] = tb[(T_FIRST + c) * 64 + lane];
+                if (X < 2) {
+                    // v rows 32 X + lane / 2, columns v0 + 8 (lane % 2) .. + 7
+                    const uint16_t *vb = a.v + ((size_t)t0 * a.H_v + j) * D + v0 + 8 * (lane & 1);
+                    s.v = *(const u32x4 *)(vb + (uint32_t)min(32 * X + (lane >> 1), n - 1) * (uint32_t)a.H_v * D);
+                    s.g = a.wsGam[tv * 128 + 64 * X + lane];
+                }
             };
-            for (int it = 0; it <= n_tiles; it += 2) {
-                step(it, s1, std::integral_constant<int, 1>());
-                if (it + 1 <= n_tiles) step(it + 1, s0, std::integral_constant<int, 0>());
+            auto stage = [&](const LoadSet<D> &s, auto bufc, int g3) __attribute__((always_inline)) {
+                constexpr int buf = decltype(bufc)::value;
+                constexpr int CH = D / 8, RPI = 64 / CH;
+#pragma unroll
+                for (int c = 0; c < NK; ++c) {
+                    const int row = 16 * X + RPI * c + lane / CH, ch = lane % CH;
+                    *(u32x4 *)(&sh.K[buf][row * D + 8 * (ch ^ swz<D>(row))]) = __builtin_bit_cast(u32x4, bf16x8_to_f16(s.k[c]));
+                }
+#pragma unroll
+                for (int c = 0; c < NT; ++c) sh.T[buf][T_FIRST + c][lane] = s.t[c];
+                if (X < 2) {
+                    *(u32x4 *)(&sh.V[buf][(32 * X + (lane >> 1)) * 16 + 8 * (lane & 1)]) = s.v;
+                    sh.G[g3][X][lane] = s.g;
+                }
+            };
+            // drift sums: the state waves leave per-lane sums of a frame ending in
+            // tile t in LDS; loader 3 reduces them after the next barrier (the
+            // buffer of that frame's parity is written again two frames later,
+            // after a barrier this wave only reaches once it is done reading)
+            int frame = frame_base;
+            int frame_end = a.frame_len > 0 ? min(a.frame_len, len) : len;
+            auto drift_reduce = [&](int it) __attribute__((always_inline)) {
+                if (!DRIFT || X != 3 || it < 1) return;
+                const int lt = it - 1;
+                if (TILE * lt + min(TILE, len - TILE * lt) != frame_end) return;
+                if (a.wsDrift && frame < a.n_frames) {
+                    const float2 p0 = sh.DR[frame & 1][0][lane], p1 = sh.DR[frame & 1][1][lane];
+                    const float num = wave_sum(p0.x + p1.x), den = wave_sum(p0.y + p1.y);
+                    if (lane == 0) *(float2 *)(a.wsDrift + (((size_t)frame * a.H_v + j) * a.n_split + sl) * 2) = float2{num, den};
+                }
+                ++frame;
+                frame_end = min(frame_end + a.frame_len, len);
+            };
+            // tile t lives in register set t % 2 and LDS buffer t % 2.  Iteration it
+            // stages tile it + 1 and then loads tile it + 3 into the set just freed.
+            if (n_tiles > 0) {
+                LoadSet<D> s0, s1;
+                load(s0, 0);
+                load(s1, 1);
+                stage(s0, std::integral_constant<int, 0>(), 0);
+                load(s0, 2);
+                auto step = [&](int it, LoadSet<D> &s, auto bufc) __attribute__((always_inline)) {
+                    lds_barrier();
+                    if (it + 1 < n_tiles) stage(s, bufc, (it + 1) % 3);
+                    load(s, it + 3);
+                    drift_reduce(it);
+                };
+                for (int it = 0; it <= n_tiles; it += 2) {
+                    step(it, s1, std::integral_constant<int, 1>());
+                    if (it + 1 <= n_tiles) step(it + 1, s0, std::integral_constant<int, 0>());
+                }
             }
-        }
+        };
+        if (w == 4)
+            run(std::integral_constant<int, 0>());
+        else if (w == 5)
+            run(std::integral_constant<int, 1>());
+        else if (w == 6)
+            run(std::integral_constant<int, 2>());
+        else
+            run(std::integral_constant<int, 3>());
     }
 }
 
