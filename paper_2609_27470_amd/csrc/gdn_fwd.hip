@@ -101,6 +101,17 @@ __device__ __forceinline__ u32x4 cat_u32x4(v4i16 a, v4i16 b) {
     return __builtin_bit_cast(u32x4, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
+// Workgroup barrier that orders LDS only.  The waves of both kernels exchange
+// data through LDS alone, so their barriers need not wait for global loads in
+// flight or for global stores to be acknowledged (a full __syncthreads waits
+// for both, which drains every prefetch and costs a round trip to memory per
+// barrier after a store).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // K tile staged row-major in LDS (D bf16 per row) with the 16-byte chunks of
 // a row permuted by an XOR with swz(row), so that both the row writes and the
 // transposing reads (4 rows x 4 chunks per 16 lanes) spread over the banks.
@@ -174,7 +185,7 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
             *(u32x4 *)(a.wsQ + ((size_t)ti * a.H_k + h) * 64 * D + fq * 8) = __builtin_bit_cast(u32x4, bf16x8_to_f16(q));
         }
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- Gram blocks of row block w: K K^T and Q K^T for column blocks nb <= w,
     // fragments straight from LDS (a B fragment of K^T is an A fragment of K)
@@ -199,10 +210,14 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
             }
         }
     }
-    __syncthreads();  // K and Q tiles are dead from here on (A and T reuse them)
+    lds_barrier();  // K and Q tiles are dead from here on (A and T reuse them)
 
-    // ---- per v-head of the qk-head's group
-    for (int jj = 0; jj < a.group; ++jj) {
+    // ---- per v-head of the qk-head's group.  Groups of one or two v-heads
+    // (gates prefetched above) run as straight-line code: inside a loop with a
+    // data-dependent trip count the compiler cannot count the memory operations
+    // in flight and would wait for every earlier store before reading the
+    // prefetched gates.
+    auto vhead = [&](int jj) __attribute__((always_inline)) {
         const int j = h * a.group + jj;
         const size_t tv = (size_t)ti * a.H_v + j;
 
@@ -235,7 +250,7 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
             a.wsGam[tv * 128 + lane] = __builtin_amdgcn_exp2f(s);
             a.wsGam[tv * 128 + 64 + lane] = __builtin_amdgcn_exp2f(s_last - s);
         }
-        __syncthreads();
+        lds_barrier();
 
         // A (strictly lower) and P (lower incl. diagonal), rows of block w
         {
@@ -261,7 +276,7 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
                 }
             }
         }
-        __syncthreads();
+        lds_barrier();
 
         // diagonal blocks (wave 0, lane = 16 * block + column); P fragments (waves 1-3)
         if (w == 0) {
@@ -286,7 +301,7 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
                 dst[1] = *(const uint2 *)(&Ps[r * PLD + c4 + 16]);
             }
         }
-        __syncthreads();
+        lds_barrier();
 
         // off-diagonal blocks.  16x16x4 fp32 fragments: A lane = [ln][lg],
         // B lane = [lg][ln], C lane = [4 lg + e][ln].
@@ -317,7 +332,7 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) Ts[(16 * bi + 4 * lg + e) * ALD + 16 * bj + ln] = -t[e];
             }
-            __syncthreads();
+            lds_barrier();
         }
 
         // T diag(beta) (fp16, zero above the diagonal) in fragment order
@@ -333,7 +348,15 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
             }
             *(uint4 *)(a.wsT + tv * TP_HALVES + f * FRAG_HALVES + l * 8) = as_uint4(tv8);
         }
-        __syncthreads();  // before the next v-head reuses A, T, P and the gates
+        lds_barrier();  // before the next v-head reuses A, T, P and the gates
+    };
+    if (a.group == 1) {
+        vhead(0);
+    } else if (a.group == 2) {
+        vhead(0);
+        vhead(1);
+    } else {
+        for (int jj = 0; jj < a.group; ++jj) vhead(jj);
     }
 }
 
@@ -434,15 +457,6 @@ struct OutSet {
 };
 
 constexpr int SEQ_SPIN_LIMIT = 1 << 22;
-
-// Workgroup barrier that orders LDS only.  The waves of this kernel exchange
-// data through LDS alone, so the barrier need not wait for their global loads
-// in flight (a full __syncthreads would, and so drain every prefetch).
-__device__ __forceinline__ void lds_barrier() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
 
 template <int D, bool OUT_BF16, bool DRIFT>
 __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
