@@ -139,7 +139,16 @@ __device__ __forceinline__ void load_block(const int32_t *p, int lo, int len, in
     }
 }
 
+struct RunRec {
+    unsigned long long key;  // (orderable score, chunk id): bigger is better
+    int len;                 // candidate slots of the run
+    int bkt;                 // span of the run
+};
+constexpr int RUN_CAP = 2048;  // runs ranked from LDS
+
 __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
+    __shared__ RunRec s_run[RUN_CAP];
+    __shared__ int s_take[RUN_CAP], s_from[RUN_CAP];
     __shared__ int s_scan[SEL_THREADS / 64 + 1];
     __shared__ long long s_ll[SEL_THREADS / 64 + 1];
     __shared__ int s_bad;
@@ -210,16 +219,23 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     if (tid == 0) a.run_start[R] = c1;
     __syncthreads();
 
-    // ---- run keys and spans
+    // ---- run keys and spans.  The two ranking passes below compare every run
+    // with every other; up to RUN_CAP runs they read a copy of the run table
+    // in LDS (one 16-byte read per comparison), beyond that the global one.
     const int ncand = c1 - c0;
     const int a_min = (ncand > 0) ? a.chunk[c0] : 0;
     const int a_max = (ncand > 0) ? a.chunk[c1 - 1] : 0;
     const long long span = (long long)a_max - a_min + 1;
     const int N = max(1, a.N);
+    const bool in_lds = R <= RUN_CAP;
     for (int r = tid; r < R; r += SEL_THREADS) {
-        const int chn = a.chunk[a.run_start[r]];
-        a.run_key[r] = ((unsigned long long)orderable(a.scores[chn]) << 32) | (unsigned)chn;
-        a.run_bkt[r] = (int)(((long long)N * (chn - a_min)) / span);
+        const int rs = a.run_start[r], re = a.run_start[r + 1];
+        const int chn = a.chunk[rs];
+        const unsigned long long key = ((unsigned long long)orderable(a.scores[chn]) << 32) | (unsigned)chn;
+        const int bkt = (int)(((long long)N * (chn - a_min)) / span);
+        a.run_key[r] = key;
+        a.run_bkt[r] = bkt;
+        if (in_lds) s_run[r] = RunRec{key, re - rs, bkt};
     }
     __syncthreads();
 
@@ -227,14 +243,24 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     const long long quota = (a.M - a.n_s - a.n_w) / N;
     long long taken = 0;
     for (int r = tid; r < R; r += SEL_THREADS) {
-        const unsigned long long key = a.run_key[r];
-        const int bk = a.run_bkt[r];
-        const long long ln = a.run_start[r + 1] - a.run_start[r];
-        long long above = 0;
-        for (int r2 = 0; r2 < R; ++r2)
-            if (a.run_bkt[r2] == bk && a.run_key[r2] > key) above += a.run_start[r2 + 1] - a.run_start[r2];
+        long long above = 0, ln;
+        if (in_lds) {
+            const RunRec me = s_run[r];
+            ln = me.len;
+            for (int r2 = 0; r2 < R; ++r2) {
+                const RunRec o = s_run[r2];
+                if (o.bkt == me.bkt && o.key > me.key) above += o.len;
+            }
+        } else {
+            const unsigned long long key = a.run_key[r];
+            const int bk = a.run_bkt[r];
+            ln = a.run_start[r + 1] - a.run_start[r];
+            for (int r2 = 0; r2 < R; ++r2)
+                if (a.run_bkt[r2] == bk && a.run_key[r2] > key) above += a.run_start[r2 + 1] - a.run_start[r2];
+        }
         const long long t = min(ln, max(0LL, quota - above));
         a.run_take[r] = (int)t;
+        if (in_lds) s_take[r] = (int)t;
         taken += t;
     }
     taken = block_sum_ll(taken, s_ll);
@@ -243,16 +269,29 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     // ---- fill with the best remaining tokens over all spans; a run keeps
     // its newest tokens, slots [run_from, run end)
     for (int r = tid; r < R; r += SEL_THREADS) {
-        const unsigned long long key = a.run_key[r];
-        const long long ln = a.run_start[r + 1] - a.run_start[r];
-        const long long left = ln - a.run_take[r];
-        long long above = 0;
-        for (int r2 = 0; r2 < R; ++r2)
-            if (a.run_key[r2] > key) above += (a.run_start[r2 + 1] - a.run_start[r2]) - a.run_take[r2];
+        long long above = 0, ln, tk;
+        if (in_lds) {
+            const RunRec me = s_run[r];
+            ln = me.len;
+            tk = s_take[r];
+            for (int r2 = 0; r2 < R; ++r2) {
+                const RunRec o = s_run[r2];
+                if (o.key > me.key) above += o.len - s_take[r2];
+            }
+        } else {
+            const unsigned long long key = a.run_key[r];
+            ln = a.run_start[r + 1] - a.run_start[r];
+            tk = a.run_take[r];
+            for (int r2 = 0; r2 < R; ++r2)
+                if (a.run_key[r2] > key) above += (a.run_start[r2 + 1] - a.run_start[r2]) - a.run_take[r2];
+        }
+        const long long left = ln - tk;
         const long long f = min(left, max(0LL, fill - above));
-        a.run_from[r] = a.run_start[r + 1] - (int)(a.run_take[r] + f);
+        a.run_from[r] = a.run_start[r + 1] - (int)(tk + f);
+        if (in_lds) s_from[r] = a.run_start[r + 1] - (int)(tk + f);
     }
     __syncthreads();
+    auto run_from = [&](int r) { return in_lds ? s_from[r] : a.run_from[r]; };
 
     // ---- pass 2: keep list (ascending) and its inverse on destinations [0, M)
     int total_kept = 0;
@@ -266,7 +305,7 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
         if (a.slot) load_block(a.slot, lo, a.len, sl);
         int pc = (lo > 0 && lo <= a.len) ? a.chunk[lo - 1] : -1;
         int r = (lo < a.len) ? a.th_run[base / SEL_PER + tid] - 1 : -1;  // run holding the slot before lo
-        int from = (r >= 0 && r < R) ? a.run_from[r] : 0;
+        int from = (r >= 0 && r < R) ? run_from(r) : 0;
         unsigned mask = 0;
 #pragma unroll
         for (int k = 0; k < SEL_PER; ++k) {
@@ -276,7 +315,7 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
                 if (i >= c0 && i < c1) {
                     if (i == c0 || ch[k] != pc) {
                         ++r;
-                        from = a.run_from[r];
+                        from = run_from(r);
                     }
                     kept = i >= from;
                 }
