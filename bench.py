@@ -124,15 +124,18 @@ def streaming_bench(ds, dev, stream, n_chunks, n_layers=24):
     state_io = n_layers * 2 * H_V * D * D * 4   # every layer reads and writes its state once per chunk
     out = {"layers": n_layers, "policy": "n_sink=4, n_window=1024, N=4, M=16384",
            "state_io_bytes_per_chunk": state_io}
-    for mode in ("eager", "graph"):
+    for mode in ("eager", "graph", "graph_indexed"):
         s = DeltaSStream(n_layers, H_K, H_V, D, KV_LAYERS, row_elems, BUDGET, 132, BUDGET // 128 + total + 8,
-                         4, 1024, 4, device=dev)
+                         4, 1024, 4, device=dev, indexed=mode.endswith("indexed"))
         # start from a full cache: BUDGET tokens in 128 earlier chunks with random scores
         s.pos[:BUDGET] = torch.arange(BUDGET, dtype=torch.int32, device=dev)
         s.chunk_id[:BUDGET] = torch.arange(BUDGET, dtype=torch.int32, device=dev) // 128
         s.scores[:BUDGET // 128] = torch.rand(BUDGET // 128, generator=gen, device=dev)
         s.length, s.n_chunks, s.next_pos = BUDGET, BUDGET // 128, BUDGET
-        if mode == "graph":
+        if s.indexed:
+            s.slot[:BUDGET] = torch.arange(BUDGET, dtype=torch.int32, device=dev)
+            s.free = torch.arange(BUDGET, s.capacity, dtype=torch.int32, device=dev)
+        if mode.startswith("graph"):
             s.capture_graph()
         off = 0
         evs = []

@@ -25,6 +25,12 @@ over fixed input buffers (`inputs`); the chunk's length is read on the
 device, so the one graph serves every chunk length up to max_chunk.  The
 append and the eviction stay outside the graph: the cache length they work
 from is host state.
+
+With `indexed=True` the cache is addressed through a slot table (logical
+token i lives in physical row slot[i]): eviction is `kv_evict_topk_indexed`,
+which keeps exactly the same tokens and moves no K/V byte, and a chunk's rows
+are written into the rows the last eviction freed.  The logical view
+(rows slot[0..length)) equals the order-preserving cache of the default mode.
 """
 from __future__ import annotations
 
@@ -33,7 +39,7 @@ from dataclasses import dataclass
 import torch
 
 from . import (LAYER_FROB, deltas_drift, gdn_chunk_fwd, gdn_shape, gdn_workspace_bytes, kv_evict_topk,
-               kv_workspace_bytes)
+               kv_evict_topk_indexed, kv_indexed_workspace_bytes, kv_workspace_bytes)
 
 
 @dataclass
@@ -45,6 +51,8 @@ class Snapshot:
     pos: torch.Tensor
     chunk_id: torch.Tensor
     scores: torch.Tensor
+    slot: object
+    free: object
     length: int
     n_chunks: int
     next_pos: int
@@ -60,7 +68,7 @@ class DeltaSStream:
     """
 
     def __init__(self, n_layers, H_k, H_v, d, kv_layers, row_elems, M, max_chunk, max_chunks,
-                 n_sink=4, n_window=1024, n_buckets=4, score_mode=LAYER_FROB, device="cuda"):
+                 n_sink=4, n_window=1024, n_buckets=4, score_mode=LAYER_FROB, device="cuda", indexed=False):
         if n_sink + n_window > M:
             raise ValueError("sink + window exceed the budget")
         dev = torch.device(device)
@@ -80,8 +88,17 @@ class DeltaSStream:
         self.scores = torch.zeros(max_chunks, dtype=torch.float32, device=dev)
         shape = gdn_shape([max_chunk], H_k, H_v, d, 0)
         self.gdn_ws = torch.empty(max(gdn_workspace_bytes(shape), 1), dtype=torch.uint8, device=dev)
-        self.kv_ws = torch.empty(max(kv_workspace_bytes(kv_layers, row_elems * 2, self.capacity), 1),
-                                 dtype=torch.uint8, device=dev)
+        self.indexed = indexed
+        if indexed:
+            self.slot = torch.zeros(self.capacity, dtype=torch.int32, device=dev)
+            self.free = torch.arange(self.capacity, dtype=torch.int32, device=dev)   # rows not in use
+            self.n_free = self.capacity
+            self.freed = torch.empty(self.capacity, dtype=torch.int32, device=dev)
+            self.kv_ws = torch.empty(max(kv_indexed_workspace_bytes(self.capacity), 1), dtype=torch.uint8, device=dev)
+        else:
+            self.slot = self.free = None
+            self.kv_ws = torch.empty(max(kv_workspace_bytes(kv_layers, row_elems * 2, self.capacity), 1),
+                                     dtype=torch.uint8, device=dev)
         self.graph = None
         self.length = 0      # tokens in the cache
         self.n_chunks = 0    # chunks seen (the next chunk's id)
@@ -114,18 +131,41 @@ class DeltaSStream:
     def _append_and_evict(self, T, k_rows, v_rows, stream=None):
         c = self.n_chunks
         n = self.length
-        self.k[:, n:n + T].copy_(k_rows)
-        self.v[:, n:n + T].copy_(v_rows)
+        if self.indexed:
+            rows = self.free[:T]
+            self.k.index_copy_(1, rows.to(torch.int64), k_rows)
+            self.v.index_copy_(1, rows.to(torch.int64), v_rows)
+            self.slot[n:n + T] = rows
+            self.free = self.free[T:]
+        else:
+            self.k[:, n:n + T].copy_(k_rows)
+            self.v[:, n:n + T].copy_(v_rows)
         self.pos[n:n + T] = torch.arange(self.next_pos, self.next_pos + T, dtype=torch.int32, device=self.dev)
         self.chunk_id[n:n + T] = c
         self.next_pos += T
         self.n_chunks = c + 1
         n += T
         ns, nw, nb = self.policy
-        self.length, _ = kv_evict_topk(list(self.k), list(self.v), self.pos, self.chunk_id,
-                                       self.scores[:self.n_chunks], n, self.M, ns, nw, nb,
-                                       workspace=self.kv_ws, stream=stream)
+        if self.indexed:
+            new_len, _, freed = kv_evict_topk_indexed(self.pos, self.chunk_id, self.slot, self.scores[:self.n_chunks],
+                                                      n, self.M, ns, nw, nb, free_out=self.freed,
+                                                      workspace=self.kv_ws, stream=stream)
+            if n > self.M:
+                self.free = torch.cat([self.free, freed[:n - self.M]])
+            self.length = new_len
+        else:
+            self.length, _ = kv_evict_topk(list(self.k), list(self.v), self.pos, self.chunk_id,
+                                           self.scores[:self.n_chunks], n, self.M, ns, nw, nb,
+                                           workspace=self.kv_ws, stream=stream)
         return self.length
+
+    def logical_rows(self):
+        """(K, V) rows of the cached tokens in logical (arrival) order, [kv_layers][length][row]."""
+        n = self.length
+        if not self.indexed:
+            return self.k[:, :n], self.v[:, :n]
+        idx = self.slot[:n].to(torch.int64)
+        return self.k[:, idx], self.v[:, idx]
 
     def capture_graph(self):
         """Allocate the fixed input buffers and record one chunk's linear-attention
@@ -172,16 +212,26 @@ class DeltaSStream:
     def save(self) -> Snapshot:
         """Copy the memory aside (question time)."""
         n = self.length
+        if self.indexed:   # rows stay where they are: keep the physical planes and the tables
+            return Snapshot(self.state.clone(), self.k.clone(), self.v.clone(), self.pos[:n].clone(),
+                            self.chunk_id[:n].clone(), self.scores[:self.n_chunks].clone(), self.slot[:n].clone(),
+                            self.free.clone(), n, self.n_chunks, self.next_pos)
         return Snapshot(self.state.clone(), self.k[:, :n].clone(), self.v[:, :n].clone(), self.pos[:n].clone(),
-                        self.chunk_id[:n].clone(), self.scores[:self.n_chunks].clone(), n, self.n_chunks,
+                        self.chunk_id[:n].clone(), self.scores[:self.n_chunks].clone(), None, None, n, self.n_chunks,
                         self.next_pos)
 
     def restore(self, s: Snapshot):
         """Put a saved memory back; the stream continues as if nothing had run since."""
         n = s.length
         self.state.copy_(s.state)
-        self.k[:, :n].copy_(s.k)
-        self.v[:, :n].copy_(s.v)
+        if self.indexed:
+            self.k.copy_(s.k)
+            self.v.copy_(s.v)
+            self.slot[:n].copy_(s.slot)
+            self.free = s.free.clone()
+        else:
+            self.k[:, :n].copy_(s.k)
+            self.v[:, :n].copy_(s.v)
         self.pos[:n].copy_(s.pos)
         self.chunk_id[:n].copy_(s.chunk_id)
         self.scores[:s.n_chunks].copy_(s.scores)

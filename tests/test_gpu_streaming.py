@@ -158,3 +158,38 @@ def test_graph_replays_match_eager_steps(ds):
         assert torch.equal(a.pos[:n], b.pos[:n]) and torch.equal(a.chunk_id[:n], b.chunk_id[:n])
         assert torch.equal(a.k[:, :n], b.k[:, :n])
         off += T
+
+
+def test_indexed_stream_matches_gather_stream(ds):
+    """The slot-indexed session (no K/V row moved at eviction, new chunks
+    written into freed rows) keeps the same tokens, scores and states as the
+    order-preserving one after every chunk, and its logical rows are the
+    gathered cache bit for bit; save/restore is transparent in it too."""
+    from paper_2609_27470_amd.streaming import DeltaSStream
+    lens = chunk_lengths(14, seed=6)
+    xs = layer_streams(sum(lens) + 64, seed_cfg=100)
+    a = new_stream()
+    b = DeltaSStream(L, H_K, H_V, D, KV_L, ROW, M, 132, 128, N_SINK, N_WIN, N_BKT, device=DEV, indexed=True)
+    off = 0
+    snap = None
+    for c, T in enumerate(lens):
+        k_rows, v_rows = kv_rows(off, T)
+        ins = chunk_inputs(xs, off, off + T)
+        a.step(ins, k_rows, v_rows)
+        b.step(ins, k_rows, v_rows)
+        if c == 8:
+            snap = b.save()
+            q0 = sum(lens)
+            qk, qv = kv_rows(10 ** 6, 40)
+            b.step(chunk_inputs(xs, q0, q0 + 40), qk, qv)
+            b.restore(snap)
+        torch.cuda.synchronize()
+        n = a.length
+        assert b.length == n
+        assert torch.equal(a.state, b.state), c
+        assert torch.equal(a.scores[:c + 1], b.scores[:c + 1])
+        assert torch.equal(a.pos[:n], b.pos[:n]) and torch.equal(a.chunk_id[:n], b.chunk_id[:n])
+        ka, va = a.logical_rows()
+        kb, vb = b.logical_rows()
+        assert torch.equal(ka, kb) and torch.equal(va, vb), c
+        off += T
