@@ -13,9 +13,9 @@
 //   * the leftover budget is filled the same way over all spans from the
 //     tokens not yet kept;
 //   * kept slots -> ascending keep list and its inverse on [0, M).
-// Slot data is read in blocks of 32 consecutive slots per thread with
-// 16-byte loads, so each pass over the cache costs one memory round trip per
-// 32 Ki slots.
+// Slot data is read in blocks of 4 consecutive slots per thread with one
+// 16-byte load (adjacent lanes read adjacent 16 bytes), 4 Ki slots per
+// block and memory round trip.
 // With a slot table (the indexed variant) the K and V rows never move: the
 // select kernel itself compacts pos, chunk_id and slot (the physical row of
 // each logical token) in place and lists the freed physical rows.
@@ -40,8 +40,9 @@
 namespace ds {
 
 constexpr int SEL_THREADS = 1024;
-constexpr int SEL_PER = 32;                         // consecutive slots per thread per pass block
+constexpr int SEL_PER = 4;                          // consecutive slots per thread per pass block
 constexpr int SEL_BLOCK = SEL_THREADS * SEL_PER;
+static_assert(SEL_PER == 4, "pass 2 stores a thread's four inverse entries as one int4");
 constexpr int GATHER_U = 16;                        // uint4 per thread per group
 constexpr int SPIN_LIMIT = 1 << 22;
 constexpr long long STAGE_BYTES = 64ll << 20;       // below this much shift, rows are staged
@@ -78,30 +79,47 @@ __device__ __forceinline__ uint32_t orderable(float f) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Barrier that orders LDS only: the block reductions below exchange partial
+// sums through LDS, and a full __syncthreads would also wait for every global
+// store in flight (the keep list written in the same loop).
+__device__ __forceinline__ void lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Exclusive prefix sum over the 1024 threads of the block.
+// Inclusive prefix sum over the 64 lanes of a wave with DPP moves: row
+// shifts by 1, 2, 4, 8 within each row of 16 lanes, then the last lane of a
+// row added to the next row(s) by row broadcasts (rows 1 and 3 get lane 15,
+// rows 2 and 3 lane 31).  Lanes without a source add 0.
+__device__ __forceinline__ int wave_incl_scan(int v) {
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);  // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);  // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);  // row_shr:8
+    v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);  // row_bcast:15 into rows 1, 3
+    v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);  // row_bcast:31 into rows 2, 3
+    return v;
+}
+
+// Exclusive prefix sum over the 1024 threads of the block: a scan inside each
+// wave, then wave 0 scans the 16 wave totals the same way.
 __device__ int block_excl_scan(int x, int *s_tmp, int &total) {
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    int incl = x;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const int y = __shfl_up(incl, off, 64);
-        if (lane >= off) incl += y;
-    }
+    const int incl = wave_incl_scan(x);
     if (lane == 63) s_tmp[wid] = incl;
-    __syncthreads();
-    if (tid == 0) {
-        int acc = 0;
-        for (int i = 0; i < SEL_THREADS / 64; ++i) {
-            const int t = s_tmp[i];
-            s_tmp[i] = acc;
-            acc += t;
-        }
-        s_tmp[SEL_THREADS / 64] = acc;
+    lds_sync();
+    if (wid == 0) {
+        const int t = lane < SEL_THREADS / 64 ? s_tmp[lane] : 0;
+        const int it = wave_incl_scan(t);
+        if (lane < SEL_THREADS / 64) s_tmp[lane] = it - t;
+        if (lane == SEL_THREADS / 64 - 1) s_tmp[SEL_THREADS / 64] = it;
     }
-    __syncthreads();
+    lds_sync();
     const int res = s_tmp[wid] + incl - x;
     total = s_tmp[SEL_THREADS / 64];
-    __syncthreads();
+    lds_sync();
     return res;
 }
 
@@ -110,15 +128,15 @@ __device__ long long block_sum_ll(long long x, long long *s_tmp) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
     if (lane == 0) s_tmp[wid] = x;
-    __syncthreads();
+    lds_sync();
     if (tid == 0) {
         long long acc = 0;
         for (int i = 0; i < SEL_THREADS / 64; ++i) acc += s_tmp[i];
         s_tmp[SEL_THREADS / 64] = acc;
     }
-    __syncthreads();
+    lds_sync();
     const long long r = s_tmp[SEL_THREADS / 64];
-    __syncthreads();
+    lds_sync();
     return r;
 }
 
@@ -149,6 +167,7 @@ constexpr int RUN_CAP = 2048;  // runs ranked from LDS
 __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     __shared__ RunRec s_run[RUN_CAP];
     __shared__ int s_take[RUN_CAP], s_from[RUN_CAP];
+    __shared__ int s_keep[SEL_BLOCK], s_free[SEL_BLOCK];  // one pass-2 block's keep entries and freed slots
     __shared__ int s_scan[SEL_THREADS / 64 + 1];
     __shared__ long long s_ll[SEL_THREADS / 64 + 1];
     __shared__ int s_bad;
@@ -323,28 +342,50 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
                 pc = ch[k];
             }
         }
+        // the block's keep entries and freed slots are collected in LDS and
+        // leave as contiguous stores; the inverse leaves as one 16-byte store
+        // per thread (scattered 4-byte stores would load the memory pipeline)
         int tot = 0;
         int off = total_kept + block_excl_scan(__popc(mask), s_scan, tot);
+        const int ev_base = base - total_kept;  // tokens evicted before this block
+        int invv[SEL_PER];
 #pragma unroll
         for (int k = 0; k < SEL_PER; ++k) {
             const int i = lo + k;
+            invv[k] = -1;
             if (i < a.len) {
                 if (mask & (1u << k)) {
                     if (off < a.M) {
-                        a.keep[off] = i;
-                        if (a.keep_out) a.keep_out[off] = i;
+                        s_keep[off - total_kept] = i;
                         if (off != i) first_move = min(first_move, off);
                         if (i - off >= a.stage_shift) split = min(split, off);
                     }
-                    if (i < a.M) a.inv[i] = off;
+                    invv[k] = off;
                     ++off;
-                } else {
-                    if (i < a.M) a.inv[i] = -1;
+                } else if (a.slot) {
                     // evicted token i is the (i - off)-th evicted one in logical order
-                    if (a.slot && i - off < n_evict) a.free_out[i - off] = sl[k];
+                    s_free[i - off - ev_base] = sl[k];
                 }
             }
         }
+        if (lo + SEL_PER <= a.M) {
+            *(int4 *)(a.inv + lo) = int4{invv[0], invv[1], invv[2], invv[3]};
+        } else {
+#pragma unroll
+            for (int k = 0; k < SEL_PER; ++k)
+                if (lo + k < a.M) a.inv[lo + k] = invv[k];
+        }
+        lds_sync();
+        const int kn = min(tot, a.M - total_kept);
+        for (int q = tid; q < kn; q += SEL_THREADS) {
+            a.keep[total_kept + q] = s_keep[q];
+            if (a.keep_out) a.keep_out[total_kept + q] = s_keep[q];
+        }
+        if (a.slot) {
+            const int fn = min(min(a.len - base, SEL_BLOCK) - tot, n_evict - ev_base);
+            for (int q = tid; q < fn; q += SEL_THREADS) a.free_out[ev_base + q] = s_free[q];
+        }
+        lds_sync();
         total_kept += tot;
     }
     // ---- moving destinations form the suffix [first_move, M) (keep[d] - d is
@@ -355,10 +396,10 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
             s_first = a.M;
             s_split = a.M;
         }
-        __syncthreads();
+        lds_sync();
         if (first_move < a.M) atomicMin(&s_first, first_move);
         if (split < a.M) atomicMin(&s_split, split);
-        __syncthreads();
+        lds_sync();
         first_move = s_first;
         split = max(s_split, first_move);
     }
@@ -370,7 +411,14 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
             a.status[1] = 1;
         }
     }
-    for (int i = first_move * a.n_chunks + tid; i < a.n_flags; i += SEL_THREADS) a.flags[i] = 0;
+    {
+        // flags of the moving destinations back to zero, 16 bytes per store
+        const int fs = first_move * a.n_chunks, fe = a.n_flags;
+        const int fa = min((fs + 3) & ~3, fe), fb = max(fa, fe & ~3);
+        if (tid < fa - fs) a.flags[fs + tid] = 0;
+        for (int q = fa / 4 + tid; q < fb / 4; q += SEL_THREADS) ((int4 *)a.flags)[q] = int4{0, 0, 0, 0};
+        if (tid < fe - fb) a.flags[fb + tid] = 0;
+    }
 
     // ---- indexed variant: pos, chunk_id and slot move down in place,
     // new[d] = old[keep[d]] for the moving destinations [first_move, M).
@@ -378,6 +426,7 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     // start; each block reads everything before any thread writes, and the
     // next block's reads lie above what this block writes.
     if (a.slot && total_kept == a.M) {
+        __syncthreads();  // the keep list written above by every thread is read below
         for (int base = first_move; base < a.M; base += SEL_BLOCK) {
             int vp[SEL_PER], vc[SEL_PER], vs[SEL_PER];
 #pragma unroll
