@@ -755,7 +755,7 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                                                                                       0xF, false));
                     }
                     const int i = ln >> 1, tok = 32 * PR + 16 * (i >> 2) + 4 * lg + (i & 3);
-                    if ((ln & 1) == 0 && tok < n) a.wsWrite[((size_t)(t0 + tok) * a.H_v + j) * a.n_split + sl] = wsum;
+                    if ((ln & 1) == 0 && tok < n) a.wsWrite[((size_t)j * a.n_split + sl) * a.st.T + t0 + tok] = wsum;
                 }
                 if (PR == 0) {
                     acc[0] = mfma_f16(as_half8(s.p[0]), ef0, acc[0]);
@@ -930,11 +930,13 @@ __global__ __launch_bounds__(256) void gdn_drift_finalize_kernel(const float *ws
 
 // Write-magnitude signal per (frame, v-head): the sum over the frame's tokens
 // of sqrt(sum over slices of ||E row||^2) and the token count -> [n_frames][H_v][2].
-// One wave per (frame, v-head); fixed summation order.  Frames past the real
-// count are zeroed.
-__global__ __launch_bounds__(64) void gdn_write_finalize_kernel(const float *ws, float *out, int n_frames, int H_v,
-                                                                 int n_split, Streams st, int frame_len) {
-    const int f = blockIdx.x, j = blockIdx.y, lane = threadIdx.x;
+// One workgroup per (frame, v-head); thread i takes tokens i, i + 256, ... of
+// the frame (the slices of one token sit T_total apart, so adjacent lanes read
+// adjacent words), then a fixed-order tree over the threads.  Frames past the
+// real count are zeroed.
+__global__ __launch_bounds__(256) void gdn_write_finalize_kernel(const float *ws, float *out, int n_frames, int H_v,
+                                                                  int n_split, Streams st, int frame_len) {
+    const int f = blockIdx.x, j = blockIdx.y, tid = threadIdx.x;
     int base = 0, tb = 0, te = 0;
     for_streams(st, [&](int, int s0, int e0) {
         const int nf = frames_in(e0 - s0, frame_len);
@@ -948,14 +950,21 @@ __global__ __launch_bounds__(64) void gdn_write_finalize_kernel(const float *ws,
         return false;
     });
     double acc = 0.0;
-    for (int t = tb + lane; t < te; t += 64) {
+    const float *wj = ws + (size_t)j * n_split * st.T;
+    for (int t = tb + tid; t < te; t += 256) {
         float s = 0.f;
-        for (int q = 0; q < n_split; ++q) s += ws[((size_t)t * H_v + j) * n_split + q];
+        for (int q = 0; q < n_split; ++q) s += wj[(size_t)q * st.T + t];
         acc += sqrt((double)s);
     }
-    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
-    if (lane == 0) {
-        out[((size_t)f * H_v + j) * 2] = (float)acc;
+    __shared__ double red[256];
+    red[tid] = acc;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+        if (tid < off) red[tid] += red[tid + off];
+        __syncthreads();
+    }
+    if (tid == 0) {
+        out[((size_t)f * H_v + j) * 2] = (float)red[0];
         out[((size_t)f * H_v + j) * 2 + 1] = (float)(te - tb);
     }
 }
@@ -1042,7 +1051,7 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
         if (e != hipSuccess) return e;
     }
     if (p.write_partials && p.n_frames > 0) {
-        hipLaunchKernelGGL(gdn_write_finalize_kernel, dim3(p.n_frames, p.H_v), dim3(64), 0, stream, p.wsWrite,
+        hipLaunchKernelGGL(gdn_write_finalize_kernel, dim3(p.n_frames, p.H_v), dim3(256), 0, stream, p.wsWrite,
                            p.write_partials, p.n_frames, p.H_v, p.n_split, a.st, p.frame_len);
         e = hipGetLastError();
     }

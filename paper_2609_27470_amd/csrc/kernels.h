@@ -27,7 +27,7 @@ struct GdnLaunch {
     _Float16 *wsQ;      // [tiles_max][H_k][4][d/32][64][8] q in fp16, A-fragment order (zero past a ragged tile's end)
     float *wsGam;       // [tiles_max][H_v][2][64]   Gamma_r = exp(gamma_r), D_last,r = exp(gamma_last - gamma_r)
     float *wsDrift;     // [n_frames][H_v][n_split][2] (one pair per slice)
-    float *wsWrite;     // [T_total][H_v][n_split] per-token ||E row||^2 over each slice's columns
+    float *wsWrite;     // [H_v][n_split][T_total] per-token ||E row||^2 over each slice's columns
     int tiles_max;
     int n_split;        // d_v slices of 16 per (stream, v-head)
 };
