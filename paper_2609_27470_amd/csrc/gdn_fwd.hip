@@ -296,9 +296,8 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
                 const int f = c >> 6, l = c & 63;
                 const int fw = f < 2 ? f : 2 + ((f - 2) >> 1), fks = f < 2 ? 0 : ((f - 2) & 1);
                 const int r = 16 * fw + (l & 15), c4 = 32 * fks + 4 * (l >> 4);
-                uint2 *dst = (uint2 *)(a.wsP + tv * TP_HALVES + f * FRAG_HALVES + l * 8);
-                dst[0] = *(const uint2 *)(&Ps[r * PLD + c4]);
-                dst[1] = *(const uint2 *)(&Ps[r * PLD + c4 + 16]);
+                const uint2 p0 = *(const uint2 *)(&Ps[r * PLD + c4]), p1 = *(const uint2 *)(&Ps[r * PLD + c4 + 16]);
+                *(uint4 *)(a.wsP + tv * TP_HALVES + f * FRAG_HALVES + l * 8) = uint4{p0.x, p0.y, p1.x, p1.y};
             }
         }
         lds_barrier();
@@ -340,11 +339,16 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
             const int f = c >> 6, l = c & 63;
             const int fw = f < 2 ? f : 2 + ((f - 2) >> 1), fks = f < 2 ? 0 : ((f - 2) & 1);
             const int r = 16 * fw + (l & 15), c4 = 32 * fks + 4 * (l >> 4);
+            // columns c4 .. c4 + 3 and c4 + 16 .. c4 + 19 of row r, as two 16-byte reads each
+            const float4 ta = *(const float4 *)(&Ts[r * ALD + c4]), tb = *(const float4 *)(&Ts[r * ALD + c4 + 16]);
+            const float4 ba = *(const float4 *)(&beta_s[c4]), bb = *(const float4 *)(&beta_s[c4 + 16]);
+            const float tx[8] = {ta.x * ba.x, ta.y * ba.y, ta.z * ba.z, ta.w * ba.w,
+                                 tb.x * bb.x, tb.y * bb.y, tb.z * bb.z, tb.w * bb.w};
             half8 tv8;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const int i = c4 + 16 * (e >> 2) + (e & 3);
-                tv8[e] = (_Float16)((i <= r) ? Ts[r * ALD + i] * beta_s[i] : 0.f);
+                tv8[e] = (_Float16)((i <= r) ? tx[e] : 0.f);
             }
             *(uint4 *)(a.wsT + tv * TP_HALVES + f * FRAG_HALVES + l * 8) = as_uint4(tv8);
         }
