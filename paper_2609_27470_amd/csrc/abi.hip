@@ -123,6 +123,7 @@ ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k,
     p.wsQ = (_Float16 *)(ws + lay.offQ);
     p.wsGam = (float *)(ws + lay.offGam);
     p.wsDrift = (float *)(ws + lay.offDrift);
+    p.wsCnt = (unsigned *)(ws + lay.offCnt);
     p.wsWrite = (float *)(ws + lay.offWrite);
     p.tiles_max = lay.tiles_max;
     p.n_split = lay.n_split;

@@ -54,6 +54,9 @@ struct GdnArgs {
     float *wsGam, *wsDrift;
     float *wsWrite;  // per-token sums of squares of E over the slice's columns, or null
     int n_split;
+    // drift sums reduced inside the sequential kernel (null: a separate pass does it)
+    float *drift_out;       // [n_frames][H_v][2]
+    unsigned *drift_cnt;    // [B][H_v] slices done, zeroed by the prep kernel
 };
 
 // Global tile index -> (stream, first token, valid tokens).  Tiles are
@@ -141,6 +144,18 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
     float *As = (float *)reg_k, *Ts = (float *)reg_q;
 
     const int ti = blockIdx.x, h = blockIdx.y;  // tile, qk-head
+    if (ti == 0 && h == 0 && a.drift_out) {
+        // set-up for the sequential kernel's drift reduction: slice counters
+        // to zero, frames past the real count to zero
+        for (int i = threadIdx.x; i < a.st.B * a.H_v; i += 256) a.drift_cnt[i] = 0u;
+        int real = 0;
+        for_streams(a.st, [&](int, int s0, int e0) {
+            real += frames_in(e0 - s0, a.frame_len);
+            return false;
+        });
+        for (int i = min(real, a.n_frames) * a.H_v + (int)threadIdx.x; i < a.n_frames * a.H_v; i += 256)
+            *(float2 *)(a.drift_out + 2 * (size_t)i) = float2{0.f, 0.f};
+    }
     int t0 = 0, n = 0;
     if (!locate_tile(a.st, ti, t0, n)) return;
     const int tid = threadIdx.x, lane = tid & 63, ln = lane & 15, lg = lane >> 4;
@@ -896,6 +911,30 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                     if (it + 1 <= n_tiles) step(it + 1, s0, std::integral_constant<int, 0>());
                 }
             }
+            // the last of the stream's n_split workgroups of v-head j to finish
+            // sums the slices of every frame of the stream (fixed order)
+            if (DRIFT && X == 3 && a.drift_out) {
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // this wave's partials before the count
+                unsigned prev = 0;
+                if (lane == 0)
+                    prev = __hip_atomic_fetch_add(&a.drift_cnt[b * a.H_v + j], 1u, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+                prev = __builtin_amdgcn_readfirstlane(prev);
+                if (prev == (unsigned)a.n_split - 1u) {
+                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // every slice's partials after it
+                    const int nf = min(frames_in(len, a.frame_len), a.n_frames - frame_base);
+                    for (int f = lane; f < nf; f += 64) {
+                        const size_t fj = (size_t)(frame_base + f) * a.H_v + j;
+                        float num = 0.f, den = 0.f;
+                        for (int s = 0; s < a.n_split; ++s) {
+                            const float2 pr = *(const float2 *)(a.wsDrift + (fj * a.n_split + s) * 2);
+                            num += pr.x;
+                            den += pr.y;
+                        }
+                        *(float2 *)(a.drift_out + fj * 2) = float2{num, den};
+                    }
+                }
+            }
         };
         if (w == 4)
             run(std::integral_constant<int, 0>());
@@ -995,6 +1034,8 @@ GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, i
     off = align256(off + (size_t)n_frames * H_v * w.n_split * 2 * sizeof(float));
     w.offWrite = off;
     off = align256(off + (size_t)T_total * H_v * w.n_split * sizeof(float));
+    w.offCnt = off;
+    off = align256(off + (size_t)B * H_v * sizeof(unsigned));
     w.total = off;
     return w;
 }
@@ -1025,6 +1066,11 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     a.wsDrift = p.drift_partials ? p.wsDrift : nullptr;
     a.wsWrite = p.write_partials ? p.wsWrite : nullptr;
     a.n_split = p.n_split;
+    // drift sums reduced by the sequential kernel itself when the prep kernel
+    // runs (it clears the counters); otherwise by the finalize pass
+    const bool fused_drift = p.drift_partials && p.n_frames > 0 && p.tiles_max > 0;
+    a.drift_out = fused_drift ? p.drift_partials : nullptr;
+    a.drift_cnt = p.wsCnt;
 
     if (p.tiles_max > 0) {
         hipLaunchKernelGGL(gdn_prep_kernel<D>, dim3(p.tiles_max, p.H_k), dim3(256), 0, stream, a);
@@ -1047,7 +1093,7 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (p.drift_partials && p.n_frames > 0) {
+    if (p.drift_partials && p.n_frames > 0 && !fused_drift) {
         const int n = p.n_frames * p.H_v;
         hipLaunchKernelGGL(gdn_drift_finalize_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, p.wsDrift,
                            p.drift_partials, p.n_frames, p.H_v, p.n_split, a.st, p.frame_len);

@@ -28,13 +28,14 @@ struct GdnLaunch {
     float *wsGam;       // [tiles_max][H_v][2][64]   Gamma_r = exp(gamma_r), D_last,r = exp(gamma_last - gamma_r)
     float *wsDrift;     // [n_frames][H_v][n_split][2] (one pair per slice)
     float *wsWrite;     // [H_v][n_split][T_total] per-token ||E row||^2 over each slice's columns
+    unsigned *wsCnt;    // [B][H_v] slices whose drift sums are written (drift reduction in the sequential kernel)
     int tiles_max;
     int n_split;        // d_v slices of 16 per (stream, v-head)
 };
 
 // Workspace layout shared by the size query and the launcher.
 struct GdnWorkspace {
-    size_t offT, offP, offQ, offGam, offDrift, offWrite, total;
+    size_t offT, offP, offQ, offGam, offDrift, offWrite, offCnt, total;
     int tiles_max, n_split;
 };
 GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, int n_frames);
