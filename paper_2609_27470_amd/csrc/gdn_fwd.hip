@@ -19,7 +19,9 @@
 //             tiles in order, keeps its rows of S in fp32 registers, does the
 //             state-dependent products on fp16 matrix cores, writes o, and at
 //             every frame end the drift sums of Eq. 3 for its rows.
-//   gdn_drift_finalize sums the partial drift sums in a fixed order.
+//   The drift sums of the slices are added in a fixed order by the last
+//   workgroup of each (stream, v-head) to finish (gdn_drift_finalize when no
+//   prep pass runs).
 #include <type_traits>
 
 #include "common.h"
@@ -81,12 +83,14 @@ __device__ bool locate_tile(const Streams &s, int ti, int &t0, int &n) {
 // ============================================================================
 // gdn_prep: one workgroup per (tile, qk-head).  The K and Q rows of the tile
 // are loaded once as whole 16-byte chunks and staged in LDS; the Gram blocks
-// K K^T and Q K^T run on bf16 matrix cores (exact bf16 inputs, fp32
+// K K^T and (K Q^T) run on bf16 matrix cores (exact bf16 inputs, fp32
 // accumulation) and stay in registers.  Then, for every v-head of the group
-// (its own gates): the inverse of the unit lower-triangular I + A is blocked
-// in 16 x 16 blocks, the diagonal blocks by forward substitution and the
-// off-diagonal ones on fp32 matrix cores, T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj,
-// by distance from the diagonal.
+// (its own gates): P is scaled and written straight from the K Q^T registers
+// (their layout is already P's fragment layout), and the inverse of the unit
+// lower-triangular I + A is blocked in 16 x 16 blocks, the diagonal blocks by
+// forward substitution and the off-diagonal ones on fp32 matrix cores,
+// T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj, by distance from the diagonal.
+// 39 KiB of LDS and at most 128 VGPRs, so that four workgroups share a CU.
 // ============================================================================
 __device__ __forceinline__ f32x4 mfma_f32_16x16x4(float a, float b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -124,22 +128,32 @@ __device__ __forceinline__ int swz(int row) {
     return (((row >> 1) & 1) << 2) | ((row >> 2) & 3);
 }
 
+// Two C blocks -> one fp16 operand (8 values per lane).
+__device__ __forceinline__ half8 to_half8(const f32x4 &a, const f32x4 &b) {
+    half8 r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        r[e] = (_Float16)a[e];
+        r[4 + e] = (_Float16)b[e];
+    }
+    return r;
+}
+
 template <int D>
-__global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
+__global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
     constexpr int KS = D / 32;   // 32-wide k-steps over the head dim
     constexpr int CH = D / 8;    // 16-byte chunks per K or Q row
     constexpr int NKB = D / 16;
     constexpr int RPI = 64 / CH;  // rows per 64-lane row load
     constexpr int NI = 16 / RPI;  // row loads per wave (16 rows each)
     constexpr int ALD = 68;       // floats per LDS row of A and T (bank-conflict-free writes)
-    constexpr int PLD = 72;       // halves per LDS row of P
     constexpr int RB = (64 * D * 2 > 64 * ALD * 4) ? 64 * D * 2 : 64 * ALD * 4;
-    // K and Q tiles while the Gram blocks are formed, then A and T
+    // K and Q tiles while the Gram blocks are formed, then A and T (39.4 KiB
+    // in all for d = 128: four workgroups fit in a CU's LDS)
     __shared__ __align__(16) char reg_k[RB], reg_q[RB];
     __shared__ float Ys[4][256];
-    __shared__ __align__(16) _Float16 Ps[64 * PLD];
-    __shared__ __align__(16) float gam_s[64];
-    __shared__ __align__(16) float beta_s[64];
+    __shared__ __align__(16) float gam_s[2][64];   // log2 Gamma and beta of up to two v-heads
+    __shared__ __align__(16) float beta_s[2][64];
     uint16_t *Kl = (uint16_t *)reg_k, *Ql = (uint16_t *)reg_q;
     float *As = (float *)reg_k, *Ts = (float *)reg_q;
 
@@ -161,18 +175,7 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, ln = lane & 15, lg = lane >> 4;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-    // ---- gates of the group's v-heads (wave 0, lane = token), loaded first
-    constexpr int MAXG = 2;  // v-heads per qk-head handled with prefetched gates (more: loaded in turn)
-    float gpre[MAXG], bpre[MAXG];
-    if (w == 0) {
-        const uint32_t r = (uint32_t)min(lane, n - 1);
-#pragma unroll
-        for (int jj = 0; jj < MAXG; ++jj) {
-            const int j = h * a.group + min(jj, a.group - 1);
-            gpre[jj] = a.g[(size_t)(t0 + r) * a.H_v + j];
-            bpre[jj] = a.beta[(size_t)(t0 + r) * a.H_v + j];
-        }
-    }
+    constexpr int MAXG = 2;  // v-heads per qk-head whose gates are loaded with K and Q (more: loaded in turn)
 
     // ---- K and Q rows 16 w .. 16 w + 15: whole 16-byte chunks, RPI rows per
     // load; rows past a ragged tile's end are loaded clamped and zeroed here
@@ -187,6 +190,19 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
             kv[c] = *(const u32x4 *)(kb + off);
             qv[c] = *(const u32x4 *)(qb + off);
         }
+        // gates of the group's first v-heads (wave 0, lane = token), issued after
+        // K and Q so that waiting for K and Q does not wait for them; raw g and
+        // beta go to the gate slots of LDS, where the gate phase picks them up
+        float gpre[MAXG], bpre[MAXG];
+        if (w == 0) {
+            const uint32_t r = (uint32_t)min(lane, n - 1);
+#pragma unroll
+            for (int jj = 0; jj < MAXG; ++jj) {
+                const int j = h * a.group + min(jj, a.group - 1);
+                gpre[jj] = a.g[(size_t)(t0 + r) * a.H_v + j];
+                bpre[jj] = a.beta[(size_t)(t0 + r) * a.H_v + j];
+            }
+        }
 #pragma unroll
         for (int c = 0; c < NI; ++c) {
             const int row = 16 * w + RPI * c + lane / CH, ch = lane % CH;
@@ -199,11 +215,21 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
             const size_t fq = ((size_t)(row >> 4) * KS + (ch >> 2)) * 64 + (ch & 3) * 16 + (row & 15);
             *(u32x4 *)(a.wsQ + ((size_t)ti * a.H_k + h) * 64 * D + fq * 8) = __builtin_bit_cast(u32x4, bf16x8_to_f16(q));
         }
+        if (w == 0) {
+#pragma unroll
+            for (int jj = 0; jj < MAXG; ++jj) {
+                gam_s[jj][lane] = gpre[jj];
+                beta_s[jj][lane] = bpre[jj];
+            }
+        }
     }
     lds_barrier();
 
-    // ---- Gram blocks of row block w: K K^T and Q K^T for column blocks nb <= w,
-    // fragments straight from LDS (a B fragment of K^T is an A fragment of K)
+    // ---- Gram blocks of row block w, fragments straight from LDS (a B fragment
+    // of K^T is an A fragment of K): K K^T blocks (w, nb) and the transposed
+    // blocks (K Q^T)(nb, w) for nb <= w.  Lane (ln, lg) of the latter holds keys
+    // 16 nb + 4 lg + e of query 16 w + ln, which is half of an A fragment of P
+    // in the token order of E: P is written from the registers.
     f32x4 gk[4], gq[4];
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
@@ -221,31 +247,29 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
                 const int rb = 16 * nb + ln;
                 const bf16x8 bk = as_bf16x8(*(const u32x4 *)(&Kl[rb * D + 8 * ((4 * ks + lg) ^ swz<D>(rb))]));
                 gk[nb] = mfma_bf16(ak, bk, gk[nb]);
-                gq[nb] = mfma_bf16(aq, bk, gq[nb]);
+                gq[nb] = mfma_bf16(bk, aq, gq[nb]);
             }
         }
     }
     lds_barrier();  // K and Q tiles are dead from here on (A and T reuse them)
 
-    // ---- per v-head of the qk-head's group.  Groups of one or two v-heads
-    // (gates prefetched above) run as straight-line code: inside a loop with a
+    // ---- per v-head of the qk-head's group: gates (wave 0), P from the Gram
+    // registers, then A and its inverse.  Groups of one or two v-heads (gates
+    // prefetched above) run as straight-line code: inside a loop with a
     // data-dependent trip count the compiler cannot count the memory operations
     // in flight and would wait for every earlier store before reading the
-    // prefetched gates.
-    auto vhead = [&](int jj) __attribute__((always_inline)) {
+    // prefetched gates.  For two v-heads both gate sets and both P are formed
+    // first, so that the Q K^T registers are free during the inversions.
+    // gates: gamma = inclusive prefix sum of g in base-2 units, and beta, into
+    // LDS slot `slot`; Gamma and D_last to the workspace
+    auto gates = [&](int jj, int slot) __attribute__((always_inline)) {
         const int j = h * a.group + jj;
         const size_t tv = (size_t)ti * a.H_v + j;
-
-        // gamma = inclusive prefix sum of g, in base-2 units
         if (w == 0) {
             float gv = 0.f, bv = 0.f;
-            if (jj < MAXG) {
-#pragma unroll
-                for (int q = 0; q < MAXG; ++q)
-                    if (q == jj) {
-                        gv = gpre[q];
-                        bv = bpre[q];
-                    }
+            if (jj < MAXG) {  // loaded with K and Q (slot == jj)
+                gv = gam_s[jj][lane];
+                bv = beta_s[jj][lane];
             } else {
                 gv = a.g[(size_t)(t0 + min(lane, n - 1)) * a.H_v + j];
                 bv = a.beta[(size_t)(t0 + min(lane, n - 1)) * a.H_v + j];
@@ -258,42 +282,59 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
                 if (lane >= off) s += y;
             }
             s *= 1.4426950408889634f;  // exp(gamma) = exp2(s)
-            gam_s[lane] = s;
-            beta_s[lane] = bv;
+            gam_s[slot][lane] = s;
+            beta_s[slot][lane] = bv;
             // padding rows have g = 0, so row 63 carries the tile's last gamma
             const float s_last = __shfl(s, 63, 64);
             a.wsGam[tv * 128 + lane] = __builtin_amdgcn_exp2f(s);
             a.wsGam[tv * 128 + 64 + lane] = __builtin_amdgcn_exp2f(s_last - s);
         }
-        lds_barrier();
-
-        // A (strictly lower) and P (lower incl. diagonal), rows of block w
+    };
+    // P (lower incl. diagonal) of query block w, Gamma_i / Gamma_j (q_i . k_j)
+    // for keys j <= i, as the A fragments (w, ks) of P E (k-step ks pairs key
+    // blocks 2 ks, 2 ks + 1); block (nb, w): key 16 nb + 4 lg + e, query 16 w + ln
+    auto pfrags = [&](int jj, int slot) __attribute__((always_inline)) {
+        const size_t tv = (size_t)ti * a.H_v + h * a.group + jj;
+        const float gq_i = gam_s[slot][16 * w + ln];  // query 16 w + ln
+        auto pblock = [&](int nb) __attribute__((always_inline)) {
+            f32x4 pk = {0.f, 0.f, 0.f, 0.f};
+            if (nb <= w) {
+                const float4 gj = *(const float4 *)(&gam_s[slot][16 * nb + 4 * lg]);
+                const float gjv[4] = {gj.x, gj.y, gj.z, gj.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    pk[e] = (nb < w || 4 * lg + e <= ln) ? __builtin_amdgcn_exp2f(gq_i - gjv[e]) * gq[nb][e] : 0.f;
+            }
+            return pk;
+        };
+        _Float16 *pw = a.wsP + tv * TP_HALVES + lane * 8;
+        *(uint4 *)(pw + frag_index(w, 0) * FRAG_HALVES) = as_uint4(to_half8(pblock(0), pblock(1)));
+        if (w >= 2) *(uint4 *)(pw + frag_index(w, 1) * FRAG_HALVES) = as_uint4(to_half8(pblock(2), pblock(3)));
+    };
+    auto invert = [&](int jj, int slot) __attribute__((always_inline)) {
+        const size_t tv = (size_t)ti * a.H_v + h * a.group + jj;
+        // A (strictly lower), rows of block w
         {
-            const float4 gr = *(const float4 *)(&gam_s[16 * w + 4 * lg]);
-            const float4 br = *(const float4 *)(&beta_s[16 * w + 4 * lg]);
+            const float4 gr = *(const float4 *)(&gam_s[slot][16 * w + 4 * lg]);
+            const float4 br = *(const float4 *)(&beta_s[slot][16 * w + 4 * lg]);
             const float grv[4] = {gr.x, gr.y, gr.z, gr.w}, brv[4] = {br.x, br.y, br.z, br.w};
             float gi[4];
 #pragma unroll
-            for (int nb = 0; nb < 4; ++nb) gi[nb] = gam_s[16 * nb + ln];
+            for (int nb = 0; nb < 4; ++nb) gi[nb] = gam_s[slot][16 * nb + ln];
 #pragma unroll
             for (int nb = 0; nb < 4; ++nb) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int r = 16 * w + 4 * lg + e, i = 16 * nb + ln;
-                    float av = 0.f, pv = 0.f;
-                    if (nb <= w && i <= r) {
-                        const float dri = __builtin_amdgcn_exp2f(grv[e] - gi[nb]);
-                        pv = dri * gq[nb][e];
-                        if (i < r) av = brv[e] * dri * gk[nb][e];
-                    }
+                    float av = 0.f;
+                    if (nb <= w && i < r) av = brv[e] * __builtin_amdgcn_exp2f(grv[e] - gi[nb]) * gk[nb][e];
                     As[r * ALD + i] = av;
-                    Ps[r * PLD + i] = (_Float16)pv;
                 }
             }
         }
         lds_barrier();
 
-        // diagonal blocks (wave 0, lane = 16 * block + column); P fragments (waves 1-3)
+        // diagonal blocks (wave 0, lane = 16 * block + column)
         if (w == 0) {
             const int o = 16 * (lane >> 4), c = lane & 15;
             float x[16];
@@ -306,14 +347,6 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
             }
 #pragma unroll
             for (int r = 0; r < 16; ++r) Ts[(o + r) * ALD + o + c] = x[r];
-        } else {
-            for (int c = tid - 64; c < 6 * 64; c += 192) {
-                const int f = c >> 6, l = c & 63;
-                const int fw = f < 2 ? f : 2 + ((f - 2) >> 1), fks = f < 2 ? 0 : ((f - 2) & 1);
-                const int r = 16 * fw + (l & 15), c4 = 32 * fks + 4 * (l >> 4);
-                const uint2 p0 = *(const uint2 *)(&Ps[r * PLD + c4]), p1 = *(const uint2 *)(&Ps[r * PLD + c4 + 16]);
-                *(uint4 *)(a.wsP + tv * TP_HALVES + f * FRAG_HALVES + l * 8) = uint4{p0.x, p0.y, p1.x, p1.y};
-            }
         }
         lds_barrier();
 
@@ -356,7 +389,7 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
             const int r = 16 * fw + (l & 15), c4 = 32 * fks + 4 * (l >> 4);
             // columns c4 .. c4 + 3 and c4 + 16 .. c4 + 19 of row r, as two 16-byte reads each
             const float4 ta = *(const float4 *)(&Ts[r * ALD + c4]), tb = *(const float4 *)(&Ts[r * ALD + c4 + 16]);
-            const float4 ba = *(const float4 *)(&beta_s[c4]), bb = *(const float4 *)(&beta_s[c4 + 16]);
+            const float4 ba = *(const float4 *)(&beta_s[slot][c4]), bb = *(const float4 *)(&beta_s[slot][c4 + 16]);
             const float tx[8] = {ta.x * ba.x, ta.y * ba.y, ta.z * ba.z, ta.w * ba.w,
                                  tb.x * bb.x, tb.y * bb.y, tb.z * bb.z, tb.w * bb.w};
             half8 tv8;
@@ -367,15 +400,28 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
             }
             *(uint4 *)(a.wsT + tv * TP_HALVES + f * FRAG_HALVES + l * 8) = as_uint4(tv8);
         }
-        lds_barrier();  // before the next v-head reuses A, T, P and the gates
+        lds_barrier();  // before the next v-head reuses A, T and the gate slot
     };
     if (a.group == 1) {
-        vhead(0);
+        gates(0, 0);
+        lds_barrier();
+        pfrags(0, 0);
+        invert(0, 0);
     } else if (a.group == 2) {
-        vhead(0);
-        vhead(1);
+        gates(0, 0);
+        gates(1, 1);
+        lds_barrier();
+        pfrags(0, 0);
+        pfrags(1, 1);
+        invert(0, 0);
+        invert(1, 1);
     } else {
-        for (int jj = 0; jj < a.group; ++jj) vhead(jj);
+        for (int jj = 0; jj < a.group; ++jj) {
+            gates(jj, 0);
+            lds_barrier();
+            pfrags(jj, 0);
+            invert(jj, 0);
+        }
     }
 }
 
@@ -429,17 +475,6 @@ __global__ __launch_bounds__(256) void gdn_prep_kernel(GdnArgs a) {
 // range).  D_last E enters the state update as fp16; R, E, T diag(beta) and
 // P are fp16.  All accumulation is fp32.
 // ============================================================================
-
-// Two C blocks -> one fp16 B operand.
-__device__ __forceinline__ half8 to_half8(const f32x4 &a, const f32x4 &b) {
-    half8 r;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        r[e] = (_Float16)a[e];
-        r[4 + e] = (_Float16)b[e];
-    }
-    return r;
-}
 
 template <int D>
 struct SeqShared {
