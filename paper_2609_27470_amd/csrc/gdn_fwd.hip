@@ -59,6 +59,7 @@ struct GdnArgs {
     // drift sums reduced inside the sequential kernel (null: a separate pass does it)
     float *drift_out;       // [n_frames][H_v][2]
     unsigned *drift_cnt;    // [B][H_v] slices done, zeroed by the prep kernel
+    int prep_per_vhead;     // prep grid (tiles, H_v) instead of (tiles, H_k)
 };
 
 // Global tile index -> (stream, first token, valid tokens).  Tiles are
@@ -157,8 +158,14 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
     uint16_t *Kl = (uint16_t *)reg_k, *Ql = (uint16_t *)reg_q;
     float *As = (float *)reg_k, *Ts = (float *)reg_q;
 
-    const int ti = blockIdx.x, h = blockIdx.y;  // tile, qk-head
-    if (ti == 0 && h == 0 && a.drift_out) {
+    // tile; qk-head h and the v-heads jbase .. jbase + gcount - 1 of its group
+    // (the whole group, or with one workgroup per v-head for small launches,
+    // which halves a workgroup's latency at the cost of a second Gram product)
+    const int ti = blockIdx.x;
+    const int h = a.prep_per_vhead ? (int)blockIdx.y / a.group : (int)blockIdx.y;
+    const int jbase = a.prep_per_vhead ? (int)blockIdx.y : h * a.group;
+    const int gcount = a.prep_per_vhead ? 1 : a.group;
+    if (ti == 0 && blockIdx.y == 0 && a.drift_out) {
         // set-up for the sequential kernel's drift reduction: slice counters
         // to zero, frames past the real count to zero
         for (int i = threadIdx.x; i < a.st.B * a.H_v; i += 256) a.drift_cnt[i] = 0u;
@@ -198,7 +205,7 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
             const uint32_t r = (uint32_t)min(lane, n - 1);
 #pragma unroll
             for (int jj = 0; jj < MAXG; ++jj) {
-                const int j = h * a.group + min(jj, a.group - 1);
+                const int j = jbase + min(jj, gcount - 1);
                 gpre[jj] = a.g[(size_t)(t0 + r) * a.H_v + j];
                 bpre[jj] = a.beta[(size_t)(t0 + r) * a.H_v + j];
             }
@@ -213,7 +220,8 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
             // q in fp16 for the output waves of the sequential kernel, in A-fragment
             // order: row block row / 16, k-step ch / 4, lane (ch % 4) * 16 + row % 16
             const size_t fq = ((size_t)(row >> 4) * KS + (ch >> 2)) * 64 + (ch & 3) * 16 + (row & 15);
-            *(u32x4 *)(a.wsQ + ((size_t)ti * a.H_k + h) * 64 * D + fq * 8) = __builtin_bit_cast(u32x4, bf16x8_to_f16(q));
+            if (jbase == h * a.group)  // one writer per qk-head
+                *(u32x4 *)(a.wsQ + ((size_t)ti * a.H_k + h) * 64 * D + fq * 8) = __builtin_bit_cast(u32x4, bf16x8_to_f16(q));
         }
         if (w == 0) {
 #pragma unroll
@@ -263,7 +271,7 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
     // gates: gamma = inclusive prefix sum of g in base-2 units, and beta, into
     // LDS slot `slot`; Gamma and D_last to the workspace
     auto gates = [&](int jj, int slot) __attribute__((always_inline)) {
-        const int j = h * a.group + jj;
+        const int j = jbase + jj;
         const size_t tv = (size_t)ti * a.H_v + j;
         if (w == 0) {
             float gv = 0.f, bv = 0.f;
@@ -294,7 +302,7 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
     // for keys j <= i, as the A fragments (w, ks) of P E (k-step ks pairs key
     // blocks 2 ks, 2 ks + 1); block (nb, w): key 16 nb + 4 lg + e, query 16 w + ln
     auto pfrags = [&](int jj, int slot) __attribute__((always_inline)) {
-        const size_t tv = (size_t)ti * a.H_v + h * a.group + jj;
+        const size_t tv = (size_t)ti * a.H_v + jbase + jj;
         const float gq_i = gam_s[slot][16 * w + ln];  // query 16 w + ln
         auto pblock = [&](int nb) __attribute__((always_inline)) {
             f32x4 pk = {0.f, 0.f, 0.f, 0.f};
@@ -312,7 +320,7 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
         if (w >= 2) *(uint4 *)(pw + frag_index(w, 1) * FRAG_HALVES) = as_uint4(to_half8(pblock(2), pblock(3)));
     };
     auto invert = [&](int jj, int slot) __attribute__((always_inline)) {
-        const size_t tv = (size_t)ti * a.H_v + h * a.group + jj;
+        const size_t tv = (size_t)ti * a.H_v + jbase + jj;
         // A (strictly lower), rows of block w
         {
             const float4 gr = *(const float4 *)(&gam_s[slot][16 * w + 4 * lg]);
@@ -402,12 +410,12 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
         }
         lds_barrier();  // before the next v-head reuses A, T and the gate slot
     };
-    if (a.group == 1) {
+    if (gcount == 1) {
         gates(0, 0);
         lds_barrier();
         pfrags(0, 0);
         invert(0, 0);
-    } else if (a.group == 2) {
+    } else if (gcount == 2) {
         gates(0, 0);
         gates(1, 1);
         lds_barrier();
@@ -416,7 +424,7 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
         invert(0, 0);
         invert(1, 1);
     } else {
-        for (int jj = 0; jj < a.group; ++jj) {
+        for (int jj = 0; jj < gcount; ++jj) {
             gates(jj, 0);
             lds_barrier();
             pfrags(jj, 0);
@@ -1107,8 +1115,11 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     a.drift_out = fused_drift ? p.drift_partials : nullptr;
     a.drift_cnt = p.wsCnt;
 
+    // one prep workgroup per (tile, v-head) when a workgroup per (tile, qk-head)
+    // would leave most CUs idle (short calls, e.g. one streamed chunk)
+    a.prep_per_vhead = a.group > 1 && (long long)p.tiles_max * p.H_k < 256;
     if (p.tiles_max > 0) {
-        hipLaunchKernelGGL(gdn_prep_kernel<D>, dim3(p.tiles_max, p.H_k), dim3(256), 0, stream, a);
+        hipLaunchKernelGGL(gdn_prep_kernel<D>, dim3(p.tiles_max, a.prep_per_vhead ? p.H_v : p.H_k), dim3(256), 0, stream, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
