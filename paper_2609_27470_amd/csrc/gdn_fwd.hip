@@ -161,11 +161,17 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
     // tile; qk-head h and the v-heads jbase .. jbase + gcount - 1 of its group
     // (the whole group, or with one workgroup per v-head for small launches,
     // which halves a workgroup's latency at the cost of a second Gram product)
-    const int ti = blockIdx.x;
-    const int h = a.prep_per_vhead ? (int)blockIdx.y / a.group : (int)blockIdx.y;
-    const int jbase = a.prep_per_vhead ? (int)blockIdx.y : h * a.group;
+    // The grid is one-dimensional and tile-major per XCD (dispatch deals
+    // workgroups to the 8 XCDs in turn): the workgroups of every head of one
+    // tile run on one XCD one after another, so the gate rows of a token
+    // (all v-heads in one line) are fetched into one L2 once.
+    const int nhy = a.prep_per_vhead ? a.H_v : a.H_k;
+    const int bid = blockIdx.x, slot = bid >> 3;
+    const int ti = (slot / nhy) * 8 + (bid & 7), hy = slot % nhy;
+    const int h = a.prep_per_vhead ? hy / a.group : hy;
+    const int jbase = a.prep_per_vhead ? hy : h * a.group;
     const int gcount = a.prep_per_vhead ? 1 : a.group;
-    if (ti == 0 && blockIdx.y == 0 && a.drift_out) {
+    if (ti == 0 && hy == 0 && a.drift_out) {
         // set-up for the sequential kernel's drift reduction: slice counters
         // to zero, frames past the real count to zero
         for (int i = threadIdx.x; i < a.st.B * a.H_v; i += 256) a.drift_cnt[i] = 0u;
@@ -1119,7 +1125,9 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     // would leave most CUs idle (short calls, e.g. one streamed chunk)
     a.prep_per_vhead = a.group > 1 && (long long)p.tiles_max * p.H_k < 256;
     if (p.tiles_max > 0) {
-        hipLaunchKernelGGL(gdn_prep_kernel<D>, dim3(p.tiles_max, a.prep_per_vhead ? p.H_v : p.H_k), dim3(256), 0, stream, a);
+        // tiles rounded up to a multiple of 8 (workgroups past the last tile exit)
+        const long long n_prep = (long long)((p.tiles_max + 7) / 8) * 8 * (a.prep_per_vhead ? p.H_v : p.H_k);
+        hipLaunchKernelGGL(gdn_prep_kernel<D>, dim3((unsigned)n_prep), dim3(256), 0, stream, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
