@@ -192,14 +192,28 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     // candidates [c0, c1); th_run[block][thread] = runs starting before the
     // thread's slots
     int R = 0;
+    // the next block's entries are loaded while this one is scanned
+    int nch[SEL_PER], nps[SEL_PER], npc = -1, npp = 0;
+    auto fetch1 = [&](int base) {
+        const int lo = base + tid * SEL_PER;
+        load_block(a.chunk, lo, a.len, nch);
+        load_block(a.pos, lo, a.len, nps);
+        const bool has_prev = lo > 0 && lo <= a.len;
+        npc = has_prev ? a.chunk[lo - 1] : -1;
+        npp = has_prev ? a.pos[lo - 1] : 0;
+    };
+    if (a.len > 0) fetch1(0);
     for (int base = 0; base < a.len; base += SEL_BLOCK) {
         const int lo = base + tid * SEL_PER;
         int ch[SEL_PER], ps[SEL_PER];
-        load_block(a.chunk, lo, a.len, ch);
-        load_block(a.pos, lo, a.len, ps);
-        const bool has_prev = lo > 0 && lo <= a.len;
-        const int pc0 = has_prev ? a.chunk[lo - 1] : -1;
-        int pc = pc0, pp = has_prev ? a.pos[lo - 1] : 0;
+#pragma unroll
+        for (int k = 0; k < SEL_PER; ++k) {
+            ch[k] = nch[k];
+            ps[k] = nps[k];
+        }
+        const int pc0 = npc;
+        int pc = pc0, pp = npp;
+        if (base + SEL_BLOCK < a.len) fetch1(base + SEL_BLOCK);
         int bad = 0, cnt = 0;
 #pragma unroll
         for (int k = 0; k < SEL_PER; ++k) {
@@ -317,13 +331,27 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     int first_move = a.M;  // smallest destination d with keep[d] != d
     int split = a.M;       // smallest destination d with keep[d] - d >= stage_shift
     const int n_evict = a.len - a.M;
+    // the next block's entries are loaded while this one is processed
+    int n2ch[SEL_PER], n2sl[SEL_PER], n2pc = -1, n2r = -1;
+    auto fetch2 = [&](int base) {
+        const int lo = base + tid * SEL_PER;
+        load_block(a.chunk, lo, a.len, n2ch);
+        if (a.slot) load_block(a.slot, lo, a.len, n2sl);
+        n2pc = (lo > 0 && lo <= a.len) ? a.chunk[lo - 1] : -1;
+        n2r = (lo < a.len) ? a.th_run[base / SEL_PER + tid] - 1 : -1;  // run holding the slot before lo
+    };
+    if (a.len > 0) fetch2(0);
     for (int base = 0; base < a.len; base += SEL_BLOCK) {
         const int lo = base + tid * SEL_PER;
         int ch[SEL_PER], sl[SEL_PER];
-        load_block(a.chunk, lo, a.len, ch);
-        if (a.slot) load_block(a.slot, lo, a.len, sl);
-        int pc = (lo > 0 && lo <= a.len) ? a.chunk[lo - 1] : -1;
-        int r = (lo < a.len) ? a.th_run[base / SEL_PER + tid] - 1 : -1;  // run holding the slot before lo
+#pragma unroll
+        for (int k = 0; k < SEL_PER; ++k) {
+            ch[k] = n2ch[k];
+            sl[k] = n2sl[k];
+        }
+        int pc = n2pc;
+        int r = n2r;
+        if (base + SEL_BLOCK < a.len) fetch2(base + SEL_BLOCK);
         int from = (r >= 0 && r < R) ? run_from(r) : 0;
         unsigned mask = 0;
 #pragma unroll
@@ -391,17 +419,25 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     // ---- moving destinations form the suffix [first_move, M) (keep[d] - d is
     // nondecreasing); clear their flags for the gather
     {
-        __shared__ int s_first, s_split;
-        if (tid == 0) {
-            s_first = a.M;
-            s_split = a.M;
+        // minimum over the block: within each wave by lane exchanges, then over
+        // the 16 wave results (one LDS atomic per thread would serialize)
+        __shared__ int s_first[SEL_THREADS / 64], s_split[SEL_THREADS / 64];
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+            first_move = min(first_move, __shfl_xor(first_move, off, 64));
+            split = min(split, __shfl_xor(split, off, 64));
+        }
+        if ((tid & 63) == 0) {
+            s_first[tid >> 6] = first_move;
+            s_split[tid >> 6] = split;
         }
         lds_sync();
-        if (first_move < a.M) atomicMin(&s_first, first_move);
-        if (split < a.M) atomicMin(&s_split, split);
-        lds_sync();
-        first_move = s_first;
-        split = max(s_split, first_move);
+#pragma unroll
+        for (int w = 0; w < SEL_THREADS / 64; ++w) {
+            first_move = min(first_move, s_first[w]);
+            split = min(split, s_split[w]);
+        }
+        split = max(split, first_move);
     }
     if (tid == 0) {
         a.status[3] = first_move;
