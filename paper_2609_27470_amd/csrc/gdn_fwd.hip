@@ -100,6 +100,12 @@ __device__ __forceinline__ f32x4 mfma_f32_16x16x4(float a, float b, f32x4 c) {
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
+// L2 prefetch of 64 16-byte chunks (one per lane; 4 bytes of each are
+// loaded).  The value is only handed to an empty asm statement two tiles
+// later (see LoadSet::pf), so the load is kept and its wait comes late.
+__device__ __forceinline__ uint32_t l2_prefetch(const void *chunk) { return *(const uint32_t *)chunk; }
+__device__ __forceinline__ void l2_retire(uint32_t v) { asm volatile("" ::"v"(v)); }
+
 // Transposed 16-bit fragment read: within each group of 16 lanes, lane l
 // receives element (l % 4) of the 4 elements addressed by lane l/4 + 4 e.
 __device__ __forceinline__ v4i16 ds_read_tr16(const void *p) {
@@ -515,6 +521,7 @@ struct LoadSet {
     u32x4 t[2];
     u32x4 v;        // loaders 0, 1: v[32 x + lane / 2][v0 + 8 (lane % 2) .. + 7]
     float g;        // loaders 0, 1: Gamma (x = 0) or D_last (x = 1) of token lane
+    uint32_t pf[2]; // L2 prefetches issued with this set, retired when it is loaded again
 };
 
 // Output-wave registers for one tile (two row blocks).
@@ -888,6 +895,10 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             constexpr int NT = X < 2 ? 2 : 1;                    // T diag(beta) fragments
             constexpr int T_FIRST = X < 2 ? 2 * X : 4 + (X - 2);
             auto load = [&](LoadSet<D> &s, int lt_) __attribute__((always_inline)) {
+                if (X < 3 && lt_ >= 2) {  // the prefetches issued with this set two tiles ago
+                    l2_retire(s.pf[0]);
+                    l2_retire(s.pf[1]);
+                }
                 const int lt = min(lt_, n_tiles - 1);  // clamped: every call issues the same loads
                 const int t0 = st + TILE * lt, n = min(TILE, en - t0);
                 const size_t tv = (size_t)(tile_base + lt) * a.H_v + j;
@@ -906,6 +917,38 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                     const uint16_t *vb = a.v + ((size_t)t0 * a.H_v + j) * D + v0 + 8 * (lane & 1);
                     s.v = *(const u32x4 *)(vb + (uint32_t)min(32 * X + (lane >> 1), n - 1) * (uint32_t)a.H_v * D);
                     s.g = a.wsGam[tv * 128 + 64 * X + lane];
+                }
+                // L2 prefetch of tile lt_ + 2 (five tiles ahead of the state
+                // waves): the workgroups that share a tile run in step, so
+                // without it all of them wait on the first one's miss to HBM.
+                // Each takes a 1 KiB piece: of the qk-head's K rows and q tile
+                // (piece mem), of its v-head's T and P fragments (piece sl) and
+                // v rows (pieces 2 sl, 2 sl + 1).  (A direct-to-LDS load would
+                // need no register, but the compiler then waits for it before
+                // every LDS access.)
+                if (X < 3) {
+                    constexpr int CHP = D / 8;  // 16-byte chunks per row
+                    const int lp = min(lt_ + 2, n_tiles - 1);
+                    const int tp0 = st + TILE * lp, np = min(TILE, en - tp0);
+                    const size_t tvp = (size_t)(tile_base + lp) * a.H_v + j;
+                    // (unconditional, with clamped pieces: a load issued on some
+                    // paths only makes the compiler wait for every load later)
+                    if (X == 0) {
+                        const int idx = 64 * (mem % CHP) + lane, r = min(idx / CHP, np - 1);
+                        s.pf[0] = l2_prefetch(a.k + ((size_t)(tp0 + r) * a.H_k + qh) * D + 8 * (idx % CHP));
+                        s.pf[1] = l2_prefetch(a.wsQ + ((size_t)(tile_base + lp) * a.H_k + qh) * 64 * D + 8 * idx);
+                    }
+                    if (X == 1) {
+                        s.pf[0] = l2_prefetch(a.wsT + tvp * TP_HALVES + 8 * (64 * min(sl, 5) + lane));
+                        s.pf[1] = l2_prefetch(a.wsP + tvp * TP_HALVES + 8 * (64 * min(sl, 5) + lane));
+                    }
+                    if (X == 2) {
+#pragma unroll
+                        for (int i = 0; i < 2; ++i) {
+                            const int idx = 64 * (2 * sl + i) + lane, r = min(idx / CHP, np - 1);
+                            s.pf[i] = l2_prefetch(a.v + ((size_t)(tp0 + r) * a.H_v + j) * D + 8 * (idx % CHP));
+                        }
+                    }
                 }
             };
             auto stage = [&](const LoadSet<D> &s, auto bufc, int g3) __attribute__((always_inline)) {
