@@ -85,6 +85,33 @@ def test_varlen_packed_ragged(ds, frame_len):
     assert np.array_equal(gpu["S"][3], S0[3])
 
 
+def test_device_lengths_below_capacity(ds):
+    """Shape sized for capacity (two streams of up to 300 tokens, frames of 64)
+    while device cu_seqlens holds shorter streams, as in graph replay: the real
+    frames carry the drift sums of the real tokens and every frame past the real
+    count reads zero, whatever the buffer held before."""
+    real = [130, 65]
+    x = synth.make_gdn_inputs(real, 2, 4, 64, 64, novelty=False, config=3)
+    cap = [300, 300]
+    T_cap = sum(cap)
+    T = int(x.cu_seqlens[-1])
+    pad = lambda a: np.concatenate([a, np.zeros((T_cap - T,) + a.shape[1:], a.dtype)])
+    q, k, v = dev_bf16(pad(x.q)), dev_bf16(pad(x.k)), dev_bf16(pad(x.v))
+    g, beta = dev_f32(pad(x.g)), dev_f32(pad(x.beta))
+    cu = torch.tensor(np.asarray(x.cu_seqlens, np.int32), device=DEV)
+    n_cap = 2 * (300 // 64 + 1)
+    dp = torch.full((n_cap, 4, 2), float("nan"), dtype=torch.float32, device=DEV)
+    r = ds.gdn_chunk_fwd(q, k, v, g, beta, cap, 64, cu_seqlens=cu, drift_partials=dp)
+    torch.cuda.synchronize()
+    ref = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, 64)
+    n_real = ref["partials"].shape[0]
+    got = dp.cpu().numpy().astype(np.float64)
+    assert np.all(got[n_real:] == 0.0)
+    assert rel_fro(got[:n_real], ref["partials"]) <= TOL_DRIFT
+    assert rel_fro(r["o"][:T].cpu().numpy(), ref["o"]) <= TOL_O
+    assert rel_fro(r["state"].cpu().numpy(), ref["S"]) <= TOL_O
+
+
 def test_state_in_place(ds):
     x = synth.make_gdn_inputs([700], 1, 2, 64, 256, novelty=False, config=3)
     S0 = (np.random.default_rng(5).standard_normal((1, 2, 64, 64)) * 0.1).astype(np.float32)
