@@ -1084,14 +1084,20 @@ __global__ __launch_bounds__(256) void gdn_write_finalize_kernel(const float *ws
         base += nf;
         return false;
     });
-    double acc = 0.0;
+    // fp32 throughout (a frame's sum of at most a few thousand norms); the
+    // slices of a token are loaded together (n_split <= 8 for d <= 128)
+    float acc = 0.f;
     const float *wj = ws + (size_t)j * n_split * st.T;
     for (int t = tb + tid; t < te; t += 256) {
+        float v[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] = q < n_split ? wj[(size_t)q * st.T + t] : 0.f;
         float s = 0.f;
-        for (int q = 0; q < n_split; ++q) s += wj[(size_t)q * st.T + t];
-        acc += sqrt((double)s);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) s += v[q];
+        acc += __builtin_sqrtf(s);
     }
-    __shared__ double red[256];
+    __shared__ float red[256];
     red[tid] = acc;
     __syncthreads();
     for (int off = 128; off > 0; off >>= 1) {
@@ -1099,7 +1105,7 @@ __global__ __launch_bounds__(256) void gdn_write_finalize_kernel(const float *ws
         __syncthreads();
     }
     if (tid == 0) {
-        out[((size_t)f * H_v + j) * 2] = (float)red[0];
+        out[((size_t)f * H_v + j) * 2] = red[0];
         out[((size_t)f * H_v + j) * 2 + 1] = (float)(te - tb);
     }
 }
