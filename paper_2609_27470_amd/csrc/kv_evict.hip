@@ -498,7 +498,12 @@ struct GatherArgs {
     const int32_t *keep, *inv;
     int32_t *flags, *status;
     uint32_t *ticket;
+    char *trash;  // 8 KiB that stores with nothing to write go to (the staging area, idle by then)
 };
+
+// s_waitcnt immediate that waits until at most n vector memory operations of
+// this wave are in flight (lgkm and exp counters not waited for)
+constexpr int vmcnt_imm(int n) { return 0x0F70 | (n & 15) | ((n >> 4) << 14); }
 
 // Moving destinations [first, M) are handed out in ticket order, ROWS
 // consecutive slots per ticket; for each slot and each group of planes the
@@ -511,6 +516,8 @@ template <int KPR>
 __global__ __launch_bounds__(256) void kv_gather_kernel(GatherArgs a) {
     constexpr int PPG = GATHER_U / KPR;
     __shared__ int s_t;
+    __shared__ int s_src[GATHER_ROWS], s_dep[GATHER_ROWS];
+    __shared__ char *s_pt[KV_MAX_PLANES];
     if (a.status[1]) return;
     const int first = a.status[4];
     const int n_work = (a.M - first + GATHER_ROWS - 1) / GATHER_ROWS;
@@ -520,67 +527,98 @@ __global__ __launch_bounds__(256) void kv_gather_kernel(GatherArgs a) {
     __syncthreads();
     const int d_lo = first + s_t * GATHER_ROWS;
     const int d_hi = min(d_lo + GATHER_ROWS, a.M);
+    // sources and readers of the ticket's slots, in LDS: a global load inside
+    // the pipeline below would make the compiler wait for every load in flight
+    if (tid < d_hi - d_lo) {
+        s_src[tid] = a.keep[d_lo + tid];
+        s_dep[tid] = a.inv[d_lo + tid];  // destination whose source is row d (-1 if row d is evicted)
+    }
+    if (tid < a.n_planes) s_pt[tid] = a.plane_tab[tid];
+    __syncthreads();
 
-    for (int d = d_lo; d < d_hi; ++d) {
-        const int src = a.keep[d];
-        const int dep = a.inv[d];  // destination whose source is row d (-1 if row d is evicted)
-        for (int c = 0; c < a.n_chunks; ++c) {
-            // ---- read the source rows of this plane group.  Every load is
-            // issued (units past the row or planes past the group re-read a
-            // valid address and are never stored) so the buffer stays in registers.
-            u32x4 buf[GATHER_U];
-            const int p0 = c * a.planes_per_group;
+    // Units u = (slot d_lo + u / n_chunks, plane group u % n_chunks) in two
+    // register buffers.  Per unit: wait for its loads, signal that its source
+    // rows are held, wait for the reader of its slot, issue the next unit's
+    // loads, write the slot -- so a workgroup's writes overlap its next reads.
+    // Each unit issues exactly LPU loads and LPU stores per lane (lanes with
+    // nothing to store write to the trash area) so that the wait can count them
+    // (vmcnt counts loads and stores together, in issue order); plane pointers
+    // and slot metadata come from LDS, since a global load whose value is used
+    // at once would make the compiler wait for every load in flight.
+    constexpr int LPU = GATHER_U + 2;
+    const int n_units = (d_hi - d_lo) * a.n_chunks;
+    u32x4 bufA[GATHER_U], bufB[GATHER_U];
+    int pvA = 0, cvA = 0, pvB = 0, cvB = 0;
+    auto load = [&](int u, u32x4 (&buf)[GATHER_U], int &pv, int &cv) __attribute__((always_inline)) {
+        const int c = u % a.n_chunks;
+        const int src = s_src[u / a.n_chunks];
+        const int p0 = c * a.planes_per_group;
+        // (units past the row or planes past the group re-read a valid address)
 #pragma clang loop unroll(full)
-            for (int pi = 0; pi < PPG; ++pi) {
-                const int p = min(p0 + pi, a.n_planes - 1);
-                GPTR(const char) row = (GPTR(const char))a.plane_tab[p] + (size_t)src * a.row_bytes;
+        for (int pi = 0; pi < PPG; ++pi) {
+            const int p = min(p0 + pi, a.n_planes - 1);
+            GPTR(const char) row = (GPTR(const char))s_pt[p] + (size_t)src * a.row_bytes;
 #pragma clang loop unroll(full)
-                for (int k = 0; k < KPR; ++k) {
-                    const uint32_t unit = min((uint32_t)(tid + 256 * k), a.row_units - 1);
-                    buf[pi * KPR + k] = *(GPTR(const u32x4))(row + 16u * unit);
-                }
-            }
-            int pv = 0, cv = 0;
-            if (c == 0 && tid == 0) {
-                pv = a.pos[src];
-                cv = a.chunk[src];
-            }
-            __builtin_amdgcn_s_waitcnt(0);  // every load of this thread has returned
-            __syncthreads();
-            if (tid == 0) {
-                __hip_atomic_store(&a.flags[d * a.n_chunks + c], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                // ---- wait until the reader of row d (a lower slot, hence an
-                // earlier ticket or an earlier iteration here) holds its data
-                if (dep >= first && dep != d) {  // readers below `first` were staged earlier
-                    int it = 0;
-                    const int ft = dep * a.n_chunks + c;
-                    while (__hip_atomic_load(&a.flags[ft], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
-                        if (++it >= SPIN_LIMIT) {
-                            __hip_atomic_store(&a.status[2], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                            break;
-                        }
-                        __builtin_amdgcn_s_sleep(2);
-                    }
-                }
-            }
-            __syncthreads();
-            // ---- write slot d
-#pragma clang loop unroll(full)
-            for (int pi = 0; pi < PPG; ++pi) {
-                const int p = p0 + pi;
-                const bool plane_ok = pi < a.planes_per_group && p < a.n_planes;
-                GPTR(char) row = (GPTR(char))a.plane_tab[min(p, a.n_planes - 1)] + (size_t)d * a.row_bytes;
-#pragma clang loop unroll(full)
-                for (int k = 0; k < KPR; ++k) {
-                    const uint32_t unit = (uint32_t)(tid + 256 * k);
-                    if (plane_ok && unit < a.row_units) *(GPTR(u32x4))(row + 16u * unit) = buf[pi * KPR + k];
-                }
-            }
-            if (c == 0 && tid == 0) {
-                a.pos[d] = pv;
-                a.chunk[d] = cv;
+            for (int k = 0; k < KPR; ++k) {
+                const uint32_t unit = min((uint32_t)(tid + 256 * k), a.row_units - 1);
+                buf[pi * KPR + k] = *(GPTR(const u32x4))(row + 16u * unit);
             }
         }
+        pv = a.pos[src];  // position and chunk id of the source row (lane 0 of group 0 stores them)
+        cv = a.chunk[src];
+    };
+    auto step = [&](int u, const u32x4 (&buf)[GATHER_U], int pv, int cv, u32x4 (&nbuf)[GATHER_U], int &npv, int &ncv)
+        __attribute__((always_inline)) {
+        const int d = d_lo + u / a.n_chunks, c = u % a.n_chunks;
+        const int dep = s_dep[u / a.n_chunks];
+        // this unit's loads: after them only the previous unit's stores were issued
+        if (u == 0)
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+        else
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(LPU));
+        lds_sync();  // every lane holds this unit's source rows
+        if (tid == 0) {
+            __hip_atomic_store(&a.flags[d * a.n_chunks + c], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            // ---- wait until the reader of row d (a lower slot, hence an
+            // earlier ticket or an earlier unit here) holds its data
+            if (dep >= first && dep != d) {  // readers below `first` were staged earlier
+                int it = 0;
+                const int ft = dep * a.n_chunks + c;
+                while (__hip_atomic_load(&a.flags[ft], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
+                    if (++it >= SPIN_LIMIT) {
+                        __hip_atomic_store(&a.status[2], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(2);
+                }
+            }
+        }
+        lds_sync();
+        load(min(u + 1, n_units - 1), nbuf, npv, ncv);  // unconditional (a repeat past the end is never written)
+        // ---- write slot d
+        const int p0 = c * a.planes_per_group;
+        GPTR(u32x4) trash = (GPTR(u32x4))a.trash + tid;
+#pragma clang loop unroll(full)
+        for (int pi = 0; pi < PPG; ++pi) {
+            const int p = p0 + pi;
+            const bool plane_ok = pi < a.planes_per_group && p < a.n_planes;
+            GPTR(char) row = (GPTR(char))s_pt[min(p, a.n_planes - 1)] + (size_t)d * a.row_bytes;
+#pragma clang loop unroll(full)
+            for (int k = 0; k < KPR; ++k) {
+                const uint32_t unit = (uint32_t)(tid + 256 * k);
+                GPTR(u32x4) dst = (plane_ok && unit < a.row_units) ? (GPTR(u32x4))(row + 16u * unit) : trash;
+                *dst = buf[pi * KPR + k];
+            }
+        }
+        const bool meta = c == 0 && tid == 0;
+        int32_t *tr = (int32_t *)(a.trash + 4096) + 2 * tid;
+        *(meta ? a.pos + d : tr) = pv;
+        *(meta ? a.chunk + d : tr + 1) = cv;
+    };
+    load(0, bufA, pvA, cvA);
+    for (int u = 0; u < n_units; u += 2) {
+        step(u, bufA, pvA, cvA, bufB, pvB, cvB);
+        if (u + 1 < n_units) step(u + 1, bufB, pvB, cvB, bufA, pvA, cvA);
     }
 }
 
@@ -745,6 +783,7 @@ hipError_t launch_kv_evict(const KvLaunch &p, hipStream_t stream) {
     g.row_units = (uint32_t)(p.row_bytes / 16);
     g.n_planes = p.n_planes;
     g.planes_per_group = GATHER_U / kpr;
+    g.trash = ws + p.lay.offStage;
     g.M = p.M;
     g.n_chunks = p.lay.n_chunks;
     g.pos = p.pos;
