@@ -459,7 +459,7 @@ def main():
         "roofline": {
             "bound": "hbm", "achieved": achieved_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": achieved_gbs / HBM_PEAK_GBS, "traffic": traffic,
-            "kernel": "gdn_chunk_fwd (gdn_prep + gdn_seq)",
+            "kernel": "gdn_chunk_fwd (gdn_prep + gdn_seq + drift finalize)",
             "algorithmic_bytes_per_launch": bytes_, "launch_ms": gdn_ms,
         },
         "gdn_drift_tokens_per_s": T / ((gdn_ms + drift_ms) * 1e-3),
