@@ -450,11 +450,13 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
 // of S):
 //   waves 0 and 1, state:  carry the recurrence for the 16 rows of S in fp32
 //                    registers, wave h owning the state columns (dims of k)
-//                    of its half.  Per tile: each computes its half of
-//                    K S0^T, the two halves are exchanged through LDS (a flag
-//                    handshake between the two waves), both form
+//                    of its half.  Per tile: both compute all of K S0^T from
+//                    the fp16 copy of S0 that the two waves left in LDS at the
+//                    end of the previous tile (identical sums in both, no
+//                    handshake inside the tile), both form
 //                    R = V - diag(Gamma) K S0^T and E = T diag(beta) R, and each
-//                    updates its half, S = Gamma_last S0 + (D_last E)^T K.
+//                    updates its half, S = Gamma_last S0 + (D_last E)^T K, and
+//                    writes the half's fp16 copy for the next tile.
 //                    Every product's result becomes the next product's B
 //                    operand inside the registers.  S0 and E are published in
 //                    LDS for the output waves; at a frame end each lane
@@ -503,11 +505,11 @@ struct SeqShared {
     u32x4 T[2][6][64];         // T diag(beta) A-fragments
     uint16_t V[2][64 * 16];    // v[token][v0 .. v0 + 15] (bf16, read transposed)
     float G[3][2][64];         // Gamma_r and D_last,r of tile t in G[t % 3] (the output waves read it a tile later)
-    f32x4 X[2][2][4][64];      // exchanged halves of K S0^T: [tile % 2][state wave][rb][lane]
-    u32x4 S16[2][KS][64];      // S0 as fp16 B operand (for the output waves)
+    u32x4 S16[3][KS][64];      // S0 of tile t as fp16 B operand in S16[t % 3]: each state wave
+                               // writes its half at the end of tile t - 1, both state waves
+                               // read all of it in tile t, the output waves a tile later
     u32x4 E[2][2][64];         // E as B operand (fp16)
     float2 DR[2][2][64];       // per-lane drift sums of a frame end: [frame % 2][state wave][lane]
-    int xflag[2];              // tiles whose half of K S0^T each state wave has published
 };
 
 // One loader's share of a tile: K rows 16 x .. 16 x + 15 (whole 16-byte
@@ -530,8 +532,6 @@ struct OutSet {
     u32x4 q[2][D / 32];  // q rows 16 rb + ln (fp16), dims 32 ks + 8 lg .. + 7
     u32x4 p[4];          // P fragments of the two row blocks (2 or 4 used)
 };
-
-constexpr int SEQ_SPIN_LIMIT = 1 << 22;
 
 template <int D, bool OUT_BF16, bool DRIFT>
 __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
@@ -578,7 +578,6 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
     });
     const int len = en - st;
     const int n_tiles = (len + TILE - 1) / TILE;
-    if (tid < 2) sh.xflag[tid] = 0;
 
     if (w < 2) {
         // ================================================================ state
@@ -594,6 +593,13 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             for (int e = 0; e < 4; ++e) S[c][e] = a.state_in ? a.state_in[sbase + scol(kb, e)] : 0.f;
             S0f[c] = S[c];
         }
+        // own half of S0 as fp16 B operand for the first tile
+        auto publish = [&](int s3) __attribute__((always_inline)) {
+#pragma unroll
+            for (int c = 0; c < HKS; ++c)
+                sh.S16[s3][hh * HKS + c][lane] = __builtin_bit_cast(u32x4, to_half8(S[2 * c], S[2 * c + 1]));
+        };
+        publish(0);
         int frame = frame_base;
         int frame_end = a.frame_len > 0 ? min(a.frame_len, len) : len;  // tokens done at the next frame end
 
@@ -611,13 +617,10 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) Sn[c][e] = gl * S[c][e];
 
-            // own half of S0 as fp16 B operand, also published
-            half8 s16[HKS];
+            // S0 as fp16 B operand, both halves (written before the barrier)
+            half8 s16[KS];
 #pragma unroll
-            for (int c = 0; c < HKS; ++c) {
-                s16[c] = to_half8(S[2 * c], S[2 * c + 1]);
-                sh.S16[buf][hh * HKS + c][lane] = __builtin_bit_cast(u32x4, s16[c]);
-            }
+            for (int c = 0; c < KS; ++c) s16[c] = as_half8(sh.S16[g3][c][lane]);
 
             // every operand of the tile read now, so that the reads overlap the work below
             half8 ktf[2][HKB];
@@ -646,34 +649,22 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                 vv4[rb] = ds_read_tr16(&sh.V[buf][(16 * rb + 4 * lg + (ln >> 2)) * 16 + 4 * (ln & 3)]);
             }
 
-            // own half of K S0^T  (token rows 16 rb + 4 lg + e, column v0 + ln)
-            f32x4 acc[4];
+            // K S0^T over all of d_k in both state waves (token rows 16 rb + 4 lg + e,
+            // column v0 + ln): the same sums in the same order, so both waves hold the
+            // same E, and no exchange between them inside the tile
+            f32x4 ks0[4];
 #pragma unroll
-            for (int rb = 0; rb < 4; ++rb) acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int rb = 0; rb < 4; ++rb) ks0[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int c = 0; c < HKS; ++c) {
+            for (int c = 0; c < KS; ++c) {
                 half8 ka[4];
 #pragma unroll
                 for (int rb = 0; rb < 4; ++rb) {
                     const int row = 16 * rb + ln;
-                    ka[rb] = as_half8(*(const u32x4 *)(&sh.K[buf][row * D + 8 * ((4 * (hh * HKS + c) + lg) ^ swz<D>(row))]));
+                    ka[rb] = as_half8(*(const u32x4 *)(&sh.K[buf][row * D + 8 * ((4 * c + lg) ^ swz<D>(row))]));
                 }
 #pragma unroll
-                for (int rb = 0; rb < 4; ++rb) acc[rb] = mfma_f16(ka[rb], s16[c], acc[rb]);
-            }
-            // exchange with the other state wave
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb) sh.X[buf][hh][rb][lane] = acc[rb];
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-            __hip_atomic_store(&sh.xflag[hh], lt + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-            for (int spin = 0; spin < SEQ_SPIN_LIMIT; ++spin)
-                if (__hip_atomic_load(&sh.xflag[hh ^ 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) > lt) break;
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-            f32x4 ks0[4];
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb) {
-                const f32x4 o = sh.X[buf][hh ^ 1][rb][lane];
-                ks0[rb] = hh == 0 ? acc[rb] + o : o + acc[rb];  // same value in both waves
+                for (int rb = 0; rb < 4; ++rb) ks0[rb] = mfma_f16(ka[rb], s16[c], ks0[rb]);
             }
 
             // R = V - diag(Gamma) K S0^T
@@ -718,6 +709,7 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                 for (int c = 0; c < HKB; ++c) Sn[c] = mfma_f16(ktf[ks][c], d16[ks], Sn[c]);
 #pragma unroll
             for (int c = 0; c < HKB; ++c) S[c] = Sn[c];
+            publish((lt + 1) % 3);  // S0 of the next tile
 
             // frame end: per-lane drift sums of this half of the slice (a
             // loader wave reduces them over the lanes), optional snapshot
@@ -783,7 +775,7 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                 f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) {
-                    const half8 bs = as_half8(sh.S16[buf][ks][lane]);
+                    const half8 bs = as_half8(sh.S16[lt % 3][ks][lane]);
 #pragma unroll
                     for (int r = 0; r < 2; ++r) acc[r] = mfma_f16(as_half8(s.q[r][ks]), bs, acc[r]);
                 }
