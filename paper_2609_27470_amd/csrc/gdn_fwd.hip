@@ -886,6 +886,10 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             constexpr int NK = LoadSet<D>::NK;
             constexpr int NT = X < 2 ? 2 : 1;                    // T diag(beta) fragments
             constexpr int T_FIRST = X < 2 ? 2 * X : 4 + (X - 2);
+            // the workgroups that share a tile run in step: each starts its K rows
+            // and T fragments at a different piece, so that at any moment they ask
+            // L2 for different lines
+            const int krot = mem % NK, trot = sl % NT;
             auto load = [&](LoadSet<D> &s, int lt_) __attribute__((always_inline)) {
                 if (X < 3 && lt_ >= 2) {  // the prefetches issued with this set two tiles ago
                     l2_retire(s.pf[0]);
@@ -898,12 +902,12 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                 const uint16_t *kb = a.k + (size_t)t0 * a.H_k * D + (size_t)qh * D + 8 * (lane % CH);
 #pragma unroll
                 for (int c = 0; c < NK; ++c) {
-                    const uint32_t r = (uint32_t)min(16 * X + RPI * c + lane / CH, n - 1);
+                    const uint32_t r = (uint32_t)min(16 * X + RPI * ((c + krot) % NK) + lane / CH, n - 1);
                     s.k[c] = *(const u32x4 *)(kb + r * (uint32_t)a.H_k * D);
                 }
                 const u32x4 *tb = (const u32x4 *)(a.wsT + tv * TP_HALVES);
 #pragma unroll
-                for (int c = 0; c < NT; ++c) s.t[c] = tb[(T_FIRST + c) * 64 + lane];
+                for (int c = 0; c < NT; ++c) s.t[c] = tb[(T_FIRST + (c + trot) % NT) * 64 + lane];
                 if (X < 2) {
                     // v rows 32 X + lane / 2, columns v0 + 8 (lane % 2) .. + 7
                     const uint16_t *vb = a.v + ((size_t)t0 * a.H_v + j) * D + v0 + 8 * (lane & 1);
@@ -948,11 +952,11 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                 constexpr int CH = D / 8, RPI = 64 / CH;
 #pragma unroll
                 for (int c = 0; c < NK; ++c) {
-                    const int row = 16 * X + RPI * c + lane / CH, ch = lane % CH;
+                    const int row = 16 * X + RPI * ((c + krot) % NK) + lane / CH, ch = lane % CH;
                     *(u32x4 *)(&sh.K[buf][row * D + 8 * (ch ^ swz<D>(row))]) = __builtin_bit_cast(u32x4, bf16x8_to_f16(s.k[c]));
                 }
 #pragma unroll
-                for (int c = 0; c < NT; ++c) sh.T[buf][T_FIRST + c][lane] = s.t[c];
+                for (int c = 0; c < NT; ++c) sh.T[buf][T_FIRST + (c + trot) % NT][lane] = s.t[c];
                 if (X < 2) {
                     *(u32x4 *)(&sh.V[buf][(32 * X + (lane >> 1)) * 16 + 8 * (lane & 1)]) = s.v;
                     sh.G[g3][X][lane] = s.g;
