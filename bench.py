@@ -246,7 +246,7 @@ def main():
         # append the newest chunk (1024 tokens): rows, positions, chunk id
         n = state_ref["len"]
         cache[:, n:n + 1024].copy_(new_rows)
-        kv_pos[n:n + 1024] = append_pos + state_ref["next_pos"]
+        torch.add(append_pos, state_ref["next_pos"], out=kv_pos[n:n + 1024])
         kv_chunk[n:n + 1024] = base + n_frames - 1
         state_ref["next_pos"] += 1024
         if evs is not None:
@@ -302,7 +302,7 @@ def main():
             ev[0].record(stream)
         dst = idx_free.to(torch.int64)
         cache.index_copy_(1, dst, new_rows)
-        idx_pos[BUDGET:] = append_pos + BUDGET + 1024 * i
+        torch.add(append_pos, BUDGET + 1024 * i, out=idx_pos[BUDGET:])
         idx_chunk[BUDGET:] = n_init_chunks + i
         idx_slot[BUDGET:] = idx_free
         if ev:

@@ -511,6 +511,10 @@ constexpr int vmcnt_imm(int n) { return 0x0F70 | (n & 15) | ((n >> 4) << 14); }
 // and writes.  KPR = 16-byte units per thread per plane row
 // (row_bytes <= 4096 KPR); a plane group holds 16 / KPR plane rows.
 constexpr int GATHER_ROWS = 8;
+// workgroups of the gather, each taking tickets until none is left: three for
+// every four CUs of MI355X moved a 1 GiB eviction fastest (fewer streams of
+// copies in flight than one per CU, which also beat one per ticket)
+constexpr int GATHER_WG = 192;
 
 template <int KPR>
 __global__ __launch_bounds__(256) void kv_gather_kernel(GatherArgs a) {
@@ -523,102 +527,109 @@ __global__ __launch_bounds__(256) void kv_gather_kernel(GatherArgs a) {
     const int n_work = (a.M - first + GATHER_ROWS - 1) / GATHER_ROWS;
     if ((int)blockIdx.x >= n_work) return;  // more workgroups than moving rows: take no ticket
     const int tid = threadIdx.x;
-    if (tid == 0) s_t = (int)atomicAdd(a.ticket, 1u);
-    __syncthreads();
-    const int d_lo = first + s_t * GATHER_ROWS;
-    const int d_hi = min(d_lo + GATHER_ROWS, a.M);
-    // sources and readers of the ticket's slots, in LDS: a global load inside
-    // the pipeline below would make the compiler wait for every load in flight
-    if (tid < d_hi - d_lo) {
-        s_src[tid] = a.keep[d_lo + tid];
-        s_dep[tid] = a.inv[d_lo + tid];  // destination whose source is row d (-1 if row d is evicted)
-    }
     if (tid < a.n_planes) s_pt[tid] = a.plane_tab[tid];
-    __syncthreads();
-
-    // Units u = (slot d_lo + u / n_chunks, plane group u % n_chunks) in two
-    // register buffers.  Per unit: wait for its loads, signal that its source
-    // rows are held, wait for the reader of its slot, issue the next unit's
-    // loads, write the slot -- so a workgroup's writes overlap its next reads.
-    // Each unit issues exactly LPU loads and LPU stores per lane (lanes with
-    // nothing to store write to the trash area) so that the wait can count them
-    // (vmcnt counts loads and stores together, in issue order); plane pointers
-    // and slot metadata come from LDS, since a global load whose value is used
-    // at once would make the compiler wait for every load in flight.
-    constexpr int LPU = GATHER_U + 2;
-    const int n_units = (d_hi - d_lo) * a.n_chunks;
-    u32x4 bufA[GATHER_U], bufB[GATHER_U];
-    int pvA = 0, cvA = 0, pvB = 0, cvB = 0;
-    auto load = [&](int u, u32x4 (&buf)[GATHER_U], int &pv, int &cv) __attribute__((always_inline)) {
-        const int c = u % a.n_chunks;
-        const int src = s_src[u / a.n_chunks];
-        const int p0 = c * a.planes_per_group;
-        // (units past the row or planes past the group re-read a valid address)
-#pragma clang loop unroll(full)
-        for (int pi = 0; pi < PPG; ++pi) {
-            const int p = min(p0 + pi, a.n_planes - 1);
-            GPTR(const char) row = (GPTR(const char))s_pt[p] + (size_t)src * a.row_bytes;
-#pragma clang loop unroll(full)
-            for (int k = 0; k < KPR; ++k) {
-                const uint32_t unit = min((uint32_t)(tid + 256 * k), a.row_units - 1);
-                buf[pi * KPR + k] = *(GPTR(const u32x4))(row + 16u * unit);
-            }
+    // tickets are taken until none is left, so the grid drains evenly; a
+    // workgroup only waits for slots of lower tickets, which running
+    // workgroups hold
+    for (;;) {
+        if (tid == 0) s_t = (int)atomicAdd(a.ticket, 1u);
+        __syncthreads();
+        if (s_t >= n_work) break;
+        const int d_lo = first + s_t * GATHER_ROWS;
+        const int d_hi = min(d_lo + GATHER_ROWS, a.M);
+        // sources and readers of the ticket's slots, in LDS: a global load inside
+        // the pipeline below would make the compiler wait for every load in flight
+        if (tid < d_hi - d_lo) {
+            s_src[tid] = a.keep[d_lo + tid];
+            s_dep[tid] = a.inv[d_lo + tid];  // destination whose source is row d (-1 if row d is evicted)
         }
-        pv = a.pos[src];  // position and chunk id of the source row (lane 0 of group 0 stores them)
-        cv = a.chunk[src];
-    };
-    auto step = [&](int u, const u32x4 (&buf)[GATHER_U], int pv, int cv, u32x4 (&nbuf)[GATHER_U], int &npv, int &ncv)
-        __attribute__((always_inline)) {
-        const int d = d_lo + u / a.n_chunks, c = u % a.n_chunks;
-        const int dep = s_dep[u / a.n_chunks];
-        // this unit's loads: after them only the previous unit's stores were issued
-        if (u == 0)
-            __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-        else
-            __builtin_amdgcn_s_waitcnt(vmcnt_imm(LPU));
-        lds_sync();  // every lane holds this unit's source rows
-        if (tid == 0) {
-            __hip_atomic_store(&a.flags[d * a.n_chunks + c], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            // ---- wait until the reader of row d (a lower slot, hence an
-            // earlier ticket or an earlier unit here) holds its data
-            if (dep >= first && dep != d) {  // readers below `first` were staged earlier
-                int it = 0;
-                const int ft = dep * a.n_chunks + c;
-                while (__hip_atomic_load(&a.flags[ft], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
-                    if (++it >= SPIN_LIMIT) {
-                        __hip_atomic_store(&a.status[2], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        break;
-                    }
-                    __builtin_amdgcn_s_sleep(2);
+        __syncthreads();
+
+        // Units u = (slot d_lo + u / n_chunks, plane group u % n_chunks) in two
+        // register buffers.  Per unit: wait for its loads, signal that its source
+        // rows are held, wait for the reader of its slot, issue the next unit's
+        // loads, write the slot -- so a workgroup's writes overlap its next reads.
+        // Each unit issues exactly LPU loads and LPU stores per lane (lanes with
+        // nothing to store write to the trash area) so that the wait can count them
+        // (vmcnt counts loads and stores together, in issue order); plane pointers
+        // and slot metadata come from LDS, since a global load whose value is used
+        // at once would make the compiler wait for every load in flight.
+        constexpr int LPU = GATHER_U + 2;
+        const int n_units = (d_hi - d_lo) * a.n_chunks;
+        u32x4 bufA[GATHER_U], bufB[GATHER_U];
+        int pvA = 0, cvA = 0, pvB = 0, cvB = 0;
+        auto load = [&](int u, u32x4 (&buf)[GATHER_U], int &pv, int &cv) __attribute__((always_inline)) {
+            const int c = u % a.n_chunks;
+            const int src = s_src[u / a.n_chunks];
+            const int p0 = c * a.planes_per_group;
+            // (units past the row or planes past the group re-read a valid address)
+    #pragma clang loop unroll(full)
+            for (int pi = 0; pi < PPG; ++pi) {
+                const int p = min(p0 + pi, a.n_planes - 1);
+                GPTR(const char) row = (GPTR(const char))s_pt[p] + (size_t)src * a.row_bytes;
+    #pragma clang loop unroll(full)
+                for (int k = 0; k < KPR; ++k) {
+                    const uint32_t unit = min((uint32_t)(tid + 256 * k), a.row_units - 1);
+                    buf[pi * KPR + k] = *(GPTR(const u32x4))(row + 16u * unit);
                 }
             }
-        }
-        lds_sync();
-        load(min(u + 1, n_units - 1), nbuf, npv, ncv);  // unconditional (a repeat past the end is never written)
-        // ---- write slot d
-        const int p0 = c * a.planes_per_group;
-        GPTR(u32x4) trash = (GPTR(u32x4))a.trash + tid;
-#pragma clang loop unroll(full)
-        for (int pi = 0; pi < PPG; ++pi) {
-            const int p = p0 + pi;
-            const bool plane_ok = pi < a.planes_per_group && p < a.n_planes;
-            GPTR(char) row = (GPTR(char))s_pt[min(p, a.n_planes - 1)] + (size_t)d * a.row_bytes;
-#pragma clang loop unroll(full)
-            for (int k = 0; k < KPR; ++k) {
-                const uint32_t unit = (uint32_t)(tid + 256 * k);
-                GPTR(u32x4) dst = (plane_ok && unit < a.row_units) ? (GPTR(u32x4))(row + 16u * unit) : trash;
-                *dst = buf[pi * KPR + k];
+            pv = a.pos[src];  // position and chunk id of the source row (lane 0 of group 0 stores them)
+            cv = a.chunk[src];
+        };
+        auto step = [&](int u, const u32x4 (&buf)[GATHER_U], int pv, int cv, u32x4 (&nbuf)[GATHER_U], int &npv, int &ncv)
+            __attribute__((always_inline)) {
+            const int d = d_lo + u / a.n_chunks, c = u % a.n_chunks;
+            const int dep = s_dep[u / a.n_chunks];
+            // this unit's loads: after them only the previous unit's stores were issued
+            if (u == 0)
+                __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+            else
+                __builtin_amdgcn_s_waitcnt(vmcnt_imm(LPU));
+            lds_sync();  // every lane holds this unit's source rows
+            if (tid == 0) {
+                __hip_atomic_store(&a.flags[d * a.n_chunks + c], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                // ---- wait until the reader of row d (a lower slot, hence an
+                // earlier ticket or an earlier unit here) holds its data
+                if (dep >= first && dep != d) {  // readers below `first` were staged earlier
+                    int it = 0;
+                    const int ft = dep * a.n_chunks + c;
+                    while (__hip_atomic_load(&a.flags[ft], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
+                        if (++it >= SPIN_LIMIT) {
+                            __hip_atomic_store(&a.status[2], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            break;
+                        }
+                        __builtin_amdgcn_s_sleep(2);
+                    }
+                }
             }
+            lds_sync();
+            load(min(u + 1, n_units - 1), nbuf, npv, ncv);  // unconditional (a repeat past the end is never written)
+            // ---- write slot d
+            const int p0 = c * a.planes_per_group;
+            GPTR(u32x4) trash = (GPTR(u32x4))a.trash + tid;
+    #pragma clang loop unroll(full)
+            for (int pi = 0; pi < PPG; ++pi) {
+                const int p = p0 + pi;
+                const bool plane_ok = pi < a.planes_per_group && p < a.n_planes;
+                GPTR(char) row = (GPTR(char))s_pt[min(p, a.n_planes - 1)] + (size_t)d * a.row_bytes;
+    #pragma clang loop unroll(full)
+                for (int k = 0; k < KPR; ++k) {
+                    const uint32_t unit = (uint32_t)(tid + 256 * k);
+                    GPTR(u32x4) dst = (plane_ok && unit < a.row_units) ? (GPTR(u32x4))(row + 16u * unit) : trash;
+                    *dst = buf[pi * KPR + k];
+                }
+            }
+            const bool meta = c == 0 && tid == 0;
+            int32_t *tr = (int32_t *)(a.trash + 4096) + 2 * tid;
+            *(meta ? a.pos + d : tr) = pv;
+            *(meta ? a.chunk + d : tr + 1) = cv;
+        };
+        load(0, bufA, pvA, cvA);
+        for (int u = 0; u < n_units; u += 2) {
+            step(u, bufA, pvA, cvA, bufB, pvB, cvB);
+            if (u + 1 < n_units) step(u + 1, bufB, pvB, cvB, bufA, pvA, cvA);
         }
-        const bool meta = c == 0 && tid == 0;
-        int32_t *tr = (int32_t *)(a.trash + 4096) + 2 * tid;
-        *(meta ? a.pos + d : tr) = pv;
-        *(meta ? a.chunk + d : tr + 1) = cv;
-    };
-    load(0, bufA, pvA, cvA);
-    for (int u = 0; u < n_units; u += 2) {
-        step(u, bufA, pvA, cvA, bufB, pvB, cvB);
-        if (u + 1 < n_units) step(u + 1, bufB, pvB, cvB, bufA, pvA, cvA);
+        __syncthreads();  // every lane is done with this ticket's LDS entries
     }
 }
 
@@ -836,7 +847,7 @@ hipError_t launch_kv_evict(const KvLaunch &p, hipStream_t stream) {
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    const dim3 grid((unsigned)((p.M + GATHER_ROWS - 1) / GATHER_ROWS));
+    const dim3 grid((unsigned)std::min((p.M + GATHER_ROWS - 1) / GATHER_ROWS, GATHER_WG));
     switch (kpr) {
     case 1: hipLaunchKernelGGL(kv_gather_kernel<1>, grid, blk, 0, stream, g); break;
     case 2: hipLaunchKernelGGL(kv_gather_kernel<2>, grid, blk, 0, stream, g); break;
