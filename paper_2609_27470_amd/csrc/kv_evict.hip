@@ -123,6 +123,36 @@ __device__ int block_excl_scan(int x, int *s_tmp, int &total) {
     return res;
 }
 
+// Same DPP pattern with max; lanes without a source contribute -1 (x >= -1).
+__device__ __forceinline__ int wave_incl_max(int v) {
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, 0x111, 0xf, 0xf, false));
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, 0x112, 0xf, 0xf, false));
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, 0x114, 0xf, 0xf, false));
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, 0x118, 0xf, 0xf, false));
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, 0x142, 0xa, 0xf, false));
+    v = max(v, __builtin_amdgcn_update_dpp(-1, v, 0x143, 0xc, 0xf, false));
+    return v;
+}
+
+// Maximum of x over the lower threads of the block (-1 for thread 0); x >= -1.
+__device__ int block_excl_max(int x, int *s_tmp) {
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int incl = wave_incl_max(x);
+    const int excl = __shfl(incl, max(lane - 1, 0), 64);
+    if (lane == 63) s_tmp[wid] = incl;
+    lds_sync();
+    if (wid == 0) {
+        const int t = lane < SEL_THREADS / 64 ? s_tmp[lane] : -1;
+        const int it = wave_incl_max(t);
+        const int et = __shfl(it, max(lane - 1, 0), 64);
+        if (lane < SEL_THREADS / 64) s_tmp[lane] = lane > 0 ? et : -1;
+    }
+    lds_sync();
+    const int res = max(s_tmp[wid], lane > 0 ? excl : -1);
+    lds_sync();
+    return res;
+}
+
 __device__ long long block_sum_ll(long long x, long long *s_tmp) {
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
 #pragma unroll
@@ -163,10 +193,11 @@ struct RunRec {
     int bkt;                 // span of the run
 };
 constexpr int RUN_CAP = 2048;  // runs ranked from LDS
+constexpr int SORT_MIN = 512;  // more runs than this (up to RUN_CAP) are ranked by sorting
 
 __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     __shared__ RunRec s_run[RUN_CAP];
-    __shared__ int s_take[RUN_CAP], s_from[RUN_CAP];
+    __shared__ int s_take[RUN_CAP], s_from[RUN_CAP], s_ord[RUN_CAP];
     __shared__ int s_keep[SEL_BLOCK], s_free[SEL_BLOCK];  // one pass-2 block's keep entries and freed slots
     __shared__ int s_scan[SEL_THREADS / 64 + 1];
     __shared__ long long s_ll[SEL_THREADS / 64 + 1];
@@ -272,56 +303,161 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     }
     __syncthreads();
 
+    // ---- ranking.  Every run is compared with every other (from the LDS
+    // copy up to RUN_CAP runs, else in global memory), except from SORT_MIN to
+    // RUN_CAP runs: there the run indices are sorted in LDS (bitonic network;
+    // keys are unique, one run per chunk id) and what a run keeps follows from
+    // prefix sums over the runs ranked above it.  (Per pass on MI355X: 1024
+    // runs compared pairwise take ~230k clocks, sorted ~70k; 17 runs
+    // pairwise a few hundred.)
+    const bool by_sort = in_lds && R > SORT_MIN;
+    int Rp = 1;
+    while (Rp < R) Rp <<= 1;
+    auto sort_runs = [&](auto before) __attribute__((always_inline)) {
+        for (int i = tid; i < Rp; i += SEL_THREADS) s_ord[i] = i;
+        lds_sync();
+        for (int k = 2; k <= Rp; k <<= 1)
+            for (int j = k >> 1; j > 0; j >>= 1) {
+                for (int q = tid; q < Rp / 2; q += SEL_THREADS) {
+                    const int i = ((q & ~(j - 1)) << 1) | (q & (j - 1)), l = i + j;
+                    const int x = s_ord[i], y = s_ord[l];
+                    if ((i & k) == 0 ? before(y, x) : before(x, y)) {
+                        s_ord[i] = y;
+                        s_ord[l] = x;
+                    }
+                }
+                lds_sync();
+            }
+    };
+    // sorted positions 2 tid and 2 tid + 1 (Rp <= 2 SEL_THREADS); -1 past R
+    const int i0 = 2 * tid, i1 = i0 + 1;
+    int tot = 0;
+
     // ---- per-span quota: a run keeps what the better runs of its span left
     const long long quota = (a.M - a.n_s - a.n_w) / N;
     long long taken = 0;
-    for (int r = tid; r < R; r += SEL_THREADS) {
-        long long above = 0, ln;
-        if (in_lds) {
-            const RunRec me = s_run[r];
-            ln = me.len;
-            for (int r2 = 0; r2 < R; ++r2) {
-                const RunRec o = s_run[r2];
-                if (o.bkt == me.bkt && o.key > me.key) above += o.len;
-            }
-        } else {
-            const unsigned long long key = a.run_key[r];
-            const int bk = a.run_bkt[r];
-            ln = a.run_start[r + 1] - a.run_start[r];
-            for (int r2 = 0; r2 < R; ++r2)
-                if (a.run_bkt[r2] == bk && a.run_key[r2] > key) above += a.run_start[r2 + 1] - a.run_start[r2];
+    if (by_sort) {
+        sort_runs([&](int x, int y) {  // x ranks before y: span ascending, key descending
+            if (x >= R) return false;
+            if (y >= R) return true;
+            const RunRec rx = s_run[x], ry = s_run[y];
+            return rx.bkt < ry.bkt || (rx.bkt == ry.bkt && rx.key > ry.key);
+        });
+        const int r0 = i0 < R ? s_ord[i0] : -1, r1 = i1 < R ? s_ord[i1] : -1;
+        const int l0 = r0 >= 0 ? s_run[r0].len : 0, l1 = r1 >= 0 ? s_run[r1].len : 0;
+        const int b0 = r0 >= 0 ? s_run[r0].bkt : -1, b1 = r1 >= 0 ? s_run[r1].bkt : -1;
+        const int bp = (i0 > 0 && i0 <= R) ? s_run[s_ord[i0 - 1]].bkt : -2;
+        // slots of the runs ranked before, and where the run's span starts
+        const int e0 = block_excl_scan(l0 + l1, s_scan, tot), e1 = e0 + l0;
+        const int h0 = (r0 >= 0 && b0 != bp) ? e0 : -1, h1 = (r1 >= 0 && b1 != b0) ? e1 : -1;
+        const int hp0 = max(block_excl_max(max(h0, h1), s_scan), h0), hp1 = max(hp0, h1);
+        if (r0 >= 0) {
+            const int t = (int)min((long long)l0, max(0LL, quota - (e0 - hp0)));
+            s_take[r0] = t;
+            a.run_take[r0] = t;
+            taken += t;
         }
-        const long long t = min(ln, max(0LL, quota - above));
-        a.run_take[r] = (int)t;
-        if (in_lds) s_take[r] = (int)t;
-        taken += t;
+        if (r1 >= 0) {
+            const int t = (int)min((long long)l1, max(0LL, quota - (e1 - hp1)));
+            s_take[r1] = t;
+            a.run_take[r1] = t;
+            taken += t;
+        }
+    } else {
+        for (int r = tid; r < R; r += SEL_THREADS) {
+            long long above = 0, ln;
+            if (in_lds) {
+                const RunRec me = s_run[r];
+                ln = me.len;
+                // eight records read before they are compared: one LDS round
+                // trip per eight runs rather than per run
+                int r2 = 0;
+                for (; r2 + 8 <= R; r2 += 8) {
+                    RunRec o[8];
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) o[q] = s_run[r2 + q];
+#pragma unroll
+                    for (int q = 0; q < 8; ++q)
+                        if (o[q].bkt == me.bkt && o[q].key > me.key) above += o[q].len;
+                }
+                for (; r2 < R; ++r2) {
+                    const RunRec o = s_run[r2];
+                    if (o.bkt == me.bkt && o.key > me.key) above += o.len;
+                }
+            } else {
+                const unsigned long long key = a.run_key[r];
+                const int bk = a.run_bkt[r];
+                ln = a.run_start[r + 1] - a.run_start[r];
+                for (int r2 = 0; r2 < R; ++r2)
+                    if (a.run_bkt[r2] == bk && a.run_key[r2] > key) above += a.run_start[r2 + 1] - a.run_start[r2];
+            }
+            const long long t = min(ln, max(0LL, quota - above));
+            a.run_take[r] = (int)t;
+            if (in_lds) s_take[r] = (int)t;
+            taken += t;
+        }
     }
     taken = block_sum_ll(taken, s_ll);
     const long long fill = (long long)(a.M - a.n_s - a.n_w) - taken;
 
     // ---- fill with the best remaining tokens over all spans; a run keeps
     // its newest tokens, slots [run_from, run end)
-    for (int r = tid; r < R; r += SEL_THREADS) {
-        long long above = 0, ln, tk;
-        if (in_lds) {
-            const RunRec me = s_run[r];
-            ln = me.len;
-            tk = s_take[r];
-            for (int r2 = 0; r2 < R; ++r2) {
-                const RunRec o = s_run[r2];
-                if (o.key > me.key) above += o.len - s_take[r2];
-            }
-        } else {
-            const unsigned long long key = a.run_key[r];
-            ln = a.run_start[r + 1] - a.run_start[r];
-            tk = a.run_take[r];
-            for (int r2 = 0; r2 < R; ++r2)
-                if (a.run_key[r2] > key) above += (a.run_start[r2 + 1] - a.run_start[r2]) - a.run_take[r2];
+    if (by_sort) {
+        sort_runs([&](int x, int y) {  // key descending
+            if (x >= R) return false;
+            if (y >= R) return true;
+            return s_run[x].key > s_run[y].key;
+        });
+        const int r0 = i0 < R ? s_ord[i0] : -1, r1 = i1 < R ? s_ord[i1] : -1;
+        const int t0 = r0 >= 0 ? s_take[r0] : 0, t1 = r1 >= 0 ? s_take[r1] : 0;
+        const int m0 = r0 >= 0 ? s_run[r0].len - t0 : 0, m1 = r1 >= 0 ? s_run[r1].len - t1 : 0;
+        const int f0 = block_excl_scan(m0 + m1, s_scan, tot), f1 = f0 + m0;  // left in better runs
+        if (r0 >= 0) {
+            const int from = a.run_start[r0 + 1] - (t0 + (int)min((long long)m0, max(0LL, fill - f0)));
+            a.run_from[r0] = from;
+            s_from[r0] = from;
         }
-        const long long left = ln - tk;
-        const long long f = min(left, max(0LL, fill - above));
-        a.run_from[r] = a.run_start[r + 1] - (int)(tk + f);
-        if (in_lds) s_from[r] = a.run_start[r + 1] - (int)(tk + f);
+        if (r1 >= 0) {
+            const int from = a.run_start[r1 + 1] - (t1 + (int)min((long long)m1, max(0LL, fill - f1)));
+            a.run_from[r1] = from;
+            s_from[r1] = from;
+        }
+    } else {
+        for (int r = tid; r < R; r += SEL_THREADS) {
+            long long above = 0, ln, tk;
+            if (in_lds) {
+                const RunRec me = s_run[r];
+                ln = me.len;
+                tk = s_take[r];
+                int r2 = 0;
+                for (; r2 + 8 <= R; r2 += 8) {
+                    RunRec o[8];
+                    int tq[8];
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) {
+                        o[q] = s_run[r2 + q];
+                        tq[q] = s_take[r2 + q];
+                    }
+#pragma unroll
+                    for (int q = 0; q < 8; ++q)
+                        if (o[q].key > me.key) above += o[q].len - tq[q];
+                }
+                for (; r2 < R; ++r2) {
+                    const RunRec o = s_run[r2];
+                    if (o.key > me.key) above += o.len - s_take[r2];
+                }
+            } else {
+                const unsigned long long key = a.run_key[r];
+                ln = a.run_start[r + 1] - a.run_start[r];
+                tk = a.run_take[r];
+                for (int r2 = 0; r2 < R; ++r2)
+                    if (a.run_key[r2] > key) above += (a.run_start[r2 + 1] - a.run_start[r2]) - a.run_take[r2];
+            }
+            const long long f = min(ln - tk, max(0LL, fill - above));
+            const int from = a.run_start[r + 1] - (int)(tk + f);
+            a.run_from[r] = from;
+            if (in_lds) s_from[r] = from;
+        }
     }
     __syncthreads();
     auto run_from = [&](int r) { return in_lds ? s_from[r] : a.run_from[r]; };

@@ -92,6 +92,26 @@ def test_random_small_caches(ds, seed):
     one_event(ds, 2, 64 * (1 + seed % 3), chunk, pos, scores, M, ns, nw, nb)
 
 
+@pytest.mark.parametrize("n_chunks,lo,hi,nb,window", [(1024, 1, 20, 1, False), (1500, 1, 16, 5, True),
+                                                      (2048, 2, 6, 3, False), (3000, 1, 8, 4, True)])
+def test_many_runs(ds, n_chunks, lo, hi, nb, window):
+    """About 1000 to 3000 runs: the ranking sorts up to 2048 runs in LDS (the
+    2048-chunk case without sinks and window has exactly 2048 candidate runs)
+    and compares every pair in global memory beyond that (the 3000-chunk
+    case).  Scores from a small set, so many runs tie on the score and are
+    ordered by chunk id."""
+    rng = np.random.default_rng(n_chunks + nb)
+    chunk, pos = random_cache(rng, n_chunks, lo, hi, thin=0.9)
+    if n_chunks == 2048:  # every chunk present: exactly 2048 runs
+        chunk = np.repeat(np.arange(n_chunks), 3).astype(np.int32)
+        pos = np.arange(len(chunk), dtype=np.int32) * 2 + 1
+    n = len(chunk)
+    scores = rng.choice([0.1, 0.2, 0.3, 0.5, 1.0], size=int(chunk.max()) + 1).astype(np.float32)
+    scores[rng.integers(0, len(scores), 3)] = np.inf
+    ns, nw = (4, n // 10) if window else (0, 0)
+    one_event(ds, 1, 8, chunk, pos, scores, n * 2 // 3, ns, nw, nb)
+
+
 def test_golden_examples_on_gpu(ds):
     import json, math, os
     gd = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "select_examples.json")))
