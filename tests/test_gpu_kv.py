@@ -276,6 +276,18 @@ def test_indexed_long_cache_several_blocks(ds):
     indexed_event(ds, chunk, pos, scores, n // 2, 4, 1000, 5, seed=4)
 
 
+@pytest.mark.parametrize("n_chunks", [1500, 2600])
+def test_indexed_many_runs(ds, n_chunks):
+    """The slot-indexed eviction over caches of 1500 and 2600 short chunks:
+    its ranking takes the sorted path (up to 2048 runs) and the pairwise one
+    over the global run table (beyond)."""
+    rng = np.random.default_rng(70 + n_chunks)
+    chunk, pos = random_cache(rng, n_chunks, 1, 12, thin=0.9)
+    scores = rng.choice([0.1, 0.2, 0.5, 1.0], size=n_chunks).astype(np.float32)
+    n = len(chunk)
+    indexed_event(ds, chunk, pos, scores, n * 3 // 4, 4, 64, 3, seed=9)
+
+
 def test_indexed_matches_gather_in_a_stream(ds):
     """Appends write each new chunk's K/V rows into the rows the previous
     eviction freed (an index_copy by the caller); after every step the rows
