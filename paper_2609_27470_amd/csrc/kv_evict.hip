@@ -799,7 +799,8 @@ __device__ __forceinline__ void kv_stage_row(const StageArgs &a, int r, int c) {
             if (unit < a.row_units) {
                 GPTR(u32x4) g = (GPTR(u32x4))(base + 16u * unit);
                 GPTR(u32x4) t = slot + (pi * KPR + k) * 256 + tid;
-                if (READ) *t = *g; else *g = *t;
+                // nontemporal stores, as in the ticket gather (streamed chunks ~1 % faster)
+                if (READ) __builtin_nontemporal_store(*g, t); else __builtin_nontemporal_store(*t, g);
             }
         }
     }
