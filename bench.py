@@ -206,7 +206,7 @@ def main():
     n_frames = T // FRAME
     partials = torch.empty((n_frames, H_V, 2), dtype=torch.float32, device=dev)
     shape = ds.gdn_shape([T], H_K, H_V, D, FRAME)
-    ws = torch.empty(ds.gdn_workspace_bytes(shape), dtype=torch.uint8, device=dev)
+    ws = torch.empty(ds.gdn_workspace_bytes(shape, write_signal=True), dtype=torch.uint8, device=dev)
 
     # ---------------- KV cache: one tensor [2L][capacity][row] so a chunk append is one copy
     row_elems = KV_HEADS * KV_DIM

@@ -137,8 +137,13 @@ typedef struct {
     int32_t n_frames;  /* frames over all streams */
 } ds_gdn_shape;
 
-/* Workspace bytes gdn_chunk_fwd needs for this shape (0 on a bad shape). */
+/* Workspace bytes gdn_chunk_fwd needs for this shape when write_partials is
+ * NULL (0 on a bad shape). */
 size_t ds_gdn_workspace_bytes(const ds_gdn_shape *shape);
+/* Workspace bytes gdn_chunk_fwd needs for this shape when write_partials is
+ * given: the above plus 4 * T_total * H_v * d_v / 16 bytes of per-token norm
+ * slices (0 on a bad shape). */
+size_t ds_gdn_write_workspace_bytes(const ds_gdn_shape *shape);
 
 ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k, const void *v,
                         const float *g, const float *beta, const int32_t *cu_seqlens,
@@ -225,8 +230,8 @@ ds_status deltas_drift_states(const float *S_before, const float *S_after, int32
  * Cache invariants (as produced by appending chunks in arrival order and
  * compacting in order): chunk_id nondecreasing and pos strictly increasing
  * over [0, len), 0 <= chunk_id < num_chunks.  If the device finds them
- * broken it leaves the cache untouched and records the failure in the
- * workspace (see ds_kv_device_status).
+ * broken it leaves the cache untouched; that and any other failure on the
+ * device is recorded in the workspace's outcome word (ds_kv_device_status).
  * Requires 0 <= n_sink, 0 <= n_window, n_sink + n_window <= M, row_bytes <= 65536,
  * len <= capacity, n_buckets <= 64.
  */
@@ -244,8 +249,19 @@ ds_status kv_evict_topk(const ds_kv_shape *shape, void *const *k_layers, void *c
                         int32_t n_window, int32_t n_buckets, int32_t *keep_out, int32_t *new_len,
                         void *workspace, size_t workspace_bytes, void *stream);
 
-/* Device address of the int32 status word kv_evict_topk leaves in its
- * workspace: 0 = ok, 1 = cache invariants broken (cache left untouched). */
+/* Device address of the int32 outcome word that kv_evict_topk and
+ * kv_evict_topk_indexed leave in their workspace.  Every call that evicts
+ * (len > M) overwrites it once its kernels have run:
+ *   0  ok;
+ *   1  the cache invariants were found broken: nothing was moved or rewritten;
+ *   2  the kept count differed from M (an internal check): nothing was moved;
+ *   3  kv_evict_topk only: a bounded wait of the in-place gather timed out;
+ *      every move stopped at once, so K/V rows, pos and chunk_id in [0, M)
+ *      are partially compacted and unspecified.
+ * The calls return DS_OK before their kernels run, so a failure shows only
+ * here: read the word after synchronising, or fold it into a device-side
+ * maximum after each call to check many events with one read.  The two
+ * int32 words after it are internal flags. */
 int32_t *ds_kv_device_status(void *workspace);
 
 /* ------------------------------------------------------------------------

@@ -20,7 +20,8 @@ DS_BF16, DS_F32 = 0, 1
 LAYER_FROB, HEAD_MEAN, PER_HEAD, WRITE_MEAN = 0, 1, 2, 3
 
 EXPORTED = [
-    "ds_status_string", "ds_last_error", "ds_gdn_workspace_bytes", "gdn_chunk_fwd", "deltas_drift",
+    "ds_status_string", "ds_last_error", "ds_gdn_workspace_bytes", "ds_gdn_write_workspace_bytes",
+    "gdn_chunk_fwd", "deltas_drift",
     "deltas_drift_states", "ds_kv_workspace_bytes", "kv_evict_topk", "ds_kv_device_status",
     "ds_kv_indexed_workspace_bytes", "kv_evict_topk_indexed", "gdn_decode_step",
 ]
@@ -58,6 +59,8 @@ def lib():
         L.ds_last_error.restype = ctypes.c_char_p
         L.ds_gdn_workspace_bytes.argtypes = [ctypes.POINTER(GdnShape)]
         L.ds_gdn_workspace_bytes.restype = SZ
+        L.ds_gdn_write_workspace_bytes.argtypes = [ctypes.POINTER(GdnShape)]
+        L.ds_gdn_write_workspace_bytes.restype = SZ
         L.gdn_chunk_fwd.argtypes = [ctypes.POINTER(GdnShape), P, P, P, P, P, P, P, P, P, I32, ctypes.c_float,
                                     P, P, P, P, SZ, P]
         L.gdn_chunk_fwd.restype = I32
@@ -113,8 +116,11 @@ def gdn_shape(lengths, H_k, H_v, d, frame_len):
                     sum(frames_of_length(n, frame_len) for n in lengths))
 
 
-def gdn_workspace_bytes(shape: GdnShape) -> int:
-    return int(lib().ds_gdn_workspace_bytes(ctypes.byref(shape)))
+def gdn_workspace_bytes(shape: GdnShape, write_signal: bool = False) -> int:
+    """Workspace bytes of gdn_chunk_fwd for this shape (with write_partials if write_signal)."""
+    L = lib()
+    q = L.ds_gdn_write_workspace_bytes if write_signal else L.ds_gdn_workspace_bytes
+    return int(q(ctypes.byref(shape)))
 
 
 def gdn_chunk_fwd(q, k, v, g, beta, lengths, frame_len, cu_seqlens=None, state_in=None, state_out=None,
@@ -149,7 +155,7 @@ def gdn_chunk_fwd(q, k, v, g, beta, lengths, frame_len, cu_seqlens=None, state_i
         else write_partials if write_partials is not False else None
     sn = torch.empty((shape.n_frames, H_v, d, d), dtype=torch.float32, device=dev) if snapshots is True \
         else snapshots if snapshots is not False else None
-    need = gdn_workspace_bytes(shape)
+    need = gdn_workspace_bytes(shape, wp is not None)
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     _check(lib().gdn_chunk_fwd(ctypes.byref(shape), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
@@ -276,5 +282,13 @@ def kv_evict_topk_indexed(pos, chunk_id, slot, chunk_scores, length, M, n_sink, 
 
 
 def kv_device_status(workspace):
-    """(invariant status, skip flag, wait-timeout flag) left by the last kv_evict_topk (synchronises)."""
+    """(outcome, moves-stopped flag, wait-timeout flag) left by the last eviction
+    that ran on this workspace (synchronises).  Outcome: 0 ok, 1 cache
+    invariants broken, 2 keep count wrong, 3 gather wait timed out."""
     return workspace[:12].view(torch.int32).cpu().tolist()
+
+
+def kv_outcome_word(workspace):
+    """The outcome word of the last eviction on this workspace as a device
+    int32 tensor of one element (a view: no synchronisation)."""
+    return workspace[:4].view(torch.int32)

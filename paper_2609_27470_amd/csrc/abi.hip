@@ -66,7 +66,14 @@ const char *ds_last_error(void) { return g_last_error; }
 
 size_t ds_gdn_workspace_bytes(const ds_gdn_shape *shape) {
     if (check_gdn_shape(shape) != DS_OK) return 0;
-    return ds::gdn_workspace_layout(shape->B, shape->T_total, shape->H_k, shape->H_v, shape->d_v, shape->n_frames).total;
+    return ds::gdn_workspace_layout(shape->B, shape->T_total, shape->H_k, shape->H_v, shape->d_v, shape->n_frames, false)
+        .total;
+}
+
+size_t ds_gdn_write_workspace_bytes(const ds_gdn_shape *shape) {
+    if (check_gdn_shape(shape) != DS_OK) return 0;
+    return ds::gdn_workspace_layout(shape->B, shape->T_total, shape->H_k, shape->H_v, shape->d_v, shape->n_frames, true)
+        .total;
 }
 
 ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k, const void *v, const float *g,
@@ -87,7 +94,8 @@ ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k,
                           snapshots, workspace};
     for (const void *p : ptrs)
         if (misaligned(p)) return fail(DS_E_ALIGN, "a pointer is not 16-byte aligned");
-    const ds::GdnWorkspace lay = ds::gdn_workspace_layout(s.B, s.T_total, s.H_k, s.H_v, s.d_v, s.n_frames);
+    const ds::GdnWorkspace lay =
+        ds::gdn_workspace_layout(s.B, s.T_total, s.H_k, s.H_v, s.d_v, s.n_frames, write_partials != nullptr);
     if (!workspace || workspace_bytes < lay.total)
         return fail(DS_E_WORKSPACE, "workspace needs %zu bytes, got %zu", lay.total, workspace_bytes);
     if (s.n_frames > 0 && s.frame_len == 0 && s.n_frames > s.B)

@@ -20,8 +20,8 @@
 //             state-dependent products on fp16 matrix cores, writes o, and at
 //             every frame end the drift sums of Eq. 3 for its rows.
 //   The drift sums of the slices are added in a fixed order by the last
-//   workgroup of each (stream, v-head) to finish (gdn_drift_finalize when no
-//   prep pass runs).
+//   workgroup of each (stream, v-head) to finish (gdn_drift_finalize only
+//   for a call without tokens).
 #include <type_traits>
 
 #include "common.h"
@@ -501,6 +501,38 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
 // P are fp16.  All accumulation is fp32.
 // ============================================================================
 
+// Sum of squares over the 16 columns of an E k-step held as a B operand (lane
+// (ln, lg) element i is token kappa(ks, lg, i), column ln), reduced over the
+// 16 lanes of each row by a transposing butterfly: afterwards lane ln holds
+// the sum of element ln / 2 (lanes ln and ln ^ 1 agree).
+__device__ __forceinline__ float row_sq_sum16(half8 ef, int ln) {
+    float x[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = (float)ef[i] * (float)ef[i];
+    const bool b3 = (ln >> 3) & 1, b2 = (ln >> 2) & 1, b1 = (ln >> 1) & 1;
+    float y[4], z[2];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {  // partner ln ^ 8 (rotate the row of 16 by 8)
+        const float send = b3 ? x[q] : x[4 + q];
+        const float recv = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, send), 0x128,
+                                                                                  0xF, 0xF, false));
+        y[q] = (b3 ? x[4 + q] : x[q]) + recv;
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {  // partner ln ^ 4 (swizzle with xor mask 4)
+        const float send = b2 ? y[q] : y[2 + q];
+        const float recv = __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, send), 0x101F));
+        z[q] = (b2 ? y[2 + q] : y[q]) + recv;
+    }
+    // partner ln ^ 2, then ln ^ 1 (quad permutations)
+    const float send = b1 ? z[0] : z[1];
+    const float recv =
+        __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, send), 0x4E, 0xF, 0xF, false));
+    float w = (b1 ? z[1] : z[0]) + recv;
+    w += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, w), 0xB1, 0xF, 0xF, false));
+    return w;
+}
+
 template <int D>
 struct SeqShared {
     static constexpr int KS = D / 32, NKB = D / 16;
@@ -791,42 +823,6 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                     acc[r][3] *= g4.w;
                 }
                 const half8 ef0 = as_half8(sh.E[buf][0][lane]);
-                if (a.wsWrite) {
-                    // ||E row||^2 over this slice's 16 columns for the wave's 32 tokens
-                    // (E k-step PR: lane (ln, lg) element i is token kappa(PR, lg, i),
-                    // column ln), summed over the 16 lanes of each row by a transposing
-                    // butterfly: after it, lane ln holds the sum for element ln / 2
-                    const half8 ef = PR == 0 ? ef0 : as_half8(sh.E[buf][1][lane]);
-                    float x[8];
-#pragma unroll
-                    for (int i = 0; i < 8; ++i) x[i] = (float)ef[i] * (float)ef[i];
-                    const bool b3 = (ln >> 3) & 1, b2 = (ln >> 2) & 1, b1 = (ln >> 1) & 1;
-                    float y[4], z[2];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {  // partner ln ^ 8 (rotate the row of 16 by 8)
-                        const float send = b3 ? x[q] : x[4 + q];
-                        const float recv = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
-                                                                         0, __builtin_bit_cast(int, send), 0x128, 0xF, 0xF, false));
-                        y[q] = (b3 ? x[4 + q] : x[q]) + recv;
-                    }
-#pragma unroll
-                    for (int q = 0; q < 2; ++q) {  // partner ln ^ 4 (swizzle with xor mask 4)
-                        const float send = b2 ? y[q] : y[2 + q];
-                        const float recv = __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, send), 0x101F));
-                        z[q] = (b2 ? y[2 + q] : y[q]) + recv;
-                    }
-                    float wsum;
-                    {  // partner ln ^ 2, then ln ^ 1 (quad permutations)
-                        const float send = b1 ? z[0] : z[1];
-                        const float recv = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
-                                                                         0, __builtin_bit_cast(int, send), 0x4E, 0xF, 0xF, false));
-                        wsum = (b1 ? z[1] : z[0]) + recv;
-                        wsum += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, wsum), 0xB1, 0xF,
-                                                                                      0xF, false));
-                    }
-                    const int i = ln >> 1, tok = 32 * PR + 16 * (i >> 2) + 4 * lg + (i & 3);
-                    if ((ln & 1) == 0 && tok < n) a.wsWrite[((size_t)j * a.n_split + sl) * a.st.T + t0 + tok] = wsum;
-                }
                 if (PR == 0) {
                     acc[0] = mfma_f16(as_half8(s.p[0]), ef0, acc[0]);
                     acc[1] = mfma_f16(as_half8(s.p[1]), ef0, acc[1]);
@@ -983,6 +979,23 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                 ++frame;
                 frame_end = min(frame_end + a.frame_len, len);
             };
+            // write signal: ||E row||^2 over the slice's 16 columns for every token
+            // of tile it - 1, from the E the state waves left in LDS (valid until
+            // they write that buffer again in tile it + 1), one store per k-step.
+            // Loader 3 has slack at the barrier; on the output waves this cost
+            // every tile of the chain
+            auto write_norms = [&](int it) __attribute__((always_inline)) {
+                if (X != 3 || it < 1 || !a.wsWrite) return;
+                const int lt = it - 1;
+                const int t0 = st + TILE * lt, n = min(TILE, en - t0);
+                float *wb = a.wsWrite + ((size_t)j * a.n_split + sl) * a.st.T + t0;
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) {
+                    const float wsum = row_sq_sum16(as_half8(sh.E[lt & 1][ks][lane]), ln);
+                    const int i = ln >> 1, tok = 32 * ks + 16 * (i >> 2) + 4 * lg + (i & 3);
+                    if ((ln & 1) == 0 && tok < n) wb[tok] = wsum;
+                }
+            };
             // tile t lives in register set t % 2 and LDS buffer t % 2.  Iteration it
             // stages tile it + 1 and then loads tile it + 3 into the set just freed.
             if (n_tiles > 0) {
@@ -996,6 +1009,7 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                     if (it + 1 < n_tiles) stage(s, bufc, (it + 1) % 3);
                     load(s, it + 3);
                     drift_reduce(it);
+                    write_norms(it);
                 };
                 for (int it = 0; it <= n_tiles; it += 2) {
                     step(it, s1, std::integral_constant<int, 1>());
@@ -1120,7 +1134,7 @@ __global__ __launch_bounds__(256) void gdn_write_finalize_kernel(const float *ws
 // ============================================================================
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, int n_frames) {
+GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, int n_frames, bool with_write) {
     GdnWorkspace w{};
     w.tiles_max = (int)(((long long)T_total + 63LL * B) / 64);
     w.n_split = d / 16;
@@ -1135,8 +1149,8 @@ GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, i
     off = align256(off + (size_t)w.tiles_max * H_v * 128 * sizeof(float));
     w.offDrift = off;
     off = align256(off + (size_t)n_frames * H_v * w.n_split * 2 * sizeof(float));
-    w.offWrite = off;
-    off = align256(off + (size_t)T_total * H_v * w.n_split * sizeof(float));
+    w.offWrite = off;  // per-token norm slices, reserved only for calls that ask for the write signal
+    if (with_write) off = align256(off + (size_t)T_total * H_v * w.n_split * sizeof(float));
     w.offCnt = off;
     off = align256(off + (size_t)B * H_v * sizeof(unsigned));
     w.total = off;
@@ -1169,12 +1183,11 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     a.wsDrift = p.drift_partials ? p.wsDrift : nullptr;
     a.wsWrite = p.write_partials ? p.wsWrite : nullptr;
     a.n_split = p.n_split;
-    // drift sums reduced by the sequential kernel itself (the last workgroup of
-    // each stream and v-head) when each stream has few frames, e.g. a streamed
-    // chunk, where a separate pass would cost more than the sums; otherwise, and
-    // when no prep kernel runs to clear the counters, by the finalize pass
-    // (measured: equal within 2 us at 32 frames, 4 us saved at one frame)
-    const bool fused_drift = p.drift_partials && p.n_frames > 0 && p.tiles_max > 0 && p.n_frames <= 2 * p.B;
+    // drift sums of the slices added by the sequential kernel itself (the last
+    // workgroup of each stream and v-head to finish), so the drift costs no
+    // launch of its own; only a call without tokens (no prep pass clears the
+    // counters) leaves it to the finalize pass, which then writes zeros
+    const bool fused_drift = p.drift_partials && p.n_frames > 0 && p.tiles_max > 0;
     a.drift_out = fused_drift ? p.drift_partials : nullptr;
     a.drift_cnt = p.wsCnt;
 

@@ -38,7 +38,8 @@ struct GdnWorkspace {
     size_t offT, offP, offQ, offGam, offDrift, offWrite, offCnt, total;
     int tiles_max, n_split;
 };
-GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, int n_frames);
+// with_write: also the per-token norm area of the write signal (write_partials != NULL)
+GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, int n_frames, bool with_write);
 hipError_t launch_gdn(const GdnLaunch &p, hipStream_t stream);
 
 // ---------------------------------------------------------------- decode step

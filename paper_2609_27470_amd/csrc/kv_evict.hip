@@ -46,7 +46,7 @@ static_assert(SEL_PER == 4, "pass 2 stores a thread's four inverse entries as on
 constexpr int GATHER_U = 16;                        // uint4 per thread per group
 constexpr int SPIN_LIMIT = 1 << 22;
 constexpr long long STAGE_BYTES = 64ll << 20;       // below this much shift, rows are staged
-constexpr long long STAGE_AREA = 1ll << 30;         // staging area of one block of destinations
+constexpr long long STAGE_AREA = 256ll << 20;       // staging area of one block of destinations
 constexpr int STAGE_WG = 1024;                      // workgroups per staging launch (each loops over rows)
 
 // pointer into global memory (lets the compiler emit global rather than flat accesses)
@@ -60,7 +60,8 @@ struct KvArgs {
     int num_chunks, len, M, n_s, n_w, N;
     int n_flags, n_chunks;
     int stage_shift;   // destinations with keep[d] - d below this are staged
-    int32_t *status;   // [0] invariants broken, [1] skip gather, [2] wait timed out, [3] first moved slot,
+    int32_t *status;   // [0] outcome (0 ok, 1 invariants broken, 2 keep count wrong, 3 gather wait timed
+                       // out), [1] skip or stop the moves, [2] wait timed out, [3] first moved slot,
                        // [4] first slot moved by the ticket gather (the staged ones lie in [3], [4])
     uint32_t *ticket;
     int32_t *keep, *inv, *run_start, *run_bkt, *run_take, *run_from, *th_run;
@@ -399,6 +400,11 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     }
     taken = block_sum_ll(taken, s_ll);
     const long long fill = (long long)(a.M - a.n_s - a.n_w) - taken;
+    // beyond RUN_CAP runs the fill pass below reads run_take of runs that other
+    // waves stored to global memory: a full barrier (workgroup-scope release and
+    // acquire of global memory) orders those stores before the reads; the
+    // barriers inside block_sum_ll fence LDS only
+    __syncthreads();
 
     // ---- fill with the best remaining tokens over all spans; a run keeps
     // its newest tokens, slots [run_from, run end)
@@ -667,10 +673,15 @@ __global__ __launch_bounds__(256) void kv_gather_kernel(GatherArgs a) {
     // tickets are taken until none is left, so the grid drains evenly; a
     // workgroup only waits for slots of lower tickets, which running
     // workgroups hold
+    __shared__ int s_stop;
     for (;;) {
-        if (tid == 0) s_t = (int)atomicAdd(a.ticket, 1u);
+        if (tid == 0) {
+            s_t = (int)atomicAdd(a.ticket, 1u);
+            // a workgroup whose wait timed out stopped every move: take no more work
+            s_stop = __hip_atomic_load(&a.status[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
         __syncthreads();
-        if (s_t >= n_work) break;
+        if (s_t >= n_work || s_stop) break;
         const int d_lo = first + s_t * GATHER_ROWS;
         const int d_hi = min(d_lo + GATHER_ROWS, a.M);
         // sources and readers of the ticket's slots, in LDS: a global load inside
@@ -725,13 +736,24 @@ __global__ __launch_bounds__(256) void kv_gather_kernel(GatherArgs a) {
             if (tid == 0) {
                 __hip_atomic_store(&a.flags[d * a.n_chunks + c], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 // ---- wait until the reader of row d (a lower slot, hence an
-                // earlier ticket or an earlier unit here) holds its data
+                // earlier ticket or an earlier unit here) holds its data.  The
+                // wait is bounded: on a timeout every move stops (status[1]) and
+                // the call's outcome becomes 3; a workgroup that sees the stop
+                // while waiting leaves as well, without writing
                 if (dep >= first && dep != d) {  // readers below `first` were staged earlier
                     int it = 0;
                     const int ft = dep * a.n_chunks + c;
                     while (__hip_atomic_load(&a.flags[ft], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
                         if (++it >= SPIN_LIMIT) {
                             __hip_atomic_store(&a.status[2], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            __hip_atomic_store(&a.status[0], 3, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            __hip_atomic_store(&a.status[1], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            s_stop = 1;
+                            break;
+                        }
+                        if ((it & 63) == 0 &&
+                            __hip_atomic_load(&a.status[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+                            s_stop = 1;
                             break;
                         }
                         __builtin_amdgcn_s_sleep(2);
@@ -739,6 +761,7 @@ __global__ __launch_bounds__(256) void kv_gather_kernel(GatherArgs a) {
                 }
             }
             lds_sync();
+            if (s_stop) return false;
             load(min(u + 1, n_units - 1), nbuf, npv, ncv);  // unconditional (a repeat past the end is never written)
             // ---- write slot d
             const int p0 = c * a.planes_per_group;
@@ -759,11 +782,12 @@ __global__ __launch_bounds__(256) void kv_gather_kernel(GatherArgs a) {
             int32_t *tr = (int32_t *)(a.trash + 4096) + 2 * tid;
             *(meta ? a.pos + d : tr) = pv;
             *(meta ? a.chunk + d : tr + 1) = cv;
+            return true;
         };
         load(0, bufA, pvA, cvA);
         for (int u = 0; u < n_units; u += 2) {
-            step(u, bufA, pvA, cvA, bufB, pvB, cvB);
-            if (u + 1 < n_units) step(u + 1, bufB, pvB, cvB, bufA, pvA, cvA);
+            if (!step(u, bufA, pvA, cvA, bufB, pvB, cvB)) return;  // moves stopped (s_stop is workgroup-uniform)
+            if (u + 1 < n_units && !step(u + 1, bufB, pvB, cvB, bufA, pvA, cvA)) return;
         }
         __syncthreads();  // every lane is done with this ticket's LDS entries
     }

@@ -5,8 +5,8 @@ One `DeltaSStream` holds, on the device, everything the retention policy
 carries from chunk to chunk: the fp32 state of every linear-attention layer,
 the full-attention layers' K/V cache with each slot's position and chunk id,
 and the drift score of every chunk seen so far.  `step` consumes one chunk of
-any length (the paper's chunks are about two seconds of video, 118 to 132
-tokens): each linear-attention layer runs `gdn_chunk_fwd` over the chunk as
+any length (a chunk of the paper is one second of video -- two frames at
+2 fps -- of 118 to 132 tokens): each linear-attention layer runs `gdn_chunk_fwd` over the chunk as
 one frame (so its drift sums cover exactly the chunk), `deltas_drift` turns
 the per-layer sums into the chunk's score (Eq. 3, mean over layers), the
 chunk's K/V rows are appended, and `kv_evict_topk` cuts the cache back to the
@@ -26,20 +26,35 @@ device, so the one graph serves every chunk length up to max_chunk.  The
 append and the eviction stay outside the graph: the cache length they work
 from is host state.
 
-With `indexed=True` the cache is addressed through a slot table (logical
-token i lives in physical row slot[i]): eviction is `kv_evict_topk_indexed`,
-which keeps exactly the same tokens and moves no K/V byte, and a chunk's rows
-are written into the rows the last eviction freed.  The logical view
-(rows slot[0..length)) equals the order-preserving cache of the default mode.
+By default (`indexed=True`) the cache is addressed through a slot table
+(logical token i lives in physical row slot[i]): eviction is
+`kv_evict_topk_indexed`, which keeps exactly the same tokens and moves no K/V
+byte, and a chunk's rows are written into the rows the last eviction freed.
+The logical view (rows slot[0..length)) equals the order-preserving cache
+that `indexed=False` keeps with `kv_evict_topk` (rows compacted in place).
+
+Every eviction's outcome word (0 = ok) is folded into a device-side maximum
+without a host synchronisation; `check()` reads it and raises if any
+eviction since the session began reported a failure, and `save`, `restore`
+and `logical_rows` call it.
 """
 from __future__ import annotations
 
+import contextlib
 from dataclasses import dataclass
 
 import torch
 
 from . import (LAYER_FROB, deltas_drift, gdn_chunk_fwd, gdn_shape, gdn_workspace_bytes, kv_evict_topk,
-               kv_evict_topk_indexed, kv_indexed_workspace_bytes, kv_workspace_bytes)
+               kv_evict_topk_indexed, kv_indexed_workspace_bytes, kv_outcome_word, kv_workspace_bytes)
+
+
+class EvictionFailed(RuntimeError):
+    """An eviction reported a failure on the device (see ds_kv_device_status)."""
+
+
+def _on(stream):
+    return torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
 
 
 @dataclass
@@ -64,11 +79,14 @@ class DeltaSStream:
     n_layers linear-attention layers of (H_k, H_v, d) heads; kv_layers
     full-attention layers whose K and V rows are row_elems bf16 values per
     token; budget M tokens, cache capacity M + max_chunk; the policy's sink,
-    window and span counts (the paper uses 4, 1024 and 4).
+    window and span counts (the paper uses 4, 1024 and 4).  `o` holds every
+    linear-attention layer's output of the latest chunk ([layer][token]
+    [H_v][d] in o_dtype).
     """
 
     def __init__(self, n_layers, H_k, H_v, d, kv_layers, row_elems, M, max_chunk, max_chunks,
-                 n_sink=4, n_window=1024, n_buckets=4, score_mode=LAYER_FROB, device="cuda", indexed=False):
+                 n_sink=4, n_window=1024, n_buckets=4, score_mode=LAYER_FROB, device="cuda", indexed=True,
+                 o_dtype=torch.bfloat16):
         if n_sink + n_window > M:
             raise ValueError("sink + window exceed the budget")
         dev = torch.device(device)
@@ -80,7 +98,7 @@ class DeltaSStream:
         self.capacity = M + max_chunk
         self.state = torch.zeros((n_layers, 1, H_v, d, d), dtype=torch.float32, device=dev)
         self.partials = torch.zeros((n_layers, 1, H_v, 2), dtype=torch.float32, device=dev)
-        self.o = torch.empty((max_chunk, H_v, d), dtype=torch.bfloat16, device=dev)
+        self.o = torch.empty((n_layers, max_chunk, H_v, d), dtype=o_dtype, device=dev)
         self.k = torch.zeros((kv_layers, self.capacity, row_elems), dtype=torch.int16, device=dev)
         self.v = torch.zeros((kv_layers, self.capacity, row_elems), dtype=torch.int16, device=dev)
         self.pos = torch.zeros(self.capacity, dtype=torch.int32, device=dev)
@@ -99,6 +117,7 @@ class DeltaSStream:
             self.slot = self.free = None
             self.kv_ws = torch.empty(max(kv_workspace_bytes(kv_layers, row_elems * 2, self.capacity), 1),
                                      dtype=torch.uint8, device=dev)
+        self.kv_fail = torch.zeros(1, dtype=torch.int32, device=dev)   # max outcome word of every eviction
         self.graph = None
         self.length = 0      # tokens in the cache
         self.n_chunks = 0    # chunks seen (the next chunk's id)
@@ -121,14 +140,24 @@ class DeltaSStream:
         c = self.n_chunks
         if c >= self.scores.numel():
             raise ValueError("score table full")
-        for l, (q, k, v, g, beta) in enumerate(layer_inputs):
-            st = self.state[l]
-            gdn_chunk_fwd(q, k, v, g, beta, [T], 0, state_in=st, state_out=st, o=self.o[:T],
-                          drift_partials=self.partials[l], workspace=self.gdn_ws, stream=stream)
-        deltas_drift(self.partials, self.score_mode, scores=self.scores[c:c + 1], stream=stream)
-        return self._append_and_evict(T, k_rows, v_rows, stream)
+        # every launch and copy of the step on one stream (the caller's, else the current one)
+        with _on(stream):
+            for l, (q, k, v, g, beta) in enumerate(layer_inputs):
+                st = self.state[l]
+                gdn_chunk_fwd(q, k, v, g, beta, [T], 0, state_in=st, state_out=st, o=self.o[l, :T],
+                              drift_partials=self.partials[l], workspace=self.gdn_ws)
+            deltas_drift(self.partials, self.score_mode, scores=self.scores[c:c + 1])
+            return self._append_and_evict(T, k_rows, v_rows)
 
-    def _append_and_evict(self, T, k_rows, v_rows, stream=None):
+    def check(self):
+        """Raise EvictionFailed if any eviction of this session reported a
+        failure on the device (synchronises with the current stream)."""
+        code = int(self.kv_fail.item())
+        if code != 0:
+            raise EvictionFailed(f"an eviction reported outcome {code} (1: cache invariants broken, "
+                                 "2: keep count wrong, 3: gather wait timed out)")
+
+    def _append_and_evict(self, T, k_rows, v_rows):
         c = self.n_chunks
         n = self.length
         if self.indexed:
@@ -149,18 +178,21 @@ class DeltaSStream:
         if self.indexed:
             new_len, _, freed = kv_evict_topk_indexed(self.pos, self.chunk_id, self.slot, self.scores[:self.n_chunks],
                                                       n, self.M, ns, nw, nb, free_out=self.freed,
-                                                      workspace=self.kv_ws, stream=stream)
+                                                      workspace=self.kv_ws)
             if n > self.M:
                 self.free = torch.cat([self.free, freed[:n - self.M]])
             self.length = new_len
         else:
             self.length, _ = kv_evict_topk(list(self.k), list(self.v), self.pos, self.chunk_id,
                                            self.scores[:self.n_chunks], n, self.M, ns, nw, nb,
-                                           workspace=self.kv_ws, stream=stream)
+                                           workspace=self.kv_ws)
+        if n > self.M:   # the call evicted: fold its outcome word in (device side, no sync)
+            torch.maximum(self.kv_fail, kv_outcome_word(self.kv_ws), out=self.kv_fail)
         return self.length
 
     def logical_rows(self):
         """(K, V) rows of the cached tokens in logical (arrival) order, [kv_layers][length][row]."""
+        self.check()
         n = self.length
         if not self.indexed:
             return self.k[:, :n], self.v[:, :n]
@@ -190,7 +222,7 @@ class DeltaSStream:
         for l in range(self.L):
             st = self.state[l]
             gdn_chunk_fwd(q[l], k[l], v[l], g[l], b[l], [self.max_chunk], 0, cu_seqlens=self.cu, state_in=st,
-                          state_out=st, o=self.o, drift_partials=self.partials[l], workspace=self.gdn_ws)
+                          state_out=st, o=self.o[l], drift_partials=self.partials[l], workspace=self.gdn_ws)
         deltas_drift(self.partials, self.score_mode, scores=self.score_buf)
 
     def step_inputs(self, T, k_rows, v_rows):
@@ -211,6 +243,7 @@ class DeltaSStream:
 
     def save(self) -> Snapshot:
         """Copy the memory aside (question time)."""
+        self.check()
         n = self.length
         if self.indexed:   # rows stay where they are: keep the physical planes and the tables
             return Snapshot(self.state.clone(), self.k.clone(), self.v.clone(), self.pos[:n].clone(),
@@ -222,6 +255,7 @@ class DeltaSStream:
 
     def restore(self, s: Snapshot):
         """Put a saved memory back; the stream continues as if nothing had run since."""
+        self.check()
         n = s.length
         self.state.copy_(s.state)
         if self.indexed:

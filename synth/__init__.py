@@ -7,8 +7,10 @@ path read what it produces, so neither side can leak into the other here.
 Recipe (stated once, used everywhere):
 
 * generator: numpy ``PCG64`` seeded with ``SeedSequence([config, layer,
-  stream])``; everything is drawn in fp64 and rounded to the stored dtype
-  (fp64 -> fp32 round-to-nearest-even -> bf16 round-to-nearest-even);
+  stream, group])``, one generator per group of four frames (novelty streams)
+  or per block of 1024 tokens (iid streams), so that groups are drawn in
+  parallel threads; everything is drawn in fp64 and rounded to the stored
+  dtype (fp64 -> fp32 round-to-nearest-even -> bf16 round-to-nearest-even);
 * q, k ~ N(0, 1) per element, L2-normalised per (token, head) in fp64, then
   bf16 (the method takes unit keys, Section 3.2 after Eq. 1);
 * v ~ N(0, 1), bf16;
@@ -21,12 +23,16 @@ Recipe (stated once, used everywhere):
   replacement (one source index per token, shared by all heads and by k and
   v) plus N(0, 0.05) noise added before normalisation.  q stays iid.
 
-Draw order inside one frame: [basis per qk-head, z] or [src, k-noise],
-then v (or v-noise), q, g_raw, beta_raw.
+A novelty group is one novel frame followed by the three frames that
+re-present it (frames 4 i .. 4 i + 3 of the stream).  Draw order inside one
+frame: [basis per qk-head, z] or [src, k-noise], then v (or v-noise), q,
+g_raw, beta_raw.  An iid block draws q, k, v, g_raw, beta_raw in that order.
 """
 from __future__ import annotations
 
 import math
+import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -49,12 +55,12 @@ CONFIG_INDEX = {"tiny": 0, "single_layer": 1, "stack": 2, "varlen": 3, "eviction
 # dtype helpers (bit patterns, so nothing depends on a bf16 numpy dtype)
 # ----------------------------------------------------------------------------
 def to_bf16_bits(x) -> np.ndarray:
-    """fp64/fp32 array -> bf16 bit patterns (uint16), round to nearest even."""
+    """fp64/fp32 array -> bf16 bit patterns (uint16), round to nearest even
+    (finite values: the sum below stays inside 32 bits)."""
     f = np.ascontiguousarray(np.asarray(x, dtype=np.float32))
-    u = f.view(np.uint32).astype(np.uint64)
-    lsb = (u >> np.uint64(16)) & np.uint64(1)
-    r = (u + np.uint64(0x7FFF) + lsb) >> np.uint64(16)
-    return r.astype(np.uint16)
+    u = f.view(np.uint32)
+    r = u + (np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))
+    return (r >> np.uint32(16)).astype(np.uint16)
 
 
 def bf16_bits_to_f64(b) -> np.ndarray:
@@ -75,8 +81,20 @@ def _unit_rows(x):
     return x / np.where(n > 0, n, 1.0)
 
 
-def rng_for(config: int, layer: int = 0, stream: int = 0) -> np.random.Generator:
-    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([config, layer, stream])))
+def rng_for(config: int, layer: int = 0, stream: int = 0, *more: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([config, layer, stream, *more])))
+
+
+IID_BLOCK = 1024      # tokens per generator of an iid stream
+NOVELTY_GROUP = 4     # frames per generator of a novelty stream (one novel frame, three re-presenting it)
+_pool = None
+
+
+def _executor():
+    global _pool
+    if _pool is None:
+        _pool = ThreadPoolExecutor(max_workers=max(1, min(16, os.cpu_count() or 1)))
+    return _pool
 
 
 # ----------------------------------------------------------------------------
@@ -132,23 +150,22 @@ def _gates(rng, n, H_v, gates="standard", head_x=None):
     return g.astype(np.float32), beta.astype(np.float32)
 
 
-def gen_plain_stream(rng, T, H_k, H_v, d, gates="standard", head_x=None):
-    """iid stream (the tiny workload): returns fp64 q,k (normalised), v, and fp32 gates."""
-    q = _unit_rows(rng.standard_normal((T, H_k, d)))
-    k = _unit_rows(rng.standard_normal((T, H_k, d)))
-    v = rng.standard_normal((T, H_v, d))
-    g, beta = _gates(rng, T, H_v, gates, head_x)
+def _plain_block(rng, n, H_k, H_v, d, gates="standard", head_x=None):
+    """n iid tokens: fp64 q, k (normalised), v, and fp32 gates."""
+    q = _unit_rows(rng.standard_normal((n, H_k, d)))
+    k = _unit_rows(rng.standard_normal((n, H_k, d)))
+    v = rng.standard_normal((n, H_v, d))
+    g, beta = _gates(rng, n, H_v, gates, head_x)
     return q, k, v, g, beta
 
 
-def gen_novelty_frames(rng, T, H_k, H_v, d, frame_len, sub=32, sigma=0.05,
-                       gates="standard", head_x=None):
-    """Yield (q, k, v, g, beta) frame by frame for a novelty-structured stream."""
+def _novelty_group(rng, lens, H_k, H_v, d, sub=32, sigma=0.05, gates="standard", head_x=None):
+    """Yield (q, k, v, g, beta) for the frames of one novelty group (frame
+    lengths `lens`): the first frame is novel, each later one re-presents
+    tokens of the frame before it."""
     k_prev = v_prev = None
-    n_fr = frames_of_length(T, frame_len)
-    for c in range(n_fr):
-        n = min(frame_len, T - c * frame_len)
-        if c % 4 == 0 or k_prev is None:
+    for c, n in enumerate(lens):
+        if c == 0:
             k_raw = np.empty((n, H_k, d))
             for h in range(H_k):
                 basis, _ = np.linalg.qr(rng.standard_normal((d, sub)))
@@ -165,37 +182,61 @@ def gen_novelty_frames(rng, T, H_k, H_v, d, frame_len, sub=32, sigma=0.05,
         yield _unit_rows(q), _unit_rows(k_raw), v_raw, g, beta
 
 
-def _pack(parts, H_k, H_v, d):
-    T = sum(p[0].shape[0] for p in parts)
-    q = np.empty((T, H_k, d), np.uint16)
-    k = np.empty((T, H_k, d), np.uint16)
-    v = np.empty((T, H_v, d), np.uint16)
-    g = np.empty((T, H_v), np.float32)
-    beta = np.empty((T, H_v), np.float32)
-    t = 0
-    for pq, pk, pv, pg, pb in parts:
-        n = pq.shape[0]
-        q[t:t + n] = to_bf16_bits(pq)
-        k[t:t + n] = to_bf16_bits(pk)
-        v[t:t + n] = to_bf16_bits(pv)
-        g[t:t + n] = pg
-        beta[t:t + n] = pb
-        t += n
-    return q, k, v, g, beta
+def _store(out, t, part):
+    """Round one generated piece into the packed arrays at token offset t."""
+    q, k, v, g, beta = out
+    pq, pk, pv, pg, pb = part
+    n = pq.shape[0]
+    q[t:t + n] = to_bf16_bits(pq)
+    k[t:t + n] = to_bf16_bits(pk)
+    v[t:t + n] = to_bf16_bits(pv)
+    g[t:t + n] = pg
+    beta[t:t + n] = pb
+
+
+def _stream_tasks(out, t0, config, layer, stream, T, H_k, H_v, d, frame_len, novelty, gates):
+    """Independent generation tasks that fill one stream's tokens [t0, t0 + T)."""
+    head_x = None
+    if gates == "long_memory":   # per-head gate offsets, drawn from the stream's own generator
+        head_x = rng_for(config, layer, stream).uniform(-10.0, -2.0, size=H_v)
+    tasks = []
+    if novelty:
+        F = frame_len if frame_len > 0 else T
+        n_fr = frames_of_length(T, F)
+        for grp in range((n_fr + NOVELTY_GROUP - 1) // NOVELTY_GROUP):
+            f0 = grp * NOVELTY_GROUP
+            lens = [min(F, T - f * F) for f in range(f0, min(f0 + NOVELTY_GROUP, n_fr))]
+
+            def task(grp=grp, lens=lens, ts=t0 + f0 * F):
+                rng = rng_for(config, layer, stream, grp)
+                t = ts
+                for part in _novelty_group(rng, lens, H_k, H_v, d, gates=gates, head_x=head_x):
+                    _store(out, t, part)
+                    t += part[0].shape[0]
+            tasks.append(task)
+    else:
+        for blk in range((T + IID_BLOCK - 1) // IID_BLOCK):
+            n = min(IID_BLOCK, T - blk * IID_BLOCK)
+
+            def task(blk=blk, n=n):
+                rng = rng_for(config, layer, stream, blk)
+                _store(out, t0 + blk * IID_BLOCK, _plain_block(rng, n, H_k, H_v, d, gates, head_x))
+            tasks.append(task)
+    return tasks
+
+
+def _run(tasks):
+    for f in [_executor().submit(t) for t in tasks]:
+        f.result()
 
 
 def make_stream(config: int, layer: int, stream: int, T: int, H_k: int, H_v: int, d: int,
                 frame_len: int, novelty: bool, gates: str = "standard"):
-    """One stream's arrays (bf16 bits / fp32) from its own seed."""
-    rng = rng_for(config, layer, stream)
-    head_x = None
-    if gates == "long_memory":
-        head_x = rng.uniform(-10.0, -2.0, size=H_v)
-    if novelty:
-        parts = list(gen_novelty_frames(rng, T, H_k, H_v, d, frame_len, gates=gates, head_x=head_x))
-    else:
-        parts = [gen_plain_stream(rng, T, H_k, H_v, d, gates=gates, head_x=head_x)]
-    return _pack(parts, H_k, H_v, d)
+    """One stream's arrays (bf16 bits / fp32) from its own seeds."""
+    out = (np.empty((T, H_k, d), np.uint16), np.empty((T, H_k, d), np.uint16), np.empty((T, H_v, d), np.uint16),
+           np.empty((T, H_v), np.float32), np.empty((T, H_v), np.float32))
+    _run(_stream_tasks(out, 0, config, layer, stream, T, H_k, H_v, d, frame_len, novelty, gates))
+    return out
 
 
 def make_gdn_inputs(lengths, H_k, H_v, d, frame_len, novelty, config=0, layer=0,
@@ -210,12 +251,12 @@ def make_gdn_inputs(lengths, H_k, H_v, d, frame_len, novelty, config=0, layer=0,
     v = np.empty((T, H_v, d), np.uint16)
     g = np.empty((T, H_v), np.float32)
     beta = np.empty((T, H_v), np.float32)
+    tasks = []
     for b, n in enumerate(lengths):
-        if n == 0:
-            continue
-        sq, sk, sv, sg, sb = make_stream(config, layer, b, n, H_k, H_v, d, frame_len, novelty, gates)
-        s = slice(int(cu[b]), int(cu[b + 1]))
-        q[s], k[s], v[s], g[s], beta[s] = sq, sk, sv, sg, sb
+        if n > 0:
+            tasks += _stream_tasks((q, k, v, g, beta), int(cu[b]), config, layer, b, n, H_k, H_v, d, frame_len,
+                                   novelty, gates)
+    _run(tasks)
     return GdnInputs(q, k, v, g, beta, cu, frame_len, H_k, H_v, d,
                      meta=dict(config=config, layer=layer, novelty=novelty, gates=gates))
 

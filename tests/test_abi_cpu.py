@@ -29,6 +29,7 @@ def _declared():
 def test_header_declares_the_entry_points():
     names = _declared()
     for n in ["gdn_chunk_fwd", "deltas_drift", "deltas_drift_states", "kv_evict_topk", "ds_gdn_workspace_bytes",
+              "ds_gdn_write_workspace_bytes",
               "ds_kv_workspace_bytes", "ds_status_string", "ds_last_error", "ds_kv_device_status",
               "kv_evict_topk_indexed", "ds_kv_indexed_workspace_bytes"]:
         assert n in names
@@ -51,12 +52,14 @@ def test_gdn_workspace_size(ds):
     s = ds.gdn_shape([32768], 16, 32, 128, 1024)
     assert s.n_frames == 32
     nb = ds.gdn_workspace_bytes(s)
+    nw = ds.gdn_workspace_bytes(s, write_signal=True)
     tiles = 512
     per = 2 * 6 * 64 * 8 * 2 + 128 * 4     # T and P fragments (fp16) + decay factors per (tile, v-head)
     wr = 32768 * 32 * 8 * 4                # per-token write norms per 16-row slice
     qh = tiles * 16 * 64 * 128 * 2         # q tiles in fp16 per qk-head
-    assert nb >= tiles * 32 * per + wr + qh
-    assert nb <= tiles * 32 * per + wr + qh + 32 * 32 * 8 * 2 * 4 + 4096   # + drift sums per slice
+    assert nb >= tiles * 32 * per + qh
+    assert nb <= tiles * 32 * per + qh + 32 * 32 * 8 * 2 * 4 + 4096   # + drift sums per slice
+    assert nw - nb >= wr and nw - nb <= wr + 256          # the norm area only when the signal is asked for
     bad = ds.gdn_shape([64], 1, 1, 96, 64)
     assert ds.gdn_workspace_bytes(bad) == 0
 
@@ -84,8 +87,9 @@ def test_gdn_rejects_bad_arguments(ds):
     assert _call_gdn(ds, good, od=7) == 3
     assert _call_gdn(ds, good, v=P((1 << 20) + 4)) == 4                    # alignment
     assert _call_gdn(ds, good, wsb=16) == 8                                # workspace
+    assert b"workspace" in ds.lib().ds_last_error()
     assert _call_gdn(ds, ds.gdn_shape([10, 20], 1, 1, 64, 64), cu=None) == 1
-    assert b"workspace" in ds.lib().ds_last_error() or True
+    assert b"cu_seqlens" in ds.lib().ds_last_error()
 
 
 def test_drift_rejects_bad_arguments(ds):

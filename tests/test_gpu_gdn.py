@@ -237,25 +237,6 @@ def test_drift_kernel_modes(ds):
         assert drift_rel_err(sc, rs) <= 1e-6
 
 
-def test_single_layer_full_size_sampled_heads(ds):
-    """The single-layer workload at full size (16 qk / 32 v heads, d=128,
-    T=32768, frames of 1024) in the launch configuration the benchmark
-    times; the oracle recomputes three sampled v-heads over the whole stream."""
-    x = synth.workload_inputs("single_layer")
-    gpu = run_gpu(ds, x, o_dtype=torch.float32)
-    for j in (0, 17, 31):
-        h = j // 2
-        ref = oracle.gdn_forward(x.q[:, h:h + 1], x.k[:, h:h + 1], x.v[:, j:j + 1], x.g[:, j:j + 1],
-                                 x.beta[:, j:j + 1], x.cu_seqlens, x.frame_len)
-        eo = rel_fro(gpu["o"][:, j], ref["o"][:, 0])
-        es = rel_fro(gpu["S"][:, j], ref["S"][:, 0])
-        assert eo <= TOL_O and es <= TOL_O, (j, eo, es)
-        ph = oracle.drift_scores(gpu["partials"][None, :, j:j + 1], oracle.PER_HEAD)
-        rh = oracle.drift_scores(ref["partials"][None], oracle.PER_HEAD)
-        assert drift_rel_err(ph, rh) <= TOL_DRIFT, j
-        print(f"head {j}: o {eo:.2e} S {es:.2e}")
-
-
 @pytest.mark.gpu
 def test_drift_states_kernel(ds):
     """deltas_drift_states on the frame-end snapshots of the tiny workload equals
@@ -280,48 +261,19 @@ def test_drift_states_kernel(ds):
     assert np.allclose(p2.cpu().numpy().astype(np.float64), oracle.drift_states(A, Bm), rtol=1e-5, atol=0.0)
 
 
-def test_varlen_full_lengths_one_group(ds):
-    """The varlen workload's stream lengths at full size (8 packed streams,
-    about 590k tokens) for one GQA group (1 qk-head, 2 v-heads, d = 128, frames
-    of 1024), against the oracle over every stream."""
-    x = synth.workload_inputs("varlen", H_k=1, H_v=2)
-    assert x.T_total > 8 * 16384
-    gpu = run_gpu(ds, x)
-    ref = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, x.frame_len)
+def test_long_run_near_unity_decay(ds):
+    """Ten frames of 1024 tokens with log decay g = -1e-4 (alpha = 0.9999:
+    almost nothing is forgotten, so rounding errors of the fp16 matrix-core
+    operands are not damped by decay), d = 128, GQA 2 -> 4, a non-zero entry
+    state: o, state and every drift aggregation against the oracle."""
+    x = synth.workload_inputs("single_layer", T=10 * 1024, H_k=2, H_v=4)
+    x.g[:] = -1e-4
+    S0 = (np.random.default_rng(12).standard_normal((1, 4, 128, 128)) * 0.05).astype(np.float32).astype(np.float64)
+    gpu = run_gpu(ds, x, state_in=S0)
+    ref = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, x.frame_len, S0=S0)
     eo, es = _check_all(gpu, ref, ds)
-    print(f"varlen T_total={x.T_total}: o {eo:.2e} S {es:.2e}")
-
-
-def test_stack_layer_chained_calls_one_group(ds):
-    """One layer of the stack workload at full length (T = 262144, frames of
-    1024) run the way the stack runs it: 256 calls of 1024 tokens with the fp32
-    state carried between calls (ping-pong buffers), one GQA group; against a
-    single oracle pass over the whole stream."""
-    x = synth.workload_inputs("stack", H_k=1, H_v=2)
-    T, C = x.T_total, 1024
-    q, k, v = dev_bf16(x.q), dev_bf16(x.k), dev_bf16(x.v)
-    g, beta = dev_f32(x.g), dev_f32(x.beta)
-    S = torch.zeros((1, 2, 128, 128), dtype=torch.float32, device=DEV)
-    S2 = torch.empty_like(S)
-    o = torch.empty((T, 2, 128), dtype=torch.float32, device=DEV)
-    parts = torch.empty((T // C, 2, 2), dtype=torch.float32, device=DEV)
-    ws = None
-    for c in range(T // C):
-        sl = slice(c * C, (c + 1) * C)
-        r = ds.gdn_chunk_fwd(q[sl], k[sl], v[sl], g[sl], beta[sl], [C], C, state_in=S, state_out=S2, o=o[sl],
-                             workspace=ws)
-        ws = r["workspace"]
-        parts[c] = r["drift_partials"][0]
-        S, S2 = S2, S
-    torch.cuda.synchronize()
-    ref = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, C)
-    eo = rel_fro(o.cpu().numpy().astype(np.float64), ref["o"])
-    es = rel_fro(S.cpu().numpy().astype(np.float64), ref["S"])
-    assert eo <= TOL_O and es <= TOL_O, (eo, es)
-    ph = oracle.drift_scores(parts.cpu().numpy().astype(np.float64)[None], oracle.PER_HEAD)
-    rh = oracle.drift_scores(ref["partials"][None], oracle.PER_HEAD)
-    assert drift_rel_err(ph, rh) <= TOL_DRIFT
-    print(f"stack layer, 256 chained calls: o {eo:.2e} S {es:.2e}")
+    assert np.linalg.norm(ref["S"]) > 5 * np.linalg.norm(S0)   # the state grew: writes were kept
+    print(f"near-unity decay, 10 frames: o {eo:.2e} S {es:.2e}")
 
 
 def test_write_signal_parity(ds):

@@ -5,11 +5,17 @@ save/restore.
 
 Parity: after every chunk the GPU chunk score matches the oracle's (fp64
 recurrence per layer chained over the chunks, Eq. 3 over the layers) within
-1e-3; the cache (positions, chunk ids, K/V rows) equals the oracle selection
-replayed on the GPU's own scores, bit for bit; the final states match within
-2e-3.  Save/restore: a stream that answers a question in the middle (extra
-tokens and decode steps) and restores afterwards ends bit-identical to one
-that never stopped."""
+1e-3; every layer's output o of every chunk and the final states match within
+2e-3; the cache (positions, chunk ids, K/V rows) equals the oracle selection
+replayed on the GPU's own scores, bit for bit.  Both cache forms (rows
+compacted in place, slot-indexed) are checked, eager and as a replayed HIP
+graph, on a small shape and on the benchmark's streamed shape.
+
+Save/restore: a stream that answers a question in the middle (extra tokens
+and decode steps) and restores afterwards ends bit-identical to one that
+never stopped."""
+import math
+
 import numpy as np
 import pytest
 import torch
@@ -53,17 +59,32 @@ def kv_rows(pos0, T):
     return k, v
 
 
-def new_stream():
+def new_stream(indexed=False, o_dtype=torch.bfloat16):
     from paper_2609_27470_amd.streaming import DeltaSStream
-    return DeltaSStream(L, H_K, H_V, D, KV_L, ROW, M, 132, 128, N_SINK, N_WIN, N_BKT, device=DEV)
+    return DeltaSStream(L, H_K, H_V, D, KV_L, ROW, M, 132, 128, N_SINK, N_WIN, N_BKT, device=DEV, indexed=indexed,
+                        o_dtype=o_dtype)
 
 
-def test_stream_matches_oracle_replay(ds):
+class Fro:
+    def __init__(self):
+        self.num = self.den = 0.0
+
+    def add(self, got, ref):
+        self.num += float(np.sum((np.asarray(got, np.float64) - ref) ** 2))
+        self.den += float(np.sum(np.asarray(ref, np.float64) ** 2))
+
+    def err(self):
+        return math.sqrt(self.num / self.den)
+
+
+@pytest.mark.parametrize("indexed", [False, True])
+def test_stream_matches_oracle_replay(ds, indexed):
     lens = chunk_lengths(24)
     xs = layer_streams(sum(lens))
-    s = new_stream()
+    s = new_stream(indexed, o_dtype=torch.float32)
     S_ref = [np.zeros((1, H_V, D, D)) for _ in range(L)]
     ref_pos, ref_chunk = np.zeros(0, np.int64), np.zeros(0, np.int64)
+    fo = Fro()
     off = 0
     for c, T in enumerate(lens):
         k_rows, v_rows = kv_rows(off, T)
@@ -74,6 +95,9 @@ def test_stream_matches_oracle_replay(ds):
                                    x.beta[off:off + T], np.array([0, T], np.int32), 0, S0=S_ref[l])
             S_ref[l] = r["S"]
             parts.append(r["partials"])
+            got = s.o[l, :T].cpu().numpy()
+            assert rel_fro(got, r["o"]) <= 2e-3, (c, l)
+            fo.add(got, r["o"])
         ref_score = oracle.drift_scores(np.stack(parts), oracle.LAYER_FROB)
         gpu_scores = s.scores[:c + 1].cpu().numpy()
         assert drift_rel_err(gpu_scores[c:c + 1], ref_score) <= 1e-3, (c, gpu_scores[c], ref_score)
@@ -88,11 +112,15 @@ def test_stream_matches_oracle_replay(ds):
         assert np.array_equal(s.pos[:n].cpu().numpy(), ref_pos)
         assert np.array_equal(s.chunk_id[:n].cpu().numpy(), ref_chunk)
     ep = torch.as_tensor(ref_pos, device=DEV)
+    kl, vl = s.logical_rows()
     for l in range(KV_L):
-        assert torch.equal(s.k[l, :n], synth.kv_row_bits_torch(l, 0, ep, ROW))
-        assert torch.equal(s.v[l, :n], synth.kv_row_bits_torch(l, 1, ep, ROW))
+        assert torch.equal(kl[l], synth.kv_row_bits_torch(l, 0, ep, ROW))
+        assert torch.equal(vl[l], synth.kv_row_bits_torch(l, 1, ep, ROW))
     for l in range(L):
         assert rel_fro(s.state[l].cpu().numpy(), S_ref[l]) <= 2e-3
+    assert fo.err() <= 2e-3
+    s.check()
+    print(f"streamed o over {len(lens)} chunks x {L} layers: {fo.err():.2e}")
 
 
 def test_question_save_restore_is_transparent(ds):
@@ -168,7 +196,7 @@ def test_indexed_stream_matches_gather_stream(ds):
     from paper_2609_27470_amd.streaming import DeltaSStream
     lens = chunk_lengths(14, seed=6)
     xs = layer_streams(sum(lens) + 64, seed_cfg=100)
-    a = new_stream()
+    a = new_stream(indexed=False)
     b = DeltaSStream(L, H_K, H_V, D, KV_L, ROW, M, 132, 128, N_SINK, N_WIN, N_BKT, device=DEV, indexed=True)
     off = 0
     snap = None
@@ -193,3 +221,94 @@ def test_indexed_stream_matches_gather_stream(ds):
         kb, vb = b.logical_rows()
         assert torch.equal(ka, kb) and torch.equal(va, vb), c
         off += T
+
+
+# ---------------------------------------------------------------------------
+# the benchmark's streamed shape: 24 linear-attention layers of 16 qk / 32 v
+# heads (d = 128), 8 full-attention layers of 8 KV heads x 256, budget 16384,
+# the paper's policy, starting from a full cache of 128 earlier chunks
+BL, BH_K, BH_V, BD = 24, 16, 32, 128
+BKV_L, BROW, BM = 8, 8 * 256, 16384
+PRE_CHUNK = 128
+
+
+def _bench_kv_rows(pos0, T):
+    p = torch.arange(pos0, pos0 + T, dtype=torch.int64, device=DEV)
+    return (torch.stack([synth.kv_row_bits_torch(l, 0, p, BROW) for l in range(BKV_L)]),
+            torch.stack([synth.kv_row_bits_torch(l, 1, p, BROW) for l in range(BKV_L)]))
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("mode", ["eager_gather", "graph_indexed"])
+def test_stream_bench_shape(ds, mode):
+    """Six chunks of 118-132 tokens through the benchmark's streamed shape,
+    from a cache pre-filled with 16384 tokens (128 chunks with given scores):
+    every chunk's score, every layer's o (fp32) and the final states against
+    the oracle chained per layer; every eviction against the oracle selection
+    replayed on the GPU's scores; the cached rows at the end against the rows
+    of the kept positions."""
+    from paper_2609_27470_amd.streaming import DeltaSStream
+    lens = chunk_lengths(6, seed=21)
+    total = sum(lens)
+    xs = [synth.make_gdn_inputs([total], BH_K, BH_V, BD, 128, True, config=96, layer=l) for l in range(BL)]
+    indexed = mode.endswith("indexed")
+    s = DeltaSStream(BL, BH_K, BH_V, BD, BKV_L, BROW, BM, 132, BM // PRE_CHUNK + 16, 4, 1024, 4, device=DEV,
+                     indexed=indexed, o_dtype=torch.float32)
+    pre_scores = torch.rand(BM // PRE_CHUNK, generator=torch.Generator().manual_seed(5)).to(DEV)
+    pk, pv = _bench_kv_rows(0, BM)
+    s.k[:, :BM].copy_(pk)
+    s.v[:, :BM].copy_(pv)
+    del pk, pv
+    s.pos[:BM] = torch.arange(BM, dtype=torch.int32, device=DEV)
+    s.chunk_id[:BM] = torch.arange(BM, dtype=torch.int32, device=DEV) // PRE_CHUNK
+    s.scores[:BM // PRE_CHUNK] = pre_scores
+    s.length, s.n_chunks, s.next_pos = BM, BM // PRE_CHUNK, BM
+    if indexed:
+        s.slot[:BM] = torch.arange(BM, dtype=torch.int32, device=DEV)
+        s.free = torch.arange(BM, s.capacity, dtype=torch.int32, device=DEV)
+    if mode.startswith("graph"):
+        s.capture_graph()
+    ref_pos = np.arange(BM)
+    ref_chunk = np.arange(BM) // PRE_CHUNK
+    S_ref = [np.zeros((1, BH_V, BD, BD)) for _ in range(BL)]
+    fo = Fro()
+    off = 0
+    for c, T in enumerate(lens):
+        k_rows, v_rows = _bench_kv_rows(BM + off, T)
+        ins = [(dev_bf16(x.q[off:off + T]), dev_bf16(x.k[off:off + T]), dev_bf16(x.v[off:off + T]),
+                dev_f32(x.g[off:off + T]), dev_f32(x.beta[off:off + T])) for x in xs]
+        if mode.startswith("graph"):
+            for i, buf in enumerate(s.inputs):
+                for l in range(BL):
+                    buf[l, :T].copy_(ins[l][i])
+            s.step_inputs(T, k_rows, v_rows)
+        else:
+            s.step(ins, k_rows, v_rows)
+        parts = []
+        for l, x in enumerate(xs):
+            r = oracle.gdn_forward(x.q[off:off + T], x.k[off:off + T], x.v[off:off + T], x.g[off:off + T],
+                                   x.beta[off:off + T], np.array([0, T], np.int32), 0, S0=S_ref[l])
+            S_ref[l] = r["S"]
+            parts.append(r["partials"])
+            fo.add(s.o[l, :T].cpu().numpy(), r["o"])
+        ref_score = oracle.drift_scores(np.stack(parts), oracle.LAYER_FROB)
+        gpu_scores = s.scores[:s.n_chunks].cpu().numpy()
+        assert drift_rel_err(gpu_scores[-1:], ref_score) <= 1e-3, (c, gpu_scores[-1], ref_score)
+        ref_pos = np.concatenate([ref_pos, np.arange(BM + off, BM + off + T)])
+        ref_chunk = np.concatenate([ref_chunk, np.full(T, BM // PRE_CHUNK + c)])
+        keep = oracle.select_keep(ref_chunk, ref_pos, gpu_scores, len(ref_pos), BM, 4, 1024, 4)
+        ref_pos, ref_chunk = ref_pos[keep], ref_chunk[keep]
+        off += T
+        n = s.length
+        assert n == len(ref_pos) == BM
+        assert np.array_equal(s.pos[:n].cpu().numpy(), ref_pos), c
+        assert np.array_equal(s.chunk_id[:n].cpu().numpy(), ref_chunk), c
+    assert fo.err() <= 2e-3, fo.err()
+    for l in range(BL):
+        assert rel_fro(s.state[l].cpu().numpy(), S_ref[l]) <= 2e-3, l
+    kl, vl = s.logical_rows()
+    ep = torch.as_tensor(ref_pos, device=DEV)
+    for l in range(BKV_L):
+        assert torch.equal(kl[l], synth.kv_row_bits_torch(l, 0, ep, BROW)), l
+        assert torch.equal(vl[l], synth.kv_row_bits_torch(l, 1, ep, BROW)), l
+    print(f"bench streamed shape ({mode}): o {fo.err():.2e} over {len(lens)} chunks x {BL} layers")
