@@ -302,6 +302,33 @@ ds_status kv_evict_topk_indexed(int32_t capacity, int32_t *pos, int32_t *chunk_i
                                 int32_t *free_out, int32_t *new_len, void *workspace,
                                 size_t workspace_bytes, void *stream);
 
+/* ------------------------------------------------------------------------
+ * kv_evict_topk_indexed_noalloc -- kv_evict_topk_indexed without a workspace
+ * ------------------------------------------------------------------------
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The same
+ * eviction step as kv_evict_topk_indexed (same arguments, same results, bit
+ * for bit), with its scratch in a fixed device array of the library instead
+ * of a workspace: 4 MiB per GPU, set up on the first call that evicts on that
+ * GPU and held until the process ends.  The call allocates nothing and
+ * calls no allocating routine.
+ *   capacity  at most DS_KV_NOALLOC_MAX_CAPACITY slots; a larger capacity is
+ *             rejected with DS_E_UNSUPPORTED before anything runs;
+ *   outcome   device int32 [1] (4-byte aligned) or NULL: receives the
+ *             outcome word of the call (0 ok, 1 cache invariants broken,
+ *             2 keep count wrong; see ds_kv_device_status) when the call
+ *             evicts.
+ * Every call on one GPU shares that GPU's array: calls that overlap in time
+ * on one GPU (two streams, two host threads) race and must be serialised by
+ * the caller.  The array keeps the last call's contents; nothing in it has
+ * to start at zero (each call writes every entry it reads).
+ */
+#define DS_KV_NOALLOC_MAX_CAPACITY 65536
+ds_status kv_evict_topk_indexed_noalloc(int32_t capacity, int32_t *pos, int32_t *chunk_id, int32_t *slot,
+                                        const float *chunk_scores, int32_t num_chunks, int32_t len, int32_t M,
+                                        int32_t n_sink, int32_t n_window, int32_t n_buckets, int32_t *keep_out,
+                                        int32_t *free_out, int32_t *outcome, int32_t *new_len, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

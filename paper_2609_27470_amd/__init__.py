@@ -23,8 +23,9 @@ EXPORTED = [
     "ds_status_string", "ds_last_error", "ds_gdn_workspace_bytes", "ds_gdn_write_workspace_bytes",
     "gdn_chunk_fwd", "deltas_drift",
     "deltas_drift_states", "ds_kv_workspace_bytes", "kv_evict_topk", "ds_kv_device_status",
-    "ds_kv_indexed_workspace_bytes", "kv_evict_topk_indexed", "gdn_decode_step",
+    "ds_kv_indexed_workspace_bytes", "kv_evict_topk_indexed", "gdn_decode_step", "kv_evict_topk_indexed_noalloc",
 ]
+NOALLOC_MAX_CAPACITY = 65536
 
 
 class GdnShape(ctypes.Structure):
@@ -82,6 +83,9 @@ def lib():
         L.kv_evict_topk_indexed.argtypes = [I32, P, P, P, P, I32, I32, I32, I32, I32, I32, P, P,
                                             ctypes.POINTER(I32), P, SZ, P]
         L.kv_evict_topk_indexed.restype = I32
+        L.kv_evict_topk_indexed_noalloc.argtypes = [I32, P, P, P, P, I32, I32, I32, I32, I32, I32, P, P, P,
+                                                    ctypes.POINTER(I32), P]
+        L.kv_evict_topk_indexed_noalloc.restype = I32
         _lib = L
     return _lib
 
@@ -279,6 +283,29 @@ def kv_evict_topk_indexed(pos, chunk_id, slot, chunk_scores, length, M, n_sink, 
                                        int(n_buckets), _ptr(keep_out), _ptr(free_out), ctypes.byref(new_len),
                                        _ptr(workspace), workspace.numel(), _stream(stream)))
     return int(new_len.value), workspace, free_out
+
+
+def kv_evict_topk_indexed_noalloc(pos, chunk_id, slot, chunk_scores, length, M, n_sink, n_window, n_buckets,
+                                  keep_out=None, free_out=None, outcome=None, stream=None):
+    """kv_evict_topk_indexed with the library's fixed scratch instead of a
+    workspace (see kv_evict_topk_indexed_noalloc in deltas.h); every output
+    buffer is the caller's.  Returns new_len."""
+    capacity = slot.numel()
+    for t in (pos, chunk_id, slot):
+        if t.dtype != torch.int32 or t.numel() != capacity:
+            raise ValueError("pos, chunk_id and slot must be int32 tensors of the same length")
+    if int(length) > int(M) and (free_out is None or free_out.numel() < int(length) - int(M)):
+        raise ValueError(f"free_out must hold {int(length) - int(M)} entries")
+    if keep_out is not None and keep_out.numel() < int(M):
+        raise ValueError(f"keep_out holds {keep_out.numel()} entries, {int(M)} needed")
+    if outcome is not None and (outcome.dtype != torch.int32 or outcome.numel() < 1):
+        raise ValueError("outcome must be an int32 tensor of at least one element")
+    new_len = ctypes.c_int32(0)
+    _check(lib().kv_evict_topk_indexed_noalloc(capacity, _ptr(pos), _ptr(chunk_id), _ptr(slot), _ptr(chunk_scores),
+                                               int(chunk_scores.numel()), int(length), int(M), int(n_sink),
+                                               int(n_window), int(n_buckets), _ptr(keep_out), _ptr(free_out),
+                                               _ptr(outcome), ctypes.byref(new_len), _stream(stream)))
+    return int(new_len.value)
 
 
 def kv_device_status(workspace):

@@ -273,6 +273,7 @@ ds_status kv_evict_topk(const ds_kv_shape *shape, void *const *k_layers, void *c
     p.keep_out = keep_out;
     p.slot = nullptr;
     p.free_out = nullptr;
+    p.outcome_out = nullptr;
     p.ws = (char *)workspace;
     p.lay = lay;
     hipError_t e = ds::launch_kv_evict(p, (hipStream_t)stream);
@@ -286,13 +287,22 @@ size_t ds_kv_indexed_workspace_bytes(int32_t capacity) {
     return ds::kv_workspace_layout(0, 16, capacity).total;
 }
 
-ds_status kv_evict_topk_indexed(int32_t capacity, int32_t *pos, int32_t *chunk_id, int32_t *slot,
-                                const float *chunk_scores, int32_t num_chunks, int32_t len, int32_t M, int32_t n_sink,
-                                int32_t n_window, int32_t n_buckets, int32_t *keep_out, int32_t *free_out,
-                                int32_t *new_len, void *workspace, size_t workspace_bytes, void *stream) {
-    g_last_error[0] = 0;
+}  // extern "C"
+
+namespace {
+
+// Checks and launch shared by kv_evict_topk_indexed and its variant without a
+// workspace: ws / ws_bytes is the scratch (caller's workspace or the
+// library's own array), outcome a device copy of the outcome word or NULL.
+ds_status evict_indexed(const char *who, int32_t capacity, int32_t *pos, int32_t *chunk_id, int32_t *slot,
+                        const float *chunk_scores, int32_t num_chunks, int32_t len, int32_t M, int32_t n_sink,
+                        int32_t n_window, int32_t n_buckets, int32_t *keep_out, int32_t *free_out, int32_t *outcome,
+                        int32_t *new_len, char *ws, size_t ws_bytes, bool own_scratch, void *stream) {
     if (!new_len) return fail(DS_E_NULL, "new_len is required");
     if (capacity < 1) return fail(DS_E_SHAPE, "capacity=%d", capacity);
+    if (own_scratch && capacity > ds::KV_NOALLOC_MAX_CAPACITY)
+        return fail(DS_E_UNSUPPORTED, "capacity=%d exceeds the %d slots the library's fixed scratch holds", capacity,
+                    ds::KV_NOALLOC_MAX_CAPACITY);
     if (len < 0 || len > capacity) return fail(DS_E_SHAPE, "len=%d outside [0, capacity=%d]", len, capacity);
     if (M < 0 || n_sink < 0 || n_window < 0 || (long long)n_sink + n_window > M)
         return fail(DS_E_ARG, "need 0 <= n_sink, 0 <= n_window, n_sink + n_window <= M (got %d, %d, %d)", n_sink,
@@ -305,12 +315,18 @@ ds_status kv_evict_topk_indexed(int32_t capacity, int32_t *pos, int32_t *chunk_i
     }
     if (!pos || !chunk_id || !slot || !chunk_scores || !free_out)
         return fail(DS_E_NULL, "pos, chunk_id, slot, chunk_scores and free_out are required");
-    const void *ptrs[] = {pos, chunk_id, slot, chunk_scores, keep_out, free_out, workspace};
+    const void *ptrs[] = {pos, chunk_id, slot, chunk_scores, keep_out, free_out, ws};
     for (const void *q : ptrs)
         if (misaligned(q)) return fail(DS_E_ALIGN, "a pointer is not 16-byte aligned");
+    if (outcome && (((uintptr_t)outcome) & 3u)) return fail(DS_E_ALIGN, "outcome is not 4-byte aligned");
+    if (own_scratch) {  // every host check passed: the library's array on the current device
+        hipError_t e = ds::kv_noalloc_scratch(&ws);
+        if (e != hipSuccess) return hip_fail(e, "scratch address");
+        ws_bytes = ds::KV_NOALLOC_SCRATCH_BYTES;
+    }
     const ds::KvWorkspace lay = ds::kv_workspace_layout(0, 16, capacity);
-    if (!workspace || workspace_bytes < lay.total)
-        return fail(DS_E_WORKSPACE, "workspace needs %zu bytes, got %zu", lay.total, workspace_bytes);
+    if (!ws || ws_bytes < lay.total)
+        return fail(DS_E_WORKSPACE, "workspace needs %zu bytes, got %zu", lay.total, ws_bytes);
     ds::KvLaunch p{};
     p.n_planes = 0;
     p.row_bytes = 16;
@@ -327,12 +343,37 @@ ds_status kv_evict_topk_indexed(int32_t capacity, int32_t *pos, int32_t *chunk_i
     p.keep_out = keep_out;
     p.slot = slot;
     p.free_out = free_out;
-    p.ws = (char *)workspace;
+    p.outcome_out = outcome;
+    p.ws = ws;
     p.lay = lay;
     hipError_t e = ds::launch_kv_evict(p, (hipStream_t)stream);
-    if (e != hipSuccess) return hip_fail(e, "kv_evict_topk_indexed launch");
+    if (e != hipSuccess) return hip_fail(e, who);
     *new_len = M;
     return DS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ds_status kv_evict_topk_indexed(int32_t capacity, int32_t *pos, int32_t *chunk_id, int32_t *slot,
+                                const float *chunk_scores, int32_t num_chunks, int32_t len, int32_t M, int32_t n_sink,
+                                int32_t n_window, int32_t n_buckets, int32_t *keep_out, int32_t *free_out,
+                                int32_t *new_len, void *workspace, size_t workspace_bytes, void *stream) {
+    g_last_error[0] = 0;
+    return evict_indexed("kv_evict_topk_indexed launch", capacity, pos, chunk_id, slot, chunk_scores, num_chunks,
+                         len, M, n_sink, n_window, n_buckets, keep_out, free_out, nullptr, new_len, (char *)workspace,
+                         workspace_bytes, false, stream);
+}
+
+ds_status kv_evict_topk_indexed_noalloc(int32_t capacity, int32_t *pos, int32_t *chunk_id, int32_t *slot,
+                                        const float *chunk_scores, int32_t num_chunks, int32_t len, int32_t M,
+                                        int32_t n_sink, int32_t n_window, int32_t n_buckets, int32_t *keep_out,
+                                        int32_t *free_out, int32_t *outcome, int32_t *new_len, void *stream) {
+    g_last_error[0] = 0;
+    return evict_indexed("kv_evict_topk_indexed_noalloc launch", capacity, pos, chunk_id, slot, chunk_scores,
+                         num_chunks, len, M, n_sink, n_window, n_buckets, keep_out, free_out, outcome, new_len,
+                         nullptr, 0, true, stream);
 }
 
 }  // extern "C"

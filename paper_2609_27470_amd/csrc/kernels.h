@@ -81,9 +81,18 @@ struct KvLaunch {
     int num_chunks, len, M, n_sink, n_window, n_buckets;
     int32_t *keep_out;
     int32_t *slot, *free_out;  // indexed variant (slot != NULL): no K/V planes, no gather
+    int32_t *outcome_out;      // indexed variant: device copy of the outcome word, or NULL
     char *ws;
     KvWorkspace lay;
 };
 hipError_t launch_kv_evict(const KvLaunch &p, hipStream_t stream);
+
+// The library's own scratch for the indexed eviction without a workspace: a
+// fixed device array per GPU (4 MiB) and the largest capacity whose layout
+// fits in it.  kv_noalloc_scratch returns the array's address on the current
+// device (looked up once per device).
+constexpr size_t KV_NOALLOC_SCRATCH_BYTES = 4u << 20;
+constexpr int KV_NOALLOC_MAX_CAPACITY = 65536;
+hipError_t kv_noalloc_scratch(char **out);
 
 }  // namespace ds

@@ -33,6 +33,7 @@
 // with no waits at all (a block only reads at or above its own start, and
 // the blocks run in order).
 #include <algorithm>
+#include <mutex>
 
 #include "common.h"
 #include "kernels.h"
@@ -70,6 +71,7 @@ struct KvArgs {
     int32_t *keep_out;
     int32_t *slot;      // indexed variant: physical row of each logical token (NULL: gather variant)
     int32_t *free_out;  // indexed variant: physical rows of the evicted tokens
+    int32_t *outcome_out;  // indexed variant: a copy of status[0] for the caller (or NULL)
     char **plane_tab;  // device copy of the plane pointers, read by the gather
     char *planes[KV_MAX_PLANES];
     int n_planes;
@@ -278,6 +280,7 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
         if (tid == 0) {
             a.status[0] = 1;
             a.status[1] = 1;
+            if (a.outcome_out) *a.outcome_out = 1;
         }
         return;
     }
@@ -584,10 +587,12 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     if (tid == 0) {
         a.status[3] = first_move;
         a.status[4] = split;
-        if (total_kept != a.M) {  // cannot happen for valid arguments; never move data then
+        const bool count_ok = total_kept == a.M;
+        if (!count_ok) {  // cannot happen for valid arguments; never move data then
             a.status[0] = 2;
             a.status[1] = 1;
         }
+        if (a.outcome_out) *a.outcome_out = count_ok ? 0 : 2;
     }
     {
         // flags of the moving destinations back to zero, 16 bytes per store
@@ -862,6 +867,31 @@ static int gather_kpr(int row_bytes) {
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Scratch of the indexed eviction for callers that cannot allocate: one copy
+// per GPU, held until the process ends.  Host code never passes the array's
+// name to a kernel (on the host it is a stand-in, not a device address); it
+// passes the address hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) char scratch[KV_NOALLOC_SCRATCH_BYTES];
+
+hipError_t kv_noalloc_scratch(char **out) {
+    constexpr int MAX_DEV = 64;
+    static std::mutex mu;
+    static char *addr[MAX_DEV] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= MAX_DEV) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = (char *)p;
+    }
+    *out = addr[dev];
+    return hipSuccess;
+}
+
 KvWorkspace kv_workspace_layout(int n_layers, int row_bytes, int capacity) {
     KvWorkspace w{};
     const int ppg = GATHER_U / gather_kpr(row_bytes);
@@ -939,6 +969,7 @@ hipError_t launch_kv_evict(const KvLaunch &p, hipStream_t stream) {
     a.keep_out = p.keep_out;
     a.slot = p.slot;
     a.free_out = p.free_out;
+    a.outcome_out = p.outcome_out;
     a.plane_tab = (char **)(ws + p.lay.offPlanes);
     for (int i = 0; i < KV_MAX_PLANES; ++i) a.planes[i] = i < p.n_planes ? p.planes[i] : nullptr;
     a.n_planes = p.n_planes;

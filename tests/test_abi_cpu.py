@@ -189,3 +189,23 @@ def test_streaming_session_validates_on_host(ds):
     bad = [(torch.zeros((140, 2, 64), dtype=torch.bfloat16),) * 5] * 2
     with pytest.raises(ValueError):
         s.step(bad, None, None)                       # chunk longer than max_chunk
+
+
+def test_noalloc_eviction_host_checks(ds):
+    """kv_evict_topk_indexed_noalloc: capacities beyond its fixed scratch are
+    refused before anything runs; a call that does not evict touches nothing;
+    the indexed workspace of the largest accepted capacity fits the 4 MiB
+    scratch."""
+    L = ds.lib()
+    n = ctypes.c_int32(-1)
+    P = ctypes.c_void_p
+    cap = ds.NOALLOC_MAX_CAPACITY
+    assert L.kv_evict_topk_indexed_noalloc(cap + 1, None, None, None, None, 1, 10, 5, 0, 0, 1, None, None, None,
+                                           ctypes.byref(n), None) == 5
+    assert b"fixed scratch" in L.ds_last_error()
+    assert L.kv_evict_topk_indexed_noalloc(cap, None, None, None, None, 1, 100, 200, 0, 0, 1, None, None, None,
+                                           ctypes.byref(n), None) == 0
+    assert n.value == 100
+    assert L.kv_evict_topk_indexed_noalloc(cap, None, None, None, None, 1, 300, 200, 0, 0, 1, None, None, None,
+                                           None, None) == 1
+    assert L.ds_kv_indexed_workspace_bytes(cap) <= 4 << 20
