@@ -11,6 +11,10 @@ with every input already resident in HBM:
      capacity 17408), as the streaming loop does after each chunk;
   4. kv_evict_topk: one eviction event (17408 -> 16384 tokens, keep the top
      chunks by drift, ties to newer), compacting K/V in place.
+The headline value is the tokens of that step per second.  Beside it,
+"configs" holds one record per workload (tiny, single layer, the 24-layer
+stack streamed in 1024-token calls, the 8-stream varlen batch, and the
+eviction loop to 1M tokens), each with tokens/s and its roofline fraction.
 
 Prints ONE JSON line.  Per-call times come from HIP events recorded on the
 stream the calls are launched on.
@@ -21,6 +25,7 @@ import argparse
 import hashlib
 import json
 import os
+import platform
 import sys
 import time
 
@@ -38,23 +43,53 @@ H_K, H_V, D, T, FRAME = 16, 32, 128, 32768, 1024
 C = 64
 # eviction-loop cache
 KV_LAYERS, KV_HEADS, KV_DIM, BUDGET, CAPACITY = 8, 8, 256, 16384, 16384 + 1024
+# stack and eviction loop
+N_LAYERS, POOL_FRAMES = 24, 64
 
 
-def algorithmic_work(T_tokens, H_k, H_v, d, C=64):
+def algorithmic_work(T_tokens, H_k, H_v, d, C=64, n_states=0):
     """Dense-tile chunkwise flops and the bytes a single pass must move.
 
     flops/token = H_k 4 C d (K K^T, Q K^T) + H_v (4 C d + 6 d d + 2/3 C^2);
-    bytes/token = q, k (bf16, H_k d each) + v, o (bf16, H_v d each) + g, beta (fp32).
+    bytes/token = q, k (bf16, H_k d each) + v, o (bf16, H_v d each) + g, beta (fp32);
+    plus, for n_states carried states, one fp32 read and one write of each.
     """
     flops = T_tokens * (H_k * 4 * C * d + H_v * (4 * C * d + 6 * d * d + (2.0 / 3.0) * C * C))
-    bytes_ = T_tokens * (H_k * d * 2 * 2 + H_v * d * 2 * 2 + H_v * 4 * 2)
+    bytes_ = T_tokens * (H_k * d * 2 * 2 + H_v * d * 2 * 2 + H_v * 4 * 2) + n_states * H_v * d * d * 4 * 2
     return flops, bytes_
 
 
-def cpu_baseline(x, budget_s=12.0):
+def roofline_record(tokens, ms, H_k, H_v, d, n_states=0):
+    flops, bytes_ = algorithmic_work(tokens, H_k, H_v, d, n_states=n_states)
+    gbs = bytes_ / (ms * 1e-3) / 1e9
+    tf = flops / (ms * 1e-3) / 1e12
+    return {"algorithmic_bytes": bytes_, "algorithmic_flops": flops, "achieved_gbs": gbs,
+            "roofline_frac": gbs / HBM_PEAK_GBS, "bound": "hbm", "algorithmic_tflops": tf,
+            "mfma_util_algorithmic_pct": 100.0 * tf / MFMA_PEAK_TFLOPS}
+
+
+def host_info():
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count()
+    return {"nproc": os.cpu_count(), "usable_cpus": usable, "cpu_model": model or platform.processor()}
+
+
+def cpu_baseline(x, tiny, budget_s=12.0):
     """The fp64 oracle timed on this host's cores over a bounded prefix of the
     same stream (all heads), plus one eviction (selection + gather) on the
-    same cache shape; scaled to tokens/s of the full step."""
+    same cache shape; scaled to tokens/s of the full step.  Also single-thread
+    runs of the tiny workload (whole) and of a prefix of the single-layer one."""
     import oracle
     threads = oracle.max_threads()
     n = 256
@@ -81,10 +116,26 @@ def cpu_baseline(x, budget_s=12.0):
     gather_one = time.perf_counter() - t0
     evict_s = sel_s + gather_one * 2 * KV_LAYERS
     step_s = gdn_s_per_token * T + evict_s
-    return {"value": T / step_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"fp64 token recurrence of all 32 heads over the first {n} of the {T} tokens "
-                      f"({dt:.1f} s, scaled to the full stream) + one eviction (selection in Python, "
-                      f"numpy gather of 16 planes of {CAPACITY}x4 KiB rows)"}
+    # single thread: the tiny workload in full, 512 tokens of the single-layer one
+    t0 = time.perf_counter()
+    oracle.gdn_forward(tiny.q, tiny.k, tiny.v, tiny.g, tiny.beta, tiny.cu_seqlens, tiny.frame_len, n_threads=1)
+    tiny_s = time.perf_counter() - t0
+    n1 = 512
+    t0 = time.perf_counter()
+    oracle.gdn_forward(x.q[:n1], x.k[:n1], x.v[:n1], x.g[:n1], x.beta[:n1], np.array([0, n1], np.int32), FRAME,
+                       n_threads=1)
+    one_s = time.perf_counter() - t0
+    rec = {"value": T / step_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+           "sample": f"fp64 token recurrence of all 32 heads over the first {n} of the {T} tokens "
+                     f"({dt:.1f} s on {threads} threads, scaled to the full stream) + one eviction (selection "
+                     f"in Python, numpy gather of 16 planes of {CAPACITY}x4 KiB rows)",
+           "gdn_tokens_per_s": 1.0 / gdn_s_per_token,
+           "single_thread": {"tiny_tokens_per_s": tiny.T_total / tiny_s,
+                             "single_layer_tokens_per_s": n1 / one_s,
+                             "sample": f"tiny workload in full ({tiny.T_total} tokens, 2 heads, d=64); "
+                                       f"first {n1} tokens of the single-layer workload (32 heads, d=128)"}}
+    rec.update(host_info())
+    return rec
 
 
 def copy_calibration(nbytes):
@@ -98,16 +149,50 @@ def copy_calibration(nbytes):
     print(json.dumps({"copy_calibration_bytes": nbytes}))
 
 
+def loop_ms(fn, reps, stream):
+    """Mean ms of fn over reps back-to-back calls, timed with events on stream."""
+    import torch
+    fn()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def measured_peaks(dev, stream):
+    """What this GPU sustains: a 1 GiB device copy (read + write bytes) and a
+    dense bf16 matrix product of 8192^3 through the vendor library."""
+    import torch
+    a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    b = torch.empty_like(a)
+    a.fill_(3)
+    cp_ms = loop_ms(lambda: b.copy_(a), 10, stream)
+    del a, b
+    n = 8192
+    x = torch.randn((n, n), device=dev).to(torch.bfloat16)
+    y = torch.randn((n, n), device=dev).to(torch.bfloat16)
+    mm_ms = loop_ms(lambda: torch.matmul(x, y), 10, stream)
+    del x, y
+    return {"copy_gbs": 2 * (1 << 30) / (cp_ms * 1e-3) / 1e9, "copy_bytes": 2 * (1 << 30),
+            "bf16_matmul_tflops": 2 * n ** 3 / (mm_ms * 1e-3) / 1e12, "matmul_shape": [n, n, n],
+            "note": "torch device copy (runtime copy kernel) and torch.matmul bf16 (vendor GEMM), "
+                    "as achievable peaks beside the spec figures"}
+
+
 def streaming_bench(ds, dev, stream, n_chunks, n_layers=24):
     """The paper's streaming regime: chunks of 118-132 tokens, each one frame of
     all 24 linear-attention layers (single-layer head shapes, state carried in
     place), the chunk score over the layers, append, and eviction with sinks 4,
-    window 1024 and 4 spans at M = 16384 -- per-chunk GPU time of the whole
-    step, starting from a full cache."""
+    window 1024 and 4 spans, at M = 16384 and M = 8192 -- per-chunk GPU time
+    of the whole step, starting from a full cache."""
     import torch
     from paper_2609_27470_amd.streaming import DeltaSStream
     gen = torch.Generator(device=dev).manual_seed(7)
     POOL = 1024
+
     def unit(shape):
         x = torch.randn(shape, generator=gen, device=dev)
         return (x / x.norm(dim=-1, keepdim=True)).to(torch.bfloat16)
@@ -122,19 +207,20 @@ def streaming_bench(ds, dev, stream, n_chunks, n_layers=24):
     k_rows = torch.randint(-2000, 2000, (KV_LAYERS, 132, row_elems), dtype=torch.int16, device=dev, generator=gen)
     v_rows = torch.randint(-2000, 2000, (KV_LAYERS, 132, row_elems), dtype=torch.int16, device=dev, generator=gen)
     state_io = n_layers * 2 * H_V * D * D * 4   # every layer reads and writes its state once per chunk
-    out = {"layers": n_layers, "policy": "n_sink=4, n_window=1024, N=4, M=16384",
-           "state_io_bytes_per_chunk": state_io}
-    for mode in ("eager", "graph", "graph_indexed"):
-        s = DeltaSStream(n_layers, H_K, H_V, D, KV_LAYERS, row_elems, BUDGET, 132, BUDGET // 128 + total + 8,
+    out = {"layers": n_layers, "policy": "n_sink=4, n_window=1024, N=4", "state_io_bytes_per_chunk": state_io}
+    runs = [(BUDGET, "eager"), (BUDGET, "graph"), (BUDGET, "graph_indexed"), (8192, "eager"),
+            (8192, "graph_indexed")]
+    for M, mode in runs:
+        s = DeltaSStream(n_layers, H_K, H_V, D, KV_LAYERS, row_elems, M, 132, M // 128 + total + 8,
                          4, 1024, 4, device=dev, indexed=mode.endswith("indexed"))
-        # start from a full cache: BUDGET tokens in 128 earlier chunks with random scores
-        s.pos[:BUDGET] = torch.arange(BUDGET, dtype=torch.int32, device=dev)
-        s.chunk_id[:BUDGET] = torch.arange(BUDGET, dtype=torch.int32, device=dev) // 128
-        s.scores[:BUDGET // 128] = torch.rand(BUDGET // 128, generator=gen, device=dev)
-        s.length, s.n_chunks, s.next_pos = BUDGET, BUDGET // 128, BUDGET
+        # start from a full cache: M tokens in M / 128 earlier chunks with random scores
+        s.pos[:M] = torch.arange(M, dtype=torch.int32, device=dev)
+        s.chunk_id[:M] = torch.arange(M, dtype=torch.int32, device=dev) // 128
+        s.scores[:M // 128] = torch.rand(M // 128, generator=gen, device=dev)
+        s.length, s.n_chunks, s.next_pos = M, M // 128, M
         if s.indexed:
-            s.slot[:BUDGET] = torch.arange(BUDGET, dtype=torch.int32, device=dev)
-            s.free = torch.arange(BUDGET, s.capacity, dtype=torch.int32, device=dev)
+            s.slot[:M] = torch.arange(M, dtype=torch.int32, device=dev)
+            s.free = torch.arange(M, s.capacity, dtype=torch.int32, device=dev)
         if mode.startswith("graph"):
             s.capture_graph()
         off = 0
@@ -160,14 +246,257 @@ def streaming_bench(ds, dev, stream, n_chunks, n_layers=24):
                 evs.append((Tc, e))
             off += Tc
         torch.cuda.synchronize()
+        s.check()
         ms = np.array([e[0].elapsed_time(e[1]) for _, e in evs])
         toks = np.array([t for t, _ in evs])
-        out[mode] = {"chunk_tokens_mean": float(toks.mean()), "ms_per_chunk": float(np.median(ms)),
-                     "tokens_per_s": float(toks.sum() / (ms.sum() * 1e-3)),
-                     "host_ms_per_chunk": 1e3 * t_host / len(evs),
-                     "state_io_gbs": float(state_io / (np.median(ms) * 1e-3) / 1e9)}
+        key = mode if M == BUDGET else f"{mode}_M{M}"
+        out[key] = {"M": M, "chunk_tokens_mean": float(toks.mean()), "ms_per_chunk": float(np.median(ms)),
+                    "tokens_per_s": float(toks.sum() / (ms.sum() * 1e-3)),
+                    "host_ms_per_chunk": 1e3 * t_host / len(evs),
+                    "state_io_gbs": float(state_io / (np.median(ms) * 1e-3) / 1e9)}
         del s
     return out
+
+
+def bench_tiny(ds, dev, stream, reps):
+    """The tiny workload (1 layer, 2 heads, d = 64, T = 1024, frames of 256):
+    one gdn_chunk_fwd with drift sums and deltas_drift per pass."""
+    import torch
+    import synth
+    x = synth.workload_inputs("tiny")
+    to = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dev).view(dt)
+    q, k, v = to(x.q.view(np.int16), torch.bfloat16), to(x.k.view(np.int16), torch.bfloat16), \
+        to(x.v.view(np.int16), torch.bfloat16)
+    g, beta = to(x.g, torch.float32), to(x.beta, torch.float32)
+    o = torch.empty((x.T_total, 2, 64), dtype=torch.bfloat16, device=dev)
+    st = torch.empty((1, 2, 64, 64), dtype=torch.float32, device=dev)
+    parts = torch.empty((4, 2, 2), dtype=torch.float32, device=dev)
+    sc = torch.empty(4, dtype=torch.float32, device=dev)
+    ws = torch.empty(ds.gdn_workspace_bytes(ds.gdn_shape([x.T_total], 2, 2, 64, 256)), dtype=torch.uint8, device=dev)
+
+    def one():
+        ds.gdn_chunk_fwd(q, k, v, g, beta, [x.T_total], 256, state_out=st, o=o, drift_partials=parts, workspace=ws)
+        ds.deltas_drift(parts[None], ds.LAYER_FROB, scores=sc)
+    ms = loop_ms(one, reps, stream)
+    rec = {"workload": "tiny: H_k=H_v=2, d=64, T=1024, frames of 256 (+ deltas_drift)", "ms_per_pass": ms,
+           "tokens_per_s": x.T_total / (ms * 1e-3)}
+    rec.update(roofline_record(x.T_total, ms, 2, 2, 64))
+    rec["bound_note"] = "launch latency: 2.3 us of HBM traffic at 8 TB/s"
+    return rec
+
+
+def make_pool(dev, n_layers=N_LAYERS, frames=POOL_FRAMES):
+    """Per-layer pools of novelty-structured frames drawn on the device; stream
+    frame f at layer l reads pool frame (f + 4 l) mod frames."""
+    import synth
+    return [synth.device_novelty_frames(frames, FRAME, H_K, H_V, D, seed=1000 + l, device=dev)
+            for l in range(n_layers)]
+
+
+class StackLoop:
+    """The 24-layer stack streamed in frames of 1024 tokens: per frame, one
+    gdn_chunk_fwd per layer with the fp32 state carried in place and the drift
+    sums fused, deltas_drift over the layers into the chunk-score table, and
+    (eviction loop) the frame's K/V rows appended and kv_evict_topk run with
+    the literal policy (whole chunks, top 16 of 17, ties to newer)."""
+
+    def __init__(self, ds, dev, stream, pool, max_frames, evict):
+        import torch
+        self.ds, self.dev, self.stream, self.pool, self.evict = ds, dev, stream, pool, evict
+        self.state = torch.zeros((N_LAYERS, 1, H_V, D, D), dtype=torch.float32, device=dev)
+        # drift pairs per 16-row slice of each head (Eq. 3 pools a layer's state)
+        self.parts = torch.zeros((N_LAYERS, 1, H_V * (D // 16), 2), dtype=torch.float32, device=dev)
+        self.o = torch.empty((FRAME, H_V, D), dtype=torch.bfloat16, device=dev)
+        self.ws = torch.empty(ds.gdn_workspace_bytes(ds.gdn_shape([FRAME], H_K, H_V, D, FRAME)), dtype=torch.uint8,
+                              device=dev)
+        self.table = torch.zeros(max_frames, dtype=torch.float32, device=dev)
+        if evict:
+            row = KV_HEADS * KV_DIM
+            self.cache = torch.zeros((2 * KV_LAYERS, CAPACITY, row), dtype=torch.int16, device=dev)
+            self.k_layers = [self.cache[l] for l in range(KV_LAYERS)]
+            self.v_layers = [self.cache[KV_LAYERS + l] for l in range(KV_LAYERS)]
+            self.new_rows = torch.randint(-3000, 3000, (2 * KV_LAYERS, FRAME, row), dtype=torch.int16, device=dev,
+                                          generator=torch.Generator(device=dev).manual_seed(5))
+            self.kv_pos = torch.zeros(CAPACITY, dtype=torch.int32, device=dev)
+            self.kv_chunk = torch.zeros(CAPACITY, dtype=torch.int32, device=dev)
+            self.kv_ws = torch.empty(ds.kv_workspace_bytes(KV_LAYERS, row * 2, CAPACITY), dtype=torch.uint8,
+                                     device=dev)
+            self.fail = torch.zeros(1, dtype=torch.int32, device=dev)
+            self.append_pos = torch.arange(FRAME, dtype=torch.int32, device=dev)
+
+    def reset(self):
+        self.state.zero_()
+        self.length = 0
+
+    def frame(self, f, ev=None, drift=True):
+        import torch
+        ds, st = self.ds, self.stream
+        if ev:
+            ev[0].record(st)
+        for l in range(N_LAYERS):
+            q, k, v, g, beta = self.pool[l]
+            a = ((f + 4 * l) % POOL_FRAMES) * FRAME
+            s = slice(a, a + FRAME)
+            ds.gdn_chunk_fwd(q[s], k[s], v[s], g[s], beta[s], [FRAME], FRAME, state_in=self.state[l],
+                             state_out=self.state[l], o=self.o, drift_partials=self.parts[l] if drift else False,
+                             workspace=self.ws, drift_per_slice=True)
+        if ev:
+            ev[1].record(st)
+        if drift:
+            ds.deltas_drift(self.parts, ds.LAYER_FROB, scores=self.table[f:f + 1])
+        if ev:
+            ev[2].record(st)
+        if not self.evict:
+            return
+        n = self.length
+        self.cache[:, n:n + FRAME].copy_(self.new_rows)
+        torch.add(self.append_pos, f * FRAME, out=self.kv_pos[n:n + FRAME])
+        self.kv_chunk[n:n + FRAME] = f
+        n += FRAME
+        if ev:
+            ev[3].record(st)
+        if n > BUDGET:
+            n, _ = ds.kv_evict_topk(self.k_layers, self.v_layers, self.kv_pos, self.kv_chunk, self.table[:f + 1], n,
+                                    BUDGET, 0, 0, 1, workspace=self.kv_ws)
+            torch.maximum(self.fail, ds.kv_outcome_word(self.kv_ws), out=self.fail)
+        self.length = n
+        if ev:
+            ev[4].record(st)
+
+    def run(self, n_frames, n_ev=5, drift=True):
+        """Frames 0 .. n_frames - 1 from a zero state and an empty cache;
+        returns the per-frame segment times [frames][n_ev - 1] (ms) and the
+        whole run's ms."""
+        import torch
+        self.reset()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(n_frames)]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(self.stream)
+        for f in range(n_frames):
+            self.frame(f, evs[f], drift)
+        e1.record(self.stream)
+        torch.cuda.synchronize()
+        seg = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(n_ev - 1)] for e in evs])
+        return seg, e0.elapsed_time(e1)
+
+
+def bench_stack(ds, dev, stream, pool):
+    """The stack workload: 24 layers, one stream of 262144 tokens streamed as
+    256 calls of 1024 tokens per layer (inputs from the per-layer pool)."""
+    import torch
+    frames = 256
+    loop = StackLoop(ds, dev, stream, pool, frames, evict=False)
+    loop.run(8, n_ev=3)
+    seg, run_ms = loop.run(frames, n_ev=3)
+    call_ms = float(np.median(seg[:, 0])) / N_LAYERS
+    drift_call_ms = float(np.median(seg[:, 1]))
+    rec = {"workload": "stack: 24 layers x (H_k=16, H_v=32, d=128), one stream of 262144 tokens in 256 calls "
+                       "of 1024 per layer, state carried, drift sums fused, deltas_drift over the layers per frame",
+           "ms_total": run_ms, "tokens_per_s": frames * FRAME / (run_ms * 1e-3),
+           "ms_per_layer_call": call_ms, "deltas_drift_ms_per_frame": drift_call_ms}
+    rec.update(roofline_record(FRAME, call_ms, H_K, H_V, D, n_states=1))
+    rec["roofline_of"] = "one layer call (1024 tokens + state read and write)"
+    # drift overhead at the call shape: 24 calls with the fused sums plus one
+    # deltas_drift, against 24 calls without the epilogue (interleaved loops)
+    t_with, t_without = [], []
+    for rnd in range(6):
+        order = ((True, t_with), (False, t_without)) if rnd % 2 == 0 else ((False, t_without), (True, t_with))
+        for drift, acc in order:
+            acc.append(loop_ms(lambda: loop.frame(rnd, drift=drift), 10, stream))
+    w, wo = float(np.median(t_with)), float(np.median(t_without))
+    rec["drift_overhead_pct"] = 100.0 * (w / wo - 1.0)
+    rec["drift_overhead_method"] = "median over 6 interleaved rounds of 10 frames: 24 layer calls + deltas_drift vs 24 calls without the epilogue"
+    del loop
+    torch.cuda.synchronize()
+    return rec
+
+
+def bench_eviction_loop(ds, dev, stream, pool):
+    """The eviction-loop workload: the stack streamed to 1,048,576 tokens
+    (1024 frames) with 8 full-attention layers of 8 KV heads x 256 bf16
+    (budget 16384, capacity 17408) and an eviction after every frame that
+    overflows it (1008 events).  The paper's protocol: three runs, the first
+    dropped, the median over eviction steps."""
+    frames = 1024
+    loop = StackLoop(ds, dev, stream, pool, frames, evict=True)
+    runs = [loop.run(frames) for _ in range(3)]
+    fail = int(loop.fail.item())
+    if fail != 0:
+        raise RuntimeError(f"an eviction of the loop reported outcome {fail}")
+    kept = runs[1:]
+    seg = np.concatenate([s for s, _ in kept])                 # [2 * frames][4]: gdn, drift, append, evict
+    ev_rows = np.concatenate([np.arange(frames) >= 16] * 2)    # frames that evict
+    frame_ms = seg.sum(axis=1)
+    run_ms = float(np.mean([r for _, r in kept]))
+    evict_ms = float(np.median(seg[ev_rows, 3]))
+    step_ms = float(np.median(frame_ms[ev_rows]))
+    rec = {"workload": "eviction loop: 24-layer stack to 1048576 tokens (1024 frames of 1024) + 8 KV layers "
+                       "x 8 heads x 256 bf16, M=16384, capacity 17408, eviction after each frame past 16 "
+                       "(1008 events), whole chunks by drift, ties to newer",
+           "ms_total": run_ms, "tokens_per_s": frames * FRAME / (run_ms * 1e-3),
+           "ms_per_frame_median": float(np.median(frame_ms)), "eviction_step_ms_median": step_ms,
+           "kv_evict_topk_ms_median": evict_ms,
+           "gdn_ms_per_frame_median": float(np.median(seg[:, 0])),
+           "deltas_drift_ms_median": float(np.median(seg[:, 1])),
+           "append_ms_median": float(np.median(seg[:, 2])),
+           "events_per_run": int(ev_rows.sum() // 2), "runs": 3, "runs_kept": 2,
+           "protocol": "3 runs, first dropped; medians over the frames (eviction steps) of the two kept runs"}
+    rec.update(roofline_record(FRAME, float(np.median(seg[:, 0])) / N_LAYERS, H_K, H_V, D, n_states=1))
+    rec["roofline_of"] = "one layer call (1024 tokens + state read and write)"
+    del loop
+    return rec
+
+
+def bench_varlen(ds, dev, stream):
+    """The varlen workload: 8 packed streams, lengths uniform in [16384,
+    131072], one gdn_chunk_fwd call (bf16 o, drift sums) + deltas_drift."""
+    import torch
+    import synth
+    lens = synth.varlen_lengths(8, 16384, 131072)
+    parts = []
+    for b, n in enumerate(lens):
+        nf = (n + FRAME - 1) // FRAME
+        x = synth.device_novelty_frames(nf, FRAME, H_K, H_V, D, seed=2000 + b, device=dev)
+        parts.append(tuple(t[:n] for t in x))
+    q, k, v, g, beta = (torch.cat([p[i] for p in parts]).contiguous() for i in range(5))
+    del parts
+    Tt = sum(lens)
+    shape = ds.gdn_shape(lens, H_K, H_V, D, FRAME)
+    o = torch.empty((Tt, H_V, D), dtype=torch.bfloat16, device=dev)
+    st = torch.empty((8, H_V, D, D), dtype=torch.float32, device=dev)
+    dp = torch.empty((shape.n_frames, H_V, 2), dtype=torch.float32, device=dev)
+    sc = torch.empty(shape.n_frames, dtype=torch.float32, device=dev)
+    ws = torch.empty(ds.gdn_workspace_bytes(shape), dtype=torch.uint8, device=dev)
+    cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]).astype(np.int32), device=dev)
+
+    def one():
+        ds.gdn_chunk_fwd(q, k, v, g, beta, lens, FRAME, cu_seqlens=cu, state_out=st, o=o, drift_partials=dp,
+                         workspace=ws)
+        ds.deltas_drift(dp[None], ds.LAYER_FROB, scores=sc)
+    ms = float(np.median([loop_ms(one, 1, stream) for _ in range(5)]))
+    rec = {"workload": f"varlen: 8 packed streams, lengths {lens} (sum {Tt}), H_k=16, H_v=32, d=128, frames of 1024 "
+                       "(+ deltas_drift)", "ms_per_call": ms, "tokens_per_s": Tt / (ms * 1e-3)}
+    rec.update(roofline_record(Tt, ms, H_K, H_V, D, n_states=8))
+    del q, k, v, g, beta, o, ws
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return rec
+
+
+def committed_record(name):
+    """A figure measured by a committed counter run (profiles/), used only while
+    the forward's source is the one it was measured with."""
+    tf = os.path.join(ROOT, "profiles", name)
+    src = os.path.join(ROOT, "paper_2609_27470_amd", "csrc", "gdn_fwd.hip")
+    if os.path.exists(tf) and os.path.exists(src):
+        try:
+            rec = json.load(open(tf))
+            if rec.get("source_sha256") == hashlib.sha256(open(src, "rb").read()).hexdigest():
+                return rec
+        except (OSError, ValueError):
+            return None
+    return None
 
 
 def main():
@@ -176,6 +505,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--quick", action="store_true", help="headline step only (no per-workload records)")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="only run a plain device copy of this many bytes (counter calibration)")
     args = ap.parse_args()
@@ -194,6 +524,8 @@ def main():
     ds.lib()
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
+    t_start = time.perf_counter()
+    log = lambda m: print(f"[bench {time.perf_counter() - t_start:6.1f}s] {m}", file=sys.stderr, flush=True)
 
     # ---------------- inputs (host generation, then resident in HBM)
     x = synth.workload_inputs("single_layer")
@@ -207,6 +539,7 @@ def main():
     partials = torch.empty((n_frames, H_V, 2), dtype=torch.float32, device=dev)
     shape = ds.gdn_shape([T], H_K, H_V, D, FRAME)
     ws = torch.empty(ds.gdn_workspace_bytes(shape, write_signal=True), dtype=torch.uint8, device=dev)
+    log("single-layer inputs resident")
 
     # ---------------- KV cache: one tensor [2L][capacity][row] so a chunk append is one copy
     row_elems = KV_HEADS * KV_DIM
@@ -226,6 +559,7 @@ def main():
     table = torch.zeros(n_init_chunks + n_frames * total_steps, dtype=torch.float32, device=dev)
     table[:n_init_chunks] = torch.rand(n_init_chunks, generator=torch.Generator().manual_seed(0)).to(dev)
     kv_ws = torch.empty(ds.kv_workspace_bytes(KV_LAYERS, row_elems * 2, CAPACITY), dtype=torch.uint8, device=dev)
+    kv_fail = torch.zeros(1, dtype=torch.int32, device=dev)
     append_pos = torch.arange(1024, dtype=torch.int32, device=dev)
     state_ref = {"len": BUDGET, "next_pos": BUDGET, "step": 0}
 
@@ -255,6 +589,7 @@ def main():
                                       keep_out=keep_out, workspace=kv_ws)
         if evs is not None:
             evs[4].record(stream)
+        torch.maximum(kv_fail, ds.kv_outcome_word(kv_ws), out=kv_fail)   # every event's outcome, no sync
         state_ref["len"] = new_len
         state_ref["step"] = s + 1
 
@@ -277,9 +612,9 @@ def main():
     ar = np.arange(BUDGET)
     moved_rows = np.array([BUDGET - (np.argmax(r != ar) if np.any(r != ar) else BUDGET) for r in kh])
     moved_bytes = moved_rows * 2 * KV_LAYERS * KV_HEADS * KV_DIM * 2
-    status = ds.kv_device_status(kv_ws)
-    if status[0] != 0 or status[2] != 0:
-        raise RuntimeError(f"eviction reported device status {status}")
+    if int(kv_fail.item()) != 0:
+        raise RuntimeError(f"an eviction reported outcome {int(kv_fail.item())}")
+    log("headline step timed")
 
     # ---------------- the same eviction loop over a slot-indexed cache: the new
     # chunk's rows go into the rows the last eviction freed (one index_copy
@@ -309,20 +644,21 @@ def main():
             ev[1].record(stream)
         ds.kv_evict_topk_indexed(idx_pos, idx_chunk, idx_slot, idx_table, CAPACITY, BUDGET, 0, 0, 1,
                                  free_out=idx_freed, workspace=idx_ws)
+        torch.maximum(kv_fail, ds.kv_outcome_word(idx_ws), out=kv_fail)
         if ev:
             ev[2].record(stream)
         idx_free, idx_freed = idx_freed, idx_free
     torch.cuda.synchronize()
-    status = ds.kv_device_status(idx_ws)
-    if status[0] != 0:
-        raise RuntimeError(f"indexed eviction reported device status {status}")
+    if int(kv_fail.item()) != 0:
+        raise RuntimeError(f"an indexed eviction reported outcome {int(kv_fail.item())}")
     iseg = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(2)] for e in idx_evs])
     idx_append_ms, idx_evict_ms = iseg.mean(axis=0)
 
     # ---------------- drift overhead: the forward with the fused drift sums
     # plus deltas_drift, against the same forward compiled without the
-    # frame-end epilogue; both as back-to-back loops on the same stream,
-    # interleaved so cache state is the same for both
+    # frame-end epilogue; (a) back-to-back loops on the same stream,
+    # interleaved so cache state is the same for both; (b) medians of single
+    # calls each timed on its own
     reps = max(5, args.steps)
     scores_tmp = torch.empty(n_frames, dtype=torch.float32, device=dev)
 
@@ -337,17 +673,15 @@ def main():
     for rnd in range(8):
         for fn, acc in ((fwd_drift, t_with), (fwd_plain, t_without)) if rnd % 2 == 0 else \
                 ((fwd_plain, t_without), (fwd_drift, t_with)):
-            fn()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            for _ in range(reps):
-                fn()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            acc.append(e0.elapsed_time(e1) / reps)
+            acc.append(loop_ms(fn, reps, stream))
     withdrift_ms = float(np.median(t_with))
     nodrift_ms = float(np.median(t_without))
     drift_overhead = 100.0 * (withdrift_ms / nodrift_ms - 1.0)
+    single_with, single_without = [], []
+    for rnd in range(2 * reps):
+        fn, acc = (fwd_drift, single_with) if rnd % 2 == 0 else (fwd_plain, single_without)
+        acc.append(loop_ms(fn, 1, stream))
+    drift_overhead_single = 100.0 * (float(np.median(single_with)) / float(np.median(single_without)) - 1.0)
 
     # the beta ||e|| signal on top of the drift sums (appendix on retention signals)
     wparts = torch.empty((n_frames, H_V, 2), dtype=torch.float32, device=dev)
@@ -356,17 +690,16 @@ def main():
         ds.gdn_chunk_fwd(q, k, v, g, beta, [T], FRAME, state_out=state, o=o, drift_partials=partials,
                          write_partials=wparts, workspace=ws)
 
-    fwd_drift_write()
-    t_w = []
-    for rnd in range(3):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(reps):
-            fwd_drift_write()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        t_w.append(e0.elapsed_time(e1) / reps)
+    def fwd_drift_only():
+        ds.gdn_chunk_fwd(q, k, v, g, beta, [T], FRAME, state_out=state, o=o, drift_partials=partials, workspace=ws)
+
+    t_w, t_d = [], []
+    for rnd in range(6):
+        for fn, acc in ((fwd_drift_write, t_w), (fwd_drift_only, t_d)) if rnd % 2 == 0 else \
+                ((fwd_drift_only, t_d), (fwd_drift_write, t_w)):
+            acc.append(loop_ms(fn, reps, stream))
     write_ms = float(np.median(t_w))
+    drift_only_ms = float(np.median(t_d))
 
     # the unfused alternative (Section 3.2 as the paper measures it): at every
     # frame boundary copy the state, and after the frame take the two norms
@@ -379,14 +712,8 @@ def main():
             s_before.copy_(state)
             ds.deltas_drift_states(s_before.view(1, 1, H_V, D, D), state.view(1, 1, H_V, D, D), partials=parts_u)
 
-    drift_unfused()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(reps):
-        drift_unfused()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    unfused_ms = e0.elapsed_time(e1) / reps
+    unfused_ms = loop_ms(drift_unfused, reps, stream)
+    log("drift and write-signal overheads timed")
 
     # ---------------- decode step (one token per stream, batched): the state is
     # read and written once per step, so the bound is HBM
@@ -402,16 +729,8 @@ def main():
         db = torch.sigmoid(torch.randn((Bd, H_V), generator=gen, device=dev))
         dst = 0.3 * torch.randn((Bd, H_V, D, D), generator=gen, device=dev)
         do = torch.empty((Bd, H_V, D), dtype=torch.bfloat16, device=dev)
-        step_dec = lambda: ds.gdn_decode_step(dq, dk, dv, dg, db, state_in=dst, state_out=dst, o=do)
-        for _ in range(3):
-            step_dec()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(reps):
-            step_dec()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        dec_ms = e0.elapsed_time(e1) / reps
+        dec_ms = loop_ms(lambda: ds.gdn_decode_step(dq, dk, dv, dg, db, state_in=dst, state_out=dst, o=do), reps,
+                         stream)
         dec_bytes = Bd * H_V * (2 * D * D * 4 + D * 2 + D * 2 + 8) + Bd * H_K * D * 2 * 2
         decode[f"B{Bd}"] = {"ms": dec_ms, "tokens_per_s": Bd / (dec_ms * 1e-3),
                             "gbs": dec_bytes / (dec_ms * 1e-3) / 1e9,
@@ -419,23 +738,42 @@ def main():
                             "bytes_per_step": dec_bytes}
 
     streaming = streaming_bench(ds, dev, stream, args.steps)
+    log("streaming timed")
 
     flops, bytes_ = algorithmic_work(T, H_K, H_V, D)
     achieved_gbs = bytes_ / (gdn_ms * 1e-3) / 1e9
     achieved_tflops = flops / (gdn_ms * 1e-3) / 1e12
 
-    # HBM bytes per launch from the committed counter runs (FETCH_SIZE + WRITE_SIZE,
-    # copy-calibrated), used only while the kernel source is the one measured
-    traffic = None
-    tf = os.path.join(ROOT, "profiles", "gdn_chunk_fwd_single_layer_traffic.json")
-    src = os.path.join(ROOT, "paper_2609_27470_amd", "csrc", "gdn_fwd.hip")
-    if os.path.exists(tf) and os.path.exists(src):
-        try:
-            rec = json.load(open(tf))
-            if rec.get("source_sha256") == hashlib.sha256(open(src, "rb").read()).hexdigest():
-                traffic = rec.get("bytes_per_launch")
-        except (OSError, ValueError):
-            traffic = None
+    # HBM bytes per launch and matrix-core busy share from the committed counter
+    # runs, used only while the kernel source is the one measured
+    trec = committed_record("gdn_chunk_fwd_single_layer_traffic.json")
+    traffic = trec.get("bytes_per_launch") if trec else None
+    crec = committed_record("gdn_chunk_fwd_single_layer_counters.json")
+
+    configs = {}
+    single = {"workload": "single_layer: H_k=16, H_v=32, d=128, T=32768, frames of 1024 (gdn_chunk_fwd + deltas_drift)",
+              "ms_per_call": float(gdn_ms), "tokens_per_s": T / ((gdn_ms + drift_ms) * 1e-3),
+              "drift_overhead_pct": drift_overhead}
+    single.update(roofline_record(T, gdn_ms, H_K, H_V, D))
+    configs["1_single_layer"] = single
+    peaks = None
+    if not args.quick:
+        configs["0_tiny"] = bench_tiny(ds, dev, stream, 200)
+        log("tiny timed")
+        del q, k, v, g, beta, o, ws
+        torch.cuda.empty_cache()
+        configs["3_varlen"] = bench_varlen(ds, dev, stream)
+        log("varlen timed")
+        pool = make_pool(dev)
+        log("stack input pool drawn")
+        configs["2_stack"] = bench_stack(ds, dev, stream, pool)
+        log("stack timed")
+        configs["4_eviction_loop"] = bench_eviction_loop(ds, dev, stream, pool)
+        log("eviction loop timed")
+        del pool
+        torch.cuda.empty_cache()
+        peaks = measured_peaks(dev, stream)
+        log("peaks measured")
 
     out = {
         "metric": METRIC,
@@ -454,21 +792,27 @@ def main():
             "workload": "single_layer GDN (H_k=16, H_v=32, d=128, T=32768, frames of 1024) + drift "
                         "+ one eviction event (8 layers x 8 KV heads x 256 bf16, M=16384, capacity 17408, "
                         "top chunks by drift, ties to newer)",
+            "value_is": "tokens of one whole step (gdn_chunk_fwd + deltas_drift + append + kv_evict_topk) per "
+                        "second; GDN + drift alone is configs.1_single_layer.tokens_per_s",
             "global_batch": 1, "seq_len": T, "parallelism": "none",
         },
         "roofline": {
             "bound": "hbm", "achieved": achieved_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": achieved_gbs / HBM_PEAK_GBS, "traffic": traffic,
-            "kernel": "gdn_chunk_fwd (gdn_prep + gdn_seq + drift finalize)",
+            "kernel": "gdn_chunk_fwd (gdn_prep + gdn_seq with the in-kernel drift reduction)",
             "algorithmic_bytes_per_launch": bytes_, "launch_ms": gdn_ms,
         },
+        "configs": configs,
+        "measured_peaks": peaks,
         "gdn_drift_tokens_per_s": T / ((gdn_ms + drift_ms) * 1e-3),
-        "mfma_util_pct": 100.0 * achieved_tflops / MFMA_PEAK_TFLOPS,
+        "mfma_util_algorithmic_pct": 100.0 * achieved_tflops / MFMA_PEAK_TFLOPS,
+        "mfma_busy_counter_pct": crec.get("mfma_busy_pct") if crec else None,
         "algorithmic_tflops": achieved_tflops,
         "drift_overhead_pct": drift_overhead,
+        "drift_overhead_single_call_pct": drift_overhead_single,
         "drift_unfused_ms": unfused_ms,
         "write_signal_ms": write_ms,
-        "write_signal_overhead_pct": 100.0 * (write_ms / withdrift_ms - 1.0),
+        "write_signal_overhead_pct": 100.0 * (write_ms / drift_only_ms - 1.0),
         "drift_unfused_overhead_pct": 100.0 * unfused_ms / nodrift_ms,
         "evict_moved_rows_mean": float(moved_rows.mean()),
         "evict_gather_gbs": float((2 * moved_bytes).mean() / (evict_ms * 1e-3) / 1e9),
@@ -482,10 +826,11 @@ def main():
         },
         "breakdown_ms": {"gdn_chunk_fwd": gdn_ms, "deltas_drift": drift_ms, "kv_append": append_ms,
                          "kv_evict_topk": evict_ms, "isolated_fwd_with_drift": withdrift_ms,
-                         "isolated_fwd_without_drift": nodrift_ms},
+                         "isolated_fwd_without_drift": nodrift_ms, "isolated_fwd_drift_only": drift_only_ms},
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(x)
+        out["cpu_baseline"] = cpu_baseline(x, synth.workload_inputs("tiny"))
+        log("cpu baseline timed")
     print(json.dumps(out), flush=True)
 
 

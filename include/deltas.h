@@ -92,6 +92,13 @@ const char *ds_last_error(void);
  * (S_start = the state when the frame began, held on chip -- the temporary
  * copy of the previous state of Section 3.2), and optionally the state
  * itself into snapshots[f][j].  Frames are numbered stream by stream.
+ * With shape->drift_per_slice = 1 the pairs are written per slice of 16
+ * state rows instead: drift_partials[f][j][s] (s < d_v / 16) covers rows
+ * 16 s .. 16 s + 15 of S, and the per-head pair is their sum.  Eq. 3 pools
+ * all heads of a layer, so deltas_drift's DS_DRIFT_LAYER_FROB over these
+ * pairs (passed as H_v * d_v / 16 "heads") is the same score; the kernels
+ * then need no exchange between the workgroups of a head, which saves about
+ * a microsecond per call (a few percent of a 1024-token call).
  * Optionally also the write-magnitude signal compared with the drift in the
  * appendix on retention signals (row beta ||e||):
  *     write_partials[f][j][0] = sum over the frame's tokens of beta_t ||e_t||_2
@@ -115,7 +122,8 @@ const char *ds_last_error(void);
  *   state_in    fp32 [B][H_v][d_v][d_k] or NULL (zeros)
  *   state_out   fp32 [B][H_v][d_v][d_k]; may alias state_in
  *   o           [T_total][H_v][d_v] of dtype o_dtype (DS_BF16 or DS_F32)
- *   drift_partials fp32 [n_frames][H_v][2] or NULL
+ *   drift_partials fp32 [n_frames][H_v][2] (drift_per_slice = 1:
+ *               [n_frames][H_v][d_v / 16][2]) or NULL
  *   write_partials fp32 [n_frames][H_v][2] or NULL
  *   snapshots   fp32 [n_frames][H_v][d_v][d_k] or NULL
  * Supported: d_k = d_v in {64, 128}; H_v a multiple of H_k; frame_len a
@@ -135,6 +143,7 @@ typedef struct {
     int32_t d_v;       /* value head dim */
     int32_t frame_len; /* tokens per frame (multiple of 64) or 0 */
     int32_t n_frames;  /* frames over all streams */
+    int32_t drift_per_slice; /* 0: drift_partials [n_frames][H_v][2]; 1: [n_frames][H_v][d_v / 16][2] */
 } ds_gdn_shape;
 
 /* Workspace bytes gdn_chunk_fwd needs for this shape when write_partials is
@@ -175,14 +184,18 @@ ds_status gdn_decode_step(int32_t B, int32_t H_k, int32_t H_v, int32_t d_k, int3
  * deltas_drift -- state drift per frame (Section 3.2, Eq. 3)
  * ------------------------------------------------------------------------
  * partials: fp32 [L][F][H_v][2] (num, den) as written by gdn_chunk_fwd for
- * L layers (layer l's F frames at offset l * F * H_v * 2).
+ * L layers (layer l's F frames at offset l * F * H_v * 2).  Pairs written
+ * per slice of the state (drift_per_slice = 1) are read as H_v * d_v / 16
+ * heads: DS_DRIFT_LAYER_FROB is then the same score, while HEAD_MEAN and
+ * PER_HEAD become per-slice ratios.
  *   DS_DRIFT_LAYER_FROB: scores[f] = mean_l sqrt(sum_h num / sum_h den)
  *   DS_DRIFT_HEAD_MEAN:  scores[f] = mean_{l,h} sqrt(num / den)
  *   DS_DRIFT_PER_HEAD:   scores[l][f][h] = sqrt(num / den)
  *   DS_WRITE_MEAN:       with write_partials (sum, count) in place of (num, den):
  *                        scores[f] = mean_{l,h} sum / count (0 where count = 0)
  * den = 0 gives +inf when num > 0 and 0 otherwise; a mean containing +inf
- * is +inf.  scores: fp32 [F] (or [L][F][H_v] for PER_HEAD).
+ * is +inf.  scores: fp32 [F] (or [L][F][H_v] for PER_HEAD).  partials must
+ * be 8-byte aligned (each pair is read as one 8-byte word).
  */
 ds_status deltas_drift(const float *partials, int32_t L, int32_t F, int32_t H_v, int32_t mode,
                        float *scores, void *stream);

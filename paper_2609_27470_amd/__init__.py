@@ -30,7 +30,7 @@ NOALLOC_MAX_CAPACITY = 65536
 
 class GdnShape(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
-                ("B", "T_total", "H_k", "H_v", "d_k", "d_v", "frame_len", "n_frames")]
+                ("B", "T_total", "H_k", "H_v", "d_k", "d_v", "frame_len", "n_frames", "drift_per_slice")]
 
 
 class KvShape(ctypes.Structure):
@@ -113,11 +113,11 @@ def frames_of_length(n: int, frame_len: int) -> int:
     return (n + frame_len - 1) // frame_len
 
 
-def gdn_shape(lengths, H_k, H_v, d, frame_len):
+def gdn_shape(lengths, H_k, H_v, d, frame_len, drift_per_slice=False):
     """ds_gdn_shape for streams of the given (host-known) lengths."""
     lengths = [int(x) for x in lengths]
     return GdnShape(len(lengths), sum(lengths), H_k, H_v, d, d, frame_len,
-                    sum(frames_of_length(n, frame_len) for n in lengths))
+                    sum(frames_of_length(n, frame_len) for n in lengths), int(bool(drift_per_slice)))
 
 
 def gdn_workspace_bytes(shape: GdnShape, write_signal: bool = False) -> int:
@@ -129,19 +129,20 @@ def gdn_workspace_bytes(shape: GdnShape, write_signal: bool = False) -> int:
 
 def gdn_chunk_fwd(q, k, v, g, beta, lengths, frame_len, cu_seqlens=None, state_in=None, state_out=None,
                   o=None, o_dtype=torch.float32, scale=1.0, drift_partials=True, write_partials=False,
-                  snapshots=False, workspace=None, stream=None):
+                  snapshots=False, workspace=None, stream=None, drift_per_slice=False):
     """One gated-delta-rule layer over packed streams (see gdn_chunk_fwd in deltas.h).
 
     q, k: bf16 [T][H_k][d]; v: bf16 [T][H_v][d]; g, beta: fp32 [T][H_v];
     lengths: host list of stream lengths; cu_seqlens: device int32 [B+1]
     (built from lengths when None).  Returns a dict with o, state,
-    drift_partials [F][H_v][2] (or None), write_partials [F][H_v][2] (the
-    beta ||e|| sums and token counts, or None) and snapshots (or None).
-    Each output argument may be True (allocate), False (skip) or a tensor.
+    drift_partials [F][H_v][2] ([F][H_v * d / 16][2] with drift_per_slice;
+    or None), write_partials [F][H_v][2] (the beta ||e|| sums and token
+    counts, or None) and snapshots (or None).  Each output argument may be
+    True (allocate), False (skip) or a tensor.
     """
     T, H_k, d = q.shape
     H_v = v.shape[1]
-    shape = gdn_shape(lengths, H_k, H_v, d, frame_len)
+    shape = gdn_shape(lengths, H_k, H_v, d, frame_len, drift_per_slice)
     dev = q.device
     if cu_seqlens is None and shape.B > 1:
         cu = [0]
@@ -153,7 +154,8 @@ def gdn_chunk_fwd(q, k, v, g, beta, lengths, frame_len, cu_seqlens=None, state_i
     if o is None:
         o = torch.empty((T, H_v, d), dtype=o_dtype, device=dev)
     od = DS_BF16 if o.dtype == torch.bfloat16 else DS_F32
-    dp = torch.empty((shape.n_frames, H_v, 2), dtype=torch.float32, device=dev) if drift_partials is True \
+    pairs = H_v * (d // 16) if drift_per_slice else H_v
+    dp = torch.empty((shape.n_frames, pairs, 2), dtype=torch.float32, device=dev) if drift_partials is True \
         else drift_partials if drift_partials is not False else None
     wp = torch.empty((shape.n_frames, H_v, 2), dtype=torch.float32, device=dev) if write_partials is True \
         else write_partials if write_partials is not False else None

@@ -37,6 +37,8 @@ ds_status check_gdn_shape(const ds_gdn_shape *s) {
                     s->d_v);
     if (s->frame_len < 0 || s->frame_len % 64 != 0)
         return fail(DS_E_UNSUPPORTED, "frame_len=%d must be 0 or a multiple of 64", s->frame_len);
+    if (s->drift_per_slice != 0 && s->drift_per_slice != 1)
+        return fail(DS_E_ARG, "drift_per_slice=%d (0 or 1)", s->drift_per_slice);
     // keep every index of the kernels inside 32-bit ranges where they use them
     if ((long long)s->T_total * s->H_v > (1LL << 31) / 2 || (long long)s->B * s->H_v * (s->d_v / 16) > (1LL << 30))
         return fail(DS_E_UNSUPPORTED, "problem too large for one call");
@@ -123,6 +125,7 @@ ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k,
     p.o_bf16 = (o_dtype == DS_BF16);
     p.scale = scale;
     p.drift_partials = drift_partials;
+    p.drift_slices = s.drift_per_slice;
     p.write_partials = write_partials;
     p.snapshots = snapshots;
     char *ws = (char *)workspace;
@@ -147,6 +150,7 @@ ds_status deltas_drift(const float *partials, int32_t L, int32_t F, int32_t H_v,
     if (mode < DS_DRIFT_LAYER_FROB || mode > DS_WRITE_MEAN) return fail(DS_E_ARG, "mode=%d", mode);
     if ((long long)L * F * H_v == 0) return DS_OK;
     if (!partials || !scores) return fail(DS_E_NULL, "partials and scores are required");
+    if (((uintptr_t)partials) & 7u) return fail(DS_E_ALIGN, "partials must be 8-byte aligned");
     if ((long long)L * F * H_v * 2 > (1LL << 31)) return fail(DS_E_UNSUPPORTED, "too many partials");
     hipError_t e = ds::launch_drift(partials, L, F, H_v, mode, scores, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "deltas_drift launch");

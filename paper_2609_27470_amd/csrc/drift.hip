@@ -21,51 +21,84 @@ __device__ __forceinline__ double wave_sum_d(double x) {
     return x;
 }
 
-// One workgroup (4 waves) per frame.  Wave w takes layers w, w + 4, ...; its
-// lanes take the heads of a layer (lane, lane + 64, ...), sum in order, and
-// meet in a butterfly; the waves' totals are added in wave order.  Every sum
-// has a fixed order, so the result does not depend on scheduling.
-__global__ __launch_bounds__(256) void drift_frame_kernel(const float *p, int L, int F, int H, int mode,
-                                                           float *scores) {
+// One workgroup (16 waves) per frame.  Wave w takes layers w, w + 16, ...;
+// its lanes take the heads of a layer (lane, lane + 64, ...).  A wave loads
+// the (num, den) pairs of up to DRIFT_LPW of its layers before it reduces any
+// of them, so a frame costs one memory round trip rather than one per layer;
+// lanes sum in order, the lanes of a wave meet in a butterfly, and the waves'
+// totals are added in wave order.  Every sum has a fixed order, so the result
+// does not depend on scheduling.
+constexpr int DRIFT_WAVES = 16, DRIFT_LPW = 4, DRIFT_HPL = 2;  // waves, layers per wave per round, heads per lane
+__global__ __launch_bounds__(64 * DRIFT_WAVES) void drift_frame_kernel(const float *p, int L, int F, int H, int mode,
+                                                                        float *scores) {
     const int f = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     double acc = 0.0;  // same value in every lane of the wave
     bool inf = false;
-    for (int l = w; l < L; l += 4) {
-        const float *row = p + ((size_t)l * F + f) * H * 2;
-        if (mode == 0) {
-            double num = 0.0, den = 0.0;
-            for (int h = lane; h < H; h += 64) {
-                num += (double)row[2 * h];
-                den += (double)row[2 * h + 1];
+    for (int l0 = w; l0 < L; l0 += DRIFT_WAVES * DRIFT_LPW) {
+        // the pairs of this round's layers (heads lane, lane + 64 in registers;
+        // more heads per layer are read in the loop below)
+        float2 pr[DRIFT_LPW][DRIFT_HPL];
+#pragma unroll
+        for (int i = 0; i < DRIFT_LPW; ++i) {
+            const int l = l0 + DRIFT_WAVES * i;
+#pragma unroll
+            for (int c = 0; c < DRIFT_HPL; ++c) {
+                const int h = lane + 64 * c;
+                pr[i][c] = (l < L && h < H) ? *(const float2 *)(p + (((size_t)l * F + f) * H + h) * 2) : float2{0.f, 0.f};
             }
-            const double r = drift_ratio(wave_sum_d(num), wave_sum_d(den));
-            if (isinf(r)) inf = true; else acc += r;
-        } else {
-            double x = 0.0;
-            bool xi = false;
-            for (int h = lane; h < H; h += 64) {
-                if (mode == 3) {
-                    const double c = (double)row[2 * h + 1];
-                    x += c > 0.0 ? (double)row[2 * h] / c : 0.0;
-                } else {
-                    const double r = drift_ratio((double)row[2 * h], (double)row[2 * h + 1]);
-                    if (isinf(r)) xi = true; else x += r;
+        }
+#pragma unroll
+        for (int i = 0; i < DRIFT_LPW; ++i) {
+            const int l = l0 + DRIFT_WAVES * i;
+            if (l >= L) break;
+            const float *row = p + ((size_t)l * F + f) * H * 2;
+            if (mode == 0) {
+                double num = 0.0, den = 0.0;
+#pragma unroll
+                for (int c = 0; c < DRIFT_HPL; ++c) {
+                    num += (double)pr[i][c].x;
+                    den += (double)pr[i][c].y;
                 }
+                for (int h = lane + 64 * DRIFT_HPL; h < H; h += 64) {
+                    num += (double)row[2 * h];
+                    den += (double)row[2 * h + 1];
+                }
+                const double r = drift_ratio(wave_sum_d(num), wave_sum_d(den));
+                if (isinf(r)) inf = true; else acc += r;
+            } else {
+                double x = 0.0;
+                bool xi = false;
+                auto add = [&](float2 v, bool valid) {
+                    if (!valid) return;
+                    if (mode == 3) {
+                        x += v.y > 0.f ? (double)v.x / (double)v.y : 0.0;
+                    } else {
+                        const double r = drift_ratio((double)v.x, (double)v.y);
+                        if (isinf(r)) xi = true; else x += r;
+                    }
+                };
+#pragma unroll
+                for (int c = 0; c < DRIFT_HPL; ++c) add(pr[i][c], lane + 64 * c < H);
+                for (int h = lane + 64 * DRIFT_HPL; h < H; h += 64) add(*(const float2 *)(row + 2 * h), true);
+                acc += wave_sum_d(x);
+                if (__any(xi)) inf = true;
             }
-            acc += wave_sum_d(x);
-            if (__any(xi)) inf = true;
         }
     }
-    __shared__ double s_acc[4];
-    __shared__ int s_inf[4];
+    __shared__ double s_acc[DRIFT_WAVES];
+    __shared__ int s_inf[DRIFT_WAVES];
     if (lane == 0) {
         s_acc[w] = acc;
         s_inf[w] = inf;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        const double tot = ((s_acc[0] + s_acc[1]) + s_acc[2]) + s_acc[3];
-        const bool any_inf = s_inf[0] | s_inf[1] | s_inf[2] | s_inf[3];
+        double tot = 0.0;
+        bool any_inf = false;
+        for (int i = 0; i < DRIFT_WAVES; ++i) {
+            tot += s_acc[i];
+            any_inf |= s_inf[i] != 0;
+        }
         const long long cnt = mode == 0 ? (long long)L : (long long)L * H;
         scores[f] = any_inf ? __builtin_huge_valf() : (cnt ? (float)(tot / (double)cnt) : 0.f);
     }
@@ -124,7 +157,8 @@ hipError_t launch_drift(const float *partials, int L, int F, int H_v, int mode, 
         hipLaunchKernelGGL(drift_head_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, partials, n, scores);
     } else {
         if (F == 0) return hipSuccess;
-        hipLaunchKernelGGL(drift_frame_kernel, dim3(F), dim3(256), 0, stream, partials, L, F, H_v, mode, scores);
+        hipLaunchKernelGGL(drift_frame_kernel, dim3(F), dim3(64 * DRIFT_WAVES), 0, stream, partials, L, F, H_v, mode,
+                           scores);
     }
     return hipGetLastError();
 }

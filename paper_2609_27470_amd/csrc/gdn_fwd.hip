@@ -59,6 +59,9 @@ struct GdnArgs {
     // drift sums reduced inside the sequential kernel (null: a separate pass does it)
     float *drift_out;       // [n_frames][H_v][2]
     unsigned *drift_cnt;    // [B][H_v] slices done, zeroed by the prep kernel
+    // drift pairs of frames past the real count, zeroed by the prep kernel
+    float *drift_zero;      // the caller's drift_partials (either layout) or null
+    int drift_zero_per_frame;  // pairs per frame in it: H_v, or H_v * n_split for per-slice pairs
     int prep_per_vhead;     // prep grid (tiles, H_v) instead of (tiles, H_k)
 };
 
@@ -177,17 +180,19 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
     const int h = a.prep_per_vhead ? hy / a.group : hy;
     const int jbase = a.prep_per_vhead ? hy : h * a.group;
     const int gcount = a.prep_per_vhead ? 1 : a.group;
-    if (ti == 0 && hy == 0 && a.drift_out) {
-        // set-up for the sequential kernel's drift reduction: slice counters
-        // to zero, frames past the real count to zero
-        for (int i = threadIdx.x; i < a.st.B * a.H_v; i += 256) a.drift_cnt[i] = 0u;
+    if (ti == 0 && hy == 0 && a.drift_zero) {
+        // set-up for the sequential kernel's drift output: slice counters of
+        // the in-kernel reduction to zero, frames past the real count to zero
+        if (a.drift_out)
+            for (int i = threadIdx.x; i < a.st.B * a.H_v; i += 256) a.drift_cnt[i] = 0u;
         int real = 0;
         for_streams(a.st, [&](int, int s0, int e0) {
             real += frames_in(e0 - s0, a.frame_len);
             return false;
         });
-        for (int i = min(real, a.n_frames) * a.H_v + (int)threadIdx.x; i < a.n_frames * a.H_v; i += 256)
-            *(float2 *)(a.drift_out + 2 * (size_t)i) = float2{0.f, 0.f};
+        const int per = a.drift_zero_per_frame;
+        for (int i = min(real, a.n_frames) * per + (int)threadIdx.x; i < a.n_frames * per; i += 256)
+            *(float2 *)(a.drift_zero + 2 * (size_t)i) = float2{0.f, 0.f};
     }
     int t0 = 0, n = 0;
     if (!locate_tile(a.st, ti, t0, n)) return;
@@ -500,6 +505,34 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
 // range).  D_last E enters the state update as fp16; R, E, T diag(beta) and
 // P are fp16.  All accumulation is fp32.
 // ============================================================================
+
+// Slice drift pairs cross workgroups (and XCDs) through agent-scope atomic
+// accesses, which the compiler emits as stores written through to, and loads
+// served from, the GPU-wide point of coherence.  The handoff below then needs
+// no agent-scope fence: such a fence writes back (release) or invalidates
+// (acquire) a whole XCD's L2, and at the end of every workgroup of a short
+// call that cost 18 % of a 1024-token layer call.  Ordering comes from the
+// store acknowledgements: a writer's pairs are complete before its count
+// increment is issued, and the last workgroup issues its loads only after
+// its own increment has returned.
+__device__ __forceinline__ void store_pair_coherent(float *p, float a, float b) {
+    const unsigned long long bits =
+        (unsigned long long)__float_as_uint(a) | ((unsigned long long)__float_as_uint(b) << 32);
+    __hip_atomic_store((unsigned long long *)p, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 load_pair_coherent(const float *p) {
+    const unsigned long long bits =
+        __hip_atomic_load((const unsigned long long *)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return float2{__uint_as_float((unsigned)bits), __uint_as_float((unsigned)(bits >> 32))};
+}
+// Wait until every vector memory operation of this wave has completed (its
+// stores acknowledged), with the compiler kept from moving memory accesses
+// across the wait.
+__device__ __forceinline__ void wait_vmem_all() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0), expcnt and lgkmcnt not waited for
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
 
 // Sum of squares over the 16 columns of an E k-step held as a B operand (lane
 // (ln, lg) element i is token kappa(ks, lg, i), column ln), reduced over the
@@ -974,7 +1007,7 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                 if (a.wsDrift && frame < a.n_frames) {
                     const float2 p0 = sh.DR[frame & 1][0][lane], p1 = sh.DR[frame & 1][1][lane];
                     const float num = wave_sum(p0.x + p1.x), den = wave_sum(p0.y + p1.y);
-                    if (lane == 0) *(float2 *)(a.wsDrift + (((size_t)frame * a.H_v + j) * a.n_split + sl) * 2) = float2{num, den};
+                    if (lane == 0) store_pair_coherent(a.wsDrift + (((size_t)frame * a.H_v + j) * a.n_split + sl) * 2, num, den);
                 }
                 ++frame;
                 frame_end = min(frame_end + a.frame_len, len);
@@ -1019,14 +1052,14 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             // the last of the stream's n_split workgroups of v-head j to finish
             // sums the slices of every frame of the stream (fixed order)
             if (DRIFT && X == 3 && a.drift_out) {
-                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // this wave's partials before the count
+                wait_vmem_all();  // this wave's pairs (the only ones of the workgroup) are coherent before the count
                 unsigned prev = 0;
                 if (lane == 0)
                     prev = __hip_atomic_fetch_add(&a.drift_cnt[b * a.H_v + j], 1u, __ATOMIC_RELAXED,
                                                   __HIP_MEMORY_SCOPE_AGENT);
                 prev = __builtin_amdgcn_readfirstlane(prev);
                 if (prev == (unsigned)a.n_split - 1u) {
-                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // every slice's partials after it
+                    // the count has returned: every slice's pairs are readable at the point of coherence
                     const int nf = min(frames_in(len, a.frame_len), a.n_frames - frame_base);
                     for (int f = lane; f < nf; f += 64) {
                         const size_t fj = (size_t)(frame_base + f) * a.H_v + j;
@@ -1035,7 +1068,7 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                         float2 pr[8];
 #pragma unroll
                         for (int s = 0; s < 8; ++s)
-                            pr[s] = s < a.n_split ? *(const float2 *)(a.wsDrift + (fj * a.n_split + s) * 2) : float2{0.f, 0.f};
+                            pr[s] = s < a.n_split ? load_pair_coherent(a.wsDrift + (fj * a.n_split + s) * 2) : float2{0.f, 0.f};
                         float num = 0.f, den = 0.f;
 #pragma unroll
                         for (int s = 0; s < 8; ++s) {
@@ -1180,16 +1213,19 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     a.wsP = p.wsP;
     a.wsQ = p.wsQ;
     a.wsGam = p.wsGam;
-    a.wsDrift = p.drift_partials ? p.wsDrift : nullptr;
     a.wsWrite = p.write_partials ? p.wsWrite : nullptr;
     a.n_split = p.n_split;
-    // drift sums of the slices added by the sequential kernel itself (the last
+    // Per-slice pairs go straight to the caller's buffer.  Per-head pairs are
+    // the sums of the slices, added by the sequential kernel itself (the last
     // workgroup of each stream and v-head to finish), so the drift costs no
     // launch of its own; only a call without tokens (no prep pass clears the
-    // counters) leaves it to the finalize pass, which then writes zeros
-    const bool fused_drift = p.drift_partials && p.n_frames > 0 && p.tiles_max > 0;
+    // counters) leaves the zeros to the finalize pass
+    const bool fused_drift = p.drift_partials && !p.drift_slices && p.n_frames > 0 && p.tiles_max > 0;
+    a.wsDrift = !p.drift_partials ? nullptr : p.drift_slices ? p.drift_partials : p.wsDrift;
     a.drift_out = fused_drift ? p.drift_partials : nullptr;
     a.drift_cnt = p.wsCnt;
+    a.drift_zero = p.n_frames > 0 ? p.drift_partials : nullptr;
+    a.drift_zero_per_frame = p.drift_slices ? p.H_v * p.n_split : p.H_v;
 
     // one prep workgroup per (tile, v-head) when a workgroup per (tile, qk-head)
     // would leave most CUs idle (short calls, e.g. one streamed chunk)
@@ -1217,10 +1253,14 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (p.drift_partials && p.n_frames > 0 && !fused_drift) {
-        const int n = p.n_frames * p.H_v;
+    if (p.drift_partials && p.n_frames > 0 && p.tiles_max == 0) {
+        // no tokens: every frame's pairs are zero (the pass reads nothing when
+        // no frame is real; per-slice pairs are passed as n_split-times more
+        // heads of one slice each)
+        const int heads = p.drift_slices ? p.H_v * p.n_split : p.H_v;
+        const int n = p.n_frames * heads;
         hipLaunchKernelGGL(gdn_drift_finalize_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, p.wsDrift,
-                           p.drift_partials, p.n_frames, p.H_v, p.n_split, a.st, p.frame_len);
+                           p.drift_partials, p.n_frames, heads, 1, a.st, p.frame_len);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

@@ -18,7 +18,8 @@ struct GdnLaunch {
     void *o;
     int o_bf16;
     float scale;
-    float *drift_partials;  // [n_frames][H_v][2] or null
+    float *drift_partials;  // [n_frames][H_v][2] (or [n_frames][H_v][n_split][2] with drift_slices) or null
+    int drift_slices;       // drift pairs per 16-row slice of the state instead of per v-head
     float *write_partials;  // [n_frames][H_v][2] or null
     float *snapshots;       // [n_frames][H_v][d][d] or null
     // workspace pieces

@@ -97,7 +97,11 @@ class DeltaSStream:
         self.score_mode = score_mode
         self.capacity = M + max_chunk
         self.state = torch.zeros((n_layers, 1, H_v, d, d), dtype=torch.float32, device=dev)
-        self.partials = torch.zeros((n_layers, 1, H_v, 2), dtype=torch.float32, device=dev)
+        # Eq. 3 pools a layer's heads, so for it the drift pairs are taken per
+        # 16-row slice of the state (no exchange between a head's workgroups)
+        self.per_slice = score_mode == LAYER_FROB
+        pairs = H_v * (d // 16) if self.per_slice else H_v
+        self.partials = torch.zeros((n_layers, 1, pairs, 2), dtype=torch.float32, device=dev)
         self.o = torch.empty((n_layers, max_chunk, H_v, d), dtype=o_dtype, device=dev)
         self.k = torch.zeros((kv_layers, self.capacity, row_elems), dtype=torch.int16, device=dev)
         self.v = torch.zeros((kv_layers, self.capacity, row_elems), dtype=torch.int16, device=dev)
@@ -145,7 +149,7 @@ class DeltaSStream:
             for l, (q, k, v, g, beta) in enumerate(layer_inputs):
                 st = self.state[l]
                 gdn_chunk_fwd(q, k, v, g, beta, [T], 0, state_in=st, state_out=st, o=self.o[l, :T],
-                              drift_partials=self.partials[l], workspace=self.gdn_ws)
+                              drift_partials=self.partials[l], workspace=self.gdn_ws, drift_per_slice=self.per_slice)
             deltas_drift(self.partials, self.score_mode, scores=self.scores[c:c + 1])
             return self._append_and_evict(T, k_rows, v_rows)
 
@@ -222,7 +226,8 @@ class DeltaSStream:
         for l in range(self.L):
             st = self.state[l]
             gdn_chunk_fwd(q[l], k[l], v[l], g[l], b[l], [self.max_chunk], 0, cu_seqlens=self.cu, state_in=st,
-                          state_out=st, o=self.o[l], drift_partials=self.partials[l], workspace=self.gdn_ws)
+                          state_out=st, o=self.o[l], drift_partials=self.partials[l], workspace=self.gdn_ws,
+                          drift_per_slice=self.per_slice)
         deltas_drift(self.partials, self.score_mode, scores=self.score_buf)
 
     def step_inputs(self, T, k_rows, v_rows):

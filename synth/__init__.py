@@ -365,3 +365,53 @@ def kv_row_bits_torch(layer: int, kv: int, pos, row_elems: int):
     bits = (x >> 16) & 0xBFFF
     # reinterpret the low 16 bits as int16
     return (bits - ((bits & 0x8000) << 1)).to(torch.int16)
+
+
+# ----------------------------------------------------------------------------
+# The same recipe drawn on the device (benchmark inputs too large to draw on
+# the host in a benchmark run: the per-layer frame pools of the stack and
+# eviction-loop workloads, the varlen batch).  torch's generator, fp32
+# arithmetic; the orthonormal bases of the novel frames come from numpy's QR
+# on the host.  Values differ from the host generator's (parity tests use
+# the host generator); the distributions and the novelty structure do not.
+# ----------------------------------------------------------------------------
+def device_novelty_frames(n_frames, frame_len, H_k, H_v, d, seed, device, sub=32, sigma=0.05):
+    """(q, k, v, g, beta) for n_frames frames of frame_len tokens on `device`:
+    q, k, v bf16 [n_frames * frame_len][H][d], g, beta fp32 [..][H_v].  Frames
+    4 i are novel (keys from a fresh 32-dim subspace per qk-head, fresh
+    values); the others re-present a uniformly chosen token of the frame
+    before them (one source per token, shared by heads, k and v) plus
+    N(0, 0.05) noise before normalisation; q iid; g = -softplus(N(0, 1)),
+    beta = sigmoid(N(0, 1))."""
+    import torch
+    gen = torch.Generator(device=device).manual_seed(int(seed))
+    hrng = rng_for(7000, int(seed) & 0x7FFFFFFF, 0)
+    T = n_frames * frame_len
+    q = torch.empty((T, H_k, d), dtype=torch.bfloat16, device=device)
+    k = torch.empty((T, H_k, d), dtype=torch.bfloat16, device=device)
+    v = torch.empty((T, H_v, d), dtype=torch.bfloat16, device=device)
+    n = frame_len
+
+    def unit(x):
+        return x / x.norm(dim=-1, keepdim=True)
+
+    k_prev = v_prev = None
+    for f in range(n_frames):
+        s = slice(f * n, (f + 1) * n)
+        if f % 4 == 0:
+            bases = np.stack([np.linalg.qr(hrng.standard_normal((d, sub)))[0] for _ in range(H_k)])
+            B = torch.as_tensor(bases, dtype=torch.float32, device=device)           # [H_k][d][sub]
+            z = torch.randn((H_k, n, sub), generator=gen, device=device)
+            k_raw = (torch.matmul(z, B.transpose(1, 2).contiguous()) * math.sqrt(d / sub)).transpose(0, 1)
+            v_raw = torch.randn((n, H_v, d), generator=gen, device=device)
+        else:
+            src = torch.randint(0, n, (n,), generator=gen, device=device)
+            k_raw = k_prev[src] + sigma * torch.randn((n, H_k, d), generator=gen, device=device)
+            v_raw = v_prev[src] + sigma * torch.randn((n, H_v, d), generator=gen, device=device)
+        k[s] = unit(k_raw).to(torch.bfloat16)
+        v[s] = v_raw.to(torch.bfloat16)
+        q[s] = unit(torch.randn((n, H_k, d), generator=gen, device=device)).to(torch.bfloat16)
+        k_prev, v_prev = k_raw.contiguous(), v_raw
+    g = -torch.nn.functional.softplus(torch.randn((T, H_v), generator=gen, device=device))
+    beta = torch.sigmoid(torch.randn((T, H_v), generator=gen, device=device))
+    return q, k, v, g, beta

@@ -88,6 +88,9 @@ def test_gdn_rejects_bad_arguments(ds):
     assert _call_gdn(ds, good, v=P((1 << 20) + 4)) == 4                    # alignment
     assert _call_gdn(ds, good, wsb=16) == 8                                # workspace
     assert b"workspace" in ds.lib().ds_last_error()
+    bad_slices = ds.gdn_shape([1024], 2, 4, 64, 256)
+    bad_slices.drift_per_slice = 2
+    assert _call_gdn(ds, bad_slices) == 6
     assert _call_gdn(ds, ds.gdn_shape([10, 20], 1, 1, 64, 64), cu=None) == 1
     assert b"cu_seqlens" in ds.lib().ds_last_error()
 

@@ -225,16 +225,21 @@ def test_deterministic(ds):
     assert np.array_equal(a["partials"], b["partials"])
 
 
-def test_drift_kernel_modes(ds):
+@pytest.mark.parametrize("shape", [(3, 7, 5), (24, 2, 32), (70, 3, 150)])
+def test_drift_kernel_modes(ds, shape):
+    """Every aggregation of deltas_drift against the oracle's, including more
+    layers than one round of the kernel's waves takes (70) and more heads
+    than two per lane (150), with zero and 0/0 denominators."""
     rng = np.random.default_rng(9)
-    p = rng.uniform(0.01, 3.0, (3, 7, 5, 2)).astype(np.float32)
-    p[0, 2, :, 1] = 0.0          # a frame with zero previous state in layer 0
-    p[1, 4, 3, :] = 0.0          # 0 / 0 for one head
+    L, F, H = shape
+    p = rng.uniform(0.01, 3.0, (L, F, H, 2)).astype(np.float32)
+    p[0, F // 2, :, 1] = 0.0          # a frame with zero previous state in layer 0
+    p[1, F - 1, H // 2, :] = 0.0      # 0 / 0 for one head
     pt = torch.from_numpy(p).to(DEV)
-    for mode in (0, 1, 2):
+    for mode in (0, 1, 2, 3):
         sc = ds.deltas_drift(pt, mode).cpu().numpy()
         rs = oracle.drift_scores(p.astype(np.float64), mode)
-        assert drift_rel_err(sc, rs) <= 1e-6
+        assert drift_rel_err(sc, rs) <= 1e-6, mode
 
 
 @pytest.mark.gpu
@@ -259,6 +264,63 @@ def test_drift_states_kernel(ds):
     p2 = ds.deltas_drift_states(torch.from_numpy(A).cuda(), torch.from_numpy(Bm).cuda())
     torch.cuda.synchronize()
     assert np.allclose(p2.cpu().numpy().astype(np.float64), oracle.drift_states(A, Bm), rtol=1e-5, atol=0.0)
+
+
+def test_drift_per_slice_layout(ds):
+    """Drift pairs written per 16-row slice of the state (drift_per_slice):
+    the slice pairs of a head, added in slice order in fp32, are the per-head
+    pairs bit for bit; Eq. 3 over the slice pairs (deltas_drift LAYER_FROB,
+    slices passed as heads) matches the oracle; frames the device lengths do
+    not reach, and a call without tokens, read zero."""
+    lens = [1500, 0, 2048 + 37]
+    x = synth.make_gdn_inputs(lens, 2, 4, 128, 512, novelty=True, config=1)
+    q, k, v = dev_bf16(x.q), dev_bf16(x.k), dev_bf16(x.v)
+    g, beta = dev_f32(x.g), dev_f32(x.beta)
+    head = ds.gdn_chunk_fwd(q, k, v, g, beta, lens, 512)
+    sl = ds.gdn_chunk_fwd(q, k, v, g, beta, lens, 512, drift_per_slice=True)
+    torch.cuda.synchronize()
+    ph = head["drift_partials"].cpu().numpy()
+    ps = sl["drift_partials"].cpu().numpy().reshape(ph.shape[0], 4, 8, 2)
+    acc = np.zeros(ph.shape, np.float32)
+    for s_ in range(8):
+        acc += ps[:, :, s_, :]
+    assert np.array_equal(acc, ph)
+    assert torch.equal(head["o"], sl["o"]) and torch.equal(head["state"], sl["state"])
+    ref = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, 512)
+    sc = ds.deltas_drift(sl["drift_partials"][None], ds.LAYER_FROB).cpu().numpy()
+    rs = oracle.drift_scores(ref["partials"][None], oracle.LAYER_FROB)
+    assert drift_rel_err(sc, rs) <= TOL_DRIFT
+    # capacity beyond the device lengths: the frames past the real count read 0
+    cap = [3000, 100, 3000]
+    T_cap = sum(cap)
+    pad = lambda a: torch.cat([a, torch.zeros((T_cap - a.shape[0],) + tuple(a.shape[1:]), dtype=a.dtype, device=DEV)])
+    cu = torch.tensor(np.asarray(x.cu_seqlens, np.int32), device=DEV)
+    n_cap = ds.gdn_shape(cap, 2, 4, 128, 512).n_frames
+    dp = torch.full((n_cap, 32, 2), float("nan"), dtype=torch.float32, device=DEV)
+    ds.gdn_chunk_fwd(pad(q), pad(k), pad(v), pad(g), pad(beta), cap, 512, cu_seqlens=cu, drift_partials=dp,
+                     drift_per_slice=True)
+    torch.cuda.synchronize()
+    got = dp.cpu().numpy()
+    n_real = ps.shape[0]
+    assert np.array_equal(got[:n_real], sl["drift_partials"].cpu().numpy())
+    assert np.all(got[n_real:] == 0.0)
+    # no tokens at all: every frame of the shape reads 0
+    z = torch.full((2, 32, 2), float("nan"), dtype=torch.float32, device=DEV)
+    e = torch.empty((0, 2, 128), dtype=torch.bfloat16, device=DEV)
+    shp = ds.gdn_shape([0, 0], 2, 4, 128, 512, drift_per_slice=True)
+    shp.n_frames = 2
+    L = ds.lib()
+    st = torch.empty((2, 4, 128, 128), dtype=torch.float32, device=DEV)
+    o = torch.empty((0, 4, 128), dtype=torch.float32, device=DEV)
+    ws = torch.empty(max(ds.gdn_workspace_bytes(shp), 1), dtype=torch.uint8, device=DEV)
+    cu0 = torch.zeros(3, dtype=torch.int32, device=DEV)
+    import ctypes
+    P = lambda t: ctypes.c_void_p(t.data_ptr())
+    rc = L.gdn_chunk_fwd(ctypes.byref(shp), P(e), P(e), P(e), P(z), P(z), P(cu0), None, P(st), P(o), 1, 1.0, P(z),
+                         None, None, P(ws), ws.numel(), ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+    torch.cuda.synchronize()
+    assert rc == 0
+    assert torch.all(z == 0.0)
 
 
 def test_long_run_near_unity_decay(ds):
