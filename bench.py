@@ -506,6 +506,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--quick", action="store_true", help="headline step only (no per-workload records)")
+    ap.add_argument("--step-only", action="store_true",
+                    help="time the headline step and stop (short runs under counters)")
+    ap.add_argument("--only", choices=["tiny", "single_layer", "stack", "varlen", "eviction_loop"], default=None,
+                    help="time one workload's record and print it alone (for profiling runs)")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="only run a plain device copy of this many bytes (counter calibration)")
     args = ap.parse_args()
@@ -526,6 +530,16 @@ def main():
     stream = torch.cuda.current_stream()
     t_start = time.perf_counter()
     log = lambda m: print(f"[bench {time.perf_counter() - t_start:6.1f}s] {m}", file=sys.stderr, flush=True)
+    if args.only and args.only != "single_layer":
+        if args.only == "tiny":
+            rec = bench_tiny(ds, dev, stream, 200)
+        elif args.only == "varlen":
+            rec = bench_varlen(ds, dev, stream)
+        else:
+            pool = make_pool(dev)
+            rec = (bench_stack if args.only == "stack" else bench_eviction_loop)(ds, dev, stream, pool)
+        print(json.dumps({"only": args.only, "record": rec}), flush=True)
+        return
 
     # ---------------- inputs (host generation, then resident in HBM)
     x = synth.workload_inputs("single_layer")
@@ -615,6 +629,10 @@ def main():
     if int(kv_fail.item()) != 0:
         raise RuntimeError(f"an eviction reported outcome {int(kv_fail.item())}")
     log("headline step timed")
+    if args.step_only:
+        print(json.dumps({"step_only": True, "ms_per_step": ms_per_step, "value": T / (ms_per_step * 1e-3),
+                          "gdn_chunk_fwd_ms": float(gdn_ms), "kv_evict_topk_ms": float(evict_ms)}), flush=True)
+        return
 
     # ---------------- the same eviction loop over a slot-indexed cache: the new
     # chunk's rows go into the rows the last eviction freed (one index_copy
@@ -737,7 +755,7 @@ def main():
                             "hbm_frac": dec_bytes / (dec_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
                             "bytes_per_step": dec_bytes}
 
-    streaming = streaming_bench(ds, dev, stream, args.steps)
+    streaming = streaming_bench(ds, dev, stream, args.steps) if not args.only else None
     log("streaming timed")
 
     flops, bytes_ = algorithmic_work(T, H_K, H_V, D)
@@ -757,7 +775,7 @@ def main():
     single.update(roofline_record(T, gdn_ms, H_K, H_V, D))
     configs["1_single_layer"] = single
     peaks = None
-    if not args.quick:
+    if not args.quick and not args.only:
         configs["0_tiny"] = bench_tiny(ds, dev, stream, 200)
         log("tiny timed")
         del q, k, v, g, beta, o, ws
