@@ -1227,9 +1227,12 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     a.drift_zero = p.n_frames > 0 ? p.drift_partials : nullptr;
     a.drift_zero_per_frame = p.drift_slices ? p.H_v * p.n_split : p.H_v;
 
-    // one prep workgroup per (tile, v-head) when a workgroup per (tile, qk-head)
-    // would leave most CUs idle (short calls, e.g. one streamed chunk)
-    a.prep_per_vhead = a.group > 1 && (long long)p.tiles_max * p.H_k < 256;
+    // one prep workgroup per (tile, v-head) whenever all of them are resident at
+    // once (four per CU): a workgroup then inverts one v-head's system instead
+    // of the group's in turn, at the price of a second Gram product per tile
+    // (1024-token calls: 13.4 -> see the kernel trace; one streamed chunk:
+    // 11.2 -> 8.6 us).  Longer calls share the Gram products of a qk-head.
+    a.prep_per_vhead = a.group > 1 && (long long)p.tiles_max * p.H_v <= 1024;
     if (p.tiles_max > 0) {
         // tiles rounded up to a multiple of 8 (workgroups past the last tile exit)
         const long long n_prep = (long long)((p.tiles_max + 7) / 8) * 8 * (a.prep_per_vhead ? p.H_v : p.H_k);
