@@ -7,7 +7,7 @@ from pathlib import Path
 
 PKG = Path(__file__).resolve().parent
 ROOT = PKG.parent
-SOURCES = ["gdn_fwd.hip", "gdn_decode.hip", "drift.hip", "kv_evict.hip", "abi.hip"]
+SOURCES = ["gdn_fwd.hip", "gdn_wide.hip", "gdn_decode.hip", "drift.hip", "kv_evict.hip", "abi.hip"]
 LIB = PKG / "libdeltas.so"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

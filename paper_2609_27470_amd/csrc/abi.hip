@@ -136,6 +136,7 @@ ds_status gdn_chunk_fwd(const ds_gdn_shape *shape, const void *q, const void *k,
     p.wsDrift = (float *)(ws + lay.offDrift);
     p.wsCnt = (unsigned *)(ws + lay.offCnt);
     p.wsWrite = (float *)(ws + lay.offWrite);
+    p.wsStart = (float *)(ws + lay.offStart);
     p.tiles_max = lay.tiles_max;
     p.n_split = lay.n_split;
     hipError_t e = ds::launch_gdn(p, (hipStream_t)stream);

@@ -1,0 +1,476 @@
+// Sequential part of the chunkwise gated-delta-rule forward (Section 3.2,
+// Eq. 2) with one workgroup per (stream, v-head): all 128 rows of the state
+// of a head live in one workgroup.
+//
+// The per-slice kernel (gdn_fwd.hip) splits a head over 8 workgroups of 16
+// state rows so that a single stream fills the GPU, but each of them pulls
+// the whole tile (K, q, T diag(beta), P: about 46 KiB) from L2 for its 16
+// rows.  With B * H_v heads enough to fill the GPU (several streams, the
+// varlen batch), this kernel loads each tile once per head:
+//   waves 0-3 (compute): wave w carries rows 32 w .. 32 w + 31 of S (two
+//       16-row slices) in fp32 registers and does the whole tile for them:
+//       K S0^T and Q S0^T against the fp16 copy of its own rows (no exchange
+//       between waves), R = V - diag(Gamma) K S0^T, E = T diag(beta) R,
+//       O = diag(Gamma) Q S0^T + P E (stored at once), and the update
+//       S = Gamma_last S0 + (D_last E)^T K.  Every A fragment read from LDS
+//       (rows of K, Q, T, P, K^T) feeds both slices.
+//   waves 4-7 (loaders): load the tile two tiles ahead and stage it in LDS
+//       one tile ahead (K converted to fp16, the q, T and P fragments of the
+//       prep pass, v rows, Gamma and D_last); loader 3 also adds the frame-end
+//       drift sums of the 8 slices (fixed order) and writes them, per slice or
+//       per head, with no exchange between workgroups.
+// One barrier per tile (LDS-only).  The state at a frame's start, needed for
+// ||S_end - S_start||^2, is kept in a scratch area of the workspace (64 KiB
+// per head) rather than in registers, and read back at the frame's end.
+#include <type_traits>
+
+#include "gdn_common.h"
+
+namespace ds {
+
+constexpr int WIDE_VLD = 128 + 8;  // halves per LDS row of the v tile (272 B: rows start on different banks)
+
+struct WideShared {
+    uint16_t K[2][64 * 128];  // K tile (fp16), row-major, 16-byte chunks XOR-swizzled by row (swz)
+    u32x4 Q[2][16][64];       // q (fp16) A-fragments [row block * 4 + k-step][lane], as the prep pass wrote them
+    u32x4 T[2][6][64];        // T diag(beta) A-fragments
+    u32x4 P[2][6][64];        // P A-fragments
+    uint16_t V[2][64 * WIDE_VLD];  // v rows (bf16)
+    float G[2][2][64];        // Gamma_r, D_last,r
+    float2 DR[2][4][2][64];   // frame-end drift sums per [frame % 2][compute wave][slice][lane]
+};
+
+// One loader's share of a tile: K rows 16 X .. 16 X + 15, the q fragments of
+// row block X, v rows 16 X .. 16 X + 15, T and P fragments {2 X, 2 X + 1}
+// (X < 2) or {4 + X - 2}; loader 0 also Gamma, loader 1 D_last.
+struct WideLoad {
+    u32x4 k[4], q[4], v[4], t[2], p[2];
+    float g;
+};
+
+template <bool OUT_BF16, bool DRIFT>
+__global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
+    constexpr int D = 128, KS = D / 32, NKB = D / 16;
+    __shared__ __align__(16) WideShared sh;
+    const int tid = threadIdx.x, lane = tid & 63, ln = lane & 15, lg = lane >> 4;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+    // ---- workgroup -> (stream, v-head); the v-heads of one qk-head of one
+    // stream sit on one XCD (dispatch deals workgroups to the 8 XCDs in turn),
+    // so its K and q tiles are fetched into that XCD's L2 once
+    const int n_groups = a.st.B * a.H_k;
+    const int bid = blockIdx.x;
+    int gidx, mem;
+    if (n_groups % 8 == 0) {
+        const int xcd = bid & 7, slot = bid >> 3;
+        gidx = xcd + 8 * (slot / a.group);
+        mem = slot % a.group;
+    } else {
+        gidx = bid / a.group;
+        mem = bid % a.group;
+    }
+    const int b = gidx / a.H_k, qh = gidx % a.H_k;
+    const int j = qh * a.group + mem;
+
+    int st = 0, en = 0, tile_base = 0, frame_base = 0;
+    for_streams(a.st, [&](int bb, int s0, int e0) {
+        if (bb == b) {
+            st = s0;
+            en = e0;
+            return true;
+        }
+        tile_base += (e0 - s0 + TILE - 1) / TILE;
+        frame_base += frames_in(e0 - s0, a.frame_len);
+        return false;
+    });
+    const int len = en - st;
+    const int n_tiles = (len + TILE - 1) / TILE;
+
+    if (w < 4) {
+        // ============================================================ compute
+        // S^T block kb of slice sl, lane (ln, lg), element e =
+        //   S[32 w + 16 sl + ln][sigma(kb, 4 lg + e)]
+        auto scol = [&](int kb, int e) { return 32 * (kb >> 1) + 8 * lg + 4 * (kb & 1) + e; };
+        auto srow = [&](int sl) { return 32 * w + 16 * sl + ln; };
+        const size_t hbase = ((size_t)b * a.H_v + j) * D * D;
+        // 16-byte pieces of the head's state rows go through buffer resources
+        // (a uniform base in scalar registers, 32-bit lane offsets): S[sl][kb]
+        // holds 4 consecutive columns of row srow(sl)
+        // byte offset of S[sl][kb]'s 4 columns = a per-lane base + a constant (passed
+        // as the scalar offset, so that no per-(sl, kb) offset register stays live)
+        const uint32_t lane_row = (uint32_t)((32 * w + ln) * D + 8 * lg) * 4u;
+        auto sconst = [&](int sl, int kb) { return (int)((16 * sl * D + 32 * (kb >> 1) + 4 * (kb & 1)) * 4); };
+        constexpr int RSRC_FLAGS = 0x00020000;
+        f32x4 S[2][NKB];
+        if (a.state_in) {
+            const __amdgpu_buffer_rsrc_t rin =
+                __builtin_amdgcn_make_buffer_rsrc((void *)(a.state_in + hbase), (short)0, D * D * 4, RSRC_FLAGS);
+#pragma unroll
+            for (int sl = 0; sl < 2; ++sl)
+#pragma unroll
+                for (int kb = 0; kb < NKB; ++kb)
+                    S[sl][kb] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rin, lane_row, sconst(sl, kb), 0));
+        } else {
+#pragma unroll
+            for (int sl = 0; sl < 2; ++sl)
+#pragma unroll
+                for (int kb = 0; kb < NKB; ++kb) S[sl][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        // the state at the start of the current frame, in this wave's own
+        // register order (16-byte pieces, lane-contiguous)
+        const __amdgpu_buffer_rsrc_t rstart = __builtin_amdgcn_make_buffer_rsrc(
+            (void *)(a.wsStart + ((((size_t)b * a.H_v + j) * 4 + w) * 2) * NKB * 64 * 4), (short)0, 2 * NKB * 64 * 16,
+            RSRC_FLAGS);
+        const uint32_t lane16 = (uint32_t)lane * 16u;
+        auto start_const = [&](int sl, int kb) { return (sl * NKB + kb) * 64 * 16; };
+        auto save_start = [&]() __attribute__((always_inline)) {
+#pragma unroll
+            for (int sl = 0; sl < 2; ++sl)
+#pragma unroll
+                for (int kb = 0; kb < NKB; ++kb)
+                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, S[sl][kb]), rstart, lane16, start_const(sl, kb), 0);
+        };
+        if (DRIFT) save_start();
+        int frame = frame_base;
+        int frame_end = a.frame_len > 0 ? min(a.frame_len, len) : len;  // tokens done at the next frame end
+
+        auto tile = [&](int lt, auto bufc) __attribute__((always_inline)) {
+            constexpr int buf = decltype(bufc)::value;  // == lt % 2
+            const int t0 = st + TILE * lt, n = min(TILE, en - t0);
+            lds_barrier();
+            const float gl = sh.G[buf][0][63];
+
+            // S0 as fp16 B operands (k-step ks pairs state blocks 2 ks, 2 ks + 1)
+            half8 s16[2][KS];
+#pragma unroll
+            for (int sl = 0; sl < 2; ++sl)
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) s16[sl][ks] = to_half8(S[sl][2 * ks], S[sl][2 * ks + 1]);
+
+            // K S0^T: token rows 16 rb + 4 lg + e, state row 32 w + 16 sl + ln
+            f32x4 ks0[4][2];
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+                for (int sl = 0; sl < 2; ++sl) ks0[rb][sl] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                half8 ka[4];
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) {
+                    const int row = 16 * rb + ln;
+                    ka[rb] = as_half8(*(const u32x4 *)(&sh.K[buf][row * D + 8 * ((4 * ks + lg) ^ swz<D>(row))]));
+                }
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+                    for (int sl = 0; sl < 2; ++sl) ks0[rb][sl] = mfma_f16(ka[rb], s16[sl][ks], ks0[rb][sl]);
+            }
+
+            // R = V - diag(Gamma) K S0^T; v[16 rb + 4 lg + e][32 w + 16 sl + ln] by transposing reads
+            half8 rf[2][2];
+#pragma unroll
+            for (int sl = 0; sl < 2; ++sl) {
+                f32x4 R[4];
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) {
+                    const v4i16 vv = ds_read_tr16(&sh.V[buf][(16 * rb + 4 * lg + (ln >> 2)) * WIDE_VLD + 32 * w + 16 * sl +
+                                                            4 * (ln & 3)]);
+                    const float4 g4 = *(const float4 *)(&sh.G[buf][0][16 * rb + 4 * lg]);
+                    R[rb][0] = bf16_to_f32((uint16_t)vv[0]) - g4.x * ks0[rb][sl][0];
+                    R[rb][1] = bf16_to_f32((uint16_t)vv[1]) - g4.y * ks0[rb][sl][1];
+                    R[rb][2] = bf16_to_f32((uint16_t)vv[2]) - g4.z * ks0[rb][sl][2];
+                    R[rb][3] = bf16_to_f32((uint16_t)vv[3]) - g4.w * ks0[rb][sl][3];
+                }
+                rf[sl][0] = to_half8(R[0], R[1]);
+                rf[sl][1] = to_half8(R[2], R[3]);
+            }
+
+            // E = T diag(beta) R, then D_last E; both as fp16 B operands
+            half8 e16[2][2], d16[2][2];
+            {
+                half8 tf[6];
+#pragma unroll
+                for (int f = 0; f < 6; ++f) tf[f] = as_half8(sh.T[buf][f][lane]);
+#pragma unroll
+                for (int sl = 0; sl < 2; ++sl) {
+                    f32x4 E[4];
+#pragma unroll
+                    for (int rb = 0; rb < 4; ++rb) E[rb] = mfma_f16(tf[frag_index(rb, 0)], rf[sl][0], f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+                    for (int rb = 2; rb < 4; ++rb) E[rb] = mfma_f16(tf[frag_index(rb, 1)], rf[sl][1], E[rb]);
+                    e16[sl][0] = to_half8(E[0], E[1]);
+                    e16[sl][1] = to_half8(E[2], E[3]);
+#pragma unroll
+                    for (int rb = 0; rb < 4; ++rb) {
+                        const float4 d4 = *(const float4 *)(&sh.G[buf][1][16 * rb + 4 * lg]);
+                        E[rb][0] *= d4.x;
+                        E[rb][1] *= d4.y;
+                        E[rb][2] *= d4.z;
+                        E[rb][3] *= d4.w;
+                    }
+                    d16[sl][0] = to_half8(E[0], E[1]);
+                    d16[sl][1] = to_half8(E[2], E[3]);
+                }
+            }
+
+            // O = diag(Gamma) Q S0^T + P E, stored straight from the accumulators
+            // through a buffer resource covering the tile's n valid rows (before
+            // the update, so that the fp16 S0 dies here)
+            constexpr int ES = OUT_BF16 ? 2 : 4;
+            const uint32_t row_bytes = (uint32_t)a.H_v * D * ES;
+            const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                (char *)a.o + (size_t)t0 * row_bytes, (short)0, (int)(row_bytes * (uint32_t)n), 0x00020000);
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) {
+                f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    const half8 qa = as_half8(sh.Q[buf][rb * KS + ks][lane]);
+#pragma unroll
+                    for (int sl = 0; sl < 2; ++sl) acc[sl] = mfma_f16(qa, s16[sl][ks], acc[sl]);
+                }
+                const float4 g4 = *(const float4 *)(&sh.G[buf][0][16 * rb + 4 * lg]);
+#pragma unroll
+                for (int sl = 0; sl < 2; ++sl) {
+                    acc[sl][0] *= g4.x;
+                    acc[sl][1] *= g4.y;
+                    acc[sl][2] *= g4.z;
+                    acc[sl][3] *= g4.w;
+                }
+                const half8 p0 = as_half8(sh.P[buf][frag_index(rb, 0)][lane]);
+#pragma unroll
+                for (int sl = 0; sl < 2; ++sl) acc[sl] = mfma_f16(p0, e16[sl][0], acc[sl]);
+                if (rb >= 2) {
+                    const half8 p1 = as_half8(sh.P[buf][frag_index(rb, 1)][lane]);
+#pragma unroll
+                    for (int sl = 0; sl < 2; ++sl) acc[sl] = mfma_f16(p1, e16[sl][1], acc[sl]);
+                }
+#pragma unroll
+                for (int sl = 0; sl < 2; ++sl) {
+                    const uint32_t col = (uint32_t)(j * D + 32 * w + 16 * sl + ln) * ES;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const uint32_t off = (uint32_t)(16 * rb + 4 * lg + e) * row_bytes + col;
+                        const float val = a.scale * acc[sl][e];
+                        if (OUT_BF16)
+                            __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, (__bf16)val), rs, off, 0, 0);
+                        else
+                            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, val), rs, off, 0, 0);
+                    }
+                }
+            }
+
+            // S = Gamma_last S0 + (D_last E)^T K
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) {
+                // K^T fragments by transposing reads (each used by both slices): source
+                // lane (ln, lg) addresses token 32 ks + 16 r + 4 lg + ln / 4 and dims
+                // 32 (kb / 2) + 8 (ln % 4) + 4 (kb % 2) .. + 3
+                half8 kt[2];
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) {
+                    const int r0 = 32 * ks + 4 * lg + (ln >> 2), r1 = r0 + 16;
+                    const int ch = 4 * (kb >> 1) + (ln & 3), hf = 4 * (kb & 1);
+                    kt[ks] = __builtin_bit_cast(half8, cat_u32x4(ds_read_tr16(&sh.K[buf][r0 * D + 8 * (ch ^ swz<D>(r0)) + hf]),
+                                                                 ds_read_tr16(&sh.K[buf][r1 * D + 8 * (ch ^ swz<D>(r1)) + hf])));
+                }
+#pragma unroll
+                for (int sl = 0; sl < 2; ++sl) {
+                    f32x4 sn;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) sn[e] = gl * S[sl][kb][e];
+                    sn = mfma_f16(kt[0], d16[sl][0], sn);
+                    S[sl][kb] = mfma_f16(kt[1], d16[sl][1], sn);
+                }
+            }
+
+            // write signal: ||E row||^2 over each slice's 16 columns per token
+            if (a.wsWrite) {
+#pragma unroll
+                for (int sl = 0; sl < 2; ++sl) {
+                    float *wb = a.wsWrite + ((size_t)j * a.n_split + 2 * w + sl) * a.st.T + t0;
+#pragma unroll
+                    for (int ks = 0; ks < 2; ++ks) {
+                        const float wsum = row_sq_sum16(e16[sl][ks], ln);
+                        const int i = ln >> 1, tok = 32 * ks + 16 * (i >> 2) + 4 * lg + (i & 3);
+                        if ((ln & 1) == 0 && tok < n) wb[tok] = wsum;
+                    }
+                }
+            }
+
+            // frame end: per-lane drift sums of both slices against the state the
+            // frame started from (read back from the scratch area), snapshot
+            if (DRIFT && TILE * lt + n == frame_end) {
+#pragma unroll
+                for (int sl = 0; sl < 2; ++sl) {
+                    float num = 0.f, den = 0.f;
+#pragma unroll
+                    for (int kb = 0; kb < NKB; ++kb) {
+                        const f32x4 s0 = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rstart, lane16, start_const(sl, kb), 0));
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const float dl = S[sl][kb][e] - s0[e];
+                            num += dl * dl;
+                            den += s0[e] * s0[e];
+                        }
+                    }
+                    sh.DR[frame & 1][w][sl][lane] = float2{num, den};
+                }
+                if (a.snapshots && frame < a.n_frames) {
+                    const __amdgpu_buffer_rsrc_t rsn = __builtin_amdgcn_make_buffer_rsrc(
+                        (void *)(a.snapshots + ((size_t)frame * a.H_v + j) * D * D), (short)0, D * D * 4, RSRC_FLAGS);
+#pragma unroll
+                    for (int sl = 0; sl < 2; ++sl)
+#pragma unroll
+                        for (int kb = 0; kb < NKB; ++kb)
+                            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, S[sl][kb]), rsn, lane_row, sconst(sl, kb), 0);
+                }
+                save_start();
+                ++frame;
+                frame_end = min(frame_end + a.frame_len, len);
+            }
+        };
+        for (int lt = 0; lt < n_tiles; lt += 2) {
+            tile(lt, std::integral_constant<int, 0>());
+            if (lt + 1 < n_tiles) tile(lt + 1, std::integral_constant<int, 1>());
+        }
+        if (n_tiles > 0) lds_barrier();  // loader 3 reduces the last frame after it
+        const __amdgpu_buffer_rsrc_t rout =
+            __builtin_amdgcn_make_buffer_rsrc((void *)(a.state_out + hbase), (short)0, D * D * 4, RSRC_FLAGS);
+#pragma unroll
+        for (int sl = 0; sl < 2; ++sl)
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb)
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, S[sl][kb]), rout, lane_row, sconst(sl, kb), 0);
+    } else {
+        // ============================================================ loaders
+        auto run = [&](auto xc) __attribute__((always_inline)) {
+            constexpr int X = decltype(xc)::value;
+            constexpr int NT = X < 2 ? 2 : 1;  // T and P fragments
+            constexpr int F_FIRST = X < 2 ? 2 * X : 4 + (X - 2);
+            constexpr int CH = D / 8, RPI = 64 / CH;  // 16-byte chunks per row, rows per 64-lane load
+            auto load = [&](WideLoad &s, int lt_) __attribute__((always_inline)) {
+                const int lt = min(lt_, n_tiles - 1);  // clamped: every call issues the same loads
+                const int t0 = st + TILE * lt, n = min(TILE, en - t0);
+                const size_t tv = (size_t)(tile_base + lt) * a.H_v + j;
+                const uint16_t *kb = a.k + (size_t)t0 * a.H_k * D + (size_t)qh * D + 8 * (lane % CH);
+                const uint16_t *vb = a.v + ((size_t)t0 * a.H_v + j) * D + 8 * (lane % CH);
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const uint32_t r = (uint32_t)min(16 * X + RPI * c + lane / CH, n - 1);
+                    s.k[c] = *(const u32x4 *)(kb + r * (uint32_t)a.H_k * D);
+                    s.v[c] = *(const u32x4 *)(vb + r * (uint32_t)a.H_v * D);
+                }
+                const u32x4 *qb = (const u32x4 *)(a.wsQ + ((size_t)(tile_base + lt) * a.H_k + qh) * 64 * D);
+#pragma unroll
+                for (int c = 0; c < 4; ++c) s.q[c] = qb[(X * KS + c) * 64 + lane];
+                const u32x4 *tb = (const u32x4 *)(a.wsT + tv * TP_HALVES);
+                const u32x4 *pb = (const u32x4 *)(a.wsP + tv * TP_HALVES);
+#pragma unroll
+                for (int c = 0; c < NT; ++c) {
+                    s.t[c] = tb[(F_FIRST + c) * 64 + lane];
+                    s.p[c] = pb[(F_FIRST + c) * 64 + lane];
+                }
+                if (X < 2) s.g = a.wsGam[tv * 128 + 64 * X + lane];
+            };
+            auto stage = [&](const WideLoad &s, auto bufc) __attribute__((always_inline)) {
+                constexpr int buf = decltype(bufc)::value;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int row = 16 * X + RPI * c + lane / CH, ch = lane % CH;
+                    *(u32x4 *)(&sh.K[buf][row * D + 8 * (ch ^ swz<D>(row))]) = __builtin_bit_cast(u32x4, bf16x8_to_f16(s.k[c]));
+                    *(u32x4 *)(&sh.V[buf][row * WIDE_VLD + 8 * ch]) = s.v[c];
+                    sh.Q[buf][X * KS + c][lane] = s.q[c];
+                }
+#pragma unroll
+                for (int c = 0; c < NT; ++c) {
+                    sh.T[buf][F_FIRST + c][lane] = s.t[c];
+                    sh.P[buf][F_FIRST + c][lane] = s.p[c];
+                }
+                if (X < 2) sh.G[buf][X][lane] = s.g;
+            };
+            // drift: loader 3 adds the 8 slices' sums of a frame that ended in
+            // the previous tile (fixed order) and writes them
+            int frame = frame_base;
+            int frame_end = a.frame_len > 0 ? min(a.frame_len, len) : len;
+            auto drift_reduce = [&](int it) __attribute__((always_inline)) {
+                if (!DRIFT || X != 3 || it < 1) return;
+                const int lt = it - 1;
+                if (TILE * lt + min(TILE, len - TILE * lt) != frame_end) return;
+                if (a.wsDrift && frame < a.n_frames) {
+                    float2 pr[8];
+#pragma unroll
+                    for (int s = 0; s < 8; ++s) {
+                        const float2 p = sh.DR[frame & 1][s >> 1][s & 1][lane];
+                        pr[s] = float2{wave_sum(p.x), wave_sum(p.y)};
+                    }
+                    const size_t fj = (size_t)frame * a.H_v + j;
+                    if (a.drift_out) {  // per-head pair: the slices in order
+                        float num = 0.f, den = 0.f;
+#pragma unroll
+                        for (int s = 0; s < 8; ++s) {
+                            num += pr[s].x;
+                            den += pr[s].y;
+                        }
+                        if (lane == 0) *(float2 *)(a.drift_out + fj * 2) = float2{num, den};
+                    } else {  // per-slice pairs
+                        if (lane < 8) {
+                            float2 mine = pr[0];
+#pragma unroll
+                            for (int s = 1; s < 8; ++s)
+                                if (lane == s) mine = pr[s];
+                            *(float2 *)(a.wsDrift + (fj * a.n_split + lane) * 2) = mine;
+                        }
+                    }
+                }
+                ++frame;
+                frame_end = min(frame_end + a.frame_len, len);
+            };
+            if (n_tiles > 0) {
+                WideLoad s0, s1;
+                load(s0, 0);
+                load(s1, 1);
+                stage(s0, std::integral_constant<int, 0>());
+                load(s0, 2);
+                auto step = [&](int it, WideLoad &s, auto bufc) __attribute__((always_inline)) {
+                    lds_barrier();
+                    if (it + 1 < n_tiles) stage(s, bufc);
+                    load(s, it + 3);
+                    drift_reduce(it);
+                };
+                // tile t lives in register set t % 2 and LDS buffer t % 2; iteration it
+                // stages tile it + 1 and then loads tile it + 3 into the set just freed
+                for (int it = 0; it <= n_tiles; it += 2) {
+                    step(it, s1, std::integral_constant<int, 1>());
+                    if (it + 1 <= n_tiles) step(it + 1, s0, std::integral_constant<int, 0>());
+                }
+            }
+        };
+        if (w == 4)
+            run(std::integral_constant<int, 0>());
+        else if (w == 5)
+            run(std::integral_constant<int, 1>());
+        else if (w == 6)
+            run(std::integral_constant<int, 2>());
+        else
+            run(std::integral_constant<int, 3>());
+    }
+}
+
+hipError_t launch_gdn_wide(const GdnArgs &a, int n_wg, bool o_bf16, bool drift, hipStream_t stream) {
+    if (o_bf16) {
+        if (drift)
+            hipLaunchKernelGGL((gdn_wide_kernel<true, true>), dim3(n_wg), dim3(512), 0, stream, a);
+        else
+            hipLaunchKernelGGL((gdn_wide_kernel<true, false>), dim3(n_wg), dim3(512), 0, stream, a);
+    } else {
+        if (drift)
+            hipLaunchKernelGGL((gdn_wide_kernel<false, true>), dim3(n_wg), dim3(512), 0, stream, a);
+        else
+            hipLaunchKernelGGL((gdn_wide_kernel<false, false>), dim3(n_wg), dim3(512), 0, stream, a);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace ds

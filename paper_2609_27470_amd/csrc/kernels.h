@@ -30,13 +30,14 @@ struct GdnLaunch {
     float *wsDrift;     // [n_frames][H_v][n_split][2] (one pair per slice)
     float *wsWrite;     // [H_v][n_split][T_total] per-token ||E row||^2 over each slice's columns
     unsigned *wsCnt;    // [B][H_v] slices whose drift sums are written (drift reduction in the sequential kernel)
+    float *wsStart;     // [B][H_v][d][d] frame-start state of the whole-head sequential kernel
     int tiles_max;
     int n_split;        // d_v slices of 16 per (stream, v-head)
 };
 
 // Workspace layout shared by the size query and the launcher.
 struct GdnWorkspace {
-    size_t offT, offP, offQ, offGam, offDrift, offWrite, offCnt, total;
+    size_t offT, offP, offQ, offGam, offDrift, offWrite, offCnt, offStart, total;
     int tiles_max, n_split;
 };
 // with_write: also the per-token norm area of the write signal (write_partials != NULL)
