@@ -3,6 +3,8 @@
 // sequential kernel that owns whole heads): tile constants, the fragment
 // layout of the prep pass's workspace, the kernel arguments and small helpers.
 #pragma once
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -98,12 +100,29 @@ __device__ __forceinline__ void lds_barrier() {
 }
 
 // K tile staged row-major in LDS (D bf16 per row) with the 16-byte chunks of
-// a row permuted by an XOR with swz(row), so that both the row writes and the
-// transposing reads (4 rows x 4 chunks per 16 lanes) spread over the banks.
+// a row permuted by an XOR with swz(row).  A bank group (4 banks, one chunk)
+// is the chunk index mod 8, and a row starts on bank 0 (D = 64, 128), so:
+// 8 consecutive rows read at one logical chunk (16-byte row reads, 8 lanes a
+// cycle) see swz = a permutation of 0..7 and hit 8 distinct groups; the row
+// writes cover a row's chunks; and a transposing read (4 rows 4 q .. 4 q + 3
+// x 4 chunks 4 c .. 4 c + 3, 16 lanes of 8 bytes) sees swz in {0, 4, 1, 5} or
+// {2, 6, 3, 7} and so touches each bank group twice, the least 16 such reads
+// of one half-chunk can.
 template <int D>
 __device__ __forceinline__ int swz(int row) {
-    if (D == 128) return ((row & 3) << 2) | ((row >> 2) & 3);
-    return (((row >> 1) & 1) << 2) | ((row >> 2) & 3);
+    static_assert(D == 64 || D == 128, "head dim");
+    return ((row & 1) << 2) | ((row >> 1) & 3);
+}
+
+// Four consecutive output values of one lane to o at byte offset off of the
+// buffer resource rs: as bf16 (one 8-byte store) or fp32 (one 16-byte store).
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void store_o4(const f32x4 &v, __amdgpu_buffer_rsrc_t rs, uint32_t off, std::true_type) {
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, __builtin_convertvector(v, bf16x4)), rs, off, 0, 0);
+}
+__device__ __forceinline__ void store_o4(const f32x4 &v, __amdgpu_buffer_rsrc_t rs, uint32_t off, std::false_type) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rs, off, 0, 0);
 }
 
 // Two C blocks -> one fp16 operand (8 values per lane).

@@ -33,8 +33,9 @@ namespace ds {
 // are loaded once as whole 16-byte chunks and staged in LDS; the Gram blocks
 // K K^T and (K Q^T) run on bf16 matrix cores (exact bf16 inputs, fp32
 // accumulation) and stay in registers.  Then, for every v-head of the group
-// (its own gates): P is scaled and written straight from the K Q^T registers
-// (their layout is already P's fragment layout), and the inverse of the unit
+// (its own gates): P is gated, multiplied by the output scale and written
+// straight from the K Q^T registers (their layout is already P's fragment
+// layout), and the inverse of the unit
 // lower-triangular I + A is blocked in 16 x 16 blocks, the diagonal blocks by
 // forward substitution and the off-diagonal ones on fp32 matrix cores,
 // T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj, by distance from the diagonal.
@@ -170,6 +171,12 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
             }
         }
     }
+    // P carries the output scale (o = scale (diag(Gamma) Q S0^T + P E)): one
+    // multiply here instead of one per output element in the sequential pass
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) gq[nb][e] *= a.scale;
     lds_barrier();  // K and Q tiles are dead from here on (A and T reuse them)
 
     // ---- per v-head of the qk-head's group: gates (wave 0), P from the Gram
@@ -209,7 +216,7 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
             a.wsGam[tv * 128 + 64 + lane] = __builtin_amdgcn_exp2f(s_last - s);
         }
     };
-    // P (lower incl. diagonal) of query block w, Gamma_i / Gamma_j (q_i . k_j)
+    // P (lower incl. diagonal) of query block w, scale Gamma_i / Gamma_j (q_i . k_j)
     // for keys j <= i, as the A fragments (w, ks) of P E (k-step ks pairs key
     // blocks 2 ks, 2 ks + 1); block (nb, w): key 16 nb + 4 lg + e, query 16 w + ln
     auto pfrags = [&](int jj, int slot) __attribute__((always_inline)) {
@@ -360,8 +367,10 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
 //                    operand inside the registers.  S0 and E are published in
 //                    LDS for the output waves; at a frame end each lane
 //                    leaves its share of the drift sums in LDS.
-//   waves 2 and 3, output:  one tile behind, O = diag(Gamma) Q S0^T + P E for
-//                    row blocks {0, 1} and {2, 3}; they load q, P and Gamma
+//   waves 2 and 3, output:  one tile behind, O = scale diag(Gamma) Q S0^T + P E
+//                    (the prep pass folded the scale into P) for row blocks
+//                    {0, 1} and {2, 3}, as O^T so that a lane holds four
+//                    consecutive output dims of a token; they load q and P
 //                    themselves.
 //   waves 4 - 7, loaders: each loads a quarter of the K rows, T diag(beta),
 //                    v rows and the decay factors of a tile three tiles ahead
@@ -647,8 +656,9 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             for (int e = 0; e < 4; ++e) a.state_out[sbase + scol(hh * HKB + c, e)] = S[c][e];
     } else if (w < 4) {
         // =============================================================== output
-        // O = diag(Gamma) Q S0^T + P E for row blocks {2 PR, 2 PR + 1}, one tile
-        // behind the state waves (Gamma from the loaders' LDS copy)
+        // O = scale diag(Gamma) Q S0^T + P E (P carries the scale) for row blocks
+        // {2 PR, 2 PR + 1}, one tile behind the state waves (Gamma from the
+        // loaders' LDS copy), computed transposed
         auto run = [&](auto prc) __attribute__((always_inline)) {
             constexpr int PR = decltype(prc)::value;
             constexpr int NP = PR == 0 ? 2 : 4;  // P fragments of the two row blocks
@@ -671,52 +681,48 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             auto compute = [&](const OutSet<D> &s, int lt, auto bufc) __attribute__((always_inline)) {
                 constexpr int buf = decltype(bufc)::value;  // == lt % 2
                 const int t0 = st + TILE * lt, n = min(TILE, en - t0);
+                // O^T blocks: S0 as the A operand and q as the B operand, so that lane
+                // (ln, lg) holds output dims v0 + 4 lg + e of token 16 (2 PR + r) + ln
                 f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) {
-                    const half8 bs = as_half8(sh.S16[lt % 3][ks][lane]);
+                    const half8 as = as_half8(sh.S16[lt % 3][ks][lane]);
 #pragma unroll
-                    for (int r = 0; r < 2; ++r) acc[r] = mfma_f16(as_half8(s.q[r][ks]), bs, acc[r]);
+                    for (int r = 0; r < 2; ++r) acc[r] = mfma_f16(as, as_half8(s.q[r][ks]), acc[r]);
                 }
+                // scale Gamma of the token (P carries the scale already)
 #pragma unroll
                 for (int r = 0; r < 2; ++r) {
-                    const float4 g4 = *(const float4 *)(&sh.G[lt % 3][0][16 * (2 * PR + r) + 4 * lg]);
-                    acc[r][0] *= g4.x;
-                    acc[r][1] *= g4.y;
-                    acc[r][2] *= g4.z;
-                    acc[r][3] *= g4.w;
+                    const float gs = a.scale * sh.G[lt % 3][0][16 * (2 * PR + r) + ln];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) acc[r][e] *= gs;
                 }
+                // + (P E)^T = E^T P^T: the E B operand read as the A operand, the P
+                // A fragments as B operands
                 const half8 ef0 = as_half8(sh.E[buf][0][lane]);
                 if (PR == 0) {
-                    acc[0] = mfma_f16(as_half8(s.p[0]), ef0, acc[0]);
-                    acc[1] = mfma_f16(as_half8(s.p[1]), ef0, acc[1]);
+                    acc[0] = mfma_f16(ef0, as_half8(s.p[0]), acc[0]);
+                    acc[1] = mfma_f16(ef0, as_half8(s.p[1]), acc[1]);
                 } else {
                     const half8 ef1 = as_half8(sh.E[buf][1][lane]);
-                    acc[0] = mfma_f16(as_half8(s.p[0]), ef0, acc[0]);
-                    acc[1] = mfma_f16(as_half8(s.p[2]), ef0, acc[1]);
-                    acc[0] = mfma_f16(as_half8(s.p[1]), ef1, acc[0]);
-                    acc[1] = mfma_f16(as_half8(s.p[3]), ef1, acc[1]);
+                    acc[0] = mfma_f16(ef0, as_half8(s.p[0]), acc[0]);
+                    acc[1] = mfma_f16(ef0, as_half8(s.p[2]), acc[1]);
+                    acc[0] = mfma_f16(ef1, as_half8(s.p[1]), acc[0]);
+                    acc[1] = mfma_f16(ef1, as_half8(s.p[3]), acc[1]);
                 }
-                // o straight from the accumulators (lane (ln, lg): rows 16 r + 4 lg + e
-                // of the wave's 32, column v0 + ln), through a buffer resource covering
-                // the tile's n valid rows: stores past a ragged tile's end fall outside
-                // it and are dropped
+                // o straight from the accumulators, 4 consecutive dims per lane,
+                // through a buffer resource covering the tile's n valid rows: stores
+                // past a ragged tile's end fall outside it and are dropped
                 constexpr int ES = OUT_BF16 ? 2 : 4;
                 const uint32_t row_bytes = (uint32_t)a.H_v * D * ES;
                 const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
                     (char *)a.o + (size_t)t0 * row_bytes, (short)0, (int)(row_bytes * (uint32_t)n), 0x00020000);
-                const uint32_t col = (uint32_t)(j * D + v0 + ln) * ES;
+                const uint32_t col = (uint32_t)(j * D + v0 + 4 * lg) * ES;
 #pragma unroll
-                for (int r = 0; r < 2; ++r)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const uint32_t off = (uint32_t)(32 * PR + 16 * r + 4 * lg + e) * row_bytes + col;
-                        const float val = a.scale * acc[r][e];
-                        if (OUT_BF16)
-                            __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, (__bf16)val), rs, off, 0, 0);
-                        else
-                            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, val), rs, off, 0, 0);
-                    }
+                for (int r = 0; r < 2; ++r) {
+                    const uint32_t off = (uint32_t)(32 * PR + 16 * r + ln) * row_bytes + col;
+                    store_o4(acc[r], rs, off, std::integral_constant<bool, OUT_BF16>());
+                }
             };
             // iteration it computes tile it - 1 and then loads tile it + 1 into the
             // same register set (set (it + 1) % 2)

@@ -9,16 +9,18 @@
 // varlen batch), this kernel loads each tile once per head:
 //   waves 0-3 (compute): wave w carries rows 32 w .. 32 w + 31 of S (two
 //       16-row slices) in fp32 registers and does the whole tile for them:
-//       K S0^T and Q S0^T against the fp16 copy of its own rows (no exchange
+//       K S0^T and S0 Q^T against the fp16 copy of its own rows (no exchange
 //       between waves), R = V - diag(Gamma) K S0^T, E = T diag(beta) R,
-//       O = diag(Gamma) Q S0^T + P E (stored at once), and the update
-//       S = Gamma_last S0 + (D_last E)^T K.  Every A fragment read from LDS
-//       (rows of K, Q, T, P, K^T) feeds both slices.
+//       O^T = scale diag(Gamma) S0 Q^T + (P E)^T (P carries the scale), and
+//       the update S = Gamma_last S0 + (D_last E)^T K.  Every fragment read
+//       from LDS (rows of K, Q, T, P, K^T) feeds both slices.
 //   waves 4-7 (loaders): load the tile two tiles ahead and stage it in LDS
 //       one tile ahead (K converted to fp16, the q, T and P fragments of the
-//       prep pass, v rows, Gamma and D_last); loader 3 also adds the frame-end
-//       drift sums of the 8 slices (fixed order) and writes them, per slice or
-//       per head, with no exchange between workgroups.
+//       prep pass, v rows, Gamma and D_last), and store the previous tile's
+//       bf16 o, which the compute waves left in LDS, as whole rows; loader 3
+//       also adds the frame-end drift sums of the 8 slices (fixed order) and
+//       writes them, per slice or per head, with no exchange between
+//       workgroups.
 // One barrier per tile (LDS-only).  The state at a frame's start, needed for
 // ||S_end - S_start||^2, is kept in a scratch area of the workspace (64 KiB
 // per head) rather than in registers, and read back at the frame's end.
@@ -28,7 +30,23 @@
 
 namespace ds {
 
-constexpr int WIDE_VLD = 128 + 8;  // halves per LDS row of the v tile (272 B: rows start on different banks)
+constexpr int WIDE_VLD = 128 + 16;  // halves per LDS row of the v tile (288 B: the 4 rows of a transposing
+                                    // read start 8 banks apart, so its 16 lanes cover all 32 banks)
+
+// A bf16 o tile is staged in the v buffer of its tile once the v rows are
+// consumed: compute wave w writes output dims 32 w .. 32 w + 31 of every token,
+// exactly the band of columns of v that it alone read, so no wave overwrites
+// v that another still reads.  Inside the band the 8-byte pieces (4 dims) are
+// permuted by an XOR with (row / 4) % 4, so that the 16 rows of one 8-byte
+// write hit distinct banks.  Returns the halves offset of dims d .. d + 3
+// (d % 4 == 0) of token row r.
+__device__ __forceinline__ int o_stage_at(int r, int d) {
+    return r * WIDE_VLD + 32 * (d >> 5) + 4 * (((d >> 2) & 7) ^ ((r >> 2) & 3));
+}
+
+// instruction classes of __builtin_amdgcn_sched_group_barrier
+constexpr int SG_VALU = 0x2, SG_MFMA = 0x8, SG_DSR = 0x100;
+#define WIDE_SG(mask, n) __builtin_amdgcn_sched_group_barrier((mask), (n), 0)
 
 struct WideShared {
     uint16_t K[2][64 * 128];  // K tile (fp16), row-major, 16-byte chunks XOR-swizzled by row (swz)
@@ -134,140 +152,32 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
         int frame = frame_base;
         int frame_end = a.frame_len > 0 ? min(a.frame_len, len) : len;  // tokens done at the next frame end
 
+        // The tile runs as software-pipelined regions: every LDS operand is read
+        // one step before its products, and scheduling groups interleave the
+        // matrix-core products with the vector work that does not depend on them
+        // (a compute wave is alone on its SIMD apart from a loader, so its own
+        // instruction order has to hide the latencies).
         auto tile = [&](int lt, auto bufc) __attribute__((always_inline)) {
             constexpr int buf = decltype(bufc)::value;  // == lt % 2
             const int t0 = st + TILE * lt, n = min(TILE, en - t0);
             lds_barrier();
             const float gl = sh.G[buf][0][63];
 
-            // S0 as fp16 B operands (k-step ks pairs state blocks 2 ks, 2 ks + 1)
-            half8 s16[2][KS];
-#pragma unroll
-            for (int sl = 0; sl < 2; ++sl)
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) s16[sl][ks] = to_half8(S[sl][2 * ks], S[sl][2 * ks + 1]);
-
-            // K S0^T: token rows 16 rb + 4 lg + e, state row 32 w + 16 sl + ln
-            f32x4 ks0[4][2];
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-                for (int sl = 0; sl < 2; ++sl) ks0[rb][sl] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                half8 ka[4];
+            auto kread = [&](int ks, half8(&ka)[4]) __attribute__((always_inline)) {
 #pragma unroll
                 for (int rb = 0; rb < 4; ++rb) {
                     const int row = 16 * rb + ln;
                     ka[rb] = as_half8(*(const u32x4 *)(&sh.K[buf][row * D + 8 * ((4 * ks + lg) ^ swz<D>(row))]));
                 }
+            };
+            auto qread = [&](int ks, half8(&qa)[4]) __attribute__((always_inline)) {
 #pragma unroll
-                for (int rb = 0; rb < 4; ++rb)
-#pragma unroll
-                    for (int sl = 0; sl < 2; ++sl) ks0[rb][sl] = mfma_f16(ka[rb], s16[sl][ks], ks0[rb][sl]);
-            }
-
-            // R = V - diag(Gamma) K S0^T; v[16 rb + 4 lg + e][32 w + 16 sl + ln] by transposing reads
-            half8 rf[2][2];
-#pragma unroll
-            for (int sl = 0; sl < 2; ++sl) {
-                f32x4 R[4];
-#pragma unroll
-                for (int rb = 0; rb < 4; ++rb) {
-                    const v4i16 vv = ds_read_tr16(&sh.V[buf][(16 * rb + 4 * lg + (ln >> 2)) * WIDE_VLD + 32 * w + 16 * sl +
-                                                            4 * (ln & 3)]);
-                    const float4 g4 = *(const float4 *)(&sh.G[buf][0][16 * rb + 4 * lg]);
-                    R[rb][0] = bf16_to_f32((uint16_t)vv[0]) - g4.x * ks0[rb][sl][0];
-                    R[rb][1] = bf16_to_f32((uint16_t)vv[1]) - g4.y * ks0[rb][sl][1];
-                    R[rb][2] = bf16_to_f32((uint16_t)vv[2]) - g4.z * ks0[rb][sl][2];
-                    R[rb][3] = bf16_to_f32((uint16_t)vv[3]) - g4.w * ks0[rb][sl][3];
-                }
-                rf[sl][0] = to_half8(R[0], R[1]);
-                rf[sl][1] = to_half8(R[2], R[3]);
-            }
-
-            // E = T diag(beta) R, then D_last E; both as fp16 B operands
-            half8 e16[2][2], d16[2][2];
-            {
-                half8 tf[6];
-#pragma unroll
-                for (int f = 0; f < 6; ++f) tf[f] = as_half8(sh.T[buf][f][lane]);
-#pragma unroll
-                for (int sl = 0; sl < 2; ++sl) {
-                    f32x4 E[4];
-#pragma unroll
-                    for (int rb = 0; rb < 4; ++rb) E[rb] = mfma_f16(tf[frag_index(rb, 0)], rf[sl][0], f32x4{0.f, 0.f, 0.f, 0.f});
-#pragma unroll
-                    for (int rb = 2; rb < 4; ++rb) E[rb] = mfma_f16(tf[frag_index(rb, 1)], rf[sl][1], E[rb]);
-                    e16[sl][0] = to_half8(E[0], E[1]);
-                    e16[sl][1] = to_half8(E[2], E[3]);
-#pragma unroll
-                    for (int rb = 0; rb < 4; ++rb) {
-                        const float4 d4 = *(const float4 *)(&sh.G[buf][1][16 * rb + 4 * lg]);
-                        E[rb][0] *= d4.x;
-                        E[rb][1] *= d4.y;
-                        E[rb][2] *= d4.z;
-                        E[rb][3] *= d4.w;
-                    }
-                    d16[sl][0] = to_half8(E[0], E[1]);
-                    d16[sl][1] = to_half8(E[2], E[3]);
-                }
-            }
-
-            // O = diag(Gamma) Q S0^T + P E, stored straight from the accumulators
-            // through a buffer resource covering the tile's n valid rows (before
-            // the update, so that the fp16 S0 dies here)
-            constexpr int ES = OUT_BF16 ? 2 : 4;
-            const uint32_t row_bytes = (uint32_t)a.H_v * D * ES;
-            const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-                (char *)a.o + (size_t)t0 * row_bytes, (short)0, (int)(row_bytes * (uint32_t)n), 0x00020000);
-#pragma unroll
-            for (int rb = 0; rb < 4; ++rb) {
-                f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
-#pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    const half8 qa = as_half8(sh.Q[buf][rb * KS + ks][lane]);
-#pragma unroll
-                    for (int sl = 0; sl < 2; ++sl) acc[sl] = mfma_f16(qa, s16[sl][ks], acc[sl]);
-                }
-                const float4 g4 = *(const float4 *)(&sh.G[buf][0][16 * rb + 4 * lg]);
-#pragma unroll
-                for (int sl = 0; sl < 2; ++sl) {
-                    acc[sl][0] *= g4.x;
-                    acc[sl][1] *= g4.y;
-                    acc[sl][2] *= g4.z;
-                    acc[sl][3] *= g4.w;
-                }
-                const half8 p0 = as_half8(sh.P[buf][frag_index(rb, 0)][lane]);
-#pragma unroll
-                for (int sl = 0; sl < 2; ++sl) acc[sl] = mfma_f16(p0, e16[sl][0], acc[sl]);
-                if (rb >= 2) {
-                    const half8 p1 = as_half8(sh.P[buf][frag_index(rb, 1)][lane]);
-#pragma unroll
-                    for (int sl = 0; sl < 2; ++sl) acc[sl] = mfma_f16(p1, e16[sl][1], acc[sl]);
-                }
-#pragma unroll
-                for (int sl = 0; sl < 2; ++sl) {
-                    const uint32_t col = (uint32_t)(j * D + 32 * w + 16 * sl + ln) * ES;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const uint32_t off = (uint32_t)(16 * rb + 4 * lg + e) * row_bytes + col;
-                        const float val = a.scale * acc[sl][e];
-                        if (OUT_BF16)
-                            __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, (__bf16)val), rs, off, 0, 0);
-                        else
-                            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, val), rs, off, 0, 0);
-                    }
-                }
-            }
-
-            // S = Gamma_last S0 + (D_last E)^T K
-#pragma unroll
-            for (int kb = 0; kb < NKB; ++kb) {
-                // K^T fragments by transposing reads (each used by both slices): source
-                // lane (ln, lg) addresses token 32 ks + 16 r + 4 lg + ln / 4 and dims
-                // 32 (kb / 2) + 8 (ln % 4) + 4 (kb % 2) .. + 3
-                half8 kt[2];
+                for (int rb = 0; rb < 4; ++rb) qa[rb] = as_half8(sh.Q[buf][rb * KS + ks][lane]);
+            };
+            // K^T fragments of state block kb by transposing reads (each used by both
+            // slices): source lane (ln, lg) addresses token 32 ks + 16 r + 4 lg + ln / 4
+            // and dims 32 (kb / 2) + 8 (ln % 4) + 4 (kb % 2) .. + 3
+            auto ktread = [&](int kb, half8(&kt)[2]) __attribute__((always_inline)) {
 #pragma unroll
                 for (int ks = 0; ks < 2; ++ks) {
                     const int r0 = 32 * ks + 4 * lg + (ln >> 2), r1 = r0 + 16;
@@ -275,15 +185,205 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                     kt[ks] = __builtin_bit_cast(half8, cat_u32x4(ds_read_tr16(&sh.K[buf][r0 * D + 8 * (ch ^ swz<D>(r0)) + hf]),
                                                                  ds_read_tr16(&sh.K[buf][r1 * D + 8 * (ch ^ swz<D>(r1)) + hf])));
                 }
+            };
+
+            // ---- (1) K S0^T (token rows 16 rb + 4 lg + e, state row 32 w + 16 sl + ln)
+            // from the fp16 copy of S0 (k-step ks pairs state blocks 2 ks, 2 ks + 1).
+            // Under it: the fp16 copy of the next k-step, and S <- Gamma_last S in place
+            // for the blocks already copied (from here on the fp32 S is only the
+            // update's accumulator).
+            half8 s16[2][KS];
+            f32x4 ks0[4][2];
+            half8 ka[2][4];
 #pragma unroll
-                for (int sl = 0; sl < 2; ++sl) {
-                    f32x4 sn;
+            for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) sn[e] = gl * S[sl][kb][e];
-                    sn = mfma_f16(kt[0], d16[sl][0], sn);
-                    S[sl][kb] = mfma_f16(kt[1], d16[sl][1], sn);
+                for (int sl = 0; sl < 2; ++sl) ks0[rb][sl] = f32x4{0.f, 0.f, 0.f, 0.f};
+            kread(0, ka[0]);
+#pragma unroll
+            for (int sl = 0; sl < 2; ++sl) s16[sl][0] = to_half8(S[sl][0], S[sl][1]);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                if (ks + 1 < KS) {
+                    kread(ks + 1, ka[(ks + 1) & 1]);
+#pragma unroll
+                    for (int sl = 0; sl < 2; ++sl) s16[sl][ks + 1] = to_half8(S[sl][2 * ks + 2], S[sl][2 * ks + 3]);
+                }
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+                    for (int sl = 0; sl < 2; ++sl) ks0[rb][sl] = mfma_f16(ka[ks & 1][rb], s16[sl][ks], ks0[rb][sl]);
+#pragma unroll
+                for (int sl = 0; sl < 2; ++sl)
+#pragma unroll
+                    for (int c = 0; c < 2; ++c)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) S[sl][2 * ks + c][e] *= gl;
+                if (ks + 1 < KS) WIDE_SG(SG_DSR, 4);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    WIDE_SG(SG_MFMA, 1);
+                    WIDE_SG(SG_VALU, 3);
                 }
             }
+            // operands of (2): q of the first k-step, Gamma, and v (transposed) of
+            // the first quarter of R
+            half8 qa[2][4];
+            v4i16 vv[2][2];
+            float4 g4[4];
+            // v[16 rb + 4 lg + e][32 w + 16 sl + ln], rb = 2 pr + h, for quarter (sl, pr)
+            auto vread = [&](int sl, int pr, v4i16(&vq)[2]) __attribute__((always_inline)) {
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+                    vq[h] = ds_read_tr16(&sh.V[buf][(16 * (2 * pr + h) + 4 * lg + (ln >> 2)) * WIDE_VLD + 32 * w + 16 * sl + 4 * (ln & 3)]);
+            };
+            qread(0, qa[0]);
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) g4[rb] = *(const float4 *)(&sh.G[buf][0][16 * rb + 4 * lg]);
+            vread(0, 0, vv[0]);
+            __builtin_amdgcn_sched_barrier(0);
+
+            // ---- (2) O^T = S0 Q^T, S0 as the A operand and q as the B operand: lane
+            // (ln, lg) holds state rows 32 w + 16 sl + 4 lg + e of token 16 rb + ln.
+            // Under it, a quarter of R = V - diag(Gamma) K S0^T per k-step (slice
+            // ks / 2, row blocks 2 (ks % 2), 2 (ks % 2) + 1), straight to fp16.
+            f32x4 oacc[4][2];
+            half8 rf[2][2];
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+                for (int sl = 0; sl < 2; ++sl) oacc[rb][sl] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                if (ks + 1 < KS) {
+                    qread(ks + 1, qa[(ks + 1) & 1]);
+                    vread((ks + 1) >> 1, (ks + 1) & 1, vv[(ks + 1) & 1]);
+                }
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+                    for (int sl = 0; sl < 2; ++sl) oacc[rb][sl] = mfma_f16(s16[sl][ks], qa[ks & 1][rb], oacc[rb][sl]);
+                {
+                    const int sl = ks >> 1, pr = ks & 1;
+                    f32x4 R[2];
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const int rb = 2 * pr + h;
+                        const v4i16 v = vv[ks & 1][h];
+                        R[h][0] = bf16_to_f32((uint16_t)v[0]) - g4[rb].x * ks0[rb][sl][0];
+                        R[h][1] = bf16_to_f32((uint16_t)v[1]) - g4[rb].y * ks0[rb][sl][1];
+                        R[h][2] = bf16_to_f32((uint16_t)v[2]) - g4[rb].z * ks0[rb][sl][2];
+                        R[h][3] = bf16_to_f32((uint16_t)v[3]) - g4[rb].w * ks0[rb][sl][3];
+                    }
+                    rf[sl][pr] = to_half8(R[0], R[1]);
+                }
+                if (ks + 1 < KS) WIDE_SG(SG_DSR, 6);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    WIDE_SG(SG_MFMA, 1);
+                    WIDE_SG(SG_VALU, 3);
+                }
+            }
+            // operands of (3) - (5): T diag(beta) and P fragments, D_last, the
+            // scale Gamma of each token, the first K^T fragments
+            half8 tf[6], pf[6], kt[2][2];
+            float4 d4[4];
+            float gs[4];
+#pragma unroll
+            for (int f = 0; f < 6; ++f) tf[f] = as_half8(sh.T[buf][f][lane]);
+#pragma unroll
+            for (int rb = 0; rb < 4; ++rb) {
+                d4[rb] = *(const float4 *)(&sh.G[buf][1][16 * rb + 4 * lg]);
+                gs[rb] = a.scale * sh.G[buf][0][16 * rb + ln];
+            }
+#pragma unroll
+            for (int f = 0; f < 6; ++f) pf[f] = as_half8(sh.P[buf][f][lane]);
+            ktread(0, kt[0]);
+            __builtin_amdgcn_sched_barrier(0);
+
+            // ---- (3) E = T diag(beta) R and D_last E (fp16 B operands) per slice,
+            // under them the scale Gamma of each token on (2)
+            half8 e16[2][2], d16[2][2];
+#pragma unroll
+            for (int sl = 0; sl < 2; ++sl) {
+                f32x4 E[4];
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) E[rb] = mfma_f16(tf[frag_index(rb, 0)], rf[sl][0], f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+                for (int rb = 2; rb < 4; ++rb) E[rb] = mfma_f16(tf[frag_index(rb, 1)], rf[sl][1], E[rb]);
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) oacc[rb][sl][e] *= gs[rb];
+                e16[sl][0] = to_half8(E[0], E[1]);
+                e16[sl][1] = to_half8(E[2], E[3]);
+#pragma unroll
+                for (int rb = 0; rb < 4; ++rb) {
+                    E[rb][0] *= d4[rb].x;
+                    E[rb][1] *= d4[rb].y;
+                    E[rb][2] *= d4[rb].z;
+                    E[rb][3] *= d4[rb].w;
+                }
+                d16[sl][0] = to_half8(E[0], E[1]);
+                d16[sl][1] = to_half8(E[2], E[3]);
+            }
+#pragma unroll
+            for (int i = 0; i < 12; ++i) {
+                WIDE_SG(SG_MFMA, 1);
+                WIDE_SG(SG_VALU, 4);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+
+            // ---- (4) + (5): O^T += (P E)^T = E^T P^T (E's B operand read as the A
+            // operand, P's A fragments as B operands; P carries the scale),
+            // interleaved with the update S = Gamma_last S0 + (D_last E)^T K.  A bf16
+            // o goes to LDS, four consecutive dims per lane (the loaders store it a
+            // tile later as whole rows: global stores from these waves would queue
+            // behind the loaders' tile loads in the CU's vector-memory path); an fp32
+            // o is stored at once through a buffer resource covering the tile's n
+            // valid rows.
+            constexpr int ES = OUT_BF16 ? 2 : 4;
+            const uint32_t row_bytes = (uint32_t)a.H_v * D * ES;
+            const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                (char *)a.o + (size_t)t0 * row_bytes, (short)0, (int)(row_bytes * (uint32_t)n), 0x00020000);
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) {
+                if (kb + 1 < NKB) ktread(kb + 1, kt[(kb + 1) & 1]);
+#pragma unroll
+                for (int sl = 0; sl < 2; ++sl) {
+                    S[sl][kb] = mfma_f16(kt[kb & 1][0], d16[sl][0], S[sl][kb]);
+                    S[sl][kb] = mfma_f16(kt[kb & 1][1], d16[sl][1], S[sl][kb]);
+                }
+                if (kb < 4) {
+                    const int rb = kb;
+#pragma unroll
+                    for (int sl = 0; sl < 2; ++sl) {
+                        oacc[rb][sl] = mfma_f16(e16[sl][0], pf[frag_index(rb, 0)], oacc[rb][sl]);
+                        if (rb >= 2) oacc[rb][sl] = mfma_f16(e16[sl][1], pf[frag_index(rb, 1)], oacc[rb][sl]);
+                    }
+#pragma unroll
+                    for (int sl = 0; sl < 2; ++sl) {
+                        if constexpr (OUT_BF16) {
+                            // into this wave's band of the v tile (o_stage_at), for the
+                            // loaders to store as whole rows
+                            const int r = 16 * rb + ln;
+                            *(u32x2 *)(&sh.V[buf][o_stage_at(r, 32 * w + 16 * sl + 4 * lg)]) =
+                                __builtin_bit_cast(u32x2, __builtin_convertvector(oacc[rb][sl], bf16x4));
+                        } else {
+                            const uint32_t off = (uint32_t)(16 * rb + ln) * row_bytes + (uint32_t)(j * D + 32 * w + 16 * sl + 4 * lg) * ES;
+                            store_o4(oacc[rb][sl], rs, off, std::false_type());
+                        }
+                    }
+                }
+                if (kb + 1 < NKB) WIDE_SG(SG_DSR, 4);
+                const int nm = 4 + (kb < 2 ? 2 : kb < 4 ? 4 : 0);
+                for (int i = 0; i < nm; ++i) {
+                    WIDE_SG(SG_MFMA, 1);
+                    WIDE_SG(SG_VALU, 2);
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
 
             // write signal: ||E row||^2 over each slice's 16 columns per token
             if (a.wsWrite) {
@@ -390,6 +490,26 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                 }
                 if (X < 2) sh.G[buf][X][lane] = s.g;
             };
+            // bf16 o of tile lt from the v buffer it was staged in (rows 16 X .. 16 X +
+            // 15, the rows this loader restages next): 16-byte pieces read back in
+            // order, stored as whole 256-byte rows; stores past a ragged tile's end
+            // fall outside the buffer resource and are dropped
+            auto store_o = [&](int lt, auto bufc) __attribute__((always_inline)) {
+                constexpr int buf = decltype(bufc)::value;  // == lt % 2
+                const int t0 = st + TILE * lt, n = min(TILE, en - t0);
+                const uint32_t row_bytes = (uint32_t)a.H_v * D * 2;
+                const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                    (char *)a.o + (size_t)t0 * row_bytes, (short)0, (int)(row_bytes * (uint32_t)n), 0x00020000);
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int r = 16 * X + RPI * c + lane / CH, ch = lane % CH;
+                    // dims 8 ch .. 8 ch + 7 = two 4-dim pieces, kept adjacent by the permutation
+                    // and swapped when (r / 4) % 2 == 1
+                    u32x4 v = *(const u32x4 *)(&sh.V[buf][o_stage_at(r, 8 * ch) & ~7]);
+                    if ((r >> 2) & 1) v = u32x4{v[2], v[3], v[0], v[1]};
+                    __builtin_amdgcn_raw_buffer_store_b128(v, rs, (uint32_t)r * row_bytes + (uint32_t)(j * D + 8 * ch) * 2, 0, 0);
+                }
+            };
             // drift: loader 3 adds the 8 slices' sums of a frame that ended in
             // the previous tile (fixed order) and writes them
             int frame = frame_base;
@@ -435,6 +555,7 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                 load(s0, 2);
                 auto step = [&](int it, WideLoad &s, auto bufc) __attribute__((always_inline)) {
                     lds_barrier();
+                    if (OUT_BF16 && it >= 1) store_o(it - 1, bufc);
                     if (it + 1 < n_tiles) stage(s, bufc);
                     load(s, it + 3);
                     drift_reduce(it);
