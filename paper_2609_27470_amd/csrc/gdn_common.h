@@ -33,7 +33,8 @@ struct GdnArgs {
     void *o;
     float scale;
     float *snapshots;
-    _Float16 *wsT, *wsP, *wsQ;
+    _Float16 *wsT, *wsP;
+    _Float16 *wsQ;  // fp16 q fragments for the per-slice kernel (null for the whole-head kernel)
     float *wsGam, *wsDrift;
     float *wsWrite;  // per-token sums of squares of E over the slice's columns, or null
     float *wsStart;  // [B][H_v][d][d] state at the current frame's start (whole-head kernel)
@@ -114,14 +115,11 @@ __device__ __forceinline__ int swz(int row) {
     return ((row & 1) << 2) | ((row >> 1) & 3);
 }
 
-// Four consecutive output values of one lane to o at byte offset off of the
-// buffer resource rs: as bf16 (one 8-byte store) or fp32 (one 16-byte store).
+// Four consecutive fp32 output values of one lane to o at byte offset off of
+// the buffer resource rs (one 16-byte store).
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ void store_o4(const f32x4 &v, __amdgpu_buffer_rsrc_t rs, uint32_t off, std::true_type) {
-    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, __builtin_convertvector(v, bf16x4)), rs, off, 0, 0);
-}
-__device__ __forceinline__ void store_o4(const f32x4 &v, __amdgpu_buffer_rsrc_t rs, uint32_t off, std::false_type) {
+__device__ __forceinline__ void store_o4_f32(const f32x4 &v, __amdgpu_buffer_rsrc_t rs, uint32_t off) {
     __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rs, off, 0, 0);
 }
 

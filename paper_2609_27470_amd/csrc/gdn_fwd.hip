@@ -126,13 +126,13 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
             const u32x4 q = row < n ? qv[c] : z;
             *(u32x4 *)(&Kl[row * D + 8 * (ch ^ swz<D>(row))]) = row < n ? kv[c] : z;
             *(u32x4 *)(&Ql[row * D + 8 * (ch ^ swz<D>(row))]) = q;
-            // q in fp16 for the output waves of the sequential kernel, in A-fragment
-            // order: row block row / 16, k-step ch / 4, lane (ch % 4) * 16 + row % 16.
-            // Like the T and P fragments it is stored nontemporally: the 336 MiB of
-            // fragments outgrow the caches before the sequential kernel reads them,
-            // and streaming them out made the forward 2 % faster
+            // q in fp16 for the output waves of the per-slice sequential kernel, in
+            // A-fragment order: row block row / 16, k-step ch / 4, lane (ch % 4) * 16 +
+            // row % 16 (the whole-head kernel converts q rows itself).  Like the T and
+            // P fragments it is stored nontemporally: the fragments outgrow the
+            // caches before the sequential kernel reads them
             const size_t fq = ((size_t)(row >> 4) * KS + (ch >> 2)) * 64 + (ch & 3) * 16 + (row & 15);
-            if (jbase == h * a.group)  // one writer per qk-head
+            if (a.wsQ && jbase == h * a.group)  // one writer per qk-head
                 __builtin_nontemporal_store(__builtin_bit_cast(u32x4, bf16x8_to_f16(q)), (u32x4 *)(a.wsQ + ((size_t)ti * a.H_k + h) * 64 * D + fq * 8));
         }
         if (w == 0) {
@@ -171,12 +171,6 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
             }
         }
     }
-    // P carries the output scale (o = scale (diag(Gamma) Q S0^T + P E)): one
-    // multiply here instead of one per output element in the sequential pass
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) gq[nb][e] *= a.scale;
     lds_barrier();  // K and Q tiles are dead from here on (A and T reuse them)
 
     // ---- per v-head of the qk-head's group: gates (wave 0), P from the Gram
@@ -217,7 +211,7 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
         }
     };
     // P (lower incl. diagonal) of query block w, scale Gamma_i / Gamma_j (q_i . k_j)
-    // for keys j <= i, as the A fragments (w, ks) of P E (k-step ks pairs key
+    // for keys j <= i (the output scale rides on P: o = scale diag(Gamma) Q S0^T + P E), as the A fragments (w, ks) of P E (k-step ks pairs key
     // blocks 2 ks, 2 ks + 1); block (nb, w): key 16 nb + 4 lg + e, query 16 w + ln
     auto pfrags = [&](int jj, int slot) __attribute__((always_inline)) {
         const size_t tv = (size_t)ti * a.H_v + jbase + jj;
@@ -229,7 +223,7 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
                 const float gjv[4] = {gj.x, gj.y, gj.z, gj.w};
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
-                    pk[e] = (nb < w || 4 * lg + e <= ln) ? __builtin_amdgcn_exp2f(gq_i - gjv[e]) * gq[nb][e] : 0.f;
+                    pk[e] = (nb < w || 4 * lg + e <= ln) ? __builtin_amdgcn_exp2f(gq_i - gjv[e]) * (a.scale * gq[nb][e]) : 0.f;
             }
             return pk;
         };
@@ -369,9 +363,8 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
 //                    leaves its share of the drift sums in LDS.
 //   waves 2 and 3, output:  one tile behind, O = scale diag(Gamma) Q S0^T + P E
 //                    (the prep pass folded the scale into P) for row blocks
-//                    {0, 1} and {2, 3}, as O^T so that a lane holds four
-//                    consecutive output dims of a token; they load q and P
-//                    themselves.
+//                    {0, 1} and {2, 3}; they load q (the fp16 fragments
+//                    of the prep pass) and P themselves.
 //   waves 4 - 7, loaders: each loads a quarter of the K rows, T diag(beta),
 //                    v rows and the decay factors of a tile three tiles ahead
 //                    and stages it in LDS one tile ahead.  The state waves read
@@ -658,7 +651,7 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
         // =============================================================== output
         // O = scale diag(Gamma) Q S0^T + P E (P carries the scale) for row blocks
         // {2 PR, 2 PR + 1}, one tile behind the state waves (Gamma from the
-        // loaders' LDS copy), computed transposed
+        // loaders' LDS copy)
         auto run = [&](auto prc) __attribute__((always_inline)) {
             constexpr int PR = decltype(prc)::value;
             constexpr int NP = PR == 0 ? 2 : 4;  // P fragments of the two row blocks
@@ -681,48 +674,53 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             auto compute = [&](const OutSet<D> &s, int lt, auto bufc) __attribute__((always_inline)) {
                 constexpr int buf = decltype(bufc)::value;  // == lt % 2
                 const int t0 = st + TILE * lt, n = min(TILE, en - t0);
-                // O^T blocks: S0 as the A operand and q as the B operand, so that lane
-                // (ln, lg) holds output dims v0 + 4 lg + e of token 16 (2 PR + r) + ln
                 f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) {
-                    const half8 as = as_half8(sh.S16[lt % 3][ks][lane]);
+                    const half8 bs = as_half8(sh.S16[lt % 3][ks][lane]);
 #pragma unroll
-                    for (int r = 0; r < 2; ++r) acc[r] = mfma_f16(as, as_half8(s.q[r][ks]), acc[r]);
+                    for (int r = 0; r < 2; ++r) acc[r] = mfma_f16(as_half8(s.q[r][ks]), bs, acc[r]);
                 }
-                // scale Gamma of the token (P carries the scale already)
+                // scale Gamma of each token (P carries the scale already)
 #pragma unroll
                 for (int r = 0; r < 2; ++r) {
-                    const float gs = a.scale * sh.G[lt % 3][0][16 * (2 * PR + r) + ln];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) acc[r][e] *= gs;
+                    const float4 g4 = *(const float4 *)(&sh.G[lt % 3][0][16 * (2 * PR + r) + 4 * lg]);
+                    acc[r][0] *= a.scale * g4.x;
+                    acc[r][1] *= a.scale * g4.y;
+                    acc[r][2] *= a.scale * g4.z;
+                    acc[r][3] *= a.scale * g4.w;
                 }
-                // + (P E)^T = E^T P^T: the E B operand read as the A operand, the P
-                // A fragments as B operands
                 const half8 ef0 = as_half8(sh.E[buf][0][lane]);
                 if (PR == 0) {
-                    acc[0] = mfma_f16(ef0, as_half8(s.p[0]), acc[0]);
-                    acc[1] = mfma_f16(ef0, as_half8(s.p[1]), acc[1]);
+                    acc[0] = mfma_f16(as_half8(s.p[0]), ef0, acc[0]);
+                    acc[1] = mfma_f16(as_half8(s.p[1]), ef0, acc[1]);
                 } else {
                     const half8 ef1 = as_half8(sh.E[buf][1][lane]);
-                    acc[0] = mfma_f16(ef0, as_half8(s.p[0]), acc[0]);
-                    acc[1] = mfma_f16(ef0, as_half8(s.p[2]), acc[1]);
-                    acc[0] = mfma_f16(ef1, as_half8(s.p[1]), acc[0]);
-                    acc[1] = mfma_f16(ef1, as_half8(s.p[3]), acc[1]);
+                    acc[0] = mfma_f16(as_half8(s.p[0]), ef0, acc[0]);
+                    acc[1] = mfma_f16(as_half8(s.p[2]), ef0, acc[1]);
+                    acc[0] = mfma_f16(as_half8(s.p[1]), ef1, acc[0]);
+                    acc[1] = mfma_f16(as_half8(s.p[3]), ef1, acc[1]);
                 }
-                // o straight from the accumulators, 4 consecutive dims per lane,
-                // through a buffer resource covering the tile's n valid rows: stores
-                // past a ragged tile's end fall outside it and are dropped
+                // o straight from the accumulators (lane (ln, lg): rows 16 r + 4 lg + e
+                // of the wave's 32, column v0 + ln: the 16 lanes of a row write 32
+                // contiguous bytes), through a buffer resource covering the tile's n
+                // valid rows: stores past a ragged tile's end fall outside it and are
+                // dropped
                 constexpr int ES = OUT_BF16 ? 2 : 4;
                 const uint32_t row_bytes = (uint32_t)a.H_v * D * ES;
                 const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
                     (char *)a.o + (size_t)t0 * row_bytes, (short)0, (int)(row_bytes * (uint32_t)n), 0x00020000);
-                const uint32_t col = (uint32_t)(j * D + v0 + 4 * lg) * ES;
+                const uint32_t col = (uint32_t)(j * D + v0 + ln) * ES;
 #pragma unroll
-                for (int r = 0; r < 2; ++r) {
-                    const uint32_t off = (uint32_t)(32 * PR + 16 * r + ln) * row_bytes + col;
-                    store_o4(acc[r], rs, off, std::integral_constant<bool, OUT_BF16>());
-                }
+                for (int r = 0; r < 2; ++r)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const uint32_t off = (uint32_t)(32 * PR + 16 * r + 4 * lg + e) * row_bytes + col;
+                        if (OUT_BF16)
+                            __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(unsigned short, (__bf16)acc[r][e]), rs, off, 0, 0);
+                        else
+                            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[r][e]), rs, off, 0, 0);  // (a bit cast of the vector element itself compiles to element 0)
+                    }
             };
             // iteration it computes tile it - 1 and then loads tile it + 1 into the
             // same register set (set (it + 1) % 2)
@@ -1020,8 +1018,8 @@ GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, i
     off = align256(off + (size_t)w.tiles_max * H_v * TP_HALVES * sizeof(_Float16));
     w.offP = off;
     off = align256(off + (size_t)w.tiles_max * H_v * TP_HALVES * sizeof(_Float16));
-    w.offQ = off;
-    off = align256(off + (size_t)w.tiles_max * H_k * 64 * d * sizeof(_Float16));
+    w.offQ = off;  // fp16 q fragments, only for the per-slice kernel
+    if (!use_wide(B, H_v, d)) off = align256(off + (size_t)w.tiles_max * H_k * 64 * d * sizeof(_Float16));
     w.offGam = off;
     off = align256(off + (size_t)w.tiles_max * H_v * 128 * sizeof(float));
     w.offDrift = off;
@@ -1057,7 +1055,7 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     a.snapshots = p.snapshots;
     a.wsT = p.wsT;
     a.wsP = p.wsP;
-    a.wsQ = p.wsQ;
+    a.wsQ = use_wide(p.B, p.H_v, D) ? nullptr : p.wsQ;
     a.wsGam = p.wsGam;
     a.wsWrite = p.write_partials ? p.wsWrite : nullptr;
     a.wsStart = p.wsStart;

@@ -15,8 +15,8 @@
 //       the update S = Gamma_last S0 + (D_last E)^T K.  Every fragment read
 //       from LDS (rows of K, Q, T, P, K^T) feeds both slices.
 //   waves 4-7 (loaders): load the tile two tiles ahead and stage it in LDS
-//       one tile ahead (K converted to fp16, the q, T and P fragments of the
-//       prep pass, v rows, Gamma and D_last), and store the previous tile's
+//       one tile ahead (K and q rows converted to fp16, the T and P fragments
+//       of the prep pass, v rows, Gamma and D_last), and store the previous tile's
 //       bf16 o, which the compute waves left in LDS, as whole rows; loader 3
 //       also adds the frame-end drift sums of the 8 slices (fixed order) and
 //       writes them, per slice or per head, with no exchange between
@@ -50,7 +50,7 @@ constexpr int SG_VALU = 0x2, SG_MFMA = 0x8, SG_DSR = 0x100;
 
 struct WideShared {
     uint16_t K[2][64 * 128];  // K tile (fp16), row-major, 16-byte chunks XOR-swizzled by row (swz)
-    u32x4 Q[2][16][64];       // q (fp16) A-fragments [row block * 4 + k-step][lane], as the prep pass wrote them
+    uint16_t Q[2][64 * 128];  // q tile (fp16), laid out like K
     u32x4 T[2][6][64];        // T diag(beta) A-fragments
     u32x4 P[2][6][64];        // P A-fragments
     uint16_t V[2][64 * WIDE_VLD];  // v rows (bf16)
@@ -58,9 +58,9 @@ struct WideShared {
     float2 DR[2][4][2][64];   // frame-end drift sums per [frame % 2][compute wave][slice][lane]
 };
 
-// One loader's share of a tile: K rows 16 X .. 16 X + 15, the q fragments of
-// row block X, v rows 16 X .. 16 X + 15, T and P fragments {2 X, 2 X + 1}
-// (X < 2) or {4 + X - 2}; loader 0 also Gamma, loader 1 D_last.
+// One loader's share of a tile: K, q and v rows 16 X .. 16 X + 15, T and P
+// fragments {2 X, 2 X + 1} (X < 2) or {4 + X - 2}; loader 0 also Gamma,
+// loader 1 D_last.
 struct WideLoad {
     u32x4 k[4], q[4], v[4], t[2], p[2];
     float g;
@@ -172,7 +172,10 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
             };
             auto qread = [&](int ks, half8(&qa)[4]) __attribute__((always_inline)) {
 #pragma unroll
-                for (int rb = 0; rb < 4; ++rb) qa[rb] = as_half8(sh.Q[buf][rb * KS + ks][lane]);
+                for (int rb = 0; rb < 4; ++rb) {
+                    const int row = 16 * rb + ln;
+                    qa[rb] = as_half8(*(const u32x4 *)(&sh.Q[buf][row * D + 8 * ((4 * ks + lg) ^ swz<D>(row))]));
+                }
             };
             // K^T fragments of state block kb by transposing reads (each used by both
             // slices): source lane (ln, lg) addresses token 32 ks + 16 r + 4 lg + ln / 4
@@ -372,7 +375,7 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                                 __builtin_bit_cast(u32x2, __builtin_convertvector(oacc[rb][sl], bf16x4));
                         } else {
                             const uint32_t off = (uint32_t)(16 * rb + ln) * row_bytes + (uint32_t)(j * D + 32 * w + 16 * sl + 4 * lg) * ES;
-                            store_o4(oacc[rb][sl], rs, off, std::false_type());
+                            store_o4_f32(oacc[rb][sl], rs, off);
                         }
                     }
                 }
@@ -455,16 +458,15 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                 const int t0 = st + TILE * lt, n = min(TILE, en - t0);
                 const size_t tv = (size_t)(tile_base + lt) * a.H_v + j;
                 const uint16_t *kb = a.k + (size_t)t0 * a.H_k * D + (size_t)qh * D + 8 * (lane % CH);
+                const uint16_t *qb = a.q + (size_t)t0 * a.H_k * D + (size_t)qh * D + 8 * (lane % CH);
                 const uint16_t *vb = a.v + ((size_t)t0 * a.H_v + j) * D + 8 * (lane % CH);
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
                     const uint32_t r = (uint32_t)min(16 * X + RPI * c + lane / CH, n - 1);
                     s.k[c] = *(const u32x4 *)(kb + r * (uint32_t)a.H_k * D);
+                    s.q[c] = *(const u32x4 *)(qb + r * (uint32_t)a.H_k * D);
                     s.v[c] = *(const u32x4 *)(vb + r * (uint32_t)a.H_v * D);
                 }
-                const u32x4 *qb = (const u32x4 *)(a.wsQ + ((size_t)(tile_base + lt) * a.H_k + qh) * 64 * D);
-#pragma unroll
-                for (int c = 0; c < 4; ++c) s.q[c] = qb[(X * KS + c) * 64 + lane];
                 const u32x4 *tb = (const u32x4 *)(a.wsT + tv * TP_HALVES);
                 const u32x4 *pb = (const u32x4 *)(a.wsP + tv * TP_HALVES);
 #pragma unroll
@@ -480,8 +482,8 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                 for (int c = 0; c < 4; ++c) {
                     const int row = 16 * X + RPI * c + lane / CH, ch = lane % CH;
                     *(u32x4 *)(&sh.K[buf][row * D + 8 * (ch ^ swz<D>(row))]) = __builtin_bit_cast(u32x4, bf16x8_to_f16(s.k[c]));
+                    *(u32x4 *)(&sh.Q[buf][row * D + 8 * (ch ^ swz<D>(row))]) = __builtin_bit_cast(u32x4, bf16x8_to_f16(s.q[c]));
                     *(u32x4 *)(&sh.V[buf][row * WIDE_VLD + 8 * ch]) = s.v[c];
-                    sh.Q[buf][X * KS + c][lane] = s.q[c];
                 }
 #pragma unroll
                 for (int c = 0; c < NT; ++c) {

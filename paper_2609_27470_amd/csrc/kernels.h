@@ -25,7 +25,7 @@ struct GdnLaunch {
     // workspace pieces
     _Float16 *wsT;      // [tiles_max][H_v][6][64][8]  T diag(beta), fp16 A-fragments
     _Float16 *wsP;      // [tiles_max][H_v][6][64][8]  D (.) tril(Q K^T), fp16 A-fragments
-    _Float16 *wsQ;      // [tiles_max][H_k][4][d/32][64][8] q in fp16, A-fragment order (zero past a ragged tile's end)
+    _Float16 *wsQ;      // [tiles_max][H_k][4][d/32][64][8] q in fp16, A-fragment order, for the per-slice kernel only
     float *wsGam;       // [tiles_max][H_v][2][64]   Gamma_r = exp(gamma_r), D_last,r = exp(gamma_last - gamma_r)
     float *wsDrift;     // [n_frames][H_v][n_split][2] (one pair per slice)
     float *wsWrite;     // [H_v][n_split][T_total] per-token ||E row||^2 over each slice's columns

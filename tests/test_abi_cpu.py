@@ -60,6 +60,12 @@ def test_gdn_workspace_size(ds):
     assert nb >= tiles * 32 * per + qh
     assert nb <= tiles * 32 * per + qh + 32 * 32 * 8 * 2 * 4 + 4096   # + drift sums per slice
     assert nw - nb >= wr and nw - nb <= wr + 256          # the norm area only when the signal is asked for
+    # 256 (stream, v-head) pairs run whole-head: no fp16 q tiles, a frame-start state per head instead
+    sw = ds.gdn_shape([4096] * 8, 16, 32, 128, 1024)
+    tw = (8 * 4096 + 63 * 8) // 64   # tiles_max: room for one ragged tile per stream
+    nbw = ds.gdn_workspace_bytes(sw)
+    assert nbw >= tw * 32 * per + 8 * 32 * 128 * 128 * 4
+    assert nbw <= tw * 32 * per + 8 * 32 * 128 * 128 * 4 + 4 * 32 * 8 * 8 * 2 * 4 + 8192
     bad = ds.gdn_shape([64], 1, 1, 96, 64)
     assert ds.gdn_workspace_bytes(bad) == 0
 
