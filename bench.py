@@ -508,7 +508,8 @@ def main():
     ap.add_argument("--quick", action="store_true", help="headline step only (no per-workload records)")
     ap.add_argument("--step-only", action="store_true",
                     help="time the headline step and stop (short runs under counters)")
-    ap.add_argument("--only", choices=["tiny", "single_layer", "stack", "varlen", "eviction_loop"], default=None,
+    ap.add_argument("--only", choices=["tiny", "single_layer", "stack", "varlen", "eviction_loop", "streaming"],
+                    default=None,
                     help="time one workload's record and print it alone (for profiling runs)")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="only run a plain device copy of this many bytes (counter calibration)")
@@ -535,6 +536,8 @@ def main():
             rec = bench_tiny(ds, dev, stream, 200)
         elif args.only == "varlen":
             rec = bench_varlen(ds, dev, stream)
+        elif args.only == "streaming":
+            rec = streaming_bench(ds, dev, stream, args.steps)
         else:
             pool = make_pool(dev)
             rec = (bench_stack if args.only == "stack" else bench_eviction_loop)(ds, dev, stream, pool)

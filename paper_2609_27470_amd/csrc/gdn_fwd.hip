@@ -29,7 +29,7 @@
 namespace ds {
 
 // ============================================================================
-// gdn_prep: one workgroup per (tile, qk-head).  The K and Q rows of the tile
+// The prep pass (prep_tile), per tile and qk-head.  The K and Q rows of the tile
 // are loaded once as whole 16-byte chunks and staged in LDS; the Gram blocks
 // K K^T and (K Q^T) run on bf16 matrix cores (exact bf16 inputs, fp32
 // accumulation) and stay in registers.  Then, for every v-head of the group
@@ -42,54 +42,54 @@ namespace ds {
 // 39 KiB of LDS and at most 128 VGPRs, so that four workgroups share a CU.
 // ============================================================================
 template <int D>
-__global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
-    constexpr int KS = D / 32;   // 32-wide k-steps over the head dim
-    constexpr int CH = D / 8;    // 16-byte chunks per K or Q row
-    constexpr int NKB = D / 16;
-    constexpr int RPI = 64 / CH;  // rows per 64-lane row load
-    constexpr int NI = 16 / RPI;  // row loads per wave (16 rows each)
-    constexpr int ALD = 68;       // floats per LDS row of A and T (bank-conflict-free writes)
-    constexpr int RB = (64 * D * 2 > 64 * ALD * 4) ? 64 * D * 2 : 64 * ALD * 4;
+struct PrepLds {
+    static constexpr int ALD = 68;  // floats per LDS row of A and T (bank-conflict-free writes)
+    static constexpr int RB = (64 * D * 2 > 64 * ALD * 4) ? 64 * D * 2 : 64 * ALD * 4;
     // K and Q tiles while the Gram blocks are formed, then A and T (39.4 KiB
     // in all for d = 128: four workgroups fit in a CU's LDS)
-    __shared__ __align__(16) char reg_k[RB], reg_q[RB];
-    __shared__ float Ys[4][256];
-    __shared__ __align__(16) float gam_s[2][64];   // log2 Gamma and beta of up to two v-heads
-    __shared__ __align__(16) float beta_s[2][64];
-    uint16_t *Kl = (uint16_t *)reg_k, *Ql = (uint16_t *)reg_q;
-    float *As = (float *)reg_k, *Ts = (float *)reg_q;
+    __align__(16) char reg_k[RB];
+    __align__(16) char reg_q[RB];
+    float Ys[4][256];
+    __align__(16) float gam_s[2][64];   // log2 Gamma and beta of up to two v-heads
+    __align__(16) float beta_s[2][64];
+};
 
-    // tile; qk-head h and the v-heads jbase .. jbase + gcount - 1 of its group
-    // (the whole group, or with one workgroup per v-head for small launches,
-    // which halves a workgroup's latency at the cost of a second Gram product)
-    // The grid is one-dimensional and tile-major per XCD (dispatch deals
-    // workgroups to the 8 XCDs in turn): the workgroups of every head of one
-    // tile run on one XCD one after another, so the gate rows of a token
-    // (all v-heads in one line) are fetched into one L2 once.
-    const int nhy = a.prep_per_vhead ? a.H_v : a.H_k;
-    const int bid = blockIdx.x, slot = bid >> 3;
-    const int ti = (slot / nhy) * 8 + (bid & 7), hy = slot % nhy;
-    const int h = a.prep_per_vhead ? hy / a.group : hy;
-    const int jbase = a.prep_per_vhead ? hy : h * a.group;
-    const int gcount = a.prep_per_vhead ? 1 : a.group;
-    if (ti == 0 && hy == 0 && a.drift_zero) {
-        // set-up for the sequential kernel's drift output: slice counters of
-        // the in-kernel reduction to zero, frames past the real count to zero
-        if (a.drift_out)
-            for (int i = threadIdx.x; i < a.st.B * a.H_v; i += 256) a.drift_cnt[i] = 0u;
-        int real = 0;
-        for_streams(a.st, [&](int, int s0, int e0) {
-            real += frames_in(e0 - s0, a.frame_len);
-            return false;
-        });
-        const int per = a.drift_zero_per_frame;
-        for (int i = min(real, a.n_frames) * per + (int)threadIdx.x; i < a.n_frames * per; i += 256)
-            *(float2 *)(a.drift_zero + 2 * (size_t)i) = float2{0.f, 0.f};
-    }
-    int t0 = 0, n = 0;
-    if (!locate_tile(a.st, ti, t0, n)) return;
-    const int tid = threadIdx.x, lane = tid & 63, ln = lane & 15, lg = lane >> 4;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+// Set-up for the sequential kernel's drift output by threads tid (of nt):
+// slice counters of the in-kernel reduction to zero (with the per-head sums),
+// the pairs of frames past the real count to zero.
+__device__ __forceinline__ void drift_setup(const GdnArgs &a, int tid, int nt) {
+    if (a.drift_out)
+        for (int i = tid; i < a.st.B * a.H_v; i += nt) a.drift_cnt[i] = 0u;
+    int real = 0;
+    for_streams(a.st, [&](int, int s0, int e0) {
+        real += frames_in(e0 - s0, a.frame_len);
+        return false;
+    });
+    const int per = a.drift_zero_per_frame;
+    for (int i = min(real, a.n_frames) * per + tid; i < a.n_frames * per; i += nt)
+        *(float2 *)(a.drift_zero + 2 * (size_t)i) = float2{0.f, 0.f};
+}
+
+// The prep of tile ti (tokens t0 .. t0 + n - 1 of the packed sequence) for
+// qk-head h and the v-heads jbase .. jbase + gcount - 1 of its group, by four
+// waves w = 0 .. 3 with the LDS block L.  Every call passes the same barriers
+// (lds_barrier, workgroup-wide), so that two groups of four waves of one
+// workgroup can each run a tile side by side.  write_q: this call writes the
+// tile's fp16 q fragments (when the workspace has them).
+template <int D>
+__device__ __forceinline__ void prep_tile(const GdnArgs &a, int ti, int t0, int n, int h, int jbase, int gcount,
+                                          PrepLds<D> &L, int w, int lane, bool write_q) {
+    constexpr int KS = D / 32;   // 32-wide k-steps over the head dim
+    constexpr int CH = D / 8;    // 16-byte chunks per K or Q row
+    constexpr int RPI = 64 / CH;  // rows per 64-lane row load
+    constexpr int NI = 16 / RPI;  // row loads per wave (16 rows each)
+    constexpr int ALD = PrepLds<D>::ALD;
+    uint16_t *Kl = (uint16_t *)L.reg_k, *Ql = (uint16_t *)L.reg_q;
+    float *As = (float *)L.reg_k, *Ts = (float *)L.reg_q;
+    float(&Ys)[4][256] = L.Ys;
+    float(&gam_s)[2][64] = L.gam_s;
+    float(&beta_s)[2][64] = L.beta_s;
+    const int tid = 64 * w + lane, ln = lane & 15, lg = lane >> 4;
 
     constexpr int MAXG = 2;  // v-heads per qk-head whose gates are loaded with K and Q (more: loaded in turn)
 
@@ -132,7 +132,7 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
             // P fragments it is stored nontemporally: the fragments outgrow the
             // caches before the sequential kernel reads them
             const size_t fq = ((size_t)(row >> 4) * KS + (ch >> 2)) * 64 + (ch & 3) * 16 + (row & 15);
-            if (a.wsQ && jbase == h * a.group)  // one writer per qk-head
+            if (a.wsQ && write_q)
                 __builtin_nontemporal_store(__builtin_bit_cast(u32x4, bf16x8_to_f16(q)), (u32x4 *)(a.wsQ + ((size_t)ti * a.H_k + h) * 64 * D + fq * 8));
         }
         if (w == 0) {
@@ -346,6 +346,31 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
 }
 
 // ============================================================================
+// gdn_prep: one workgroup per (tile, qk-head), or per (tile, v-head) for small
+// launches; the work of a tile is prep_tile.
+// ============================================================================
+template <int D>
+__global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
+    __shared__ __align__(16) PrepLds<D> L;
+    // The grid is one-dimensional and tile-major per XCD (dispatch deals
+    // workgroups to the 8 XCDs in turn): the workgroups of every head of one
+    // tile run on one XCD one after another, so the gate rows of a token
+    // (all v-heads in one line) are fetched into one L2 once.
+    const int nhy = a.prep_per_vhead ? a.H_v : a.H_k;
+    const int bid = blockIdx.x, slot = bid >> 3;
+    const int ti = (slot / nhy) * 8 + (bid & 7), hy = slot % nhy;
+    const int h = a.prep_per_vhead ? hy / a.group : hy;
+    const int jbase = a.prep_per_vhead ? hy : h * a.group;
+    const int gcount = a.prep_per_vhead ? 1 : a.group;
+    if (ti == 0 && hy == 0 && a.drift_zero) drift_setup(a, threadIdx.x, 256);
+    int t0 = 0, n = 0;
+    if (!locate_tile(a.st, ti, t0, n)) return;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    // one writer of the q fragments per qk-head
+    prep_tile<D>(a, ti, t0, n, h, jbase, gcount, L, w, threadIdx.x & 63, jbase == h * a.group);
+}
+
+// ============================================================================
 // gdn_seq: one workgroup of 8 waves per (stream, v-head, 16 consecutive rows
 // of S):
 //   waves 0 and 1, state:  carry the recurrence for the 16 rows of S in fp32
@@ -434,13 +459,19 @@ struct OutSet {
     u32x4 p[4];          // P fragments of the two row blocks (2 or 4 used)
 };
 
-template <int D, bool OUT_BF16, bool DRIFT>
+template <int D, bool OUT_BF16, bool DRIFT, bool FUSED>
 __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
     constexpr int KS = D / 32;   // k-steps over the head dim
     constexpr int NKB = D / 16;  // 16-row blocks of S^T
     constexpr int HKS = KS / 2, HKB = NKB / 2;  // per state wave
     using SH = SeqShared<D>;
-    __shared__ __align__(16) SH sh;
+    // FUSED (calls of at most two tiles): the prep of the workgroup's own tiles
+    // runs first, in two LDS blocks that alias the sequential kernel's
+    constexpr int NPG = 2;  // groups of four waves forming one tile's prep each
+    constexpr size_t SMEM = !FUSED ? sizeof(SH)
+                            : (sizeof(SH) > NPG * sizeof(PrepLds<D>) ? sizeof(SH) : NPG * sizeof(PrepLds<D>));
+    __shared__ __align__(16) char smem[SMEM];
+    SH &sh = *reinterpret_cast<SH *>(smem);
 
     // the wave index in a scalar register: branches on it are then plain jumps
     // rather than masked code (matrix-core ops ignore the execution mask)
@@ -479,6 +510,27 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
     });
     const int len = en - st;
     const int n_tiles = (len + TILE - 1) / TILE;
+
+    if constexpr (FUSED) {
+        // Small call, one launch: waves 4 g .. 4 g + 3 form the prep of tile g of
+        // this v-head (the same barriers in both groups; with one tile the
+        // second group takes it again) and write it to the workspace as the
+        // prep pass would.  Every workgroup of the v-head (and, for q, of the
+        // qk-head) writes the same bytes, so it may read its own copy whoever
+        // wrote last.  A workgroup-scope release / acquire then orders those
+        // stores before the loads below.
+        if (blockIdx.x == 0 && a.drift_zero) drift_setup(a, tid, 64 * 4 * NPG);
+        PrepLds<D> *pl = reinterpret_cast<PrepLds<D> *>(smem);
+        const int grp = w >> 2;
+        if (n_tiles > 0) {
+            const int lt = min(grp, n_tiles - 1);
+            const int t0 = st + TILE * lt;
+            prep_tile<D>(a, tile_base + lt, t0, min(TILE, en - t0), qh, j, 1, pl[grp], w & 3, lane, true);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    }
 
     if (w < 2) {
         // ================================================================ state
@@ -1078,7 +1130,14 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     // (1024-token calls: 13.4 -> see the kernel trace; one streamed chunk:
     // 11.2 -> 8.6 us).  Longer calls share the Gram products of a qk-head.
     a.prep_per_vhead = a.group > 1 && (long long)p.tiles_max * p.H_v <= 1024;
-    if (p.tiles_max > 0) {
+    // calls of at most two tiles on the per-slice kernel (most streamed chunks)
+    // form their prep inside it: one launch per layer, 16.1 instead of 18.4 us
+    // a layer at 24 layers x 128 tokens.  (With three tiles a second prep round,
+    // or a third group of waves, costs what the launch saves.)  Not with the
+    // per-head drift sums, whose slice counters the prep pass clears before any
+    // sequential workgroup runs.
+    const bool one_launch = !use_wide(p.B, p.H_v, D) && p.tiles_max > 0 && p.tiles_max <= 2 && !fused_drift;
+    if (p.tiles_max > 0 && !one_launch) {
         // tiles rounded up to a multiple of 8 (workgroups past the last tile exit)
         const long long n_prep = (long long)((p.tiles_max + 7) / 8) * 8 * (a.prep_per_vhead ? p.H_v : p.H_k);
         hipLaunchKernelGGL(gdn_prep_kernel<D>, dim3((unsigned)n_prep), dim3(256), 0, stream, a);
@@ -1099,17 +1158,25 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
         return e;
     }
     const int n_wg = p.B * p.H_v * p.n_split;
-    if (p.o_bf16) {
-        if (drift)
-            hipLaunchKernelGGL((gdn_seq_kernel<D, true, true>), dim3(n_wg), dim3(512), 0, stream, a);
-        else
-            hipLaunchKernelGGL((gdn_seq_kernel<D, true, false>), dim3(n_wg), dim3(512), 0, stream, a);
-    } else {
-        if (drift)
-            hipLaunchKernelGGL((gdn_seq_kernel<D, false, true>), dim3(n_wg), dim3(512), 0, stream, a);
-        else
-            hipLaunchKernelGGL((gdn_seq_kernel<D, false, false>), dim3(n_wg), dim3(512), 0, stream, a);
-    }
+    auto seq = [&](auto fc) {
+        constexpr bool F = decltype(fc)::value;
+        const int nt = 512;
+        if (p.o_bf16) {
+            if (drift)
+                hipLaunchKernelGGL((gdn_seq_kernel<D, true, true, F>), dim3(n_wg), dim3(nt), 0, stream, a);
+            else
+                hipLaunchKernelGGL((gdn_seq_kernel<D, true, false, F>), dim3(n_wg), dim3(nt), 0, stream, a);
+        } else {
+            if (drift)
+                hipLaunchKernelGGL((gdn_seq_kernel<D, false, true, F>), dim3(n_wg), dim3(nt), 0, stream, a);
+            else
+                hipLaunchKernelGGL((gdn_seq_kernel<D, false, false, F>), dim3(n_wg), dim3(nt), 0, stream, a);
+        }
+    };
+    if (one_launch)
+        seq(std::true_type());
+    else
+        seq(std::false_type());
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (p.drift_partials && p.n_frames > 0 && p.tiles_max == 0) {
