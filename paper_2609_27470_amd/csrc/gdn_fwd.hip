@@ -901,20 +901,18 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
             };
             // write signal: ||E row||^2 over the slice's 16 columns for every token
             // of tile it - 1, from the E the state waves left in LDS (valid until
-            // they write that buffer again in tile it + 1), one store per k-step.
-            // Loader 3 has slack at the barrier; on the output waves this cost
-            // every tile of the chain
+            // they write that buffer again in tile it + 1): loader 2 takes the
+            // tokens of k-step 0, loader 3 those of k-step 1 (loaders have slack at
+            // the barrier; on the output waves this cost every tile of the chain)
             auto write_norms = [&](int it) __attribute__((always_inline)) {
-                if (X != 3 || it < 1 || !a.wsWrite) return;
+                if (X < 2 || it < 1 || !a.wsWrite) return;
+                constexpr int ks = X - 2;
                 const int lt = it - 1;
                 const int t0 = st + TILE * lt, n = min(TILE, en - t0);
                 float *wb = a.wsWrite + ((size_t)j * a.n_split + sl) * a.st.T + t0;
-#pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
-                    const float wsum = row_sq_sum16(as_half8(sh.E[lt & 1][ks][lane]), ln);
-                    const int i = ln >> 1, tok = 32 * ks + 16 * (i >> 2) + 4 * lg + (i & 3);
-                    if ((ln & 1) == 0 && tok < n) wb[tok] = wsum;
-                }
+                const float wsum = row_sq_sum16(as_half8(sh.E[lt & 1][ks][lane]), ln);
+                const int i = ln >> 1, tok = 32 * ks + 16 * (i >> 2) + 4 * lg + (i & 3);
+                if ((ln & 1) == 0 && tok < n) wb[tok] = wsum;
             };
             // tile t lives in register set t % 2 and LDS buffer t % 2.  Iteration it
             // stages tile it + 1 and then loads tile it + 3 into the set just freed.
