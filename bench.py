@@ -484,15 +484,29 @@ def bench_varlen(ds, dev, stream):
     return rec
 
 
+FORWARD_SOURCES = ("gdn_common.h", "gdn_fwd.hip", "gdn_wide.hip")
+
+
+def forward_fingerprint():
+    """sha256 over the forward's kernel sources (in this order), or None."""
+    h = hashlib.sha256()
+    for f in FORWARD_SOURCES:
+        path = os.path.join(ROOT, "paper_2609_27470_amd", "csrc", f)
+        if not os.path.exists(path):
+            return None
+        h.update(open(path, "rb").read())
+    return h.hexdigest()
+
+
 def committed_record(name):
     """A figure measured by a committed counter run (profiles/), used only while
-    the forward's source is the one it was measured with."""
+    the forward's sources are the ones it was measured with."""
     tf = os.path.join(ROOT, "profiles", name)
-    src = os.path.join(ROOT, "paper_2609_27470_amd", "csrc", "gdn_fwd.hip")
-    if os.path.exists(tf) and os.path.exists(src):
+    fp = forward_fingerprint()
+    if os.path.exists(tf) and fp:
         try:
             rec = json.load(open(tf))
-            if rec.get("source_sha256") == hashlib.sha256(open(src, "rb").read()).hexdigest():
+            if rec.get("source_sha256") == fp:
                 return rec
         except (OSError, ValueError):
             return None
