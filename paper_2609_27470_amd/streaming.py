@@ -22,7 +22,10 @@ A chunk is a tiny call per layer (about 125 tokens), so launching the layers
 one by one from the host costs more than the kernels themselves.
 `capture_graph` records all layers and the score of one chunk in a HIP graph
 over fixed input buffers (`inputs`); the chunk's length is read on the
-device, so the one graph serves every chunk length up to max_chunk.  The
+device, so a graph serves every chunk length up to the capacity it was
+recorded for.  Two are recorded: one for chunks of at most two tiles
+(SMALL_CHUNK tokens), whose layer calls take the library's one-launch path,
+and one for max_chunk.  The
 append and the eviction stay outside the graph: the cache length they work
 from is host state.
 
@@ -47,6 +50,9 @@ import torch
 
 from . import (LAYER_FROB, deltas_drift, gdn_chunk_fwd, gdn_shape, gdn_workspace_bytes, kv_evict_topk,
                kv_evict_topk_indexed, kv_indexed_workspace_bytes, kv_outcome_word, kv_workspace_bytes)
+
+# the longest chunk whose layer calls fit two 64-token tiles
+SMALL_CHUNK = 128
 
 
 class EvictionFailed(RuntimeError):
@@ -214,18 +220,21 @@ class DeltaSStream:
                        torch.zeros((L, Tm, H_v), dtype=torch.float32, device=dev))
         self.cu = torch.tensor([0, Tm], dtype=torch.int32, device=dev)
         self.score_buf = torch.zeros(1, dtype=torch.float32, device=dev)
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            self._layers_fixed()
-        torch.cuda.synchronize()
-        self.graph = g
+        self.graphs = {}
+        for cap in sorted({min(Tm, SMALL_CHUNK), Tm}):
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                self._layers_fixed(cap)
+            torch.cuda.synchronize()
+            self.graphs[cap] = g
+        self.graph = self.graphs[Tm]
 
-    def _layers_fixed(self):
+    def _layers_fixed(self, cap):
         q, k, v, g, b = self.inputs
         for l in range(self.L):
             st = self.state[l]
-            gdn_chunk_fwd(q[l], k[l], v[l], g[l], b[l], [self.max_chunk], 0, cu_seqlens=self.cu, state_in=st,
+            gdn_chunk_fwd(q[l], k[l], v[l], g[l], b[l], [cap], 0, cu_seqlens=self.cu, state_in=st,
                           state_out=st, o=self.o[l], drift_partials=self.partials[l], workspace=self.gdn_ws,
                           drift_per_slice=self.per_slice)
         deltas_drift(self.partials, self.score_mode, scores=self.score_buf)
@@ -242,7 +251,7 @@ class DeltaSStream:
         if c >= self.scores.numel():
             raise ValueError("score table full")
         self.cu[1:2].fill_(T)
-        self.graph.replay()
+        self.graphs[min(self.graphs) if T <= min(self.graphs) else self.max_chunk].replay()
         self.scores[c:c + 1].copy_(self.score_buf)
         return self._append_and_evict(T, k_rows, v_rows)
 

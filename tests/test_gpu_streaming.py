@@ -161,8 +161,9 @@ def test_question_save_restore_is_transparent(ds):
 
 
 def test_graph_replays_match_eager_steps(ds):
-    """One captured graph (all layers + score, lengths read on the device)
-    replayed for chunks of different lengths, with eager work and
+    """The captured graphs (all layers + score, lengths read on the device; one
+    for chunks of at most two tiles, one for the full capacity) replayed for
+    chunks of different lengths on both sides of 128 tokens, with eager work and
     synchronisations between replays, gives the eager steps' results bit for
     bit after every chunk."""
     lens = chunk_lengths(12, seed=5)
