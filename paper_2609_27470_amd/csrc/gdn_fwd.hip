@@ -75,8 +75,11 @@ __device__ __forceinline__ void drift_setup(const GdnArgs &a, int tid, int nt) {
 // waves w = 0 .. 3 with the LDS block L.  Every call passes the same barriers
 // (lds_barrier, workgroup-wide), so that two groups of four waves of one
 // workgroup can each run a tile side by side.  write_q: this call writes the
-// tile's fp16 q fragments (when the workspace has them).
-template <int D>
+// tile's fp16 q fragments (when the workspace has them).  WP = false (the
+// whole-head sequential kernel, which forms P itself from the K and q tiles it
+// stages): no q rows, no K Q^T and no P, and the first decay slot holds
+// gamma_r in base-2 units instead of Gamma_r.
+template <int D, bool WP = true>
 __device__ __forceinline__ void prep_tile(const GdnArgs &a, int ti, int t0, int n, int h, int jbase, int gcount,
                                           PrepLds<D> &L, int w, int lane, bool write_q) {
     constexpr int KS = D / 32;   // 32-wide k-steps over the head dim
@@ -104,7 +107,7 @@ __device__ __forceinline__ void prep_tile(const GdnArgs &a, int ti, int t0, int 
             const int row = 16 * w + RPI * c + lane / CH, ch = lane % CH;
             const uint32_t off = (uint32_t)min(row, n - 1) * (uint32_t)a.H_k * D + 8 * ch;
             kv[c] = *(const u32x4 *)(kb + off);
-            qv[c] = *(const u32x4 *)(qb + off);
+            if (WP) qv[c] = *(const u32x4 *)(qb + off);
         }
         // gates of the group's first v-heads (wave 0, lane = token), issued after
         // K and Q so that waiting for K and Q does not wait for them; raw g and
@@ -123,8 +126,9 @@ __device__ __forceinline__ void prep_tile(const GdnArgs &a, int ti, int t0, int 
         for (int c = 0; c < NI; ++c) {
             const int row = 16 * w + RPI * c + lane / CH, ch = lane % CH;
             const u32x4 z = {0u, 0u, 0u, 0u};
-            const u32x4 q = row < n ? qv[c] : z;
             *(u32x4 *)(&Kl[row * D + 8 * (ch ^ swz<D>(row))]) = row < n ? kv[c] : z;
+            if (!WP) continue;
+            const u32x4 q = row < n ? qv[c] : z;
             *(u32x4 *)(&Ql[row * D + 8 * (ch ^ swz<D>(row))]) = q;
             // q in fp16 for the output waves of the per-slice sequential kernel, in
             // A-fragment order: row block row / 16, k-step ch / 4, lane (ch % 4) * 16 +
@@ -160,14 +164,14 @@ __device__ __forceinline__ void prep_tile(const GdnArgs &a, int ti, int t0, int 
     for (int ks = 0; ks < KS; ++ks) {
         const int ra = 16 * w + ln, ca = 8 * ((4 * ks + lg) ^ swz<D>(ra));
         const bf16x8 ak = as_bf16x8(*(const u32x4 *)(&Kl[ra * D + ca]));
-        const bf16x8 aq = as_bf16x8(*(const u32x4 *)(&Ql[ra * D + ca]));
+        const bf16x8 aq = WP ? as_bf16x8(*(const u32x4 *)(&Ql[ra * D + ca])) : ak;
 #pragma unroll
         for (int nb = 0; nb < 4; ++nb) {
             if (nb <= w) {
                 const int rb = 16 * nb + ln;
                 const bf16x8 bk = as_bf16x8(*(const u32x4 *)(&Kl[rb * D + 8 * ((4 * ks + lg) ^ swz<D>(rb))]));
                 gk[nb] = mfma_bf16(ak, bk, gk[nb]);
-                gq[nb] = mfma_bf16(bk, aq, gq[nb]);
+                if (WP) gq[nb] = mfma_bf16(bk, aq, gq[nb]);
             }
         }
     }
@@ -206,7 +210,7 @@ __device__ __forceinline__ void prep_tile(const GdnArgs &a, int ti, int t0, int 
             beta_s[slot][lane] = bv;
             // padding rows have g = 0, so row 63 carries the tile's last gamma
             const float s_last = __shfl(s, 63, 64);
-            a.wsGam[tv * 128 + lane] = __builtin_amdgcn_exp2f(s);
+            a.wsGam[tv * 128 + lane] = WP ? __builtin_amdgcn_exp2f(s) : s;
             a.wsGam[tv * 128 + 64 + lane] = __builtin_amdgcn_exp2f(s_last - s);
         }
     };
@@ -214,6 +218,7 @@ __device__ __forceinline__ void prep_tile(const GdnArgs &a, int ti, int t0, int 
     // for keys j <= i (the output scale rides on P: o = scale diag(Gamma) Q S0^T + P E), as the A fragments (w, ks) of P E (k-step ks pairs key
     // blocks 2 ks, 2 ks + 1); block (nb, w): key 16 nb + 4 lg + e, query 16 w + ln
     auto pfrags = [&](int jj, int slot) __attribute__((always_inline)) {
+        if (!WP) return;
         const size_t tv = (size_t)ti * a.H_v + jbase + jj;
         const float gq_i = gam_s[slot][16 * w + ln];  // query 16 w + ln
         auto pblock = [&](int nb) __attribute__((always_inline)) {
@@ -349,7 +354,7 @@ __device__ __forceinline__ void prep_tile(const GdnArgs &a, int ti, int t0, int 
 // gdn_prep: one workgroup per (tile, qk-head), or per (tile, v-head) for small
 // launches; the work of a tile is prep_tile.
 // ============================================================================
-template <int D>
+template <int D, bool WP>
 __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
     __shared__ __align__(16) PrepLds<D> L;
     // The grid is one-dimensional and tile-major per XCD (dispatch deals
@@ -367,7 +372,7 @@ __global__ __launch_bounds__(256, 4) void gdn_prep_kernel(GdnArgs a) {
     if (!locate_tile(a.st, ti, t0, n)) return;
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     // one writer of the q fragments per qk-head
-    prep_tile<D>(a, ti, t0, n, h, jbase, gcount, L, w, threadIdx.x & 63, jbase == h * a.group);
+    prep_tile<D, WP>(a, ti, t0, n, h, jbase, gcount, L, w, threadIdx.x & 63, jbase == h * a.group);
 }
 
 // ============================================================================
@@ -1138,7 +1143,11 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     if (p.tiles_max > 0 && !one_launch) {
         // tiles rounded up to a multiple of 8 (workgroups past the last tile exit)
         const long long n_prep = (long long)((p.tiles_max + 7) / 8) * 8 * (a.prep_per_vhead ? p.H_v : p.H_k);
-        hipLaunchKernelGGL(gdn_prep_kernel<D>, dim3((unsigned)n_prep), dim3(256), 0, stream, a);
+        // the whole-head kernel forms P itself (prep without q, K Q^T and P)
+        if (D == 128 && use_wide(p.B, p.H_v, D))
+            hipLaunchKernelGGL((gdn_prep_kernel<D, false>), dim3((unsigned)n_prep), dim3(256), 0, stream, a);
+        else
+            hipLaunchKernelGGL((gdn_prep_kernel<D, true>), dim3((unsigned)n_prep), dim3(256), 0, stream, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

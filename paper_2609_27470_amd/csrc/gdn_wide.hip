@@ -15,13 +15,16 @@
 //       the update S = Gamma_last S0 + (D_last E)^T K.  Every fragment read
 //       from LDS (rows of K, Q, T, P, K^T) feeds both slices.
 //   waves 4-7 (loaders): load the tile two tiles ahead and stage it in LDS
-//       one tile ahead (K and q rows converted to fp16, the T and P fragments
-//       of the prep pass, v rows, Gamma and D_last), and store the previous tile's
-//       bf16 o, which the compute waves left in LDS, as whole rows; loader 3
-//       also adds the frame-end drift sums of the 8 slices (fixed order) and
-//       writes them, per slice or per head, with no exchange between
-//       workgroups.
-// One barrier per tile (LDS-only).  The state at a frame's start, needed for
+//       one tile ahead (K and q rows converted to fp16, the T fragments of the
+//       prep pass, v rows, Gamma and D_last); form P = scale D (.) tril(Q K^T)
+//       of the staged tile from its K and q on fp16 matrix cores, so that the
+//       prep pass reads no q and writes no P; and store the previous tile's bf16 o, which the
+//       compute waves left in LDS, as whole rows.  Loader 3 also adds the
+//       frame-end drift sums of the 8 slices (fixed order) and writes them, per
+//       slice or per head, with no exchange between workgroups.
+// Two barriers per tile (LDS-only): the tile's start, and one after the
+// first two products, before which the loaders stage the next tile's rows (P
+// is formed from them during the rest of the tile).  The state at a frame's start, needed for
 // ||S_end - S_start||^2, is kept in a scratch area of the workspace (64 KiB
 // per head) rather than in registers, and read back at the frame's end.
 #include <type_traits>
@@ -55,14 +58,15 @@ struct WideShared {
     u32x4 P[2][6][64];        // P A-fragments
     uint16_t V[2][64 * WIDE_VLD];  // v rows (bf16)
     float G[2][2][64];        // Gamma_r, D_last,r
+    float Gs[2][64];          // gamma_r in base-2 units (the gates of P)
     float2 DR[2][4][2][64];   // frame-end drift sums per [frame % 2][compute wave][slice][lane]
 };
 
-// One loader's share of a tile: K, q and v rows 16 X .. 16 X + 15, T and P
-// fragments {2 X, 2 X + 1} (X < 2) or {4 + X - 2}; loader 0 also Gamma,
-// loader 1 D_last.
+// One loader's share of a tile: K, q and v rows 16 X .. 16 X + 15, T
+// fragments {2 X, 2 X + 1} (X < 2) or {4 + X - 2}; loader 0 also gamma (base
+// 2), loader 1 D_last.
 struct WideLoad {
-    u32x4 k[4], q[4], v[4], t[2], p[2];
+    u32x4 k[4], q[4], v[4], t[2];
     float g;
 };
 
@@ -288,6 +292,9 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                     WIDE_SG(SG_VALU, 3);
                 }
             }
+            // second barrier: the loaders have staged the next tile and form its P
+            // from it during (3) - (5) (P of the first tile is in LDS from here on)
+            lds_barrier();
             // operands of (3) - (5): T diag(beta) and P fragments, D_last, the
             // scale Gamma of each token, the first K^T fragments
             half8 tf[6], pf[6], kt[2][2];
@@ -468,12 +475,8 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                     s.v[c] = *(const u32x4 *)(vb + r * (uint32_t)a.H_v * D);
                 }
                 const u32x4 *tb = (const u32x4 *)(a.wsT + tv * TP_HALVES);
-                const u32x4 *pb = (const u32x4 *)(a.wsP + tv * TP_HALVES);
 #pragma unroll
-                for (int c = 0; c < NT; ++c) {
-                    s.t[c] = tb[(F_FIRST + c) * 64 + lane];
-                    s.p[c] = pb[(F_FIRST + c) * 64 + lane];
-                }
+                for (int c = 0; c < NT; ++c) s.t[c] = tb[(F_FIRST + c) * 64 + lane];
                 if (X < 2) s.g = a.wsGam[tv * 128 + 64 * X + lane];
             };
             auto stage = [&](const WideLoad &s, auto bufc) __attribute__((always_inline)) {
@@ -486,18 +489,68 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                     *(u32x4 *)(&sh.V[buf][row * WIDE_VLD + 8 * ch]) = s.v[c];
                 }
 #pragma unroll
-                for (int c = 0; c < NT; ++c) {
-                    sh.T[buf][F_FIRST + c][lane] = s.t[c];
-                    sh.P[buf][F_FIRST + c][lane] = s.p[c];
+                for (int c = 0; c < NT; ++c) sh.T[buf][F_FIRST + c][lane] = s.t[c];
+                if (X == 0) {
+                    sh.G[buf][0][lane] = __builtin_amdgcn_exp2f(s.g);
+                    sh.Gs[buf][lane] = s.g;
+                } else if (X == 1) {
+                    sh.G[buf][1][lane] = s.g;
                 }
-                if (X < 2) sh.G[buf][X][lane] = s.g;
+            };
+            // P of the tile in LDS buffer buf, query rows 16 X .. 16 X + 15:
+            // (K Q^T) blocks (nb, X) for key blocks nb <= X on fp16 matrix cores (lane
+            // (ln, lg) holds keys 16 nb + 4 lg + e of query 16 X + ln: half of an A
+            // fragment of P in the token order of E), gated by 2^(gamma_i - gamma_j)
+            // and the output scale, zero above the diagonal.  Rows past a ragged
+            // tile's end hold copies of its last row: they only reach o rows that
+            // are not stored, since P is lower triangular
+            auto form_p = [&](auto bufc) __attribute__((always_inline)) {
+                constexpr int buf = decltype(bufc)::value;
+                f32x4 gq[X + 1];
+#pragma unroll
+                for (int nb = 0; nb <= X; ++nb) gq[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int ks = 0; ks < D / 32; ++ks) {
+                    const int rq = 16 * X + ln;
+                    const half8 bq = as_half8(*(const u32x4 *)(&sh.Q[buf][rq * D + 8 * ((4 * ks + lg) ^ swz<D>(rq))]));
+#pragma unroll
+                    for (int nb = 0; nb <= X; ++nb) {
+                        const int rk = 16 * nb + ln;
+                        const half8 ak = as_half8(*(const u32x4 *)(&sh.K[buf][rk * D + 8 * ((4 * ks + lg) ^ swz<D>(rk))]));
+                        gq[nb] = mfma_f16(ak, bq, gq[nb]);
+                    }
+                }
+                const float gi = sh.Gs[buf][16 * X + ln];
+                auto pblock = [&](int nb) __attribute__((always_inline)) {
+                    f32x4 pk = {0.f, 0.f, 0.f, 0.f};
+                    if (nb <= X) {
+                        const float4 gj = *(const float4 *)(&sh.Gs[buf][16 * nb + 4 * lg]);
+                        const float gjv[4] = {gj.x, gj.y, gj.z, gj.w};
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            pk[e] = (nb < X || 4 * lg + e <= ln) ? __builtin_amdgcn_exp2f(gi - gjv[e]) * (a.scale * gq[nb][e]) : 0.f;
+                    }
+                    return pk;
+                };
+                sh.P[buf][frag_index(X, 0)][lane] = __builtin_bit_cast(u32x4, to_half8(pblock(0), pblock(1)));
+                if (X >= 2) sh.P[buf][frag_index(X, 1)][lane] = __builtin_bit_cast(u32x4, to_half8(pblock(2), pblock(3)));
             };
             // bf16 o of tile lt from the v buffer it was staged in (rows 16 X .. 16 X +
             // 15, the rows this loader restages next): 16-byte pieces read back in
             // order, stored as whole 256-byte rows; stores past a ragged tile's end
             // fall outside the buffer resource and are dropped
-            auto store_o = [&](int lt, auto bufc) __attribute__((always_inline)) {
+            // (read_o into registers before the rows are restaged, store_o later)
+            auto read_o = [&](u32x4(&ov)[4], auto bufc) __attribute__((always_inline)) {
                 constexpr int buf = decltype(bufc)::value;  // == lt % 2
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int r = 16 * X + RPI * c + lane / CH, ch = lane % CH;
+                    // dims 8 ch .. 8 ch + 7 = two 4-dim pieces, kept adjacent by the permutation
+                    // and swapped when (r / 4) % 2 == 1
+                    ov[c] = *(const u32x4 *)(&sh.V[buf][o_stage_at(r, 8 * ch) & ~7]);
+                }
+            };
+            auto store_o = [&](int lt, const u32x4(&ov)[4]) __attribute__((always_inline)) {
                 const int t0 = st + TILE * lt, n = min(TILE, en - t0);
                 const uint32_t row_bytes = (uint32_t)a.H_v * D * 2;
                 const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
@@ -505,10 +558,7 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
                     const int r = 16 * X + RPI * c + lane / CH, ch = lane % CH;
-                    // dims 8 ch .. 8 ch + 7 = two 4-dim pieces, kept adjacent by the permutation
-                    // and swapped when (r / 4) % 2 == 1
-                    u32x4 v = *(const u32x4 *)(&sh.V[buf][o_stage_at(r, 8 * ch) & ~7]);
-                    if ((r >> 2) & 1) v = u32x4{v[2], v[3], v[0], v[1]};
+                    const u32x4 v = ((r >> 2) & 1) ? u32x4{ov[c][2], ov[c][3], ov[c][0], ov[c][1]} : ov[c];
                     __builtin_amdgcn_raw_buffer_store_b128(v, rs, (uint32_t)r * row_bytes + (uint32_t)(j * D + 8 * ch) * 2, 0, 0);
                 }
             };
@@ -555,10 +605,22 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                 load(s1, 1);
                 stage(s0, std::integral_constant<int, 0>());
                 load(s0, 2);
+                // P of tile it + 1 is formed during tile it, after the tile's second
+                // barrier, from the K and q rows all four loaders staged before it, and
+                // handed to the compute waves at the next tile's first barrier (P of
+                // tile 0 before the first tile's second barrier).  Before the second
+                // barrier a loader does LDS work only (the compute waves wait there for
+                // the last loader; the o rows are read back before they are restaged);
+                // its global stores and loads follow it
                 auto step = [&](int it, WideLoad &s, auto bufc) __attribute__((always_inline)) {
                     lds_barrier();
-                    if (OUT_BF16 && it >= 1) store_o(it - 1, bufc);
+                    if (it == 0) form_p(std::integral_constant<int, 0>());
+                    u32x4 ov[4];
+                    if (OUT_BF16 && it >= 1) read_o(ov, bufc);
                     if (it + 1 < n_tiles) stage(s, bufc);
+                    if (it < n_tiles) lds_barrier();
+                    if (OUT_BF16 && it >= 1) store_o(it - 1, ov);
+                    if (it + 1 < n_tiles) form_p(bufc);
                     load(s, it + 3);
                     drift_reduce(it);
                 };
