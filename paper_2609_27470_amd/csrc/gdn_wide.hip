@@ -16,17 +16,19 @@
 //       from LDS (rows of K, Q, T, P, K^T) feeds both slices.
 //   waves 4-7 (loaders): load the tile two tiles ahead and stage it in LDS
 //       one tile ahead (K and q rows converted to fp16, the T fragments of the
-//       prep pass, v rows, Gamma and D_last); form P = scale D (.) tril(Q K^T)
-//       of the staged tile from its K and q on fp16 matrix cores, so that the
-//       prep pass reads no q and writes no P; and store the previous tile's bf16 o, which the
-//       compute waves left in LDS, as whole rows.  Loader 3 also adds the
-//       frame-end drift sums of the 8 slices (fixed order) and writes them, per
-//       slice or per head, with no exchange between workgroups.
-// Two barriers per tile (LDS-only): the tile's start, and one after the
-// first two products, before which the loaders stage the next tile's rows (P
-// is formed from them during the rest of the tile).  The state at a frame's start, needed for
-// ||S_end - S_start||^2, is kept in a scratch area of the workspace (64 KiB
-// per head) rather than in registers, and read back at the frame's end.
+//       prep pass, v rows, gamma in base 2 and D_last); form P = scale D (.)
+//       tril(Q K^T) of the staged tile from its K and q on fp16 matrix cores,
+//       so that the prep pass reads no q and writes no P; and store the
+//       previous tile's bf16 o, which the compute waves left in LDS, as whole
+//       rows.  Loader 3 also adds the frame-end drift sums of the 8 slices
+//       (fixed order) and writes them, per slice or per head, with no exchange
+//       between workgroups.
+// Two barriers per tile (LDS-only): the tile's start, and one after the first
+// two products, before which the loaders stage the next tile's rows (P is
+// formed from them during the rest of the tile).  The state at a frame's
+// start, needed for ||S_end - S_start||^2, is kept in a scratch area of the
+// workspace (64 KiB per head) rather than in registers, and read back at the
+// frame's end.
 #include <type_traits>
 
 #include "gdn_common.h"
