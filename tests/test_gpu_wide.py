@@ -3,8 +3,9 @@ when B * H_v reaches 256 at d = 128) against the fp64 oracle (Section 3.2,
 Eq. 2 and Eq. 3), on batches of many short streams that select it: ragged,
 empty and one-token streams, a non-zero entry state, snapshots, every drift
 aggregation, per-slice drift pairs, bf16 o and the write signal; frame
-split and determinism bit for bit.  The full varlen workload runs through it
-in test_gpu_full_size.py."""
+split and determinism bit for bit; P (which this kernel forms itself) under a
+non-default output scale and extreme gates.  The full varlen workload runs
+through it in test_gpu_full_size.py."""
 import numpy as np
 import pytest
 import torch
@@ -118,3 +119,36 @@ def test_wide_frame_split_and_determinism(ds):
         assert np.array_equal(part["partials"], whole["partials"].reshape(B, 3, 4, 2)[:, f])
         S = part["S"]
     assert np.array_equal(S, whole["S"])
+
+
+def test_wide_output_scale_and_extreme_gates(ds):
+    """P = scale D (.) tril(Q K^T) is formed by this kernel's loaders from the
+    staged K and q tiles: a non-default output scale (1 / sqrt(d)), streams
+    with near-unity decay (g = -1e-4), streams with decay so strong that
+    2^(gamma_i - gamma_j) underflows inside a tile (g = -30), and beta = 0 on
+    some tokens, against the oracle with the same scale."""
+    x = _batch(64, 6, lo=1, hi=300)
+    cu = x.cu_seqlens
+    for b in range(64):
+        s0, e0 = int(cu[b]), int(cu[b + 1])
+        if b % 3 == 0:
+            x.g[s0:e0] = -1e-4
+        elif b % 3 == 1:
+            x.g[s0:e0] = -30.0
+        if b % 5 == 0:
+            x.beta[s0:e0:7] = 0.0
+    scale = 1.0 / np.sqrt(128.0)
+    S0 = (np.random.default_rng(7).standard_normal((64, 4, 128, 128)) * 0.05).astype(np.float32).astype(np.float64)
+    r = ds.gdn_chunk_fwd(dev_bf16(x.q), dev_bf16(x.k), dev_bf16(x.v), dev_f32(x.g), dev_f32(x.beta), lengths_of(x),
+                         x.frame_len, state_in=dev_f32(S0), scale=scale)
+    torch.cuda.synchronize()
+    ref = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, x.frame_len, S0=S0, scale=scale)
+    o = r["o"].cpu().numpy().astype(np.float64)
+    assert np.all(np.isfinite(o))
+    eo, es = rel_fro(o, ref["o"]), rel_fro(r["state"].cpu().numpy(), ref["S"])
+    assert eo <= TOL_O and es <= TOL_O, (eo, es)
+    p = r["drift_partials"][None]
+    ed = drift_rel_err(ds.deltas_drift(p, oracle.PER_HEAD).cpu().numpy(),
+                       oracle.drift_scores(ref["partials"][None], oracle.PER_HEAD))
+    assert ed <= TOL_DRIFT, ed
+    print(f"wide, scale 1/sqrt(d), extreme gates: o {eo:.2e} S {es:.2e} drift {ed:.2e}")
