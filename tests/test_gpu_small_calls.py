@@ -2,7 +2,9 @@
 streamed chunks) form their prep inside it, in one launch, unless the per-head drift
 sums are asked for (their slice counters are cleared by the separate prep
 pass).  The same inputs through both paths give the same bits, and both match
-the fp64 oracle (Section 3.2, Eq. 2; drift sums of Eq. 3)."""
+the fp64 oracle (Section 3.2, Eq. 2; drift sums of Eq. 3); longer calls (up to
+17 tiles, a packed pair) take the prep pass on every call and are held to the
+same comparisons."""
 import numpy as np
 import pytest
 import torch
@@ -26,7 +28,8 @@ def ds():
 
 
 # (lengths, H_k, H_v, d, frame_len): one-launch cases have (T + 63 B) / 64 <= 2
-# tiles; 129 and 132 tokens (three tiles) take the two launches on both calls
+# tiles; the others (three tiles and up, to 1025 tokens) take the two launches
+# on every call
 CASES = [
     ([1], 2, 4, 128, 64),
     ([63], 2, 4, 128, 0),
@@ -39,6 +42,12 @@ CASES = [
     ([1, 1], 2, 2, 64, 64),
     ([132], 16, 32, 128, 0),
     ([129], 2, 4, 128, 64),
+    ([1024], 16, 32, 128, 1024),
+    ([1000], 2, 4, 128, 256),
+    ([511], 2, 2, 64, 128),
+    ([600, 300], 2, 4, 128, 256),
+    ([1025], 2, 4, 128, 1024),
+    ([520], 2, 2, 64, 0),
 ]
 
 
@@ -95,3 +104,30 @@ def test_one_launch_bf16_snapshots_and_unreached_frames(ds):
     assert np.array_equal(got[:1], r["drift_partials"].cpu().numpy())
     assert np.all(got[1:] == 0.0)
     assert torch.equal(o2["state"], r["state"])
+
+
+def test_capacity_call_bf16_snapshots_and_unreached_frames(ds):
+    """A call sized for 1024 tokens with 700 on the device (the prep pass and
+    the sequential kernel read the length on the device): bf16 o and snapshots
+    against the oracle, the pairs of frames the device length does not reach
+    zero, and the result bit-equal to the call sized to the device length."""
+    lens = [700]
+    x = synth.make_gdn_inputs(lens, 2, 4, 128, 256, novelty=True, config=1)
+    q, k, v = dev_bf16(x.q), dev_bf16(x.k), dev_bf16(x.v)
+    g, beta = dev_f32(x.g), dev_f32(x.beta)
+    r = ds.gdn_chunk_fwd(q, k, v, g, beta, lens, 256, o_dtype=torch.bfloat16, snapshots=True, drift_per_slice=True)
+    torch.cuda.synchronize()
+    ref = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, 256, snapshots=True)
+    assert rel_fro(r["o"].float().cpu().numpy().astype(np.float64), bf16_round(ref["o"])) <= TOL_O
+    assert rel_fro(r["snapshots"].cpu().numpy().astype(np.float64), ref["snapshots"]) <= TOL_O
+    cap = [1024]
+    pad = lambda a: torch.cat([a, torch.zeros((1024 - a.shape[0],) + tuple(a.shape[1:]), dtype=a.dtype, device=DEV)])
+    cu = torch.tensor(np.asarray(x.cu_seqlens, np.int32), device=DEV)
+    dp = torch.full((4, 4 * 8, 2), float("nan"), dtype=torch.float32, device=DEV)
+    o2 = ds.gdn_chunk_fwd(pad(q), pad(k), pad(v), pad(g), pad(beta), cap, 256, cu_seqlens=cu, drift_partials=dp,
+                          o_dtype=torch.bfloat16, drift_per_slice=True)
+    torch.cuda.synchronize()
+    got = dp.cpu().numpy()
+    assert np.array_equal(got[:3], r["drift_partials"].cpu().numpy())
+    assert np.all(got[3:] == 0.0)
+    assert torch.equal(o2["state"], r["state"]) and torch.equal(o2["o"][:700], r["o"])
