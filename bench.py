@@ -381,6 +381,41 @@ class StackLoop:
         return seg, e0.elapsed_time(e1)
 
 
+def drift_trace_run(ds, dev, stream, which, rounds=20):
+    """Alternating calls with and without the fused drift sums (and their
+    deltas_drift), for a kernel trace: the single-layer call (per-head pairs
+    reduced in the sequential kernel), or a stack frame of 24 calls of 1024
+    tokens (per-slice pairs)."""
+    import torch
+    import synth
+    if which == "stack":
+        loop = StackLoop(ds, dev, stream, make_pool(dev), 2 * rounds, evict=False)
+        for f in range(2 * rounds):
+            loop.frame(f, drift=f % 2 == 0)
+    else:
+        x = synth.workload_inputs("single_layer")
+        to = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dev).view(dt)
+        q, k, v = to(x.q.view(np.int16), torch.bfloat16), to(x.k.view(np.int16), torch.bfloat16), \
+            to(x.v.view(np.int16), torch.bfloat16)
+        g, beta = to(x.g, torch.float32), to(x.beta, torch.float32)
+        o = torch.empty((T, H_V, D), dtype=torch.bfloat16, device=dev)
+        state = torch.empty((1, H_V, D, D), dtype=torch.float32, device=dev)
+        n_frames = T // FRAME
+        partials = torch.empty((n_frames, H_V, 2), dtype=torch.float32, device=dev)
+        scores = torch.empty(n_frames, dtype=torch.float32, device=dev)
+        ws = torch.empty(ds.gdn_workspace_bytes(ds.gdn_shape([T], H_K, H_V, D, FRAME)), dtype=torch.uint8, device=dev)
+        for r in range(2 * rounds):
+            if r % 2 == 0:
+                ds.gdn_chunk_fwd(q, k, v, g, beta, [T], FRAME, state_out=state, o=o, drift_partials=partials,
+                                 workspace=ws)
+                ds.deltas_drift(partials.view(1, n_frames, H_V, 2), ds.LAYER_FROB, scores=scores)
+            else:
+                ds.gdn_chunk_fwd(q, k, v, g, beta, [T], FRAME, state_out=state, o=o, drift_partials=False,
+                                 workspace=ws)
+    torch.cuda.synchronize()
+    print(json.dumps({"drift_trace": which, "rounds": rounds}), flush=True)
+
+
 def bench_stack(ds, dev, stream, pool):
     """The stack workload: 24 layers, one stream of 262144 tokens streamed as
     256 calls of 1024 tokens per layer (inputs from the per-layer pool)."""
@@ -525,6 +560,9 @@ def main():
     ap.add_argument("--only", choices=["tiny", "single_layer", "stack", "varlen", "eviction_loop", "streaming"],
                     default=None,
                     help="time one workload's record and print it alone (for profiling runs)")
+    ap.add_argument("--drift-trace", choices=["single_layer", "stack"], default=None,
+                    help="run the forward with and without the fused drift sums, alternating, for a kernel "
+                         "trace (the trace-derived drift overhead of profiles/)")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="only run a plain device copy of this many bytes (counter calibration)")
     args = ap.parse_args()
@@ -545,6 +583,9 @@ def main():
     stream = torch.cuda.current_stream()
     t_start = time.perf_counter()
     log = lambda m: print(f"[bench {time.perf_counter() - t_start:6.1f}s] {m}", file=sys.stderr, flush=True)
+    if args.drift_trace:
+        drift_trace_run(ds, dev, stream, args.drift_trace)
+        return
     if args.only and args.only != "single_layer":
         if args.only == "tiny":
             rec = bench_tiny(ds, dev, stream, 200)
@@ -784,6 +825,10 @@ def main():
     trec = committed_record("gdn_chunk_fwd_single_layer_traffic.json")
     traffic = trec.get("bytes_per_launch") if trec else None
     crec = committed_record("gdn_chunk_fwd_single_layer_counters.json")
+    # the same overhead from kernel durations (alternating calls with and without
+    # the fused sums under a kernel trace), beside the event-timed figures
+    drec = committed_record("gdn_drift_overhead_trace.json")
+    drift_trace = {k: drec[k]["overhead_pct"] for k in ("single_layer", "stack_call")} if drec else None
 
     configs = {}
     single = {"workload": "single_layer: H_k=16, H_v=32, d=128, T=32768, frames of 1024 (gdn_chunk_fwd + deltas_drift)",
@@ -845,6 +890,7 @@ def main():
         "algorithmic_tflops": achieved_tflops,
         "drift_overhead_pct": drift_overhead,
         "drift_overhead_single_call_pct": drift_overhead_single,
+        "drift_overhead_trace_pct": drift_trace,
         "drift_unfused_ms": unfused_ms,
         "write_signal_ms": write_ms,
         "write_signal_overhead_pct": 100.0 * (write_ms / drift_only_ms - 1.0),
