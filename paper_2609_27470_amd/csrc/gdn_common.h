@@ -46,6 +46,10 @@ struct GdnArgs {
     float *drift_zero;      // the caller's drift_partials (either layout) or null
     int drift_zero_per_frame;  // pairs per frame in it: H_v, or H_v * n_split for per-slice pairs
     int prep_per_vhead;     // prep grid (tiles, H_v) instead of (tiles, H_k)
+    // whole-head kernel: 0 one launch; 1, 2 the whole-head and the half-head
+    // launch of a call split at a frame boundary (from which at most
+    // wide_tail_streams streams have tiles left)
+    int wide_phase, wide_tail_streams;
 };
 
 // Global tile index -> (stream, first token, valid tokens).  Tiles are
@@ -196,6 +200,7 @@ __device__ __forceinline__ float row_sq_sum16(half8 ef, int ln) {
 
 // Sequential kernel owning all d_v rows of a (stream, v-head) per workgroup
 // (gdn_wide.hip); returns the launch error.
-hipError_t launch_gdn_wide(const GdnArgs &a, int n_wg, bool o_bf16, bool drift, hipStream_t stream);
+hipError_t launch_gdn_wide(const GdnArgs &a, int n_heads, int tail_streams, bool o_bf16, bool drift,
+                           hipStream_t stream);
 
 }  // namespace ds

@@ -881,7 +881,7 @@ __global__ __launch_bounds__(512, 1) void gdn_seq_kernel(GdnArgs a) {
                 }
 #pragma unroll
                 for (int c = 0; c < NT; ++c) sh.T[buf][T_FIRST + (c + trot) % NT][lane] = s.t[c];
-                if (X < 2) {
+                if constexpr (X < 2) {
                     *(u32x4 *)(&sh.V[buf][(32 * X + (lane >> 1)) * 16 + 8 * (lane & 1)]) = s.v;
                     sh.G[g3][X][lane] = s.g;
                 }
@@ -1064,6 +1064,19 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 constexpr int WIDE_MIN_HEADS = 256;
 static bool use_wide(int B, int H_v, int d) { return d == 128 && (long long)B * H_v >= WIDE_MIN_HEADS; }
 
+// compute units of the current device (looked up once per device)
+static int device_cus() {
+    static int cus[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    if (cus[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+        cus[dev] = n;
+    }
+    return cus[dev];
+}
+
 GdnWorkspace gdn_workspace_layout(int B, int T_total, int H_k, int H_v, int d, int n_frames, bool with_write) {
     GdnWorkspace w{};
     w.tiles_max = (int)(((long long)T_total + 63LL * B) / 64);
@@ -1155,7 +1168,9 @@ static hipError_t launch_d(const GdnLaunch &p, hipStream_t stream) {
     const bool drift = p.drift_partials || p.snapshots;
     if (D == 128 && use_wide(p.B, p.H_v, D)) {
         // whole heads: per-head drift pairs are added by the workgroup itself
-        hipError_t e = launch_gdn_wide(a, p.B * p.H_v, p.o_bf16, drift, stream);
+        // the tail of the longest streams as half heads when at most as many
+        // streams as fill the GPU that way are left
+        hipError_t e = launch_gdn_wide(a, p.B * p.H_v, device_cus() / (2 * p.H_v), p.o_bf16, drift, stream);
         if (e != hipSuccess) return e;
         if (p.write_partials && p.n_frames > 0) {
             hipLaunchKernelGGL(gdn_write_finalize_kernel, dim3(p.n_frames, p.H_v), dim3(256), 0, stream, p.wsWrite,

@@ -29,6 +29,16 @@
 // start, needed for ||S_end - S_start||^2, is kept in a scratch area of the
 // workspace (64 KiB per head) rather than in registers, and read back at the
 // frame's end.
+//
+// A call of streams of unequal length leaves most CUs idle once the shorter
+// streams end, and the per-tile time of the heads still running is then set
+// by one workgroup's chain.  When its frames are whole tiles, the call runs as
+// two launches: whole heads up to the cut (the first frame boundary from
+// which at most as many streams are left as fill the GPU with two
+// workgroups per head), then half heads (NSL = 1: 64 rows per workgroup, one
+// 16-row slice per compute wave) from the states the first launch wrote.  A
+// half head's drift sums go out per slice; with per-head pairs the second of
+// a head's two workgroups to finish adds the 8 slices in order.
 #include <type_traits>
 
 #include "gdn_common.h"
@@ -72,29 +82,61 @@ struct WideLoad {
     float g;
 };
 
-template <bool OUT_BF16, bool DRIFT>
+// The tile index from which at most a.wide_tail_streams streams have tiles
+// left, rounded up to a frame boundary (every workgroup computes the same
+// value from the device lengths): the cut between the whole-head launch
+// and the half-head launch of a split call.
+__device__ int wide_cut(const GdnArgs &a) {
+    constexpr int MAXS = 16;
+    int top[MAXS + 1];  // the largest tile counts, descending
+    const int S = min(a.wide_tail_streams, MAXS);
+    for (int i = 0; i <= S; ++i) top[i] = 0;
+    for_streams(a.st, [&](int, int s0, int e0) {
+        int v = (e0 - s0 + TILE - 1) / TILE;
+        for (int i = 0; i <= S; ++i) {  // insert, keeping the S + 1 largest
+            if (v > top[i]) {
+                const int t = top[i];
+                top[i] = v;
+                v = t;
+            }
+        }
+        return false;
+    });
+    const int ft = a.frame_len / TILE;
+    return (top[S] + ft - 1) / ft * ft;
+}
+
+// NSL = 2: one workgroup per (stream, v-head), compute wave w carrying rows
+// 32 w .. 32 w + 31; NSL = 1: two workgroups per (stream, v-head), each with
+// 64 rows (compute wave w: rows 64 h + 16 w .. + 15), for the tail of a split
+// call, where few streams are left and half heads put more CUs to work.
+template <bool OUT_BF16, bool DRIFT, int NSL>
 __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
     constexpr int D = 128, KS = D / 32, NKB = D / 16;
+    constexpr int HW = 2 / NSL;  // workgroups per head
     __shared__ __align__(16) WideShared sh;
     const int tid = threadIdx.x, lane = tid & 63, ln = lane & 15, lg = lane >> 4;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-    // ---- workgroup -> (stream, v-head); the v-heads of one qk-head of one
-    // stream sit on one XCD (dispatch deals workgroups to the 8 XCDs in turn),
-    // so its K and q tiles are fetched into that XCD's L2 once
+    // ---- workgroup -> (stream, v-head, half); the workgroups of one qk-head of
+    // one stream sit on one XCD (dispatch deals workgroups to the 8 XCDs in
+    // turn), so its K and q tiles are fetched into that XCD's L2 once
     const int n_groups = a.st.B * a.H_k;
+    const int gsz = a.group * HW;
     const int bid = blockIdx.x;
     int gidx, mem;
     if (n_groups % 8 == 0) {
         const int xcd = bid & 7, slot = bid >> 3;
-        gidx = xcd + 8 * (slot / a.group);
-        mem = slot % a.group;
+        gidx = xcd + 8 * (slot / gsz);
+        mem = slot % gsz;
     } else {
-        gidx = bid / a.group;
-        mem = bid % a.group;
+        gidx = bid / gsz;
+        mem = bid % gsz;
     }
     const int b = gidx / a.H_k, qh = gidx % a.H_k;
-    const int j = qh * a.group + mem;
+    const int j = qh * a.group + mem / HW;
+    const int r0 = 64 * (mem % HW);  // first state row of this workgroup
+    const int sl0 = r0 / 16;          // its first 16-row slice
 
     int st = 0, en = 0, tile_base = 0, frame_base = 0;
     for_streams(a.st, [&](int bb, int s0, int e0) {
@@ -109,54 +151,66 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
     });
     const int len = en - st;
     const int n_tiles = (len + TILE - 1) / TILE;
+    // the tiles of this launch: all of them, or those before (wide_phase 1) or
+    // from (wide_phase 2) the cut, a frame boundary
+    int lt0 = 0, lt1 = n_tiles;
+    if (a.wide_phase != 0) {
+        const int c = wide_cut(a);
+        if (a.wide_phase == 1)
+            lt1 = min(n_tiles, c);
+        else
+            lt0 = min(n_tiles, c);
+    }
+    const int nt = lt1 - lt0;
+    if (a.wide_phase == 2 && nt == 0) return;  // the stream ended in the first launch
+    const int tok0 = TILE * lt0;
 
     if (w < 4) {
         // ============================================================ compute
         // S^T block kb of slice sl, lane (ln, lg), element e =
-        //   S[32 w + 16 sl + ln][sigma(kb, 4 lg + e)]
-        auto scol = [&](int kb, int e) { return 32 * (kb >> 1) + 8 * lg + 4 * (kb & 1) + e; };
-        auto srow = [&](int sl) { return 32 * w + 16 * sl + ln; };
+        //   S[r0 + 16 NSL w + 16 sl + ln][sigma(kb, 4 lg + e)]
+        const int wr0 = r0 + 16 * NSL * w;  // the wave's first row
         const size_t hbase = ((size_t)b * a.H_v + j) * D * D;
         // 16-byte pieces of the head's state rows go through buffer resources
         // (a uniform base in scalar registers, 32-bit lane offsets): S[sl][kb]
-        // holds 4 consecutive columns of row srow(sl)
+        // holds 4 consecutive columns of row wr0 + 16 sl + ln
         // byte offset of S[sl][kb]'s 4 columns = a per-lane base + a constant (passed
         // as the scalar offset, so that no per-(sl, kb) offset register stays live)
-        const uint32_t lane_row = (uint32_t)((32 * w + ln) * D + 8 * lg) * 4u;
+        const uint32_t lane_row = (uint32_t)((wr0 + ln) * D + 8 * lg) * 4u;
         auto sconst = [&](int sl, int kb) { return (int)((16 * sl * D + 32 * (kb >> 1) + 4 * (kb & 1)) * 4); };
         constexpr int RSRC_FLAGS = 0x00020000;
-        f32x4 S[2][NKB];
+        f32x4 S[NSL][NKB];
         if (a.state_in) {
             const __amdgpu_buffer_rsrc_t rin =
                 __builtin_amdgcn_make_buffer_rsrc((void *)(a.state_in + hbase), (short)0, D * D * 4, RSRC_FLAGS);
 #pragma unroll
-            for (int sl = 0; sl < 2; ++sl)
+            for (int sl = 0; sl < NSL; ++sl)
 #pragma unroll
                 for (int kb = 0; kb < NKB; ++kb)
                     S[sl][kb] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rin, lane_row, sconst(sl, kb), 0));
         } else {
 #pragma unroll
-            for (int sl = 0; sl < 2; ++sl)
+            for (int sl = 0; sl < NSL; ++sl)
 #pragma unroll
                 for (int kb = 0; kb < NKB; ++kb) S[sl][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
         // the state at the start of the current frame, in this wave's own
         // register order (16-byte pieces, lane-contiguous)
         const __amdgpu_buffer_rsrc_t rstart = __builtin_amdgcn_make_buffer_rsrc(
-            (void *)(a.wsStart + ((((size_t)b * a.H_v + j) * 4 + w) * 2) * NKB * 64 * 4), (short)0, 2 * NKB * 64 * 16,
+            (void *)(a.wsStart + (((size_t)b * a.H_v + j) * 8 + wr0 / 16) * NKB * 64 * 4), (short)0, NSL * NKB * 64 * 16,
             RSRC_FLAGS);
         const uint32_t lane16 = (uint32_t)lane * 16u;
         auto start_const = [&](int sl, int kb) { return (sl * NKB + kb) * 64 * 16; };
         auto save_start = [&]() __attribute__((always_inline)) {
 #pragma unroll
-            for (int sl = 0; sl < 2; ++sl)
+            for (int sl = 0; sl < NSL; ++sl)
 #pragma unroll
                 for (int kb = 0; kb < NKB; ++kb)
                     __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, S[sl][kb]), rstart, lane16, start_const(sl, kb), 0);
         };
         if (DRIFT) save_start();
-        int frame = frame_base;
-        int frame_end = a.frame_len > 0 ? min(a.frame_len, len) : len;  // tokens done at the next frame end
+        int frame = frame_base + (a.frame_len > 0 ? tok0 / a.frame_len : 0);
+        int frame_end = a.frame_len > 0 ? min(tok0 + a.frame_len, len) : len;  // tokens done at the next frame end
 
         // The tile runs as software-pipelined regions: every LDS operand is read
         // one step before its products, and scheduling groups interleave the
@@ -164,7 +218,7 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
         // (a compute wave is alone on its SIMD apart from a loader, so its own
         // instruction order has to hide the latencies).
         auto tile = [&](int lt, auto bufc) __attribute__((always_inline)) {
-            constexpr int buf = decltype(bufc)::value;  // == lt % 2
+            constexpr int buf = decltype(bufc)::value;  // == (lt - lt0) % 2
             const int t0 = st + TILE * lt, n = min(TILE, en - t0);
             lds_barrier();
             const float gl = sh.G[buf][0][63];
@@ -201,37 +255,37 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
             // Under it: the fp16 copy of the next k-step, and S <- Gamma_last S in place
             // for the blocks already copied (from here on the fp32 S is only the
             // update's accumulator).
-            half8 s16[2][KS];
-            f32x4 ks0[4][2];
+            half8 s16[NSL][KS];
+            f32x4 ks0[4][NSL];
             half8 ka[2][4];
 #pragma unroll
             for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-                for (int sl = 0; sl < 2; ++sl) ks0[rb][sl] = f32x4{0.f, 0.f, 0.f, 0.f};
+                for (int sl = 0; sl < NSL; ++sl) ks0[rb][sl] = f32x4{0.f, 0.f, 0.f, 0.f};
             kread(0, ka[0]);
 #pragma unroll
-            for (int sl = 0; sl < 2; ++sl) s16[sl][0] = to_half8(S[sl][0], S[sl][1]);
+            for (int sl = 0; sl < NSL; ++sl) s16[sl][0] = to_half8(S[sl][0], S[sl][1]);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
                 if (ks + 1 < KS) {
                     kread(ks + 1, ka[(ks + 1) & 1]);
 #pragma unroll
-                    for (int sl = 0; sl < 2; ++sl) s16[sl][ks + 1] = to_half8(S[sl][2 * ks + 2], S[sl][2 * ks + 3]);
+                    for (int sl = 0; sl < NSL; ++sl) s16[sl][ks + 1] = to_half8(S[sl][2 * ks + 2], S[sl][2 * ks + 3]);
                 }
 #pragma unroll
                 for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-                    for (int sl = 0; sl < 2; ++sl) ks0[rb][sl] = mfma_f16(ka[ks & 1][rb], s16[sl][ks], ks0[rb][sl]);
+                    for (int sl = 0; sl < NSL; ++sl) ks0[rb][sl] = mfma_f16(ka[ks & 1][rb], s16[sl][ks], ks0[rb][sl]);
 #pragma unroll
-                for (int sl = 0; sl < 2; ++sl)
+                for (int sl = 0; sl < NSL; ++sl)
 #pragma unroll
                     for (int c = 0; c < 2; ++c)
 #pragma unroll
                         for (int e = 0; e < 4; ++e) S[sl][2 * ks + c][e] *= gl;
                 if (ks + 1 < KS) WIDE_SG(SG_DSR, 4);
 #pragma unroll
-                for (int i = 0; i < 8; ++i) {
+                for (int i = 0; i < 4 * NSL; ++i) {
                     WIDE_SG(SG_MFMA, 1);
                     WIDE_SG(SG_VALU, 3);
                 }
@@ -245,7 +299,7 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
             auto vread = [&](int sl, int pr, v4i16(&vq)[2]) __attribute__((always_inline)) {
 #pragma unroll
                 for (int h = 0; h < 2; ++h)
-                    vq[h] = ds_read_tr16(&sh.V[buf][(16 * (2 * pr + h) + 4 * lg + (ln >> 2)) * WIDE_VLD + 32 * w + 16 * sl + 4 * (ln & 3)]);
+                    vq[h] = ds_read_tr16(&sh.V[buf][(16 * (2 * pr + h) + 4 * lg + (ln >> 2)) * WIDE_VLD + wr0 + 16 * sl + 4 * (ln & 3)]);
             };
             qread(0, qa[0]);
 #pragma unroll
@@ -254,26 +308,26 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
             __builtin_amdgcn_sched_barrier(0);
 
             // ---- (2) O^T = S0 Q^T, S0 as the A operand and q as the B operand: lane
-            // (ln, lg) holds state rows 32 w + 16 sl + 4 lg + e of token 16 rb + ln.
-            // Under it, a quarter of R = V - diag(Gamma) K S0^T per k-step (slice
-            // ks / 2, row blocks 2 (ks % 2), 2 (ks % 2) + 1), straight to fp16.
-            f32x4 oacc[4][2];
-            half8 rf[2][2];
+            // (ln, lg) holds state rows wr0 + 16 sl + 4 lg + e of token 16 rb + ln.
+            // Under it, a quarter of R = V - diag(Gamma) K S0^T in each of the first
+            // 2 NSL k-steps (slice ks / 2, row blocks 2 (ks % 2), 2 (ks % 2) + 1),
+            // straight to fp16.
+            constexpr int NQ = 2 * NSL;  // quarters of R
+            f32x4 oacc[4][NSL];
+            half8 rf[NSL][2];
 #pragma unroll
             for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-                for (int sl = 0; sl < 2; ++sl) oacc[rb][sl] = f32x4{0.f, 0.f, 0.f, 0.f};
+                for (int sl = 0; sl < NSL; ++sl) oacc[rb][sl] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                if (ks + 1 < KS) {
-                    qread(ks + 1, qa[(ks + 1) & 1]);
-                    vread((ks + 1) >> 1, (ks + 1) & 1, vv[(ks + 1) & 1]);
-                }
+                if (ks + 1 < KS) qread(ks + 1, qa[(ks + 1) & 1]);
+                if (ks + 1 < NQ) vread((ks + 1) >> 1, (ks + 1) & 1, vv[(ks + 1) & 1]);
 #pragma unroll
                 for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-                    for (int sl = 0; sl < 2; ++sl) oacc[rb][sl] = mfma_f16(s16[sl][ks], qa[ks & 1][rb], oacc[rb][sl]);
-                {
+                    for (int sl = 0; sl < NSL; ++sl) oacc[rb][sl] = mfma_f16(s16[sl][ks], qa[ks & 1][rb], oacc[rb][sl]);
+                if (ks < NQ) {
                     const int sl = ks >> 1, pr = ks & 1;
                     f32x4 R[2];
 #pragma unroll
@@ -287,11 +341,20 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                     }
                     rf[sl][pr] = to_half8(R[0], R[1]);
                 }
-                if (ks + 1 < KS) WIDE_SG(SG_DSR, 6);
+                // (scheduling-group arguments have to be literal constants)
+                if (ks + 1 < NQ) {
+                    WIDE_SG(SG_DSR, 6);
+                } else if (ks + 1 < KS) {
+                    WIDE_SG(SG_DSR, 4);
+                }
 #pragma unroll
-                for (int i = 0; i < 8; ++i) {
+                for (int i = 0; i < 4 * NSL; ++i) {
                     WIDE_SG(SG_MFMA, 1);
-                    WIDE_SG(SG_VALU, 3);
+                    if (ks < NQ) {
+                        WIDE_SG(SG_VALU, 3);
+                    } else {
+                        WIDE_SG(SG_VALU, 1);
+                    }
                 }
             }
             // second barrier: the loaders have staged the next tile and form its P
@@ -316,9 +379,9 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
 
             // ---- (3) E = T diag(beta) R and D_last E (fp16 B operands) per slice,
             // under them the scale Gamma of each token on (2)
-            half8 e16[2][2], d16[2][2];
+            half8 e16[NSL][2], d16[NSL][2];
 #pragma unroll
-            for (int sl = 0; sl < 2; ++sl) {
+            for (int sl = 0; sl < NSL; ++sl) {
                 f32x4 E[4];
 #pragma unroll
                 for (int rb = 0; rb < 4; ++rb) E[rb] = mfma_f16(tf[frag_index(rb, 0)], rf[sl][0], f32x4{0.f, 0.f, 0.f, 0.f});
@@ -341,7 +404,7 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                 d16[sl][1] = to_half8(E[2], E[3]);
             }
 #pragma unroll
-            for (int i = 0; i < 12; ++i) {
+            for (int i = 0; i < 6 * NSL; ++i) {
                 WIDE_SG(SG_MFMA, 1);
                 WIDE_SG(SG_VALU, 4);
             }
@@ -363,33 +426,33 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
             for (int kb = 0; kb < NKB; ++kb) {
                 if (kb + 1 < NKB) ktread(kb + 1, kt[(kb + 1) & 1]);
 #pragma unroll
-                for (int sl = 0; sl < 2; ++sl) {
+                for (int sl = 0; sl < NSL; ++sl) {
                     S[sl][kb] = mfma_f16(kt[kb & 1][0], d16[sl][0], S[sl][kb]);
                     S[sl][kb] = mfma_f16(kt[kb & 1][1], d16[sl][1], S[sl][kb]);
                 }
                 if (kb < 4) {
                     const int rb = kb;
 #pragma unroll
-                    for (int sl = 0; sl < 2; ++sl) {
+                    for (int sl = 0; sl < NSL; ++sl) {
                         oacc[rb][sl] = mfma_f16(e16[sl][0], pf[frag_index(rb, 0)], oacc[rb][sl]);
                         if (rb >= 2) oacc[rb][sl] = mfma_f16(e16[sl][1], pf[frag_index(rb, 1)], oacc[rb][sl]);
                     }
 #pragma unroll
-                    for (int sl = 0; sl < 2; ++sl) {
+                    for (int sl = 0; sl < NSL; ++sl) {
                         if constexpr (OUT_BF16) {
                             // into this wave's band of the v tile (o_stage_at), for the
                             // loaders to store as whole rows
                             const int r = 16 * rb + ln;
-                            *(u32x2 *)(&sh.V[buf][o_stage_at(r, 32 * w + 16 * sl + 4 * lg)]) =
+                            *(u32x2 *)(&sh.V[buf][o_stage_at(r, wr0 + 16 * sl + 4 * lg)]) =
                                 __builtin_bit_cast(u32x2, __builtin_convertvector(oacc[rb][sl], bf16x4));
                         } else {
-                            const uint32_t off = (uint32_t)(16 * rb + ln) * row_bytes + (uint32_t)(j * D + 32 * w + 16 * sl + 4 * lg) * ES;
+                            const uint32_t off = (uint32_t)(16 * rb + ln) * row_bytes + (uint32_t)(j * D + wr0 + 16 * sl + 4 * lg) * ES;
                             store_o4_f32(oacc[rb][sl], rs, off);
                         }
                     }
                 }
                 if (kb + 1 < NKB) WIDE_SG(SG_DSR, 4);
-                const int nm = 4 + (kb < 2 ? 2 : kb < 4 ? 4 : 0);
+                const int nm = 2 * NSL + (kb < 2 ? NSL : kb < 4 ? 2 * NSL : 0);
                 for (int i = 0; i < nm; ++i) {
                     WIDE_SG(SG_MFMA, 1);
                     WIDE_SG(SG_VALU, 2);
@@ -400,8 +463,8 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
             // write signal: ||E row||^2 over each slice's 16 columns per token
             if (a.wsWrite) {
 #pragma unroll
-                for (int sl = 0; sl < 2; ++sl) {
-                    float *wb = a.wsWrite + ((size_t)j * a.n_split + 2 * w + sl) * a.st.T + t0;
+                for (int sl = 0; sl < NSL; ++sl) {
+                    float *wb = a.wsWrite + ((size_t)j * a.n_split + wr0 / 16 + sl) * a.st.T + t0;
 #pragma unroll
                     for (int ks = 0; ks < 2; ++ks) {
                         const float wsum = row_sq_sum16(e16[sl][ks], ln);
@@ -415,7 +478,7 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
             // frame started from (read back from the scratch area), snapshot
             if (DRIFT && TILE * lt + n == frame_end) {
 #pragma unroll
-                for (int sl = 0; sl < 2; ++sl) {
+                for (int sl = 0; sl < NSL; ++sl) {
                     float num = 0.f, den = 0.f;
 #pragma unroll
                     for (int kb = 0; kb < NKB; ++kb) {
@@ -433,7 +496,7 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                     const __amdgpu_buffer_rsrc_t rsn = __builtin_amdgcn_make_buffer_rsrc(
                         (void *)(a.snapshots + ((size_t)frame * a.H_v + j) * D * D), (short)0, D * D * 4, RSRC_FLAGS);
 #pragma unroll
-                    for (int sl = 0; sl < 2; ++sl)
+                    for (int sl = 0; sl < NSL; ++sl)
 #pragma unroll
                         for (int kb = 0; kb < NKB; ++kb)
                             __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, S[sl][kb]), rsn, lane_row, sconst(sl, kb), 0);
@@ -443,15 +506,15 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                 frame_end = min(frame_end + a.frame_len, len);
             }
         };
-        for (int lt = 0; lt < n_tiles; lt += 2) {
-            tile(lt, std::integral_constant<int, 0>());
-            if (lt + 1 < n_tiles) tile(lt + 1, std::integral_constant<int, 1>());
+        for (int i = 0; i < nt; i += 2) {
+            tile(lt0 + i, std::integral_constant<int, 0>());
+            if (i + 1 < nt) tile(lt0 + i + 1, std::integral_constant<int, 1>());
         }
-        if (n_tiles > 0) lds_barrier();  // loader 3 reduces the last frame after it
+        if (nt > 0) lds_barrier();  // loader 3 reduces the last frame after it
         const __amdgpu_buffer_rsrc_t rout =
             __builtin_amdgcn_make_buffer_rsrc((void *)(a.state_out + hbase), (short)0, D * D * 4, RSRC_FLAGS);
 #pragma unroll
-        for (int sl = 0; sl < 2; ++sl)
+        for (int sl = 0; sl < NSL; ++sl)
 #pragma unroll
             for (int kb = 0; kb < NKB; ++kb)
                 __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, S[sl][kb]), rout, lane_row, sconst(sl, kb), 0);
@@ -462,18 +525,25 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
             constexpr int NT = X < 2 ? 2 : 1;  // T and P fragments
             constexpr int F_FIRST = X < 2 ? 2 * X : 4 + (X - 2);
             constexpr int CH = D / 8, RPI = 64 / CH;  // 16-byte chunks per row, rows per 64-lane load
-            auto load = [&](WideLoad &s, int lt_) __attribute__((always_inline)) {
-                const int lt = min(lt_, n_tiles - 1);  // clamped: every call issues the same loads
+            // the workgroup's band of v and o columns (r0 .. r0 + 64 NSL - 1)
+            constexpr int VCH = 8 * NSL, VRPI = 64 / VCH, NV = 16 / VRPI;  // chunks per row, rows per load, loads
+            // it_: the tile's place in this launch (tile lt0 + it_)
+            auto load = [&](WideLoad &s, int it_) __attribute__((always_inline)) {
+                const int lt = lt0 + min(it_, nt - 1);  // clamped: every call issues the same loads
                 const int t0 = st + TILE * lt, n = min(TILE, en - t0);
                 const size_t tv = (size_t)(tile_base + lt) * a.H_v + j;
                 const uint16_t *kb = a.k + (size_t)t0 * a.H_k * D + (size_t)qh * D + 8 * (lane % CH);
                 const uint16_t *qb = a.q + (size_t)t0 * a.H_k * D + (size_t)qh * D + 8 * (lane % CH);
-                const uint16_t *vb = a.v + ((size_t)t0 * a.H_v + j) * D + 8 * (lane % CH);
+                const uint16_t *vb = a.v + ((size_t)t0 * a.H_v + j) * D + r0 + 8 * (lane % VCH);
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
                     const uint32_t r = (uint32_t)min(16 * X + RPI * c + lane / CH, n - 1);
                     s.k[c] = *(const u32x4 *)(kb + r * (uint32_t)a.H_k * D);
                     s.q[c] = *(const u32x4 *)(qb + r * (uint32_t)a.H_k * D);
+                }
+#pragma unroll
+                for (int c = 0; c < NV; ++c) {
+                    const uint32_t r = (uint32_t)min(16 * X + VRPI * c + lane / VCH, n - 1);
                     s.v[c] = *(const u32x4 *)(vb + r * (uint32_t)a.H_v * D);
                 }
                 const u32x4 *tb = (const u32x4 *)(a.wsT + tv * TP_HALVES);
@@ -488,7 +558,11 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                     const int row = 16 * X + RPI * c + lane / CH, ch = lane % CH;
                     *(u32x4 *)(&sh.K[buf][row * D + 8 * (ch ^ swz<D>(row))]) = __builtin_bit_cast(u32x4, bf16x8_to_f16(s.k[c]));
                     *(u32x4 *)(&sh.Q[buf][row * D + 8 * (ch ^ swz<D>(row))]) = __builtin_bit_cast(u32x4, bf16x8_to_f16(s.q[c]));
-                    *(u32x4 *)(&sh.V[buf][row * WIDE_VLD + 8 * ch]) = s.v[c];
+                }
+#pragma unroll
+                for (int c = 0; c < NV; ++c) {
+                    const int row = 16 * X + VRPI * c + lane / VCH;
+                    *(u32x4 *)(&sh.V[buf][row * WIDE_VLD + r0 + 8 * (lane % VCH)]) = s.v[c];
                 }
 #pragma unroll
                 for (int c = 0; c < NT; ++c) sh.T[buf][F_FIRST + c][lane] = s.t[c];
@@ -506,7 +580,7 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
             // and the output scale, zero above the diagonal.  Rows past a ragged
             // tile's end hold copies of its last row: they only reach o rows that
             // are not stored, since P is lower triangular
-            auto form_p = [&](auto bufc) __attribute__((always_inline)) {
+            auto form_p_rows = [&](auto bufc) __attribute__((always_inline)) {
                 constexpr int buf = decltype(bufc)::value;
                 f32x4 gq[X + 1];
 #pragma unroll
@@ -537,16 +611,17 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                 sh.P[buf][frag_index(X, 0)][lane] = __builtin_bit_cast(u32x4, to_half8(pblock(0), pblock(1)));
                 if (X >= 2) sh.P[buf][frag_index(X, 1)][lane] = __builtin_bit_cast(u32x4, to_half8(pblock(2), pblock(3)));
             };
+            auto form_p = [&](auto bufc) __attribute__((always_inline)) { form_p_rows(bufc); };
             // bf16 o of tile lt from the v buffer it was staged in (rows 16 X .. 16 X +
             // 15, the rows this loader restages next): 16-byte pieces read back in
-            // order, stored as whole 256-byte rows; stores past a ragged tile's end
-            // fall outside the buffer resource and are dropped
+            // order, stored as whole rows of the workgroup's band; stores past a
+            // ragged tile's end fall outside the buffer resource and are dropped
             // (read_o into registers before the rows are restaged, store_o later)
             auto read_o = [&](u32x4(&ov)[4], auto bufc) __attribute__((always_inline)) {
-                constexpr int buf = decltype(bufc)::value;  // == lt % 2
+                constexpr int buf = decltype(bufc)::value;  // == (lt - lt0) % 2
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const int r = 16 * X + RPI * c + lane / CH, ch = lane % CH;
+                for (int c = 0; c < NV; ++c) {
+                    const int r = 16 * X + VRPI * c + lane / VCH, ch = r0 / 8 + lane % VCH;
                     // dims 8 ch .. 8 ch + 7 = two 4-dim pieces, kept adjacent by the permutation
                     // and swapped when (r / 4) % 2 == 1
                     ov[c] = *(const u32x4 *)(&sh.V[buf][o_stage_at(r, 8 * ch) & ~7]);
@@ -558,50 +633,56 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                 const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
                     (char *)a.o + (size_t)t0 * row_bytes, (short)0, (int)(row_bytes * (uint32_t)n), 0x00020000);
 #pragma unroll
-                for (int c = 0; c < 4; ++c) {
-                    const int r = 16 * X + RPI * c + lane / CH, ch = lane % CH;
+                for (int c = 0; c < NV; ++c) {
+                    const int r = 16 * X + VRPI * c + lane / VCH, ch = r0 / 8 + lane % VCH;
                     const u32x4 v = ((r >> 2) & 1) ? u32x4{ov[c][2], ov[c][3], ov[c][0], ov[c][1]} : ov[c];
                     __builtin_amdgcn_raw_buffer_store_b128(v, rs, (uint32_t)r * row_bytes + (uint32_t)(j * D + 8 * ch) * 2, 0, 0);
                 }
             };
-            // drift: loader 3 adds the 8 slices' sums of a frame that ended in
-            // the previous tile (fixed order) and writes them
-            int frame = frame_base;
-            int frame_end = a.frame_len > 0 ? min(a.frame_len, len) : len;
+            // drift: loader 3 adds the slices' sums of a frame that ended in the
+            // previous tile and writes them: a whole head's 8 slices in order as
+            // one pair, or per slice (a half head's 4 slices always per slice; the
+            // head's pair is then added after both halves are done)
+            const int fr0 = frame_base + (a.frame_len > 0 ? tok0 / a.frame_len : 0);
+            int frame = fr0;
+            int frame_end = a.frame_len > 0 ? min(tok0 + a.frame_len, len) : len;
             auto drift_reduce = [&](int it) __attribute__((always_inline)) {
                 if (!DRIFT || X != 3 || it < 1) return;
-                const int lt = it - 1;
+                const int lt = lt0 + it - 1;
                 if (TILE * lt + min(TILE, len - TILE * lt) != frame_end) return;
                 if (a.wsDrift && frame < a.n_frames) {
-                    float2 pr[8];
+                    constexpr int NS = 4 * NSL;  // this workgroup's slices sl0 .. sl0 + NS - 1
+                    float2 pr[NS];
 #pragma unroll
-                    for (int s = 0; s < 8; ++s) {
-                        const float2 p = sh.DR[frame & 1][s >> 1][s & 1][lane];
+                    for (int s = 0; s < NS; ++s) {
+                        const float2 p = sh.DR[frame & 1][s / NSL][s % NSL][lane];
                         pr[s] = float2{wave_sum(p.x), wave_sum(p.y)};
                     }
                     const size_t fj = (size_t)frame * a.H_v + j;
-                    if (a.drift_out) {  // per-head pair: the slices in order
+                    if (NSL == 2 && a.drift_out) {  // per-head pair: the slices in order
                         float num = 0.f, den = 0.f;
 #pragma unroll
-                        for (int s = 0; s < 8; ++s) {
+                        for (int s = 0; s < NS; ++s) {
                             num += pr[s].x;
                             den += pr[s].y;
                         }
                         if (lane == 0) *(float2 *)(a.drift_out + fj * 2) = float2{num, den};
-                    } else {  // per-slice pairs
-                        if (lane < 8) {
-                            float2 mine = pr[0];
+                    } else if (lane < NS) {  // per-slice pairs
+                        float2 mine = pr[0];
 #pragma unroll
-                            for (int s = 1; s < 8; ++s)
-                                if (lane == s) mine = pr[s];
-                            *(float2 *)(a.wsDrift + (fj * a.n_split + lane) * 2) = mine;
-                        }
+                        for (int s = 1; s < NS; ++s)
+                            if (lane == s) mine = pr[s];
+                        float *dst = a.wsDrift + (fj * a.n_split + sl0 + lane) * 2;
+                        if (a.drift_out)  // read by the other half's workgroup
+                            store_pair_coherent(dst, mine.x, mine.y);
+                        else
+                            *(float2 *)dst = mine;
                     }
                 }
                 ++frame;
                 frame_end = min(frame_end + a.frame_len, len);
             };
-            if (n_tiles > 0) {
+            if (nt > 0) {
                 WideLoad s0, s1;
                 load(s0, 0);
                 load(s1, 1);
@@ -619,18 +700,46 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                     if (it == 0) form_p(std::integral_constant<int, 0>());
                     u32x4 ov[4];
                     if (OUT_BF16 && it >= 1) read_o(ov, bufc);
-                    if (it + 1 < n_tiles) stage(s, bufc);
-                    if (it < n_tiles) lds_barrier();
-                    if (OUT_BF16 && it >= 1) store_o(it - 1, ov);
-                    if (it + 1 < n_tiles) form_p(bufc);
+                    if (it + 1 < nt) stage(s, bufc);
+                    if (it < nt) lds_barrier();
+                    if (OUT_BF16 && it >= 1) store_o(lt0 + it - 1, ov);
+                    if (it + 1 < nt) form_p(bufc);
                     load(s, it + 3);
                     drift_reduce(it);
                 };
-                // tile t lives in register set t % 2 and LDS buffer t % 2; iteration it
-                // stages tile it + 1 and then loads tile it + 3 into the set just freed
-                for (int it = 0; it <= n_tiles; it += 2) {
+                // tile lt0 + t lives in register set t % 2 and LDS buffer t % 2;
+                // iteration it stages tile it + 1 and then loads tile it + 3 into the set
+                // just freed
+                for (int it = 0; it <= nt; it += 2) {
                     step(it, s1, std::integral_constant<int, 1>());
-                    if (it + 1 <= n_tiles) step(it + 1, s0, std::integral_constant<int, 0>());
+                    if (it + 1 <= nt) step(it + 1, s0, std::integral_constant<int, 0>());
+                }
+            }
+            // half heads with per-head pairs: the second of the head's two
+            // workgroups to finish adds the 8 slices of this launch's frames in
+            // order (the counters were cleared by the prep pass)
+            if (NSL == 1 && DRIFT && X == 3 && a.drift_out && a.wsDrift) {
+                wait_vmem_all();  // this wave's pairs are coherent before the count
+                unsigned prev = 0;
+                if (lane == 0)
+                    prev = __hip_atomic_fetch_add(&a.drift_cnt[b * a.H_v + j], 1u, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+                prev = __builtin_amdgcn_readfirstlane(prev);
+                if (prev == (unsigned)HW - 1u) {
+                    const int fr1 = min(frame_base + frames_in(len, a.frame_len), a.n_frames);
+                    for (int f = fr0 + lane; f < fr1; f += 64) {
+                        const size_t fj = (size_t)f * a.H_v + j;
+                        float2 pr[8];
+#pragma unroll
+                        for (int s8 = 0; s8 < 8; ++s8) pr[s8] = load_pair_coherent(a.wsDrift + (fj * a.n_split + s8) * 2);
+                        float num = 0.f, den = 0.f;
+#pragma unroll
+                        for (int s8 = 0; s8 < 8; ++s8) {
+                            num += pr[s8].x;
+                            den += pr[s8].y;
+                        }
+                        *(float2 *)(a.drift_out + fj * 2) = float2{num, den};
+                    }
                 }
             }
         };
@@ -645,19 +754,38 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
     }
 }
 
-hipError_t launch_gdn_wide(const GdnArgs &a, int n_wg, bool o_bf16, bool drift, hipStream_t stream) {
+template <int NSL>
+static hipError_t launch_wide_nsl(const GdnArgs &a, int n_wg, bool o_bf16, bool drift, hipStream_t stream) {
     if (o_bf16) {
         if (drift)
-            hipLaunchKernelGGL((gdn_wide_kernel<true, true>), dim3(n_wg), dim3(512), 0, stream, a);
+            hipLaunchKernelGGL((gdn_wide_kernel<true, true, NSL>), dim3(n_wg), dim3(512), 0, stream, a);
         else
-            hipLaunchKernelGGL((gdn_wide_kernel<true, false>), dim3(n_wg), dim3(512), 0, stream, a);
+            hipLaunchKernelGGL((gdn_wide_kernel<true, false, NSL>), dim3(n_wg), dim3(512), 0, stream, a);
     } else {
         if (drift)
-            hipLaunchKernelGGL((gdn_wide_kernel<false, true>), dim3(n_wg), dim3(512), 0, stream, a);
+            hipLaunchKernelGGL((gdn_wide_kernel<false, true, NSL>), dim3(n_wg), dim3(512), 0, stream, a);
         else
-            hipLaunchKernelGGL((gdn_wide_kernel<false, false>), dim3(n_wg), dim3(512), 0, stream, a);
+            hipLaunchKernelGGL((gdn_wide_kernel<false, false, NSL>), dim3(n_wg), dim3(512), 0, stream, a);
     }
     return hipGetLastError();
+}
+
+// One launch of whole heads, or, for calls whose frames are whole tiles and
+// when at most tail_streams streams fit the GPU as half heads, whole heads up
+// to the cut (the tile from which at most tail_streams streams are left,
+// on a frame boundary) and half heads from it, the second launch starting
+// from the states the first one wrote.
+hipError_t launch_gdn_wide(const GdnArgs &a0, int n_heads, int tail_streams, bool o_bf16, bool drift,
+                           hipStream_t stream) {
+    GdnArgs a = a0;
+    const bool split = tail_streams >= 1 && a.frame_len > 0 && a.frame_len % TILE == 0;
+    a.wide_tail_streams = tail_streams;
+    a.wide_phase = split ? 1 : 0;
+    hipError_t e = launch_wide_nsl<2>(a, n_heads, o_bf16, drift, stream);
+    if (e != hipSuccess || !split) return e;
+    a.wide_phase = 2;
+    a.state_in = a.state_out;
+    return launch_wide_nsl<1>(a, 2 * n_heads, o_bf16, drift, stream);
 }
 
 }  // namespace ds
