@@ -580,7 +580,7 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
             // and the output scale, zero above the diagonal.  Rows past a ragged
             // tile's end hold copies of its last row: they only reach o rows that
             // are not stored, since P is lower triangular
-            auto form_p_rows = [&](auto bufc) __attribute__((always_inline)) {
+            auto form_p = [&](auto bufc) __attribute__((always_inline)) {
                 constexpr int buf = decltype(bufc)::value;
                 f32x4 gq[X + 1];
 #pragma unroll
@@ -611,7 +611,6 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                 sh.P[buf][frag_index(X, 0)][lane] = __builtin_bit_cast(u32x4, to_half8(pblock(0), pblock(1)));
                 if (X >= 2) sh.P[buf][frag_index(X, 1)][lane] = __builtin_bit_cast(u32x4, to_half8(pblock(2), pblock(3)));
             };
-            auto form_p = [&](auto bufc) __attribute__((always_inline)) { form_p_rows(bufc); };
             // bf16 o of tile lt from the v buffer it was staged in (rows 16 X .. 16 X +
             // 15, the rows this loader restages next): 16-byte pieces read back in
             // order, stored as whole rows of the workgroup's band; stores past a
