@@ -152,3 +152,30 @@ def test_wide_output_scale_and_extreme_gates(ds):
                        oracle.drift_scores(ref["partials"][None], oracle.PER_HEAD))
     assert ed <= TOL_DRIFT, ed
     print(f"wide, scale 1/sqrt(d), extreme gates: o {eo:.2e} S {es:.2e} drift {ed:.2e}")
+
+
+def test_wide_split_launches_full_heads(ds):
+    """8 streams x 32 v-heads of unequal lengths, frames of two tiles: the call
+    runs as whole heads up to the cut (tile 8: from there 4 streams are left)
+    and half heads from it; fp32 o, a non-zero entry state, per-head drift
+    pairs (added over the two half heads) and snapshots against the oracle,
+    and the per-slice pairs of the same call adding up to the per-head pairs
+    bit for bit."""
+    lens = [2000, 1900, 700, 600, 500, 300, 100, 0]
+    x = synth.make_gdn_inputs(lens, 16, 32, 128, 128, novelty=True, config=3, layer=11)
+    S0 = (np.random.default_rng(13).standard_normal((8, 32, 128, 128)) * 0.05).astype(np.float32).astype(np.float64)
+    gpu = run_gpu(ds, x, state_in=S0, snapshots=True)
+    ref = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, x.frame_len, S0=S0, snapshots=True)
+    eo, es = _check(ds, gpu, ref)
+    assert rel_fro(gpu["snapshots"], ref["snapshots"]) <= TOL_O
+    sl = ds.gdn_chunk_fwd(dev_bf16(x.q), dev_bf16(x.k), dev_bf16(x.v), dev_f32(x.g), dev_f32(x.beta), lens, 128,
+                          state_in=dev_f32(S0), drift_per_slice=True)
+    torch.cuda.synchronize()
+    ph = gpu["raw"]["drift_partials"].cpu().numpy()
+    ps = sl["drift_partials"].cpu().numpy().reshape(ph.shape[0], 32, 8, 2)
+    acc = np.zeros(ph.shape, np.float32)
+    for s_ in range(8):
+        acc += ps[:, :, s_, :]
+    assert np.array_equal(acc, ph)
+    assert torch.equal(sl["o"], gpu["raw"]["o"]) and torch.equal(sl["state"], gpu["raw"]["state"])
+    print(f"wide, split launches: o {eo:.2e} S {es:.2e}")
