@@ -49,8 +49,9 @@ constexpr int WIDE_VLD = 128 + 16;  // halves per LDS row of the v tile (288 B: 
                                     // read start 8 banks apart, so its 16 lanes cover all 32 banks)
 
 // A bf16 o tile is staged in the v buffer of its tile once the v rows are
-// consumed: compute wave w writes output dims 32 w .. 32 w + 31 of every token,
-// exactly the band of columns of v that it alone read, so no wave overwrites
+// consumed: a compute wave writes the output dims of its own state rows (32 of
+// a whole head, 16 of a half head) for every token, exactly the band of
+// columns of v that it alone read, so no wave overwrites
 // v that another still reads.  Inside the band the 8-byte pieces (4 dims) are
 // permuted by an XOR with (row / 4) % 4, so that the 16 rows of one 8-byte
 // write hit distinct banks.  Returns the halves offset of dims d .. d + 3
@@ -250,7 +251,7 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                 }
             };
 
-            // ---- (1) K S0^T (token rows 16 rb + 4 lg + e, state row 32 w + 16 sl + ln)
+            // ---- (1) K S0^T (token rows 16 rb + 4 lg + e, state row wr0 + 16 sl + ln)
             // from the fp16 copy of S0 (k-step ks pairs state blocks 2 ks, 2 ks + 1).
             // Under it: the fp16 copy of the next k-step, and S <- Gamma_last S in place
             // for the blocks already copied (from here on the fp32 S is only the
@@ -295,7 +296,7 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
             half8 qa[2][4];
             v4i16 vv[2][2];
             float4 g4[4];
-            // v[16 rb + 4 lg + e][32 w + 16 sl + ln], rb = 2 pr + h, for quarter (sl, pr)
+            // v[16 rb + 4 lg + e][wr0 + 16 sl + ln], rb = 2 pr + h, for quarter (sl, pr)
             auto vread = [&](int sl, int pr, v4i16(&vq)[2]) __attribute__((always_inline)) {
 #pragma unroll
                 for (int h = 0; h < 2; ++h)
@@ -474,7 +475,7 @@ __global__ __launch_bounds__(512, 1) void gdn_wide_kernel(GdnArgs a) {
                 }
             }
 
-            // frame end: per-lane drift sums of both slices against the state the
+            // frame end: per-lane drift sums of the wave's slices against the state the
             // frame started from (read back from the scratch area), snapshot
             if (DRIFT && TILE * lt + n == frame_end) {
 #pragma unroll
