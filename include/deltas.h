@@ -18,6 +18,9 @@
  *   kv_evict_topk_indexed
  *                   the same step over a slot-indexed cache: identical
  *                   selection, the K and V rows stay where they are.
+ *   kv_append_indexed
+ *                   a chunk's K and V rows and table entries into such a
+ *                   cache, in one launch.
  *
  * Conventions shared by every entry point
  *   - Pointers are DEVICE pointers unless marked "host".  The caller owns
@@ -314,6 +317,37 @@ ds_status kv_evict_topk_indexed(int32_t capacity, int32_t *pos, int32_t *chunk_i
                                 int32_t n_sink, int32_t n_window, int32_t n_buckets, int32_t *keep_out,
                                 int32_t *free_out, int32_t *new_len, void *workspace,
                                 size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------
+ * kv_append_indexed -- a chunk's K/V rows into the slot-indexed cache
+ * ------------------------------------------------------------------------
+ * The cache update of the streaming procedure (Section 3.3): before each
+ * eviction step the new chunk's tokens join the cache.  With the cache
+ * addressed through a slot table (kv_evict_topk_indexed), tokens
+ * n .. n + T - 1 take the first T rows of the free list free_a[0, na)
+ * followed by free_b[0, nb) (say, the rows the last eviction freed); for
+ * t < T, with s_t that row:
+ *     row s_t of plane p  =  new_rows[p][t]          (every plane)
+ *     pos[n + t] = pos0 + t,  chunk_id[n + t] = chunk,  slot[n + t] = s_t,
+ * and the remaining na + nb - T entries of the list go, in order, to
+ * free_rest[0, na + nb - T).  One launch on `stream`; the caller keeps n and
+ * the list lengths on the host.
+ * Layouts: planes: n_planes device pointers, each [capacity][row_bytes]
+ * (the K planes of the layers, then the V planes, as the caller likes);
+ * new_rows: n_planes device pointers, each [T][row_bytes]; free_a, free_b,
+ * free_rest: int32 (4-byte aligned; free_rest may not overlap the others);
+ * pos, chunk_id, slot: int32 [capacity].
+ * Requires 1 <= n_planes <= 64, row_bytes a multiple of 16, plane and row
+ * pointers 16-byte aligned, T <= na + nb <= capacity and n + T <= capacity;
+ * the call is rejected (nothing written) otherwise.  A free-list entry
+ * outside [0, capacity) is skipped on the device (its token's rows and
+ * table entries are not written).
+ */
+ds_status kv_append_indexed(void *const *planes, const void *const *new_rows, int32_t n_planes,
+                            int32_t row_bytes, int32_t capacity, const int32_t *free_a, int32_t na,
+                            const int32_t *free_b, int32_t nb, int32_t *free_rest, int32_t T, int32_t n,
+                            int32_t pos0, int32_t chunk, int32_t *pos, int32_t *chunk_id, int32_t *slot,
+                            void *stream);
 
 /* ------------------------------------------------------------------------
  * kv_evict_topk_indexed_noalloc -- kv_evict_topk_indexed without a workspace

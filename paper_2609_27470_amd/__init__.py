@@ -24,6 +24,7 @@ EXPORTED = [
     "gdn_chunk_fwd", "deltas_drift",
     "deltas_drift_states", "ds_kv_workspace_bytes", "kv_evict_topk", "ds_kv_device_status",
     "ds_kv_indexed_workspace_bytes", "kv_evict_topk_indexed", "gdn_decode_step", "kv_evict_topk_indexed_noalloc",
+    "kv_append_indexed",
 ]
 NOALLOC_MAX_CAPACITY = 65536
 
@@ -86,6 +87,8 @@ def lib():
         L.kv_evict_topk_indexed_noalloc.argtypes = [I32, P, P, P, P, I32, I32, I32, I32, I32, I32, P, P, P,
                                                     ctypes.POINTER(I32), P]
         L.kv_evict_topk_indexed_noalloc.restype = I32
+        L.kv_append_indexed.argtypes = [P, P, I32, I32, I32, P, I32, P, I32, P, I32, I32, I32, I32, P, P, P, P]
+        L.kv_append_indexed.restype = I32
         _lib = L
     return _lib
 
@@ -321,3 +324,32 @@ def kv_outcome_word(workspace):
     """The outcome word of the last eviction on this workspace as a device
     int32 tensor of one element (a view: no synchronisation)."""
     return workspace[:4].view(torch.int32)
+
+
+def kv_append_indexed(k_planes, v_planes, k_new, v_new, free_a, na, free_b, nb, free_rest, T, n, pos0, chunk, pos,
+                      chunk_id, slot, stream=None):
+    """A chunk's rows into a slot-indexed cache (see kv_append_indexed in
+    deltas.h): k_planes and v_planes [L][capacity][row] (2-byte elements),
+    k_new and v_new [L][>= T][row] with contiguous rows; tokens n .. n + T - 1
+    take the first T rows of free_a[:na] ++ free_b[:nb], the rest of that list
+    goes to free_rest.  pos, chunk_id, slot: int32 [capacity]."""
+    L, capacity, row = k_planes.shape
+    if v_planes.shape != k_planes.shape or k_new.shape[0] != L or v_new.shape[0] != L:
+        raise ValueError("K/V planes and new rows must have matching layer counts and shapes")
+    for t in (k_new, v_new):
+        if t.shape[-1] != row or t.stride(-1) != 1 or t.stride(-2) != row or t.shape[1] < int(T):
+            raise ValueError("new rows must be [L][>= T][row] with contiguous rows")
+    for t in (k_planes, v_planes):
+        if not t.is_contiguous():
+            raise ValueError("K/V planes must be contiguous")
+    for t in (pos, chunk_id, slot):
+        if t.dtype != torch.int32 or t.numel() != capacity:
+            raise ValueError("pos, chunk_id and slot must be int32 tensors of the cache capacity")
+    row_bytes = row * k_planes.element_size()
+    planes = (ctypes.c_void_p * (2 * L))(*[k_planes[l].data_ptr() for l in range(L)],
+                                         *[v_planes[l].data_ptr() for l in range(L)])
+    rows = (ctypes.c_void_p * (2 * L))(*[k_new[l].data_ptr() for l in range(L)],
+                                       *[v_new[l].data_ptr() for l in range(L)])
+    _check(lib().kv_append_indexed(planes, rows, 2 * L, row_bytes, capacity, _ptr(free_a), int(na), _ptr(free_b),
+                                   int(nb), _ptr(free_rest), int(T), int(n), int(pos0), int(chunk), _ptr(pos),
+                                   _ptr(chunk_id), _ptr(slot), _stream(stream)))

@@ -287,6 +287,57 @@ ds_status kv_evict_topk(const ds_kv_shape *shape, void *const *k_layers, void *c
     return DS_OK;
 }
 
+ds_status kv_append_indexed(void *const *planes, const void *const *new_rows, int32_t n_planes,
+                            int32_t row_bytes, int32_t capacity, const int32_t *free_a, int32_t na,
+                            const int32_t *free_b, int32_t nb, int32_t *free_rest, int32_t T, int32_t n,
+                            int32_t pos0, int32_t chunk, int32_t *pos, int32_t *chunk_id, int32_t *slot,
+                            void *stream) {
+    g_last_error[0] = 0;
+    if (n_planes < 1 || n_planes > ds::KV_MAX_PLANES)
+        return fail(DS_E_UNSUPPORTED, "n_planes=%d (1..%d)", n_planes, ds::KV_MAX_PLANES);
+    if (row_bytes < 16 || row_bytes % 16) return fail(DS_E_SHAPE, "row_bytes=%d must be a positive multiple of 16", row_bytes);
+    if (row_bytes > 65536) return fail(DS_E_UNSUPPORTED, "row_bytes=%d (at most 65536)", row_bytes);
+    if (capacity < 1) return fail(DS_E_SHAPE, "capacity=%d", capacity);
+    if (T < 0 || n < 0 || (long long)n + T > capacity)
+        return fail(DS_E_SHAPE, "n=%d + T=%d outside [0, capacity=%d]", n, T, capacity);
+    if (na < 0 || nb < 0 || (long long)na + nb < T)
+        return fail(DS_E_ARG, "the free list (%d + %d rows) is shorter than T=%d", na, nb, T);
+    if ((long long)na + nb > capacity) return fail(DS_E_ARG, "the free list (%d + %d rows) exceeds capacity", na, nb);
+    if ((long long)capacity * row_bytes > (1LL << 40)) return fail(DS_E_UNSUPPORTED, "cache too large");
+    if (T == 0 && na + nb == 0) return DS_OK;
+    if (!planes || !new_rows || !pos || !chunk_id || !slot || (na > 0 && !free_a) || (nb > 0 && !free_b) ||
+        (na + nb > T && !free_rest))
+        return fail(DS_E_NULL, "planes, new_rows, pos, chunk_id, slot and the free lists are required");
+    ds::KvAppendLaunch p;
+    p.n_planes = n_planes;
+    for (int i = 0; i < n_planes; ++i) {
+        if (!planes[i] || !new_rows[i]) return fail(DS_E_NULL, "plane %d has a NULL pointer", i);
+        if (misaligned(planes[i]) || misaligned(new_rows[i])) return fail(DS_E_ALIGN, "plane %d not 16-byte aligned", i);
+        p.planes[i] = (char *)planes[i];
+        p.new_rows[i] = (const char *)new_rows[i];
+    }
+    const void *ip[] = {free_a, free_b, free_rest, pos, chunk_id, slot};
+    for (const void *q : ip)
+        if (q && (((uintptr_t)q) & 3u)) return fail(DS_E_ALIGN, "an int32 pointer is not 4-byte aligned");
+    p.row_bytes = row_bytes;
+    p.capacity = capacity;
+    p.free_a = free_a;
+    p.free_b = free_b;
+    p.na = na;
+    p.nb = nb;
+    p.free_rest = free_rest;
+    p.T = T;
+    p.n = n;
+    p.pos0 = pos0;
+    p.chunk = chunk;
+    p.pos = pos;
+    p.chunk_id = chunk_id;
+    p.slot = slot;
+    hipError_t e = ds::launch_kv_append(p, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "kv_append_indexed launch");
+    return DS_OK;
+}
+
 size_t ds_kv_indexed_workspace_bytes(int32_t capacity) {
     if (capacity < 1) return 0;
     return ds::kv_workspace_layout(0, 16, capacity).total;

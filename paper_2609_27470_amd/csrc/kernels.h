@@ -89,6 +89,19 @@ struct KvLaunch {
 };
 hipError_t launch_kv_evict(const KvLaunch &p, hipStream_t stream);
 
+// A chunk's rows into a slot-indexed cache (kv_append_indexed).
+struct KvAppendLaunch {
+    char *planes[KV_MAX_PLANES];          // [capacity][row_bytes] each
+    const char *new_rows[KV_MAX_PLANES];  // [T][row_bytes] each
+    int n_planes, row_bytes, capacity;
+    const int32_t *free_a, *free_b;
+    int na, nb;
+    int32_t *free_rest;
+    int T, n, pos0, chunk;
+    int32_t *pos, *chunk_id, *slot;
+};
+hipError_t launch_kv_append(const KvAppendLaunch &p, hipStream_t stream);
+
 // The library's own scratch for the indexed eviction without a workspace: a
 // fixed device array per GPU (4 MiB) and the largest capacity whose layout
 // fits in it.  kv_noalloc_scratch returns the array's address on the current

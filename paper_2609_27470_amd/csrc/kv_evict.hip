@@ -935,6 +935,41 @@ KvWorkspace kv_workspace_layout(int n_layers, int row_bytes, int capacity) {
     return w;
 }
 
+// ---------------------------------------------------------------------------
+// kv_append_indexed: workgroup (t, p) for t < T copies row t of plane p's new
+// rows into row s_t of the plane, s_t the t-th entry of the free list
+// free_a ++ free_b, 16 bytes a thread; the workgroups of plane 0 also write the
+// token's pos, chunk id and slot; workgroups past T (plane 0) copy the rest of
+// the free list to free_rest.  Entries outside [0, capacity) are skipped.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void kv_append_kernel(KvAppendLaunch a) {
+    const int t = blockIdx.x, p = blockIdx.y;
+    auto free_at = [&](int i) { return i < a.na ? a.free_a[i] : a.free_b[i - a.na]; };
+    if (t < a.T) {
+        const int s = free_at(t);
+        if (s < 0 || s >= a.capacity) return;
+        const uint4 *src = (const uint4 *)(a.new_rows[p] + (size_t)t * a.row_bytes);
+        uint4 *dst = (uint4 *)(a.planes[p] + (size_t)s * a.row_bytes);
+        for (int i = threadIdx.x; i < a.row_bytes / 16; i += 256) dst[i] = src[i];
+        if (p == 0 && threadIdx.x == 0) {
+            a.pos[a.n + t] = a.pos0 + t;
+            a.chunk_id[a.n + t] = a.chunk;
+            a.slot[a.n + t] = s;
+        }
+    } else if (p == 0) {
+        const int i = (t - a.T) * 256 + threadIdx.x;  // index into the rest of the list
+        if (i < a.na + a.nb - a.T) a.free_rest[i] = free_at(a.T + i);
+    }
+}
+
+hipError_t launch_kv_append(const KvAppendLaunch &p, hipStream_t stream) {
+    const int rest = p.na + p.nb - p.T;
+    const int gx = p.T + (rest + 255) / 256;
+    if (gx == 0) return hipSuccess;
+    hipLaunchKernelGGL(kv_append_kernel, dim3(gx, p.n_planes), dim3(256), 0, stream, p);
+    return hipGetLastError();
+}
+
 hipError_t launch_kv_evict(const KvLaunch &p, hipStream_t stream) {
     char *ws = p.ws;
     KvArgs a;

@@ -15,8 +15,8 @@ back, so a question can be answered (more tokens, decode steps) and the
 stream then resumes exactly where it was.
 
 Only argument marshalling and buffer bookkeeping happen here; every step of
-the computation runs in the HIP kernels behind the C ABI.  Appending K/V rows
-and the snapshot copies are plain device copies.
+the computation runs in the HIP kernels behind the C ABI.  The snapshot
+copies are plain device copies.
 
 A chunk is a tiny call per layer (about 125 tokens), so launching the layers
 one by one from the host costs more than the kernels themselves.
@@ -32,7 +32,8 @@ from is host state.
 By default (`indexed=True`) the cache is addressed through a slot table
 (logical token i lives in physical row slot[i]): eviction is
 `kv_evict_topk_indexed`, which keeps exactly the same tokens and moves no K/V
-byte, and a chunk's rows are written into the rows the last eviction freed.
+byte, and a chunk's rows are written into the rows the last eviction freed
+(`kv_append_indexed`: rows and table entries in one launch).
 The logical view (rows slot[0..length)) equals the order-preserving cache
 that `indexed=False` keeps with `kv_evict_topk` (rows compacted in place).
 
@@ -48,8 +49,8 @@ from dataclasses import dataclass
 
 import torch
 
-from . import (LAYER_FROB, deltas_drift, gdn_chunk_fwd, gdn_shape, gdn_workspace_bytes, kv_evict_topk,
-               kv_evict_topk_indexed, kv_indexed_workspace_bytes, kv_outcome_word, kv_workspace_bytes)
+from . import (LAYER_FROB, deltas_drift, gdn_chunk_fwd, gdn_shape, gdn_workspace_bytes, kv_append_indexed,
+               kv_evict_topk, kv_evict_topk_indexed, kv_indexed_workspace_bytes, kv_outcome_word, kv_workspace_bytes)
 
 # the longest chunk whose layer calls fit two 64-token tiles
 SMALL_CHUNK = 128
@@ -119,12 +120,16 @@ class DeltaSStream:
         self.indexed = indexed
         if indexed:
             self.slot = torch.zeros(self.capacity, dtype=torch.int32, device=dev)
-            self.free = torch.arange(self.capacity, dtype=torch.int32, device=dev)   # rows not in use
-            self.n_free = self.capacity
+            # rows not in use: self._free_bufs[self._fa][:self._na] followed by
+            # self.freed[:self._nb] (the rows the last eviction freed); the
+            # append takes the first T and writes the rest into the other buffer
+            self._free_bufs = [torch.arange(self.capacity, dtype=torch.int32, device=dev),
+                               torch.empty(self.capacity, dtype=torch.int32, device=dev)]
+            self._fa, self._na, self._nb = 0, self.capacity, 0
             self.freed = torch.empty(self.capacity, dtype=torch.int32, device=dev)
             self.kv_ws = torch.empty(max(kv_indexed_workspace_bytes(self.capacity), 1), dtype=torch.uint8, device=dev)
         else:
-            self.slot = self.free = None
+            self.slot = None
             self.kv_ws = torch.empty(max(kv_workspace_bytes(kv_layers, row_elems * 2, self.capacity), 1),
                                      dtype=torch.uint8, device=dev)
         self.kv_fail = torch.zeros(1, dtype=torch.int32, device=dev)   # max outcome word of every eviction
@@ -132,6 +137,24 @@ class DeltaSStream:
         self.length = 0      # tokens in the cache
         self.n_chunks = 0    # chunks seen (the next chunk's id)
         self.next_pos = 0    # position of the next token
+
+    @property
+    def free(self):
+        """The physical rows not in use, in the order the next chunk takes them
+        (a new device tensor; None for the contiguous cache)."""
+        if not self.indexed:
+            return None
+        return torch.cat([self._free_bufs[self._fa][:self._na], self.freed[:self._nb]])
+
+    @free.setter
+    def free(self, rows):
+        if not self.indexed:
+            raise ValueError("the contiguous cache has no free list")
+        rows = rows.to(device=self.dev, dtype=torch.int32).reshape(-1)
+        if rows.numel() > self.capacity:
+            raise ValueError("free list longer than the cache")
+        self._free_bufs[0][:rows.numel()].copy_(rows)
+        self._fa, self._na, self._nb = 0, rows.numel(), 0
 
     def step(self, layer_inputs, k_rows, v_rows, stream=None):
         """Consume one chunk.
@@ -170,27 +193,24 @@ class DeltaSStream:
     def _append_and_evict(self, T, k_rows, v_rows):
         c = self.n_chunks
         n = self.length
-        if self.indexed:
-            rows = self.free[:T]
-            self.k.index_copy_(1, rows.to(torch.int64), k_rows)
-            self.v.index_copy_(1, rows.to(torch.int64), v_rows)
-            self.slot[n:n + T] = rows
-            self.free = self.free[T:]
+        if self.indexed:   # rows, positions, chunk ids and slots in one launch
+            rest = self._free_bufs[1 - self._fa]
+            kv_append_indexed(self.k, self.v, k_rows, v_rows, self._free_bufs[self._fa], self._na, self.freed,
+                              self._nb, rest, T, n, self.next_pos, c, self.pos, self.chunk_id, self.slot)
+            self._fa, self._na, self._nb = 1 - self._fa, self._na + self._nb - T, 0
         else:
             self.k[:, n:n + T].copy_(k_rows)
             self.v[:, n:n + T].copy_(v_rows)
-        self.pos[n:n + T] = torch.arange(self.next_pos, self.next_pos + T, dtype=torch.int32, device=self.dev)
-        self.chunk_id[n:n + T] = c
+            self.pos[n:n + T] = torch.arange(self.next_pos, self.next_pos + T, dtype=torch.int32, device=self.dev)
+            self.chunk_id[n:n + T] = c
         self.next_pos += T
         self.n_chunks = c + 1
         n += T
         ns, nw, nb = self.policy
         if self.indexed:
-            new_len, _, freed = kv_evict_topk_indexed(self.pos, self.chunk_id, self.slot, self.scores[:self.n_chunks],
-                                                      n, self.M, ns, nw, nb, free_out=self.freed,
-                                                      workspace=self.kv_ws)
-            if n > self.M:
-                self.free = torch.cat([self.free, freed[:n - self.M]])
+            new_len, _, _ = kv_evict_topk_indexed(self.pos, self.chunk_id, self.slot, self.scores[:self.n_chunks],
+                                                  n, self.M, ns, nw, nb, free_out=self.freed, workspace=self.kv_ws)
+            self._nb = max(n - self.M, 0)
             self.length = new_len
         else:
             self.length, _ = kv_evict_topk(list(self.k), list(self.v), self.pos, self.chunk_id,
@@ -262,7 +282,7 @@ class DeltaSStream:
         if self.indexed:   # rows stay where they are: keep the physical planes and the tables
             return Snapshot(self.state.clone(), self.k.clone(), self.v.clone(), self.pos[:n].clone(),
                             self.chunk_id[:n].clone(), self.scores[:self.n_chunks].clone(), self.slot[:n].clone(),
-                            self.free.clone(), n, self.n_chunks, self.next_pos)
+                            self.free, n, self.n_chunks, self.next_pos)
         return Snapshot(self.state.clone(), self.k[:, :n].clone(), self.v[:, :n].clone(), self.pos[:n].clone(),
                         self.chunk_id[:n].clone(), self.scores[:self.n_chunks].clone(), None, None, n, self.n_chunks,
                         self.next_pos)
@@ -276,7 +296,7 @@ class DeltaSStream:
             self.k.copy_(s.k)
             self.v.copy_(s.v)
             self.slot[:n].copy_(s.slot)
-            self.free = s.free.clone()
+            self.free = s.free
         else:
             self.k[:, :n].copy_(s.k)
             self.v[:, :n].copy_(s.v)

@@ -218,3 +218,34 @@ def test_noalloc_eviction_host_checks(ds):
     assert L.kv_evict_topk_indexed_noalloc(cap, None, None, None, None, 1, 300, 200, 0, 0, 1, None, None, None,
                                            None, None) == 1
     assert L.ds_kv_indexed_workspace_bytes(cap) <= 4 << 20
+
+
+def test_append_host_checks(ds):
+    """kv_append_indexed refuses, before any launch, plane counts outside
+    1..64, rows that are not whole 16-byte units, a chunk past the capacity, a
+    free list shorter than the chunk or longer than the cache, NULL and
+    misaligned pointers; an empty chunk with an empty list does nothing."""
+    L = ds.lib()
+    P = ctypes.c_void_p
+    fake = 1 << 20                                   # never dereferenced: every call below fails on the host
+    planes = (P * 2)(fake, fake)
+    rows = (P * 2)(fake, fake)
+    ok = dict(planes=planes, rows=rows, n_planes=2, row_bytes=64, capacity=100, fa=fake, na=50, fb=None, nb=0,
+              rest=fake, T=10, n=40, pos0=0, chunk=0, pos=fake, cid=fake, slot=fake)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return L.kv_append_indexed(a["planes"], a["rows"], a["n_planes"], a["row_bytes"], a["capacity"], a["fa"],
+                                   a["na"], a["fb"], a["nb"], a["rest"], a["T"], a["n"], a["pos0"], a["chunk"],
+                                   a["pos"], a["cid"], a["slot"], None)
+
+    assert call(n_planes=0) == 5 and call(n_planes=65) == 5
+    assert call(row_bytes=24) == 2 and call(row_bytes=65552) == 5
+    assert call(n=95) == 2                           # n + T > capacity
+    assert call(na=5) == 6                           # free list shorter than the chunk
+    assert call(na=60, nb=60) == 6                   # free list longer than the cache
+    assert call(pos=None) == 1 and call(fa=None) == 1
+    assert call(planes=(P * 2)(fake, fake + 8)) == 4
+    assert call(slot=fake + 2) == 4
+    assert b"int32 pointer" in L.ds_last_error()
+    assert call(T=0, na=0, planes=None, rows=None) == 0

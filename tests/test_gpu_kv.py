@@ -356,3 +356,41 @@ def test_indexed_broken_invariants_leave_table_untouched(ds):
     assert np.array_equal(p.cpu().numpy(), pos) and np.array_equal(c.cpu().numpy(), chunk)
     assert torch.equal(s, torch.arange(120, dtype=torch.int32, device=DEV))
     assert torch.equal(free, torch.full((60,), -3, dtype=torch.int32, device=DEV))
+
+
+@pytest.mark.parametrize("na,nb,T,n,row", [(50, 30, 40, 10, 64), (50, 30, 70, 20, 4096), (0, 80, 80, 0, 16),
+                                           (80, 0, 0, 7, 64), (300, 700, 257, 600, 4096), (1024, 0, 1, 0, 48)])
+def test_append_indexed_matches_indexing(ds, na, nb, T, n, row):
+    """kv_append_indexed against plain tensor indexing: each plane's rows at
+    the first T entries of free_a ++ free_b hold the new rows, every other row
+    keeps its bytes; pos, chunk_id and slot [n, n + T) hold the positions,
+    the chunk id and those rows, the rest of each table is untouched; the
+    rest of the list lands in free_rest.  Bit for bit, spanning several
+    256-entry blocks of the list copy and both list segments."""
+    capacity = 1024 + 64
+    g = torch.Generator(device=DEV).manual_seed(na * 7 + nb + T)
+    L = 3
+    kp = torch.randint(-30000, 30000, (L, capacity, row // 2), dtype=torch.int16, device=DEV, generator=g)
+    vp = torch.randint(-30000, 30000, (L, capacity, row // 2), dtype=torch.int16, device=DEV, generator=g)
+    kn = torch.randint(-30000, 30000, (L, T + 5, row // 2), dtype=torch.int16, device=DEV, generator=g)
+    vn = torch.randint(-30000, 30000, (L, T + 5, row // 2), dtype=torch.int16, device=DEV, generator=g)
+    perm = torch.randperm(capacity, generator=torch.Generator().manual_seed(T)).to(torch.int32).to(DEV)
+    fa, fb = perm[:na].clone(), perm[na:na + nb].clone()
+    rest = torch.full((capacity,), -9, dtype=torch.int32, device=DEV)
+    tabs = [torch.randint(-100, 100, (capacity,), dtype=torch.int32, device=DEV, generator=g) for _ in range(3)]
+    exp_k, exp_v, exp_tabs = kp.clone(), vp.clone(), [t.clone() for t in tabs]
+    lst = torch.cat([fa, fb]).to(torch.int64)
+    dst = lst[:T]
+    exp_k[:, dst] = kn[:, :T]
+    exp_v[:, dst] = vn[:, :T]
+    exp_tabs[0][n:n + T] = torch.arange(5000, 5000 + T, dtype=torch.int32, device=DEV)
+    exp_tabs[1][n:n + T] = 37
+    exp_tabs[2][n:n + T] = dst.to(torch.int32)
+    ds.kv_append_indexed(kp, vp, kn, vn, fa if na else None, na, fb if nb else None, nb, rest, T, n, 5000, 37,
+                         *tabs)
+    torch.cuda.synchronize()
+    assert torch.equal(kp, exp_k) and torch.equal(vp, exp_v)
+    for t, e in zip(tabs, exp_tabs):
+        assert torch.equal(t, e)
+    r = na + nb - T
+    assert torch.equal(rest[:r], lst[T:].to(torch.int32)) and bool((rest[r:] == -9).all())
