@@ -71,6 +71,26 @@ __device__ bool locate_tile(const Streams &s, int ti, int &t0, int &n) {
     return found;
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave on data-parallel
+// primitives (no LDS round trip): Hillis-Steele inside each row of 16 lanes
+// (row shifts by 1, 2, 4, 8, lanes shifted in from outside the row read 0),
+// then the total of row 0 added to row 1 and of row 2 to row 3 (broadcast of
+// lane 15 of the row before), then the total of rows 0 - 1 to rows 2 - 3
+// (broadcast of lane 31).
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float dpp_f32(float x) {  // lanes not written or shifted in from outside a row: 0
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, ROWS, 0xF, true));
+}
+__device__ __forceinline__ float wave_prefix_sum(float v) {
+    v += dpp_f32<0x111, 0xF>(v);  // row_shr:1
+    v += dpp_f32<0x112, 0xF>(v);  // row_shr:2
+    v += dpp_f32<0x114, 0xF>(v);  // row_shr:4
+    v += dpp_f32<0x118, 0xF>(v);  // row_shr:8
+    v += dpp_f32<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
+    v += dpp_f32<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
+    return v;
+}
+
 __device__ __forceinline__ f32x4 mfma_f32_16x16x4(float a, float b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }

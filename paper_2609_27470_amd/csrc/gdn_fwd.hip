@@ -36,9 +36,11 @@ namespace ds {
 // (its own gates): P is gated, multiplied by the output scale and written
 // straight from the K Q^T registers (their layout is already P's fragment
 // layout), and the inverse of the unit
-// lower-triangular I + A is blocked in 16 x 16 blocks, the diagonal blocks by
-// forward substitution and the off-diagonal ones on fp32 matrix cores,
-// T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj, by distance from the diagonal.
+// lower-triangular I + A is blocked in 16 x 16 blocks: the diagonal blocks by
+// forward substitution, then the off-diagonal ones on fp32 matrix cores
+// in two levels of the 2 x 2 block inverse
+// [[T11, 0], [T21, T22]] with T21 = -T22 A21 T11: first the 32 x 32 halves,
+// then the lower-left quarter.
 // 39 KiB of LDS and at most 128 VGPRs, so that four workgroups share a CU.
 // ============================================================================
 template <int D>
@@ -199,12 +201,7 @@ __device__ __forceinline__ void prep_tile(const GdnArgs &a, int ti, int t0, int 
                 bv = a.beta[(size_t)(t0 + min(lane, n - 1)) * a.H_v + j];
             }
             if (lane >= n) gv = bv = 0.f;
-            float s = gv;
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {
-                const float y = __shfl_up(s, off, 64);
-                if (lane >= off) s += y;
-            }
+            float s = wave_prefix_sum(gv);
             s *= 1.4426950408889634f;  // exp(gamma) = exp2(s)
             gam_s[slot][lane] = s;
             beta_s[slot][lane] = bv;
@@ -259,53 +256,74 @@ __device__ __forceinline__ void prep_tile(const GdnArgs &a, int ti, int t0, int 
         }
         lds_barrier();
 
-        // diagonal blocks (wave 0, lane = 16 * block + column)
-        if (w == 0) {
-            const int o = 16 * (lane >> 4), c = lane & 15;
-            float x[16];
+        // 16x16 block products on fp32 matrix cores from LDS (row-major blocks,
+        // leading dimension ld): acc += X Y.  16x16x4 fragments: A lane = [ln][lg],
+        // B lane = [lg][ln], C lane = [4 lg + e][ln].
+        auto bmm = [&](f32x4 acc, const float *X, int ldx, const float *Y, int ldy) __attribute__((always_inline)) {
+#pragma unroll
+            for (int s4 = 0; s4 < 4; ++s4) acc = mfma_f32_16x16x4(X[ln * ldx + 4 * s4 + lg], Y[(4 * s4 + lg) * ldy + ln], acc);
+            return acc;
+        };
+        auto blk = [&](float *M, int bi, int bj) __attribute__((always_inline)) { return M + 16 * bi * ALD + 16 * bj; };
+
+        // (1) diagonal blocks: wave w inverts block w by forward substitution,
+        // lane 4 c + p taking column c of the inverse and the terms i = p mod 4
+        // of every row's dot product (its four partial sums are added across
+        // the lane quad), so that a lane reads at most four A values per row
+        // and the dependent chain per row is one product and two adds.  Lane p
+        // keeps x_i for the rows i = p mod 4 (zero until they are formed; A is
+        // zero on and above the diagonal).
+        {
+            const int o = 16 * w, c = lane >> 2, p = lane & 3;
+            float xp[4] = {0.f, 0.f, 0.f, 0.f};  // x_{4 m + p}
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                float s = (r == c) ? 1.f : 0.f;
+                float ps = 0.f;
 #pragma unroll
-                for (int i = 0; i < r; ++i) s -= As[(o + r) * ALD + o + i] * x[i];
-                x[r] = s;
+                for (int m = 0; m < (r + 3) / 4; ++m) ps += As[(o + r) * ALD + o + 4 * m + p] * xp[m];
+                ps += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, ps), 0xB1, 0xF, 0xF, true));  // quad lanes p ^ 1
+                ps += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, ps), 0x4E, 0xF, 0xF, true));  // quad lanes p ^ 2
+                const float xr = ((r == c) ? 1.f : 0.f) - ps;
+                if (p == (r & 3)) xp[r >> 2] = xr;
             }
 #pragma unroll
-            for (int r = 0; r < 16; ++r) Ts[(o + r) * ALD + o + c] = x[r];
+            for (int m = 0; m < 4; ++m) Ts[(o + 4 * m + p) * ALD + o + c] = xp[m];
         }
         lds_barrier();
 
-        // off-diagonal blocks.  16x16x4 fp32 fragments: A lane = [ln][lg],
-        // B lane = [lg][ln], C lane = [4 lg + e][ln].
-        for (int d = 1; d <= 3; ++d) {
-            const int p = w;  // pair handled by this wave: block row bi = p + d, column bj = p
-            if (p + d <= 3) {
-                const int bi = p + d, bj = p;
-                f32x4 y = {0.f, 0.f, 0.f, 0.f};
-                for (int kb = bj; kb < bi; ++kb) {
+        // first level of the blocked inverse, waves 0 and 1:
+        // T_{2u+1,2u} = -T_{2u+1,2u+1} (A_{2u+1,2u} T_{2u,2u})
+        if (w < 2) {
+            float *yw = Ys[w];
+            const int bi = 2 * w + 1, bj = 2 * w;
+            const f32x4 y = bmm(f32x4{0.f, 0.f, 0.f, 0.f}, blk(As, bi, bj), ALD, blk(Ts, bj, bj), ALD);
 #pragma unroll
-                    for (int s = 0; s < 4; ++s) {
-                        const float av = As[(16 * bi + ln) * ALD + 16 * kb + 4 * s + lg];
-                        const float tb = Ts[(16 * kb + 4 * s + lg) * ALD + 16 * bj + ln];
-                        y = mfma_f32_16x16x4(av, tb, y);
-                    }
-                }
-                float *yw = Ys[w];
+            for (int e = 0; e < 4; ++e) yw[(4 * lg + e) * 16 + ln] = y[e];
+            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's Y is in LDS
+            const f32x4 t = bmm(f32x4{0.f, 0.f, 0.f, 0.f}, blk(Ts, bi, bi), ALD, yw, 16);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) yw[(4 * lg + e) * 16 + ln] = y[e];
-                __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's Y is in LDS
-                f32x4 t = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    const float ta = Ts[(16 * bi + ln) * ALD + 16 * bi + 4 * s + lg];
-                    const float yb = yw[(4 * s + lg) * 16 + ln];
-                    t = mfma_f32_16x16x4(ta, yb, t);
-                }
-#pragma unroll
-                for (int e = 0; e < 4; ++e) Ts[(16 * bi + 4 * lg + e) * ALD + 16 * bj + ln] = -t[e];
-            }
-            lds_barrier();
+            for (int e = 0; e < 4; ++e) Ts[(16 * bi + 4 * lg + e) * ALD + 16 * bj + ln] = -t[e];
         }
+        lds_barrier();
+
+        // (2) second level: the lower-left 32x32 quarter
+        //   T_[23][01] = -T_[23][23] (A_[23][01] T_[01][01]),
+        // wave w forming block (i, j) = (2 + w / 2, w % 2) of each product
+        {
+            const int i = 2 + (w >> 1), j = w & 1;
+            f32x4 y = bmm(f32x4{0.f, 0.f, 0.f, 0.f}, blk(As, i, j), ALD, blk(Ts, j, j), ALD);
+            if (j == 0) y = bmm(y, blk(As, i, 1), ALD, blk(Ts, 1, 0), ALD);
+            float *yw = Ys[w];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) yw[(4 * lg + e) * 16 + ln] = y[e];
+            lds_barrier();
+            // Y_{m j} of wave 2 (m - 2) + j
+            f32x4 t = bmm(f32x4{0.f, 0.f, 0.f, 0.f}, blk(Ts, i, 2), ALD, Ys[j], 16);
+            if (i == 3) t = bmm(t, blk(Ts, 3, 3), ALD, Ys[2 + j], 16);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) Ts[(16 * i + 4 * lg + e) * ALD + 16 * j + ln] = -t[e];
+        }
+        lds_barrier();
 
         // T diag(beta) (fp16, zero above the diagonal) in fragment order
         for (int c = tid; c < 6 * 64; c += 256) {
