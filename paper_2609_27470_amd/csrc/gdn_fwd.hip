@@ -217,15 +217,22 @@ __device__ __forceinline__ void prep_tile(const GdnArgs &a, int ti, int t0, int 
     auto pfrags = [&](int jj, int slot) __attribute__((always_inline)) {
         if (!WP) return;
         const size_t tv = (size_t)ti * a.H_v + jbase + jj;
+        // the gates first (one LDS round trip), then every product, masked by a
+        // select: a lane-dependent condition around the products would compile
+        // to a branch that waits for its own LDS reads
         const float gq_i = gam_s[slot][16 * w + ln];  // query 16 w + ln
+        float4 gj[4];
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) gj[nb] = *(const float4 *)(&gam_s[slot][16 * nb + 4 * lg]);
         auto pblock = [&](int nb) __attribute__((always_inline)) {
             f32x4 pk = {0.f, 0.f, 0.f, 0.f};
-            if (nb <= w) {
-                const float4 gj = *(const float4 *)(&gam_s[slot][16 * nb + 4 * lg]);
-                const float gjv[4] = {gj.x, gj.y, gj.z, gj.w};
+            if (nb <= w) {  // wave-uniform
+                const float gjv[4] = {gj[nb].x, gj[nb].y, gj[nb].z, gj[nb].w};
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    pk[e] = (nb < w || 4 * lg + e <= ln) ? __builtin_amdgcn_exp2f(gq_i - gjv[e]) * (a.scale * gq[nb][e]) : 0.f;
+                for (int e = 0; e < 4; ++e) {
+                    const float pv = __builtin_amdgcn_exp2f(gq_i - gjv[e]) * (a.scale * gq[nb][e]);
+                    pk[e] = (nb < w || 4 * lg + e <= ln) ? pv : 0.f;
+                }
             }
             return pk;
         };
@@ -249,7 +256,10 @@ __device__ __forceinline__ void prep_tile(const GdnArgs &a, int ti, int t0, int 
                 for (int e = 0; e < 4; ++e) {
                     const int r = 16 * w + 4 * lg + e, i = 16 * nb + ln;
                     float av = 0.f;
-                    if (nb <= w && i < r) av = brv[e] * __builtin_amdgcn_exp2f(grv[e] - gi[nb]) * gk[nb][e];
+                    if (nb <= w) {  // wave-uniform; the lane condition is a select (see pfrags)
+                        const float v = brv[e] * __builtin_amdgcn_exp2f(grv[e] - gi[nb]) * gk[nb][e];
+                        av = i < r ? v : 0.f;
+                    }
                     As[r * ALD + i] = av;
                 }
             }
@@ -275,12 +285,20 @@ __device__ __forceinline__ void prep_tile(const GdnArgs &a, int ti, int t0, int 
         // zero on and above the diagonal).
         {
             const int o = 16 * w, c = lane >> 2, p = lane & 3;
+            // all 36 A values of the lane read first (they do not depend on x;
+            // left to the scheduler, each row's reads were waited for in turn)
+            float am[16][4];
+#pragma unroll
+            for (int r = 1; r < 16; ++r)
+#pragma unroll
+                for (int m = 0; m < (r + 3) / 4; ++m) am[r][m] = As[(o + r) * ALD + o + 4 * m + p];
+            __builtin_amdgcn_sched_barrier(0);
             float xp[4] = {0.f, 0.f, 0.f, 0.f};  // x_{4 m + p}
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 float ps = 0.f;
 #pragma unroll
-                for (int m = 0; m < (r + 3) / 4; ++m) ps += As[(o + r) * ALD + o + 4 * m + p] * xp[m];
+                for (int m = 0; m < (r + 3) / 4; ++m) ps += am[r][m] * xp[m];
                 ps += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, ps), 0xB1, 0xF, 0xF, true));  // quad lanes p ^ 1
                 ps += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, ps), 0x4E, 0xF, 0xF, true));  // quad lanes p ^ 2
                 const float xr = ((r == c) ? 1.f : 0.f) - ps;
