@@ -72,6 +72,20 @@ def test_d128_gqa_novelty_ragged(ds, T):
     assert rel_fro(gpu["snapshots"], ref["snapshots"]) <= TOL_O
 
 
+@pytest.mark.parametrize("H_k,H_v,T", [(2, 8, 64 * 129 + 45), (2, 6, 64 * 171 + 3), (2, 8, 1500)])
+def test_wider_gqa_groups(ds, H_k, H_v, T):
+    """Three and four v-heads per qk-head.  Long enough calls (more than 1024
+    (tile, v-head) pairs) take the prep pass per qk-head with the group's
+    v-heads in turn; shorter ones the prep per v-head."""
+    x = synth.workload_inputs("single_layer", T=T, H_k=H_k, H_v=H_v)
+    S0 = np.random.default_rng(21).standard_normal((1, H_v, 128, 128)) * 0.1
+    S0 = S0.astype(np.float32).astype(np.float64)
+    gpu = run_gpu(ds, x, state_in=S0)
+    ref = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, x.frame_len, S0=S0)
+    eo, es = _check_all(gpu, ref, ds)
+    print(f"H_k={H_k} H_v={H_v} T={T}: o {eo:.2e} S {es:.2e}")
+
+
 @pytest.mark.parametrize("frame_len", [128, 0])
 def test_varlen_packed_ragged(ds, frame_len):
     """Packed streams with empty, one-token, sub-tile and multi-frame lengths."""
