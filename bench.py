@@ -98,9 +98,9 @@ def cpu_baseline(x, tiny, budget_s=12.0):
         t0 = time.perf_counter()
         oracle.gdn_forward(x.q[sl], x.k[sl], x.v[sl], x.g[sl], x.beta[sl], np.array([0, n], np.int32), FRAME)
         dt = time.perf_counter() - t0
-        if dt * 4 > budget_s or n * 4 > T:
+        if dt * 4 > budget_s or n >= T:
             break
-        n *= 4
+        n = min(n * 4, T)
     gdn_s_per_token = dt / n
     # one eviction event on the eviction-loop cache shape
     rng = np.random.default_rng(0)
@@ -126,9 +126,11 @@ def cpu_baseline(x, tiny, budget_s=12.0):
                        n_threads=1)
     one_s = time.perf_counter() - t0
     rec = {"value": T / step_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-           "sample": f"fp64 token recurrence of all 32 heads over the first {n} of the {T} tokens "
-                     f"({dt:.1f} s on {threads} threads, scaled to the full stream) + one eviction (selection "
-                     f"in Python, numpy gather of 16 planes of {CAPACITY}x4 KiB rows)",
+           "sample": (f"fp64 token recurrence of all 32 heads over " +
+                      (f"the whole stream of {T} tokens ({dt:.1f} s" if n >= T else
+                       f"the first {n} of the {T} tokens ({dt:.1f} s, scaled to the full stream") +
+                      f" on {threads} threads, {dt * threads:.0f} thread-seconds) + one eviction (selection "
+                      f"in Python, numpy gather of 16 planes of {CAPACITY}x4 KiB rows)"),
            "gdn_tokens_per_s": 1.0 / gdn_s_per_token,
            "single_thread": {"tiny_tokens_per_s": tiny.T_total / tiny_s,
                              "single_layer_tokens_per_s": n1 / one_s,
