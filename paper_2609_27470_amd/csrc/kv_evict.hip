@@ -610,13 +610,28 @@ __global__ __launch_bounds__(SEL_THREADS) void kv_select_kernel(KvArgs a) {
     // next block's reads lie above what this block writes.
     if (a.slot && total_kept == a.M) {
         __syncthreads();  // the keep list written above by every thread is read below
+        // the keep entries of the next block are loaded while this block moves
+        // (the pass never writes the keep list): one dependent round trip to
+        // memory per block instead of two
+        int nk[SEL_PER];
+        auto fetch_keep = [&](int base) __attribute__((always_inline)) {
+#pragma unroll
+            for (int k = 0; k < SEL_PER; ++k) {
+                const int d = base + k * SEL_THREADS + tid;
+                nk[k] = d < a.M ? a.keep[d] : 0;
+            }
+        };
+        if (first_move < a.M) fetch_keep(first_move);
         for (int base = first_move; base < a.M; base += SEL_BLOCK) {
-            int vp[SEL_PER], vc[SEL_PER], vs[SEL_PER];
+            int vp[SEL_PER], vc[SEL_PER], vs[SEL_PER], kk[SEL_PER];
+#pragma unroll
+            for (int k = 0; k < SEL_PER; ++k) kk[k] = nk[k];
+            if (base + SEL_BLOCK < a.M) fetch_keep(base + SEL_BLOCK);
 #pragma unroll
             for (int k = 0; k < SEL_PER; ++k) {
                 const int d = base + k * SEL_THREADS + tid;
                 if (d < a.M) {
-                    const int src = a.keep[d];
+                    const int src = kk[k];
                     vp[k] = a.pos[src];
                     vc[k] = a.chunk[src];
                     vs[k] = a.slot[src];
