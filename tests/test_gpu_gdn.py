@@ -86,6 +86,19 @@ def test_wider_gqa_groups(ds, H_k, H_v, T):
     print(f"H_k={H_k} H_v={H_v} T={T}: o {eo:.2e} S {es:.2e}")
 
 
+def test_d64_many_heads_per_slice_path(ds):
+    """d = 64 with 256 (stream, v-head) pairs: the per-slice kernel (the
+    whole-head kernel is d = 128 only) with more workgroups than CUs, per-head
+    drift sums added by the last workgroup of each (stream, v-head)."""
+    rng = np.random.default_rng(41)
+    lengths = [int(x) for x in rng.integers(0, 400, 64)]
+    lengths[:4] = [0, 1, 64, 65]
+    x = synth.make_gdn_inputs(lengths, 2, 4, 64, 128, novelty=False, config=3)
+    gpu = run_gpu(ds, x)
+    ref = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, x.frame_len)
+    _check_all(gpu, ref, ds)
+
+
 @pytest.mark.parametrize("frame_len", [128, 0])
 def test_varlen_packed_ragged(ds, frame_len):
     """Packed streams with empty, one-token, sub-tile and multi-frame lengths."""
