@@ -86,6 +86,29 @@ def test_wider_gqa_groups(ds, H_k, H_v, T):
     print(f"H_k={H_k} H_v={H_v} T={T}: o {eo:.2e} S {es:.2e}")
 
 
+@pytest.mark.parametrize("T,d,drift_per_slice", [(1500, 128, False), (100, 128, True), (130, 64, False)])
+def test_output_scale_per_slice_path(ds, T, d, drift_per_slice):
+    """A 1/sqrt(d) output scale on the per-slice kernel: prep folds it into P,
+    the output waves into scale * Gamma; long calls take two launches, calls of
+    at most two tiles with per-slice pairs the one-launch form."""
+    x = synth.make_gdn_inputs([T], 2, 4, d, 64, novelty=False, config=3)
+    scale = 1.0 / np.sqrt(float(d))
+    S0 = (np.random.default_rng(19).standard_normal((1, 4, d, d)) * 0.1).astype(np.float32).astype(np.float64)
+    r = ds.gdn_chunk_fwd(dev_bf16(x.q), dev_bf16(x.k), dev_bf16(x.v), dev_f32(x.g), dev_f32(x.beta), lengths_of(x),
+                         x.frame_len, state_in=dev_f32(S0), scale=scale, drift_per_slice=drift_per_slice)
+    torch.cuda.synchronize()
+    ref = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, x.frame_len, S0=S0, scale=scale)
+    eo = rel_fro(r["o"].cpu().numpy().astype(np.float64), ref["o"])
+    es = rel_fro(r["state"].cpu().numpy().astype(np.float64), ref["S"])
+    assert eo <= TOL_O and es <= TOL_O, (eo, es)
+    # o is linear in the scale: the same call unscaled gives o / scale
+    r1 = ds.gdn_chunk_fwd(dev_bf16(x.q), dev_bf16(x.k), dev_bf16(x.v), dev_f32(x.g), dev_f32(x.beta), lengths_of(x),
+                          x.frame_len, state_in=dev_f32(S0), drift_per_slice=drift_per_slice)
+    torch.cuda.synchronize()
+    assert rel_fro(r1["o"].cpu().numpy().astype(np.float64) * scale, r["o"].cpu().numpy().astype(np.float64)) <= 1e-3
+    assert torch.equal(r1["state"], r["state"])
+
+
 def test_d64_many_heads_per_slice_path(ds):
     """d = 64 with 256 (stream, v-head) pairs: the per-slice kernel (the
     whole-head kernel is d = 128 only) with more workgroups than CUs, per-head
