@@ -179,3 +179,18 @@ def test_wide_split_launches_full_heads(ds):
     assert np.array_equal(acc, ph)
     assert torch.equal(sl["o"], gpu["raw"]["o"]) and torch.equal(sl["state"], gpu["raw"]["state"])
     print(f"wide, split launches: o {eo:.2e} S {es:.2e}")
+
+
+def test_wide_state_in_place(ds):
+    """The state updated in place (state_out aliasing state_in) on the
+    whole-head kernel, including the split into whole-head and half-head
+    launches (the second reads the states the first wrote): bit-equal to the
+    call with a separate output state."""
+    lens = [2000, 1900, 700, 600, 500, 300, 100, 0]
+    x = synth.make_gdn_inputs(lens, 16, 32, 128, 128, novelty=True, config=3, layer=12)
+    S0 = (np.random.default_rng(14).standard_normal((8, 32, 128, 128)) * 0.05).astype(np.float32).astype(np.float64)
+    a = run_gpu(ds, x, state_in=S0)
+    b = run_gpu(ds, x, state_in=S0, in_place=True)
+    assert np.array_equal(a["o"], b["o"])
+    assert np.array_equal(a["S"], b["S"])
+    assert np.array_equal(a["partials"], b["partials"])
