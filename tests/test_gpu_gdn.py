@@ -109,6 +109,22 @@ def test_output_scale_per_slice_path(ds, T, d, drift_per_slice):
     assert torch.equal(r1["state"], r["state"])
 
 
+@pytest.mark.parametrize("T", [1500, 120])
+def test_extreme_gates_per_slice_path(ds, T):
+    """Decay that underflows inside a tile (g = -30), near-unity decay and
+    beta = 0 tokens on the per-slice kernel (two-launch and one-launch forms):
+    the masked entries of P and A whose exponent overflows are discarded."""
+    x = synth.make_gdn_inputs([T], 2, 4, 128, 64, novelty=False, config=3)
+    x.g[:, 0] = -30.0
+    x.g[:, 1] = -1e-4
+    x.beta[::5, 2] = 0.0
+    S0 = (np.random.default_rng(23).standard_normal((1, 4, 128, 128)) * 0.1).astype(np.float32).astype(np.float64)
+    gpu = run_gpu(ds, x, state_in=S0)
+    assert np.all(np.isfinite(gpu["o"])) and np.all(np.isfinite(gpu["S"]))
+    ref = oracle.gdn_forward(x.q, x.k, x.v, x.g, x.beta, x.cu_seqlens, x.frame_len, S0=S0)
+    _check_all(gpu, ref, ds)
+
+
 def test_d64_many_heads_per_slice_path(ds):
     """d = 64 with 256 (stream, v-head) pairs: the per-slice kernel (the
     whole-head kernel is d = 128 only) with more workgroups than CUs, per-head
