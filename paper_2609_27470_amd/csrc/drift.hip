@@ -23,12 +23,13 @@ __device__ __forceinline__ double wave_sum_d(double x) {
 
 // One workgroup (16 waves) per frame.  Wave w takes layers w, w + 16, ...;
 // its lanes take the heads of a layer (lane, lane + 64, ...).  A wave loads
-// the (num, den) pairs of up to DRIFT_LPW of its layers before it reduces any
-// of them, so a frame costs one memory round trip rather than one per layer;
+// the (num, den) pairs of up to DRIFT_LPW of its layers, up to 256 heads (or
+// 16-row slices of 32 heads) each, before it reduces any of them, so a frame
+// costs one memory round trip rather than one per layer;
 // lanes sum in order, the lanes of a wave meet in a butterfly, and the waves'
 // totals are added in wave order.  Every sum has a fixed order, so the result
 // does not depend on scheduling.
-constexpr int DRIFT_WAVES = 16, DRIFT_LPW = 4, DRIFT_HPL = 2;  // waves, layers per wave per round, heads per lane
+constexpr int DRIFT_WAVES = 16, DRIFT_LPW = 4, DRIFT_HPL = 4;  // waves, layers per wave per round, heads per lane
 __global__ __launch_bounds__(64 * DRIFT_WAVES) void drift_frame_kernel(const float *p, int L, int F, int H, int mode,
                                                                         float *scores) {
     const int f = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
