@@ -862,6 +862,11 @@ def main():
         torch.cuda.empty_cache()
         peaks = measured_peaks(dev, stream)
         log("peaks measured")
+    # counter-measured HBM bytes of the other forward shapes (same fingerprint rule)
+    for key, sub, per in (("3_varlen", "varlen", "launch"), ("2_stack", "stack_call", "layer call")):
+        if trec and key in configs and isinstance(trec.get(sub), dict):
+            configs[key]["traffic"] = {"bytes": trec[sub]["bytes_per_launch"], "per": per,
+                                       "ratio_to_algorithmic": trec[sub]["ratio"]}
 
     out = {
         "metric": METRIC,
